@@ -1,0 +1,106 @@
+"""The seeded input generator: published known answers and distribution checks."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2607_23099_amd import synth
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    import os
+    from paper_2607_23099_amd import build
+    if not os.path.exists(synth.LIB_PATH):
+        build.build_synth()
+
+
+def test_philox_known_answers():
+    # Known-answer vectors published with the Random123 library for philox4x32-10.
+    cases = [
+        ([0, 0, 0, 0], [0, 0], [0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8]),
+        ([0xFFFFFFFF] * 4, [0xFFFFFFFF] * 2, [0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD]),
+        ([0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344], [0xA4093822, 0x299F31D0],
+         [0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1]),
+    ]
+    for ctr, key, want in cases:
+        assert list(synth.philox4x32_10(ctr, key)) == want
+
+
+def test_bf16_fill_distribution_and_slicing():
+    n = 1 << 20
+    v = synth.fill_bf16_host(n, seed=11, tensor=synth.T_W1, sigma=0.02)
+    f = synth.bf16_to_f64(v)
+    assert abs(f.mean()) < 1e-4
+    assert abs(f.std() / 0.02 - 1) < 0.01
+    assert np.max(np.abs(f)) < 0.02 * 4.95
+    # Irwin-Hall(8) kurtosis is 3 - 1.2/8 = 2.85.
+    kurt = np.mean((f - f.mean()) ** 4) / f.var() ** 2
+    assert abs(kurt - 2.85) < 0.03
+    # A window of the stream equals the same window of the full fill.
+    w = synth.fill_bf16_host(1000, seed=11, tensor=synth.T_W1, start=5000, slab_elems=n, sigma=0.02)
+    np.testing.assert_array_equal(w, v[5000:6000])
+    # Slabs and tensors are independent streams.
+    a = synth.fill_bf16_host(4096, seed=11, tensor=synth.T_W1, slab0=1, slab_elems=4096, sigma=0.02)
+    b = synth.fill_bf16_host(4096, seed=11, tensor=synth.T_W3, slab0=1, slab_elems=4096, sigma=0.02)
+    assert np.mean(a == v[:4096]) < 0.1 and np.mean(a == b) < 0.1
+    # Crossing a slab boundary restarts the element index in the next slab.
+    two = synth.fill_bf16_host(8192, seed=11, tensor=synth.T_W1, slab0=0, slab_elems=4096, sigma=0.02)
+    np.testing.assert_array_equal(two[4096:], a)
+
+
+def test_fp8_fill_block_quantisation():
+    q, s = synth.fill_fp8_host(256, 384, 2, seed=3, tensor=synth.T_W2, sigma=0.02)
+    assert q.shape == (2, 256, 384) and s.shape == (2, 2, 3)
+    # Every block's largest magnitude maps to +-448 (code 0x7E / 0xFE).
+    for sl in range(2):
+        for rb in range(2):
+            for cb in range(3):
+                blk = q[sl, rb * 128:(rb + 1) * 128, cb * 128:(cb + 1) * 128]
+                assert np.any((blk & 0x7F) == 0x7E)
+                assert not np.any((blk & 0x7F) == 0x7F)
+    # Dequantised values are within half an e4m3 step (relative 2^-4) of the bf16 source.
+    src = synth.bf16_to_f64(synth.fill_bf16_host(256 * 384, seed=3, tensor=synth.T_W2, slab0=1,
+                                                 slab_elems=256 * 384, sigma=0.02)).reshape(256, 384)
+    code = q[1].astype(np.int64)
+    ex, man, sg = (code >> 3) & 15, code & 7, np.where(code >> 7, -1.0, 1.0)
+    val = sg * np.where(ex == 0, man * 2.0 ** -9, (1 + man / 8) * 2.0 ** (ex - 7))
+    deq = val * np.kron(s[1], np.ones((128, 128)))
+    big = np.abs(src) > 0.02 * 448 / 4.9 / 64  # normal e4m3 range after scaling
+    rel = np.abs(deq - src)[big] / np.abs(src)[big]
+    assert rel.max() <= 2.0 ** -4 + 1e-9
+
+
+@pytest.mark.parametrize("E,k,T,alpha,hot", [(8, 2, 64, 1.0, 0), (256, 8, 128, 0.05, 0),
+                                             (384, 8, 256, 0.05, 4), (256, 8, 3, None, 0),
+                                             (384, 8, 1000, 0.03, 0)])
+def test_routing_invariants(E, k, T, alpha, hot):
+    r = synth.routing(E, k, T, alpha, [1, T], n_hot=hot)
+    assert r.ids.shape == (T, k) and r.ids.dtype == np.int32
+    assert r.ids.min() >= 0 and r.ids.max() < E
+    assert all(len(set(row)) == k for row in r.ids.tolist())
+    assert np.all(r.w > 0) and np.allclose(r.w.sum(1), 1.0, atol=1e-6)
+    assert np.all(np.isfinite(r.logp)) and abs(np.logaddexp.reduce(r.logp)) < 1e-12
+    if hot:
+        assert np.sum(np.exp(r.logp) >= 0.1 - 1e-12) >= hot
+
+
+def test_routing_is_seeded_and_skew_follows_alpha():
+    a = synth.routing(256, 8, 64, 0.3, [1, 2, 3])
+    b = synth.routing(256, 8, 64, 0.3, [1, 2, 3])
+    np.testing.assert_array_equal(a.ids, b.ids)
+    np.testing.assert_array_equal(a.w, b.w)
+    # Smaller alpha concentrates p (Sec. II-D): compare mean sum p^2 over draws.
+    m = {al: np.mean([np.exp(2 * synth.routing(256, 8, 0, al, [s]).logp).sum() for s in range(200)])
+         for al in (0.05, 1.0, 10.0)}
+    for al, v in m.items():
+        assert abs(v / ((al + 1) / (256 * al + 1)) - 1) < 0.15
+    assert m[0.05] > m[1.0] > m[10.0]
+
+
+def test_trace_params_ranges():
+    ts, als = zip(*[synth.trace_step_params(s) for s in range(2000)])
+    assert min(ts) >= 1 and max(ts) <= 8192
+    assert min(als) >= 0.03 and max(als) <= 10.0
+    # log-uniform: median of log T near ln(8192)/2.
+    assert abs(np.median(np.log(ts)) - math.log(8192) / 2) < 0.3
