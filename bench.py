@@ -1,0 +1,225 @@
+#!/usr/bin/env python3
+"""Benchmark of the distribution-aware fused-MoE path on one MI355X.
+
+Workload (default): the DeepSeek-V3-shaped decode sweep, E=256, top-8,
+H=7168, I=2048, bf16 weights, T in {1, 8, 32, 128} x Dirichlet alpha in
+{0.05, 0.3, 1, 10}.  One step is one pass of the whole hot path -- routing
+histogram + Effective Experts + permutation (a2-a4), exemplar dispatch (a5)
+and the fused expert computation (a6-a8) with the variant chosen on the
+device -- over each of the 16 sweep points, every point on its own routing
+(4 routings per point, rotated between steps so the 256 MB Infinity Cache
+cannot serve repeated weights).  All inputs are resident in HBM before the
+timed region.
+
+value = geomean over the 16 points of the mean path latency (us per layer).
+roofline = the dominant kernel (grouped GEMM1 + SwiGLU): algorithmic bytes
+(W1 and W3 of every touched expert + the token rows) / its mean duration,
+timed with HIP events on its own stream inside the timed region.
+cpu_baseline = the fp64 CPU oracle on one sweep point (T=8, alpha=1).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+DECODE_T = (1, 8, 32, 128)
+DECODE_ALPHA = (0.05, 0.3, 1.0, 10.0)
+REPS = 4
+HBM_PEAK_GBS = 8000.0
+TABLE_DIR = os.path.join(ROOT, "paper_2607_23099_amd", "tables")
+PAPER_SKEWS = [1.1, 1.3, 1.5, 1.7, 2.0, 2.5, 4.0]
+EXTENDED_SKEWS = PAPER_SKEWS + [6.0, 8.0, 12.0, 16.0, 24.0, 32.0]
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def geomean(v):
+    v = [x for x in v if x > 0]
+    return math.exp(sum(math.log(x) for x in v) / len(v)) if v else 0.0
+
+
+def touched_experts(ids) -> int:
+    return int(len(np.unique(ids)))
+
+
+def cpu_baseline(shape, T, alpha):
+    """Time the CPU oracle on the full layer at one sweep point (weights pre-generated)."""
+    import oracle
+    from paper_2607_23099_amd import synth
+    oracle.build()
+    r = synth.routing(shape.E, shape.k, T, alpha, synth.seed_decode(T, alpha, 0))
+    x = synth.activations_host(T, shape.H, 7)
+    experts = np.unique(r.ids)
+    wts = {int(e): synth.expert_weights_host(shape, int(e)) for e in experts}
+    t0 = time.perf_counter()
+    oracle.moe_rows(r.ids, r.w, shape.k, np.arange(T), x, shape.H, shape.I, experts, lambda e: wts[e])
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(dt * 1e6, 1), "unit": "us", "cores": cores, "kind": "oracle",
+            "sample": f"one full DeepSeek-V3-shaped layer call, T={T} alpha={alpha} "
+                      f"({T * shape.k} assignments over {len(experts)} experts), fp64, "
+                      "weight generation excluded"}
+
+
+def load_or_tune_table(dl, x, quick):
+    from paper_2607_23099_amd import damoe
+    path = os.path.join(TABLE_DIR, f"{dl.shape.name}.damoe")
+    if os.path.exists(path) and not quick:
+        try:
+            return damoe.Table.load(path), f"loaded {os.path.relpath(path, ROOT)}"
+        except damoe.DamoeError as e:
+            log(f"table {path} unusable ({e}); tuning a quick one")
+    t0 = time.perf_counter()
+    table = damoe.tune(dl.layer, list(DECODE_T), EXTENDED_SKEWS, x, samples=3, reps=3, alpha_samples=32,
+                       alpha_iters=50, seed=0x7AB1E)
+    return table, f"quick-tuned at start-up in {time.perf_counter() - t0:.1f} s (S=3, reps=3)"
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
+    ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world})", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a ROCm GPU")
+    damoe.lib()  # fails loudly if the HIP library is not built
+
+    shape = synth.DS
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    dl = DeviceLayer(shape)
+    path = Path(dl, max(DECODE_T))
+    points = [(T, a) for T in DECODE_T for a in DECODE_ALPHA]
+    dev = "cuda"
+    ids_d, w_d, U = {}, {}, {}
+    for (T, a) in points:
+        for rep in range(REPS):
+            r = synth.routing(shape.E, shape.k, T, a, synth.seed_decode(T, a, rep))
+            ids_d[T, a, rep] = torch.from_numpy(r.ids.ravel().copy()).to(dev)
+            w_d[T, a, rep] = torch.from_numpy(r.w.ravel().copy()).to(dev)
+            U[T, a, rep] = touched_experts(r.ids)
+    path.fill_x(max(DECODE_T), 1)
+    torch.cuda.synchronize()
+
+    table, table_note = load_or_tune_table(dl, path.x, args.quick_tune)
+    log(f"dispatch table: {table_note}")
+
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    force = args.force_variant
+
+    def run_point(T, a, rep, events=None):
+        ids, w = ids_d[T, a, rep], w_d[T, a, rep]
+        if events:
+            events[0].record(stream)
+        path.route(T, ids=ids)
+        if force < 0:
+            path.dispatch(table, T)
+        if events:
+            events[1].record(stream)
+        path.fused_stage(0, T, force, w=w)
+        if events:
+            events[2].record(stream)
+        path.fused_stage(1, T, force, w=w)
+        if events:
+            events[3].record(stream)
+        path.fused_stage(2, T, force, w=w)
+        if events:
+            events[4].record(stream)
+
+    for s in range(args.warmup):
+        for (T, a) in points:
+            run_point(T, a, s % REPS)
+    torch.cuda.synchronize()
+
+    rec = {p: [] for p in points}
+    all_events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        rep = (s + args.warmup) % REPS
+        for (T, a) in points:
+            e = [ev() for _ in range(5)]
+            run_point(T, a, rep, e)
+            all_events.append(((T, a, rep), e))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    g1_bytes, g1_ms = 0.0, 0.0
+    for (T, a, rep), e in all_events:
+        path_ms = e[0].elapsed_time(e[4])
+        g1 = e[1].elapsed_time(e[2])
+        g2 = e[2].elapsed_time(e[3])
+        rec[T, a].append((path_ms, g1, g2, e[0].elapsed_time(e[1]), e[3].elapsed_time(e[4])))
+        g1_bytes += U[T, a, rep] * 2 * shape.I * shape.H * 2 + T * shape.H * 2
+        g1_ms += g1
+
+    per_point = {}
+    for (T, a), v in rec.items():
+        arr = np.array(v)
+        per_point[f"T{T}_a{a}"] = {
+            "path_us": round(float(arr[:, 0].mean()) * 1e3, 1),
+            "gemm1_us": round(float(arr[:, 1].mean()) * 1e3, 1),
+            "gemm2_us": round(float(arr[:, 2].mean()) * 1e3, 1),
+            "route_dispatch_us": round(float(arr[:, 3].mean()) * 1e3, 1),
+            "reduce_us": round(float(arr[:, 4].mean()) * 1e3, 1),
+        }
+    value = geomean([per_point[f"T{T}_a{a}"]["path_us"] for (T, a) in points])
+    achieved = g1_bytes / (g1_ms * 1e-3) / 1e9
+    for k_, v in per_point.items():
+        log(f"{k_:>12}: {v}")
+
+    out = {
+        "metric": "fused-MoE layer latency (geomean over the DeepSeek-V3 decode skew sweep)",
+        "value": round(value, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dsv3-decode-sweep: E=256 top-8 H=7168 I=2048 bf16, T in {1,8,32,128} x "
+                               "Dirichlet alpha in {0.05,0.3,1,10}, adaptive dispatch"
+                               + ("" if force < 0 else f" (forced variant {damoe.variant_name(force)})"),
+                   "points": len(points), "table": table_note},
+        "roofline": {"bound": "hbm", "kernel": "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+        "per_point": per_point,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(shape, 8, 1.0)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

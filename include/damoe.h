@@ -1,0 +1,253 @@
+/*
+ * damoe: distribution-aware fused Mixture-of-Experts layer for AMD MI355X (gfx950).
+ *
+ * C-ABI of the hot path of "Decoding the Skew: Distribution-Aware MoE
+ * Inference with Adaptive Kernel Dispatch" (DA-MoE):
+ *
+ *   damoe_route_histogram  per-expert routing histogram, Effective Experts,
+ *                          stable expert permutation and per-tile-size token
+ *                          tiles (Sec. III-A Eq. (2); Sec. IV-B step 5)
+ *   damoe_dispatch         token-count bucket, exemplar match by dot product,
+ *                          argmax -> variant id written to device memory
+ *                          (Sec. IV, IV-B, IV-C)
+ *   damoe_fused_moe        the fused expert computation: gathered GEMM1 +
+ *                          SwiGLU, GEMM2, gate-weighted unpermute-reduce, as a
+ *                          family of token-tile variants selected on the
+ *                          device by the variant id (Sec. II-A, II-C)
+ *   damoe_tune             offline auto-tuning: Alg. 1, ddist:X sweep,
+ *                          benchmark every variant, exemplar centroids
+ *                          (Sec. III-A, IV-A)
+ *
+ * Conventions
+ *   - All tensors are row-major.  Pointers are DEVICE pointers unless a
+ *     comment says "host".  bf16 values travel as uint16_t bit patterns.
+ *   - The caller owns every device buffer, including the workspace; the
+ *     stream-ordered calls (route_histogram, dispatch, fused_moe) allocate
+ *     nothing, never synchronise with the host and may be captured in a HIP
+ *     graph.  Tables are owned by the library (create / load / tune) and are
+ *     immutable after creation.
+ *   - Argument and shape errors are reported synchronously as a status code,
+ *     before any launch.  Data errors found on the device (an expert id
+ *     outside [0, E)) set a sticky code in the workspace; the offending slot
+ *     is dropped.  damoe_read_device_error() reads and clears it.
+ *   - All calls are thread-safe as long as concurrent calls use distinct
+ *     workspaces.
+ */
+#ifndef DAMOE_H
+#define DAMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum damoe_status {
+  DAMOE_OK = 0,
+  DAMOE_ERR_INVALID_ARG = -1,    /* null pointer, negative size, k > E, ...          */
+  DAMOE_ERR_UNSUPPORTED = -2,    /* shape or dtype outside the supported range        */
+  DAMOE_ERR_WORKSPACE = -3,      /* workspace smaller than damoe_workspace_size()     */
+  DAMOE_ERR_TABLE_MISMATCH = -4, /* table built for another (E, k, H, I, dtype)       */
+  DAMOE_ERR_HIP = -5,            /* a HIP runtime call failed                         */
+  DAMOE_ERR_NOMEM = -6,          /* host or device allocation failed (table / tune)   */
+  DAMOE_ERR_IO = -7              /* table file could not be read or written           */
+} damoe_status;
+
+/* Limits of this build. */
+#define DAMOE_MAX_E 1024       /* experts                                  */
+#define DAMOE_MAX_K 16         /* experts per token                        */
+#define DAMOE_MAX_T (1 << 20)  /* tokens per call                          */
+#define DAMOE_N_TILE_SIZES 5   /* token-tile sizes BM: 16, 32, 64, 128, 256 */
+
+/* Device error codes (sticky, in the workspace). */
+#define DAMOE_DEVERR_NONE 0
+#define DAMOE_DEVERR_EXPERT_ID 1 /* an id outside [0, E) was dropped                       */
+#define DAMOE_DEVERR_TILES 2     /* fused_moe found tile lists of another T; items skipped */
+
+typedef enum damoe_wdtype {
+  DAMOE_W_BF16 = 0,     /* bf16 weights                                                */
+  DAMOE_W_FP8_B128 = 1  /* OCP e4m3fn weights, one fp32 scale per 128x128 block         */
+} damoe_wdtype;
+
+/* One MoE layer of E SwiGLU experts, FFN_e(x) = W2_e (silu(W1_e x) * (W3_e x))
+ * (Sec. II-A).  Weights of expert e are contiguous slabs:
+ *   w1, w3: [E][I][H]   w2: [E][H][I]   (bf16, or e4m3 bytes for DAMOE_W_FP8_B128)
+ *   s1, s3: [E][I/128][H/128]  s2: [E][H/128][I/128]  fp32 block scales (fp8 only,
+ *   NULL otherwise).  H and I must be multiples of 128. */
+typedef struct damoe_layer {
+  int32_t E, k, H, I;
+  int32_t wdtype; /* damoe_wdtype */
+  const void* w1;
+  const void* w3;
+  const void* w2;
+  const float* s1;
+  const float* s3;
+  const float* s2;
+} damoe_layer;
+
+/* Byte offsets of the workspace regions for a call with T tokens.  The layout
+ * depends only on (E, k, H, I, T); every call of one step uses the same T.
+ *   ctrl       : int32[64] control words: [0] sticky device error,
+ *                [1] chosen exemplar index, [2..3] its int64 score (lo, hi),
+ *                [4] variant id used by the last fused_moe
+ *   tiles[s]   : token tiles for tile size BM_s = 16 << s: int32 n_tiles, int32 pad,
+ *                then n_tiles entries of int32x2 {start position, expert | rows << 16}
+ *   h          : bf16 [T*k][I]   SwiGLU activations in permuted order
+ *   out        : fp32 [T*k][H]   GEMM2 output in permuted order                     */
+typedef struct damoe_ws_layout {
+  size_t total;
+  size_t ctrl;
+  size_t tiles[DAMOE_N_TILE_SIZES];
+  size_t tiles_cap; /* entries each tile list can hold */
+  size_t h;
+  size_t out;
+} damoe_ws_layout;
+
+damoe_status damoe_workspace_layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T,
+                                    damoe_ws_layout* out /* host */);
+
+/* Workspace bytes needed by every call with up to T_max tokens on this layer
+ * (0 if the layer description is invalid). */
+size_t damoe_workspace_size(const damoe_layer* layer /* host */, int32_t T_max);
+
+/* a2-a4: routing histogram, Effective Experts and routing metadata.
+ *   topk_ids  int32 [T][k], experts of each token (Sec. II-A); ids outside [0, E)
+ *             are dropped and flag DAMOE_DEVERR_EXPERT_ID
+ *   counts    int32 [E]    t_e, tokens routed to expert e (Sec. III-A, Eq. (2))
+ *   offsets   int32 [E+1]  exclusive prefix sum of counts
+ *   perm      int32 [T*k]  flat assignment index a = t*k + j at each position,
+ *                          grouped by expert, increasing a within an expert
+ *   inv_perm  int32 [T*k]  position of assignment a (-1 if dropped)
+ *   effexp_numden uint64 [2]  (sum t_e)^2 and sum t_e^2: Eff. Experts = num / den
+ *   effexp_bucket int32 [1]   #{X in {1.1,1.3,1.5,1.7,2,2.5,4,6,8,12,16,24,32} :
+ *                             num/den <= E/X} (ddist:X grid of Sec. III-A / V-A,
+ *                             extended); -1 when T = 0
+ * Also writes the token-tile lists of every tile size into the workspace.
+ * T = 0 is valid (empty histogram).  Stream-ordered; no host sync. */
+damoe_status damoe_route_histogram(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                   int32_t* counts, int32_t* offsets, int32_t* perm,
+                                   int32_t* inv_perm, uint64_t* effexp_numden,
+                                   int32_t* effexp_bucket, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+
+/* Dispatch table: per token-count bucket, exemplars (sorted, unit-L2 token
+ * count vectors quantised as Q = round(u * 2^15)) and the kernel variant each
+ * maps to (Sec. IV-A).  Opaque and immutable; holds host and device copies. */
+typedef struct damoe_table damoe_table;
+
+/* Host description used to build a table (all arrays host, copied).
+ *   bucket_T   int32 [n_buckets] ascending token counts of the buckets
+ *   n_ex       int32 [n_buckets] exemplars per bucket (>= 1)
+ *   Q          int32 [sum n_ex][E] exemplars, bucket-major
+ *   kid        int32 [sum n_ex] variant id of each exemplar
+ *   noda       int32 [n_buckets] static per-bucket variant (used when T = 0,
+ *              and reported as the distribution-unaware baseline)            */
+typedef struct damoe_table_desc {
+  int32_t E, k, H, I, wdtype;
+  int32_t n_buckets;
+  const int32_t* bucket_T;
+  const int32_t* n_ex;
+  const int32_t* Q;
+  const int32_t* kid;
+  const int32_t* noda;
+} damoe_table_desc;
+
+damoe_status damoe_table_create(const damoe_table_desc* desc /* host */, damoe_table** out);
+void damoe_table_destroy(damoe_table* table);
+/* Copies the table back into caller arrays (host) sized as the table's; any
+ * pointer may be NULL.  n_buckets / total exemplars are returned first. */
+damoe_status damoe_table_info(const damoe_table* table, int32_t* n_buckets, int32_t* n_ex_total,
+                              int32_t* bucket_T, int32_t* n_ex, int32_t* Q, int32_t* kid,
+                              int32_t* noda);
+damoe_status damoe_table_save(const damoe_table* table, const char* path);
+damoe_status damoe_table_load(const char* path, damoe_table** out);
+
+/* a5: online dispatch (Sec. IV-B, with the bucket of Sec. IV chosen on the host
+ * from T as the smallest bucket_T >= T, else the last).  On the device: sort
+ * counts in descending order, score every exemplar of the bucket as the exact
+ * int64 dot product sum_r sorted[r] * Q[i][r], take the first maximum and write
+ * kid[i] to *variant_id (device int32).  With no tokens (all counts 0) the
+ * bucket's noda variant is written.  The chosen exemplar and its score land in
+ * the workspace control words.  Stream-ordered; no host sync. */
+damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int32_t T,
+                            int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* a6-a8: the fused expert computation.
+ *   x          bf16 [T][H] token activations
+ *   topk_w     fp32 [T][k] gate of each (token, slot)
+ *   perm, inv_perm, and the tile lists in ws: from damoe_route_histogram with
+ *   the same T
+ *   variant_id device int32: variant chosen by damoe_dispatch, read by the
+ *              kernels on the device (no host round trip)
+ *   force_variant  host int: -1 uses *variant_id; >= 0 runs that variant
+ *              (benchmarking, tuning, per-step best)
+ *   y          bf16 [T][H] output, y[t] = sum_j topk_w[t][j] FFN_{ids[t][j]}(x[t])
+ * Only experts with at least one token are read.  Stream-ordered. */
+damoe_status damoe_fused_moe(const damoe_layer* layer /* host */, const uint16_t* x,
+                             const float* topk_w, int32_t T, const int32_t* perm,
+                             const int32_t* inv_perm, const int32_t* variant_id,
+                             int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+
+/* The same computation as damoe_fused_moe, one stage at a time, so a caller can
+ * bracket each kernel with events:  stage 0 = grouped GEMM1 + SwiGLU (writes h
+ * into ws), 1 = grouped GEMM2 (reads h, writes out into ws), 2 = gate-weighted
+ * unpermute-reduce into y.  Running stages 0, 1, 2 in order on one stream is
+ * exactly damoe_fused_moe. */
+damoe_status damoe_fused_moe_stage(const damoe_layer* layer /* host */, int32_t stage,
+                                   const uint16_t* x, const float* topk_w, int32_t T,
+                                   const int32_t* perm, const int32_t* inv_perm,
+                                   const int32_t* variant_id, int32_t force_variant, uint16_t* y,
+                                   void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Variant registry.  Variant v computes with token tiles of
+ * damoe_variant_tile_m(v) rows. */
+int32_t damoe_num_variants(void);
+const char* damoe_variant_name(int32_t v);
+int32_t damoe_variant_tile_m(int32_t v);
+/* 1 if variant v supports the layer's weight dtype. */
+int32_t damoe_variant_supports(int32_t v, int32_t wdtype);
+
+/* Offline auto-tuning (Sec. IV-A, Fig. of the dispatch flow steps 1-4). */
+typedef struct damoe_tune_config {
+  int32_t n_buckets;
+  const int32_t* bucket_T;  /* host [n_buckets], ascending                          */
+  int32_t n_skews;
+  const double* skew_X;     /* host [n_skews]: ddist:X targets eff_exp* = E / X      */
+  int32_t samples;          /* S routing samples per skew (paper: 10)               */
+  int32_t reps;             /* timed repetitions per (sample, variant); median used */
+  int32_t alpha_samples;    /* Alg. 1: Dirichlet samples per bisection step          */
+  int32_t alpha_iters;      /* Alg. 1: bisection steps                              */
+  uint64_t seed;
+  const uint16_t* x;        /* device bf16 [max bucket_T][H] activations to time with */
+  int32_t verbose;          /* print progress to stderr                              */
+} damoe_tune_config;
+
+/* Builds a table: for each bucket T_b and skew X_j, alpha_j = Alg1(E / X_j);
+ * S Dirichlet routings (Gumbel-top-k at T_b tokens) are timed on every
+ * variant; kid = the variant with the lowest mean latency; the exemplar is the
+ * renormalised centroid of the S sorted unit count vectors.  The noda row holds
+ * each bucket's fastest variant under uniform routing.  Host-synchronous; the
+ * only call that allocates device memory on its own. */
+damoe_status damoe_tune(const damoe_layer* layer /* host */, const damoe_tune_config* cfg,
+                        damoe_table** out, hipStream_t stream);
+
+/* Alg. 1 (Sec. III-A): bisection over alpha in [1e-6, 1e6] for the Dirichlet
+ * concentration whose mean sampled Effective Experts over `samples` draws
+ * reaches `target`; common random numbers (Philox4x32-10 keyed by seed) at
+ * every step.  Host-only. */
+double damoe_alpha_search(int32_t E, double target, int32_t samples, int32_t iters, uint64_t seed);
+
+/* Reads and clears the sticky device error code in ws (synchronises stream). */
+damoe_status damoe_read_device_error(void* ws, int32_t* code /* host */, hipStream_t stream);
+
+const char* damoe_status_string(damoe_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DAMOE_H */

@@ -1,0 +1,431 @@
+// Host side of the C-ABI: argument validation, workspace layout, launches and tables.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+using namespace damoe;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct DeviceInfo {
+  int cus = 0;
+  bool ready = false;
+};
+
+std::mutex g_dev_mu;
+DeviceInfo g_dev[64];
+
+// Per-device one-time set-up: compute-unit count (persistent grid size) and the LDS limit
+// of the GEMM kernels.
+damoe_status device_info(DeviceInfo** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DAMOE_ERR_HIP;
+  std::lock_guard<std::mutex> g(g_dev_mu);
+  DeviceInfo& d = g_dev[dev];
+  if (!d.ready) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      return DAMOE_ERR_HIP;
+    if (gemm_set_lds_limits() != hipSuccess) return DAMOE_ERR_HIP;
+    d.cus = cus;
+    d.ready = true;
+  }
+  *out = &d;
+  return DAMOE_OK;
+}
+
+bool shape_ok(int32_t E, int32_t k) { return E >= 1 && E <= DAMOE_MAX_E && k >= 1 && k <= DAMOE_MAX_K && k <= E; }
+
+damoe_status check_layer(const damoe_layer* L) {
+  if (!L) return DAMOE_ERR_INVALID_ARG;
+  if (!shape_ok(L->E, L->k)) return DAMOE_ERR_INVALID_ARG;
+  if (L->H <= 0 || L->I <= 0) return DAMOE_ERR_INVALID_ARG;
+  if (L->H % 128 || L->I % 128) return DAMOE_ERR_UNSUPPORTED;
+  if (!L->w1 || !L->w3 || !L->w2) return DAMOE_ERR_INVALID_ARG;
+  if (L->wdtype == DAMOE_W_BF16) return DAMOE_OK;
+  if (L->wdtype == DAMOE_W_FP8_B128) {
+    if (!L->s1 || !L->s3 || !L->s2) return DAMOE_ERR_INVALID_ARG;
+    if (L->H % 512 || L->I % 512) return DAMOE_ERR_UNSUPPORTED;  // 128-blocks per wave slice
+    return DAMOE_OK;
+  }
+  return DAMOE_ERR_UNSUPPORTED;
+}
+
+size_t tiles_cap(int64_t A, int32_t E) { return (size_t)(A / 16 + std::min<int64_t>(E, A) + 1); }
+
+damoe_status layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T, damoe_ws_layout* o) {
+  if (!shape_ok(E, k) || T < 0 || T > DAMOE_MAX_T || H < 0 || I < 0) return DAMOE_ERR_INVALID_ARG;
+  const int64_t A = (int64_t)T * k;
+  size_t off = 0;
+  o->ctrl = off;
+  off += align_up(kCtrlWords * sizeof(int32_t));
+  o->tiles_cap = tiles_cap(A, E);
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) {
+    o->tiles[c] = off;
+    off += align_up(8 + 8 * o->tiles_cap);
+  }
+  o->h = off;
+  off += align_up((size_t)A * I * 2);
+  o->out = off;
+  off += align_up((size_t)A * H * 4);
+  o->total = off;
+  return DAMOE_OK;
+}
+
+}  // namespace
+
+struct damoe_table {
+  int32_t E, k, H, I, wdtype;
+  std::vector<int32_t> bucket_T, n_ex, ex_begin, Q, kid, noda;
+  int32_t* d_Q = nullptr;
+  int32_t* d_kid = nullptr;
+};
+
+extern "C" {
+
+const char* damoe_status_string(damoe_status s) {
+  switch (s) {
+    case DAMOE_OK: return "ok";
+    case DAMOE_ERR_INVALID_ARG: return "invalid argument";
+    case DAMOE_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case DAMOE_ERR_WORKSPACE: return "workspace too small";
+    case DAMOE_ERR_TABLE_MISMATCH: return "table does not match the layer or variant set";
+    case DAMOE_ERR_HIP: return "HIP runtime error";
+    case DAMOE_ERR_NOMEM: return "out of memory";
+    case DAMOE_ERR_IO: return "table file error";
+  }
+  return "unknown status";
+}
+
+int32_t damoe_num_variants(void) { return num_variants(); }
+
+const char* damoe_variant_name(int32_t v) {
+  if (v < 0 || v >= num_variants()) return nullptr;
+  return variant(v).name;
+}
+
+int32_t damoe_variant_tile_m(int32_t v) {
+  if (v < 0 || v >= num_variants()) return 0;
+  return variant(v).bm;
+}
+
+int32_t damoe_variant_supports(int32_t v, int32_t wdtype) {
+  if (v < 0 || v >= num_variants()) return 0;
+  return wdtype == DAMOE_W_BF16 || wdtype == DAMOE_W_FP8_B128;
+}
+
+damoe_status damoe_workspace_layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T,
+                                    damoe_ws_layout* out) {
+  if (!out) return DAMOE_ERR_INVALID_ARG;
+  return layout(E, k, H, I, T, out);
+}
+
+size_t damoe_workspace_size(const damoe_layer* L, int32_t T_max) {
+  if (check_layer(L) != DAMOE_OK) return 0;
+  damoe_ws_layout lo;
+  if (layout(L->E, L->k, L->H, L->I, T_max, &lo) != DAMOE_OK) return 0;
+  return lo.total;
+}
+
+damoe_status damoe_route_histogram(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                   int32_t* counts, int32_t* offsets, int32_t* perm,
+                                   int32_t* inv_perm, uint64_t* effexp_numden,
+                                   int32_t* effexp_bucket, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  if (!shape_ok(E, k) || T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
+  if (!counts || !offsets || !effexp_numden || !effexp_bucket || !ws) return DAMOE_ERR_INVALID_ARG;
+  if (T > 0 && (!topk_ids || !perm || !inv_perm)) return DAMOE_ERR_INVALID_ARG;
+  damoe_ws_layout lo;
+  layout(E, k, 0, 0, T, &lo);
+  if (ws_bytes < lo.h) return DAMOE_ERR_WORKSPACE;
+  char* base = static_cast<char*>(ws);
+  int32_t* lists[DAMOE_N_TILE_SIZES];
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) lists[c] = reinterpret_cast<int32_t*>(base + lo.tiles[c]);
+  const hipError_t e = launch_route(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden,
+                                    effexp_bucket, reinterpret_cast<int32_t*>(base + lo.ctrl), lists,
+                                    stream);
+  return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+}
+
+damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t T,
+                            int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!t || !counts || !variant_id || !ws || T < 0) return DAMOE_ERR_INVALID_ARG;
+  if (ws_bytes < kCtrlWords * sizeof(int32_t)) return DAMOE_ERR_WORKSPACE;
+  if (!t->d_Q) return DAMOE_ERR_HIP;  // table built without a device
+  const int32_t nb = (int32_t)t->bucket_T.size();
+  int32_t b = nb - 1;
+  for (int32_t i = 0; i < nb; ++i)
+    if (T <= t->bucket_T[i]) {
+      b = i;
+      break;
+    }
+  const hipError_t e = launch_dispatch(counts, t->E, t->d_Q + (size_t)t->ex_begin[b] * t->E,
+                                       t->d_kid + t->ex_begin[b], t->n_ex[b], t->noda[b], variant_id,
+                                       reinterpret_cast<int32_t*>(ws), stream);
+  return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+}
+
+static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const uint16_t* x,
+                               const float* topk_w, int32_t T, const int32_t* perm,
+                               const int32_t* inv_perm, const int32_t* variant_id,
+                               int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
+  damoe_status st = check_layer(L);
+  if (st != DAMOE_OK) return st;
+  if (T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
+  if (force_variant >= num_variants() || force_variant < -1) return DAMOE_ERR_INVALID_ARG;
+  if (force_variant >= 0 && !damoe_variant_supports(force_variant, L->wdtype)) return DAMOE_ERR_UNSUPPORTED;
+  if (T == 0) return DAMOE_OK;
+  if (!x || !topk_w || !perm || !inv_perm || !y || !ws) return DAMOE_ERR_INVALID_ARG;
+  if (force_variant < 0 && !variant_id) return DAMOE_ERR_INVALID_ARG;
+  damoe_ws_layout lo;
+  if (layout(L->E, L->k, L->H, L->I, T, &lo) != DAMOE_OK) return DAMOE_ERR_INVALID_ARG;
+  if (ws_bytes < lo.total) return DAMOE_ERR_WORKSPACE;
+  DeviceInfo* dev = nullptr;
+  if ((st = device_info(&dev)) != DAMOE_OK) return st;
+  char* base = static_cast<char*>(ws);
+
+  GemmArgs g1{};
+  g1.x = x;
+  g1.wa = L->w1;
+  g1.wb = L->w3;
+  g1.sa = L->s1;
+  g1.sb = L->s3;
+  g1.perm = perm;
+  g1.out = base + lo.h;
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c)
+    g1.tiles.list[c] = reinterpret_cast<const int32_t*>(base + lo.tiles[c]);
+  g1.variant_id = variant_id;
+  g1.force_variant = force_variant;
+  g1.ctrl = reinterpret_cast<int32_t*>(base + lo.ctrl);
+  g1.k = L->k;
+  g1.A = T * L->k;
+  g1.E = L->E;
+  g1.K = L->H;
+  g1.N = L->I;
+  g1.fp8 = L->wdtype == DAMOE_W_FP8_B128;
+
+  GemmArgs g2 = g1;
+  g2.x = reinterpret_cast<const uint16_t*>(base + lo.h);
+  g2.wa = L->w2;
+  g2.wb = nullptr;
+  g2.sa = L->s2;
+  g2.sb = nullptr;
+  g2.perm = nullptr;
+  g2.out = base + lo.out;
+  g2.K = L->I;
+  g2.N = L->H;
+
+  const int grid = dev->cus * 2;
+  if ((stage_mask & 1) && launch_gemm1(g1, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  if ((stage_mask & 2) && launch_gemm2(g2, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  ReduceArgs r{reinterpret_cast<const float*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};
+  if ((stage_mask & 4) && launch_reduce(r, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  return DAMOE_OK;
+}
+
+damoe_status damoe_fused_moe(const damoe_layer* L, const uint16_t* x, const float* topk_w, int32_t T,
+                             const int32_t* perm, const int32_t* inv_perm, const int32_t* variant_id,
+                             int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  return fused_impl(L, 7, x, topk_w, T, perm, inv_perm, variant_id, force_variant, y, ws, ws_bytes,
+                    stream);
+}
+
+damoe_status damoe_fused_moe_stage(const damoe_layer* L, int32_t stage, const uint16_t* x,
+                                   const float* topk_w, int32_t T, const int32_t* perm,
+                                   const int32_t* inv_perm, const int32_t* variant_id,
+                                   int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  if (stage < 0 || stage > 2) return DAMOE_ERR_INVALID_ARG;
+  return fused_impl(L, 1 << stage, x, topk_w, T, perm, inv_perm, variant_id, force_variant, y, ws,
+                    ws_bytes, stream);
+}
+
+damoe_status damoe_read_device_error(void* ws, int32_t* code, hipStream_t stream) {
+  if (!ws || !code) return DAMOE_ERR_INVALID_ARG;
+  int32_t v = 0;
+  const int32_t zero = 0;
+  if (hipMemcpyAsync(&v, ws, sizeof(v), hipMemcpyDeviceToHost, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  if (hipMemcpyAsync(ws, &zero, sizeof(zero), hipMemcpyHostToDevice, stream) != hipSuccess)
+    return DAMOE_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return DAMOE_ERR_HIP;
+  *code = v;
+  return DAMOE_OK;
+}
+
+// ------------------------------------------------------------------------------------------------
+// Tables
+// ------------------------------------------------------------------------------------------------
+
+damoe_status damoe_table_create(const damoe_table_desc* d, damoe_table** out) {
+  if (!d || !out) return DAMOE_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!shape_ok(d->E, d->k) || d->n_buckets < 1 || !d->bucket_T || !d->n_ex || !d->Q || !d->kid ||
+      !d->noda)
+    return DAMOE_ERR_INVALID_ARG;
+  const int32_t nv = num_variants();
+  int64_t total = 0;
+  for (int32_t b = 0; b < d->n_buckets; ++b) {
+    if (d->bucket_T[b] < 1 || (b && d->bucket_T[b] <= d->bucket_T[b - 1])) return DAMOE_ERR_INVALID_ARG;
+    if (d->n_ex[b] < 1 || d->n_ex[b] > 256) return DAMOE_ERR_INVALID_ARG;
+    if (d->noda[b] < 0 || d->noda[b] >= nv) return DAMOE_ERR_INVALID_ARG;
+    total += d->n_ex[b];
+  }
+  for (int64_t i = 0; i < total; ++i)
+    if (d->kid[i] < 0 || d->kid[i] >= nv) return DAMOE_ERR_INVALID_ARG;
+  damoe_table* t = new (std::nothrow) damoe_table;
+  if (!t) return DAMOE_ERR_NOMEM;
+  t->E = d->E;
+  t->k = d->k;
+  t->H = d->H;
+  t->I = d->I;
+  t->wdtype = d->wdtype;
+  t->bucket_T.assign(d->bucket_T, d->bucket_T + d->n_buckets);
+  t->n_ex.assign(d->n_ex, d->n_ex + d->n_buckets);
+  t->noda.assign(d->noda, d->noda + d->n_buckets);
+  t->ex_begin.resize(d->n_buckets);
+  int32_t acc = 0;
+  for (int32_t b = 0; b < d->n_buckets; ++b) {
+    t->ex_begin[b] = acc;
+    acc += d->n_ex[b];
+  }
+  t->Q.assign(d->Q, d->Q + (size_t)total * d->E);
+  t->kid.assign(d->kid, d->kid + total);
+  // Device copies (skipped when no device is present, e.g. when only inspecting tables).
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) == hipSuccess && ndev > 0) {
+    if (hipMalloc(&t->d_Q, sizeof(int32_t) * t->Q.size()) != hipSuccess ||
+        hipMalloc(&t->d_kid, sizeof(int32_t) * t->kid.size()) != hipSuccess ||
+        hipMemcpy(t->d_Q, t->Q.data(), sizeof(int32_t) * t->Q.size(), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(t->d_kid, t->kid.data(), sizeof(int32_t) * t->kid.size(), hipMemcpyHostToDevice) !=
+            hipSuccess) {
+      damoe_table_destroy(t);
+      return DAMOE_ERR_HIP;
+    }
+  } else {
+    (void)hipGetLastError();
+  }
+  *out = t;
+  return DAMOE_OK;
+}
+
+void damoe_table_destroy(damoe_table* t) {
+  if (!t) return;
+  if (t->d_Q) (void)hipFree(t->d_Q);
+  if (t->d_kid) (void)hipFree(t->d_kid);
+  delete t;
+}
+
+damoe_status damoe_table_info(const damoe_table* t, int32_t* n_buckets, int32_t* n_ex_total,
+                              int32_t* bucket_T, int32_t* n_ex, int32_t* Q, int32_t* kid,
+                              int32_t* noda) {
+  if (!t) return DAMOE_ERR_INVALID_ARG;
+  if (n_buckets) *n_buckets = (int32_t)t->bucket_T.size();
+  if (n_ex_total) *n_ex_total = (int32_t)t->kid.size();
+  if (bucket_T) std::copy(t->bucket_T.begin(), t->bucket_T.end(), bucket_T);
+  if (n_ex) std::copy(t->n_ex.begin(), t->n_ex.end(), n_ex);
+  if (Q) std::copy(t->Q.begin(), t->Q.end(), Q);
+  if (kid) std::copy(t->kid.begin(), t->kid.end(), kid);
+  if (noda) std::copy(t->noda.begin(), t->noda.end(), noda);
+  return DAMOE_OK;
+}
+
+// Text format, version 1:
+//   damoe-table 1 <variant-set signature>
+//   <E> <k> <H> <I> <wdtype> <n_buckets>
+//   per bucket: "bucket <T> <n_ex> <noda>" then n_ex lines "<kid> <Q[0]> ... <Q[E-1]>"
+static std::string variant_signature() {
+  std::string s = std::to_string(num_variants());
+  for (int32_t v = 0; v < num_variants(); ++v) {
+    s += ",";
+    s += variant(v).name;
+  }
+  return s;
+}
+
+damoe_status damoe_table_save(const damoe_table* t, const char* path) {
+  if (!t || !path) return DAMOE_ERR_INVALID_ARG;
+  FILE* f = std::fopen(path, "w");
+  if (!f) return DAMOE_ERR_IO;
+  std::fprintf(f, "damoe-table 1 %s\n%d %d %d %d %d %d\n", variant_signature().c_str(), t->E, t->k,
+               t->H, t->I, t->wdtype, (int)t->bucket_T.size());
+  for (size_t b = 0; b < t->bucket_T.size(); ++b) {
+    std::fprintf(f, "bucket %d %d %d\n", t->bucket_T[b], t->n_ex[b], t->noda[b]);
+    for (int32_t i = 0; i < t->n_ex[b]; ++i) {
+      const int32_t ex = t->ex_begin[b] + i;
+      std::fprintf(f, "%d", t->kid[ex]);
+      for (int32_t r = 0; r < t->E; ++r) std::fprintf(f, " %d", t->Q[(size_t)ex * t->E + r]);
+      std::fprintf(f, "\n");
+    }
+  }
+  const bool ok = std::fflush(f) == 0;
+  std::fclose(f);
+  return ok ? DAMOE_OK : DAMOE_ERR_IO;
+}
+
+damoe_status damoe_table_load(const char* path, damoe_table** out) {
+  if (!path || !out) return DAMOE_ERR_INVALID_ARG;
+  *out = nullptr;
+  FILE* f = std::fopen(path, "r");
+  if (!f) return DAMOE_ERR_IO;
+  damoe_status st = DAMOE_ERR_IO;
+  char magic[32] = {0}, sig[4096] = {0};
+  int ver = 0;
+  damoe_table_desc d{};
+  std::vector<int32_t> bT, nex, noda, kid, Q;
+  do {
+    if (std::fscanf(f, "%31s %d %4095s", magic, &ver, sig) != 3) break;
+    if (std::strcmp(magic, "damoe-table") != 0 || ver != 1) break;
+    if (variant_signature() != sig) {
+      st = DAMOE_ERR_TABLE_MISMATCH;
+      break;
+    }
+    if (std::fscanf(f, "%d %d %d %d %d %d", &d.E, &d.k, &d.H, &d.I, &d.wdtype, &d.n_buckets) != 6) break;
+    if (!shape_ok(d.E, d.k) || d.n_buckets < 1 || d.n_buckets > 64) break;
+    bool good = true;
+    for (int32_t b = 0; b < d.n_buckets && good; ++b) {
+      char word[16] = {0};
+      int T = 0, n = 0, nd = 0;
+      if (std::fscanf(f, "%15s %d %d %d", word, &T, &n, &nd) != 4 || std::strcmp(word, "bucket") ||
+          n < 1 || n > 256) {
+        good = false;
+        break;
+      }
+      bT.push_back(T);
+      nex.push_back(n);
+      noda.push_back(nd);
+      for (int32_t i = 0; i < n && good; ++i) {
+        int kv = 0;
+        if (std::fscanf(f, "%d", &kv) != 1) good = false;
+        kid.push_back(kv);
+        for (int32_t r = 0; r < d.E && good; ++r) {
+          int q = 0;
+          if (std::fscanf(f, "%d", &q) != 1) good = false;
+          Q.push_back(q);
+        }
+      }
+    }
+    if (!good) break;
+    d.bucket_T = bT.data();
+    d.n_ex = nex.data();
+    d.noda = noda.data();
+    d.kid = kid.data();
+    d.Q = Q.data();
+    st = damoe_table_create(&d, out);
+  } while (false);
+  std::fclose(f);
+  return st;
+}
+
+}  // extern "C"

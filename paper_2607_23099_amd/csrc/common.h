@@ -1,0 +1,111 @@
+// Internal declarations shared by the damoe kernels and the host library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "damoe.h"
+
+namespace damoe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+constexpr int kGemmThreads = 256;  // every GEMM variant runs 4 waves per workgroup
+constexpr int kRouteThreads = 1024;
+constexpr int kCtrlWords = 64;
+
+// ---------------------------------------------------------------------------------------------
+// Variant registry.  A variant is one template instance of the grouped GEMM pair; all variants
+// share the launch shape (persistent grid, 256 threads) so the device-side variant id can pick
+// among them inside one launch.
+// ---------------------------------------------------------------------------------------------
+enum VariantKind : int32_t {
+  kStream = 0,  // split-K over the 4 waves, weights streamed straight from HBM into registers
+  kTiled = 1,   // LDS-staged token and weight tiles, waves tile the output
+};
+
+struct VariantDesc {
+  const char* name;
+  int32_t kind;
+  int32_t bm;        // token-tile rows (the paper's Tile-N)
+  int32_t bn1;       // GEMM1 intermediate features per work item (gate and up each)
+  int32_t bn2;       // GEMM2 output features per work item
+  int32_t tile_cls;  // index of the tile list: bm == 16 << tile_cls
+};
+
+int32_t num_variants();
+const VariantDesc& variant(int32_t v);
+
+// ---------------------------------------------------------------------------------------------
+// Kernel arguments
+// ---------------------------------------------------------------------------------------------
+struct TileLists {
+  const int32_t* list[DAMOE_N_TILE_SIZES];  // int32 n, int32 pad, int2 entries[n]
+};
+
+struct GemmArgs {
+  const uint16_t* x;   // GEMM1: [T][H] tokens; GEMM2: h [A][I]
+  const void* wa;      // GEMM1: W1; GEMM2: W2
+  const void* wb;      // GEMM1: W3; GEMM2: unused
+  const float* sa;     // fp8 block scales of wa
+  const float* sb;     // fp8 block scales of wb
+  const int32_t* perm; // GEMM1 gathers token rows perm[p] / k
+  void* out;           // GEMM1: h bf16 [A][I]; GEMM2: out fp32 [A][H]
+  TileLists tiles;
+  const int32_t* variant_id;
+  int32_t force_variant;
+  int32_t* ctrl;
+  int32_t k;
+  int32_t A;           // assignments T * k
+  int32_t E;
+  int32_t K;           // reduction length: H for GEMM1, I for GEMM2
+  int32_t N;           // output features: I for GEMM1, H for GEMM2
+  int32_t fp8;
+};
+
+struct ReduceArgs {
+  const float* out;    // [A][H]
+  const float* w;      // [T][k]
+  const int32_t* inv_perm;
+  uint16_t* y;         // [T][H]
+  int32_t T, k, H;
+};
+
+// Launchers (return hipError_t of the launch).
+hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
+                        int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
+                        int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
+                        hipStream_t stream);
+hipError_t launch_dispatch(const int32_t* counts, int32_t E, const int32_t* Q, const int32_t* kid,
+                           int32_t n_ex, int32_t noda, int32_t* variant_id, int32_t* ctrl,
+                           hipStream_t stream);
+hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream);
+hipError_t gemm_set_lds_limits();
+
+// Dynamic LDS bytes the GEMM kernels are launched with.
+size_t gemm_lds_bytes();
+
+// ---------------------------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float((uint32_t)h << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u = u + 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+}  // namespace damoe

@@ -1,0 +1,352 @@
+// Offline auto-tuning (Sec. IV-A) and the Dirichlet reverse modelling of Alg. 1 (Sec. III-A).
+//
+// Random numbers come from a counter-based Philox4x32-10 generator (Salmon, Moraes, Dror,
+// Shaw, SC'11) keyed by the caller's seed, so every draw is addressed by a counter
+// (n, e, sample, tag) and Alg. 1 sees the same random numbers at every bisection step.
+// Gamma variates use Marsaglia and Tsang's method (ACM TOMS 2000) for shape alpha + 1 with a
+// Box-Muller normal, boosted to shape alpha by U^(1/alpha) in log space, so Dirichlet samples
+// never underflow even at alpha = 0.03.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <numeric>
+#include <vector>
+
+#include "common.h"
+
+namespace {
+
+struct Philox {
+  uint32_t k0, k1;
+  explicit Philox(uint64_t seed) : k0((uint32_t)seed), k1((uint32_t)(seed >> 32)) {}
+  void block(uint32_t n, uint32_t e, uint32_t s, uint32_t tag, uint32_t out[4]) const {
+    uint32_t x0 = n, x1 = e, x2 = s, x3 = tag, a = k0, b = k1;
+    for (int r = 0; r < 10; ++r) {
+      const uint64_t m0 = (uint64_t)0xD2511F53u * x0;
+      const uint64_t m1 = (uint64_t)0xCD9E8D57u * x2;
+      const uint32_t n0 = (uint32_t)(m1 >> 32) ^ x1 ^ a;
+      const uint32_t n2 = (uint32_t)(m0 >> 32) ^ x3 ^ b;
+      x0 = n0;
+      x1 = (uint32_t)m1;
+      x2 = n2;
+      x3 = (uint32_t)m0;
+      a += 0x9E3779B9u;
+      b += 0xBB67AE85u;
+    }
+    out[0] = x0;
+    out[1] = x1;
+    out[2] = x2;
+    out[3] = x3;
+  }
+  // Two uniforms in (0, 1), 53-bit, from one block.
+  void uniforms(uint32_t n, uint32_t e, uint32_t s, uint32_t tag, double& u0, double& u1) const {
+    uint32_t r[4];
+    block(n, e, s, tag, r);
+    const double inv = 1.0 / 9007199254740992.0;
+    u0 = ((double)(((uint64_t)(r[0] >> 5) << 26) | (r[1] >> 6)) + 0.5) * inv;
+    u1 = ((double)(((uint64_t)(r[2] >> 5) << 26) | (r[3] >> 6)) + 0.5) * inv;
+  }
+};
+
+// log of a Gamma(alpha) variate, draw (e, s).
+double log_gamma(const Philox& g, double alpha, uint32_t e, uint32_t s) {
+  const double d = alpha + 1.0 - 1.0 / 3.0;
+  const double c = 1.0 / std::sqrt(9.0 * d);
+  double val = 0.0;
+  for (uint32_t i = 0;; ++i) {
+    double u1, u2, ua, ub;
+    g.uniforms(2 * i, e, s, 0, u1, u2);
+    g.uniforms(2 * i + 1, e, s, 0, ua, ub);
+    const double z = std::sqrt(-2.0 * std::log(u1)) * std::cos(6.283185307179586 * u2);
+    double v = 1.0 + c * z;
+    if (v <= 0.0) continue;
+    v = v * v * v;
+    if (std::log(ua) < 0.5 * z * z + d - d * v + d * std::log(v)) {
+      val = d * v;
+      break;
+    }
+  }
+  double b0, b1;
+  g.uniforms(0, e, s, 1, b0, b1);
+  return std::log(val) + std::log(b0) / alpha;
+}
+
+// log p of one Dirichlet(alpha 1_E) sample.
+void dirichlet_logp(const Philox& g, double alpha, int32_t E, uint32_t s, std::vector<double>& lp) {
+  lp.resize(E);
+  double mx = -INFINITY;
+  for (int32_t e = 0; e < E; ++e) {
+    lp[e] = log_gamma(g, alpha, (uint32_t)e, s);
+    mx = std::max(mx, lp[e]);
+  }
+  double z = 0.0;
+  for (int32_t e = 0; e < E; ++e) z += std::exp(lp[e] - mx);
+  const double lz = mx + std::log(z);
+  for (int32_t e = 0; e < E; ++e) lp[e] -= lz;
+}
+
+// Mean Effective Experts (Eq. (2) applied to p) of S samples of Dir(alpha).
+double mean_effexp(const Philox& g, int32_t E, double alpha, int32_t S, std::vector<double>& lp) {
+  double acc = 0.0;
+  for (int32_t s = 0; s < S; ++s) {
+    dirichlet_logp(g, alpha, E, (uint32_t)s, lp);
+    double mx = *std::max_element(lp.begin(), lp.end());
+    double z = 0.0;
+    for (double v : lp) z += std::exp(v - mx);
+    double s1 = 0.0, s2 = 0.0;
+    for (double v : lp) {
+      const double p = std::exp(v - mx) / z;
+      s1 += p;
+      s2 += p * p;
+    }
+    acc += s1 * s1 / s2;
+  }
+  return acc / S;
+}
+
+// Gumbel-top-k routing of T tokens under log p, softmax gates of N(0,1) logits.
+void gumbel_topk(const Philox& g, const std::vector<double>& lp, int32_t T, int32_t k, uint32_t s,
+                 std::vector<int32_t>& ids, std::vector<float>& w) {
+  const int32_t E = (int32_t)lp.size();
+  ids.resize((size_t)T * k);
+  w.resize((size_t)T * k);
+  std::vector<double> key(E);
+  std::vector<int32_t> idx(E);
+  for (int32_t t = 0; t < T; ++t) {
+    for (int32_t e = 0; e < E; e += 2) {
+      double u0, u1;
+      g.uniforms((uint32_t)t, (uint32_t)e, s, 2, u0, u1);
+      key[e] = lp[e] - std::log(-std::log(u0));
+      if (e + 1 < E) key[e + 1] = lp[e + 1] - std::log(-std::log(u1));
+    }
+    std::iota(idx.begin(), idx.end(), 0);
+    std::partial_sort(idx.begin(), idx.begin() + k, idx.end(), [&](int32_t a, int32_t b) {
+      return key[a] > key[b] || (key[a] == key[b] && a < b);
+    });
+    double zs = 0.0, lg[DAMOE_MAX_K];
+    for (int32_t j = 0; j < k; ++j) {
+      double u0, u1;
+      g.uniforms((uint32_t)t, (uint32_t)j, s, 3, u0, u1);
+      lg[j] = std::sqrt(-2.0 * std::log(u0)) * std::cos(6.283185307179586 * u1);
+    }
+    const double m = *std::max_element(lg, lg + k);
+    for (int32_t j = 0; j < k; ++j) zs += std::exp(lg[j] - m);
+    for (int32_t j = 0; j < k; ++j) {
+      ids[(size_t)t * k + j] = idx[j];
+      w[(size_t)t * k + j] = (float)(std::exp(lg[j] - m) / zs);
+    }
+  }
+}
+
+// Exemplar (Sec. IV-A): mean of the sorted, unit-L2 count vectors, renormalised, times 2^15.
+void exemplar(const std::vector<std::vector<int32_t>>& counts, int32_t E, int32_t* Q) {
+  std::vector<double> c(E, 0.0);
+  for (const auto& v : counts) {
+    std::vector<int32_t> s(v);
+    std::sort(s.begin(), s.end(), std::greater<int32_t>());
+    double nn = 0.0;
+    for (int32_t x : s) nn += (double)x * x;
+    if (nn <= 0.0) continue;
+    nn = std::sqrt(nn);
+    for (int32_t r = 0; r < E; ++r) c[r] += s[r] / nn / (double)counts.size();
+  }
+  double n = 0.0;
+  for (double x : c) n += x * x;
+  n = std::sqrt(n);
+  for (int32_t r = 0; r < E; ++r) Q[r] = (int32_t)std::nearbyint(n > 0.0 ? c[r] / n * 32768.0 : 0.0);
+}
+
+#define TRY_HIP(x)                                         \
+  do {                                                     \
+    if ((x) != hipSuccess) {                               \
+      st = DAMOE_ERR_HIP;                                  \
+      goto done;                                           \
+    }                                                      \
+  } while (0)
+#define TRY(x)                                             \
+  do {                                                     \
+    if ((st = (x)) != DAMOE_OK) goto done;                 \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+double damoe_alpha_search(int32_t E, double target, int32_t samples, int32_t iters, uint64_t seed) {
+  if (E < 1 || samples < 1 || iters < 1) return NAN;
+  const Philox g(seed);
+  std::vector<double> lp;
+  double lo = 1e-6, hi = 1e6, mid = 0.5 * (lo + hi);
+  for (int32_t t = 0; t < iters; ++t) {
+    mid = 0.5 * (lo + hi);
+    const double v = mean_effexp(g, E, mid, samples, lp);
+    if (v < target) lo = mid;  // too skewed: raise alpha
+    else hi = mid;             // too uniform: lower alpha
+  }
+  return mid;
+}
+
+damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damoe_table** out,
+                        hipStream_t stream) {
+  if (!L || !cfg || !out || !cfg->bucket_T || cfg->n_buckets < 1 || !cfg->skew_X || cfg->n_skews < 1 ||
+      cfg->samples < 1 || cfg->reps < 1 || !cfg->x)
+    return DAMOE_ERR_INVALID_ARG;
+  *out = nullptr;
+  const int32_t E = L->E, k = L->k, H = L->H;
+  const int32_t nv = damoe_num_variants();
+  int32_t T_max = 0;
+  for (int32_t b = 0; b < cfg->n_buckets; ++b) T_max = std::max(T_max, cfg->bucket_T[b]);
+  const size_t ws_bytes = damoe_workspace_size(L, T_max);
+  if (ws_bytes == 0) return DAMOE_ERR_INVALID_ARG;
+  const int32_t a_samples = cfg->alpha_samples > 0 ? cfg->alpha_samples : 64;
+  const int32_t a_iters = cfg->alpha_iters > 0 ? cfg->alpha_iters : 60;
+  const Philox g(cfg->seed);
+
+  damoe_status st = DAMOE_OK;
+  void* ws = nullptr;
+  int32_t *d_ids = nullptr, *d_counts = nullptr, *d_off = nullptr, *d_perm = nullptr, *d_inv = nullptr,
+          *d_bucket = nullptr;
+  float* d_w = nullptr;
+  uint64_t* d_nd = nullptr;
+  uint16_t* d_y = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  std::vector<int32_t> t_bucket, t_nex, t_noda, t_kid, t_Q;
+  std::vector<double> alphas(cfg->n_skews);
+  std::vector<double> lp;
+  std::vector<int32_t> ids;
+  std::vector<float> w;
+  const size_t A_max = (size_t)T_max * k;
+
+  TRY_HIP(hipMalloc(&ws, ws_bytes));
+  TRY_HIP(hipMalloc(&d_ids, sizeof(int32_t) * A_max));
+  TRY_HIP(hipMalloc(&d_w, sizeof(float) * A_max));
+  TRY_HIP(hipMalloc(&d_counts, sizeof(int32_t) * E));
+  TRY_HIP(hipMalloc(&d_off, sizeof(int32_t) * (E + 1)));
+  TRY_HIP(hipMalloc(&d_perm, sizeof(int32_t) * A_max));
+  TRY_HIP(hipMalloc(&d_inv, sizeof(int32_t) * A_max));
+  TRY_HIP(hipMalloc(&d_nd, sizeof(uint64_t) * 2));
+  TRY_HIP(hipMalloc(&d_bucket, sizeof(int32_t)));
+  TRY_HIP(hipMalloc(&d_y, sizeof(uint16_t) * (size_t)T_max * H));
+  TRY_HIP(hipMemset(ws, 0, ws_bytes));
+  TRY_HIP(hipEventCreate(&e0));
+  TRY_HIP(hipEventCreate(&e1));
+
+  // Alg. 1 once per skew: the ddist:X target is E / X.
+  for (int32_t j = 0; j < cfg->n_skews; ++j) {
+    alphas[j] = damoe_alpha_search(E, (double)E / cfg->skew_X[j], a_samples, a_iters, cfg->seed);
+    if (cfg->verbose) std::fprintf(stderr, "damoe_tune: ddist:%.2f -> alpha %.5g\n", cfg->skew_X[j], alphas[j]);
+  }
+
+  for (int32_t b = 0; b < cfg->n_buckets; ++b) {
+    const int32_t T = cfg->bucket_T[b];
+    // Latency of every variant on one routing: median of reps forced runs.
+    auto time_routing = [&](std::vector<double>& lat_v, std::vector<int32_t>* counts_out) -> damoe_status {
+      if (hipMemcpyAsync(d_ids, ids.data(), sizeof(int32_t) * ids.size(), hipMemcpyHostToDevice, stream) ||
+          hipMemcpyAsync(d_w, w.data(), sizeof(float) * w.size(), hipMemcpyHostToDevice, stream))
+        return DAMOE_ERR_HIP;
+      damoe_status s2 = damoe_route_histogram(d_ids, T, k, E, d_counts, d_off, d_perm, d_inv, d_nd,
+                                              d_bucket, ws, ws_bytes, stream);
+      if (s2 != DAMOE_OK) return s2;
+      if (counts_out) {
+        counts_out->resize(E);
+        if (hipMemcpyAsync(counts_out->data(), d_counts, sizeof(int32_t) * E, hipMemcpyDeviceToHost, stream))
+          return DAMOE_ERR_HIP;
+      }
+      lat_v.assign(nv, INFINITY);
+      std::vector<float> reps(cfg->reps);
+      for (int32_t v = 0; v < nv; ++v) {
+        if (!damoe_variant_supports(v, L->wdtype)) continue;
+        // warm-up
+        s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, d_y, ws, ws_bytes, stream);
+        if (s2 != DAMOE_OK) return s2;
+        for (int32_t r = 0; r < cfg->reps; ++r) {
+          if (hipEventRecord(e0, stream)) return DAMOE_ERR_HIP;
+          s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, d_y, ws, ws_bytes, stream);
+          if (s2 != DAMOE_OK) return s2;
+          if (hipEventRecord(e1, stream) || hipEventSynchronize(e1)) return DAMOE_ERR_HIP;
+          float ms = 0.f;
+          if (hipEventElapsedTime(&ms, e0, e1)) return DAMOE_ERR_HIP;
+          reps[r] = ms;
+        }
+        std::nth_element(reps.begin(), reps.begin() + cfg->reps / 2, reps.end());
+        lat_v[v] = reps[cfg->reps / 2];
+      }
+      return hipStreamSynchronize(stream) == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+    };
+
+    t_bucket.push_back(T);
+    int32_t n_added = 0;
+    for (int32_t j = 0; j < cfg->n_skews; ++j) {
+      std::vector<std::vector<int32_t>> cs;
+      std::vector<double> mean(nv, 0.0), lat;
+      for (int32_t s = 0; s < cfg->samples; ++s) {
+        const uint32_t sid = 0x10000u + ((uint32_t)b << 20) + ((uint32_t)j << 10) + (uint32_t)s;
+        dirichlet_logp(g, alphas[j], E, sid, lp);
+        gumbel_topk(g, lp, T, k, sid, ids, w);
+        std::vector<int32_t> c;
+        TRY(time_routing(lat, &c));
+        cs.push_back(c);
+        for (int32_t v = 0; v < nv; ++v) mean[v] += lat[v] / cfg->samples;
+      }
+      int32_t best = 0;
+      for (int32_t v = 1; v < nv; ++v)
+        if (mean[v] < mean[best]) best = v;
+      t_kid.push_back(best);
+      t_Q.resize(t_Q.size() + E);
+      exemplar(cs, E, t_Q.data() + t_Q.size() - E);
+      ++n_added;
+      if (cfg->verbose)
+        std::fprintf(stderr, "damoe_tune: T=%d ddist:%.2f -> %s (%.1f us)\n", T, cfg->skew_X[j],
+                     damoe_variant_name(best), mean[best] * 1e3);
+    }
+    t_nex.push_back(n_added);
+    // Distribution-unaware baseline: the fastest variant under uniform routing.
+    {
+      std::vector<double> mean(nv, 0.0), lat;
+      lp.assign(E, -std::log((double)E));
+      for (int32_t s = 0; s < cfg->samples; ++s) {
+        const uint32_t sid = 0x8000000u + ((uint32_t)b << 10) + (uint32_t)s;
+        gumbel_topk(g, lp, T, k, sid, ids, w);
+        TRY(time_routing(lat, nullptr));
+        for (int32_t v = 0; v < nv; ++v) mean[v] += lat[v] / cfg->samples;
+      }
+      int32_t best = 0;
+      for (int32_t v = 1; v < nv; ++v)
+        if (mean[v] < mean[best]) best = v;
+      t_noda.push_back(best);
+      if (cfg->verbose)
+        std::fprintf(stderr, "damoe_tune: T=%d uniform (noda) -> %s\n", T, damoe_variant_name(best));
+    }
+  }
+  {
+    damoe_table_desc d{};
+    d.E = E;
+    d.k = k;
+    d.H = L->H;
+    d.I = L->I;
+    d.wdtype = L->wdtype;
+    d.n_buckets = (int32_t)t_bucket.size();
+    d.bucket_T = t_bucket.data();
+    d.n_ex = t_nex.data();
+    d.Q = t_Q.data();
+    d.kid = t_kid.data();
+    d.noda = t_noda.data();
+    st = damoe_table_create(&d, out);
+  }
+done:
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  (void)hipFree(ws);
+  (void)hipFree(d_ids);
+  (void)hipFree(d_w);
+  (void)hipFree(d_counts);
+  (void)hipFree(d_off);
+  (void)hipFree(d_perm);
+  (void)hipFree(d_inv);
+  (void)hipFree(d_nd);
+  (void)hipFree(d_bucket);
+  (void)hipFree(d_y);
+  return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,109 @@
+"""Device-side layer and buffers for driving the C-ABI from Python.
+
+``DeviceLayer`` holds one MoE layer's expert weights in HBM (filled on the
+device by the seeded generator), ``Path`` owns every buffer one call sequence
+needs (routing, histogram, permutation, variant id, activations, output,
+workspace).  Both only allocate at construction; the per-step methods call
+the library and nothing else.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import damoe, synth
+
+
+class DeviceLayer:
+    def __init__(self, shape: synth.Shape, device: str = "cuda"):
+        self.shape = shape
+        E, H, I = shape.E, shape.H, shape.I
+        self.wdtype = damoe.W_FP8_B128 if shape.wdtype == "fp8" else damoe.W_BF16
+        stream = torch.cuda.current_stream(device).cuda_stream
+        self.w, self.s = {}, {}
+        for name in ("w1", "w3", "w2"):
+            tid, r, c = synth.weight_dims(shape, name)
+            if self.wdtype == damoe.W_BF16:
+                t = torch.empty((E, r, c), dtype=torch.bfloat16, device=device)
+                synth.fill_bf16_device(t.data_ptr(), t.numel(), seed=shape.weight_seed, tensor=tid,
+                                       slab_elems=r * c, sigma=shape.w_sigma, stream=stream)
+                self.w[name] = t
+            else:
+                q = torch.empty((E, r, c), dtype=torch.uint8, device=device)
+                s = torch.empty((E, r // 128, c // 128), dtype=torch.float32, device=device)
+                synth.fill_fp8_device(q.data_ptr(), s.data_ptr(), r, c, E, seed=shape.weight_seed,
+                                      tensor=tid, sigma=shape.w_sigma, stream=stream)
+                self.w[name], self.s[name] = q, s
+        self.layer = damoe.make_layer(E, shape.k, H, I, self.wdtype, self.w["w1"], self.w["w3"],
+                                      self.w["w2"], self.s.get("w1"), self.s.get("w3"), self.s.get("w2"))
+
+    @property
+    def weight_bytes_per_expert(self) -> int:
+        sh = self.shape
+        if self.wdtype == damoe.W_BF16:
+            return 3 * sh.H * sh.I * 2
+        return 3 * sh.H * sh.I + 3 * (sh.H // 128) * (sh.I // 128) * 4
+
+
+class Path:
+    """Buffers for calls with up to T_max tokens on one layer."""
+
+    def __init__(self, dl: DeviceLayer, T_max: int, device: str = "cuda"):
+        sh = dl.shape
+        self.dl, self.T_max = dl, T_max
+        A = max(T_max * sh.k, 1)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.ids = torch.zeros(A, **i32)
+        self.w = torch.zeros(A, dtype=torch.float32, device=device)
+        self.counts = torch.zeros(sh.E, **i32)
+        self.offsets = torch.zeros(sh.E + 1, **i32)
+        self.perm = torch.zeros(A, **i32)
+        self.inv_perm = torch.zeros(A, **i32)
+        self.numden = torch.zeros(2, dtype=torch.int64, device=device)
+        self.bucket = torch.zeros(1, **i32)
+        self.variant = torch.zeros(1, **i32)
+        self.x = torch.zeros((max(T_max, 1), sh.H), dtype=torch.bfloat16, device=device)
+        self.y = torch.zeros((max(T_max, 1), sh.H), dtype=torch.bfloat16, device=device)
+        self.ws = torch.zeros(damoe.workspace_size(dl.layer, T_max), dtype=torch.uint8, device=device)
+
+    def set_routing(self, r: synth.Routing):
+        T = r.T
+        if T > self.T_max:
+            raise ValueError("routing larger than T_max")
+        if T:
+            self.ids[: T * r.k].copy_(torch.from_numpy(r.ids.ravel()))
+            self.w[: T * r.k].copy_(torch.from_numpy(r.w.ravel()))
+
+    def fill_x(self, T: int, tag: int):
+        if T:
+            synth.fill_bf16_device(self.x.data_ptr(), T * self.dl.shape.H, seed=synth.x_seed(tag),
+                                   tensor=synth.T_X, slab_elems=T * self.dl.shape.H, sigma=1.0,
+                                   stream=torch.cuda.current_stream().cuda_stream)
+
+    def route(self, T: int, ids=None, stream=None):
+        sh = self.dl.shape
+        damoe.route_histogram(self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
+                              self.perm, self.inv_perm, self.numden, self.bucket, self.ws, stream)
+
+    def dispatch(self, table: damoe.Table, T: int, stream=None):
+        damoe.dispatch(table, self.counts, T, self.variant, self.ws, stream)
+
+    def fused(self, T: int, force_variant: int = -1, w=None, stream=None):
+        damoe.fused_moe(self.dl.layer, self.x, self.w if w is None else w, T, self.perm, self.inv_perm,
+                        self.variant, force_variant, self.y, self.ws, stream)
+
+    def fused_stage(self, stage: int, T: int, force_variant: int = -1, w=None, stream=None):
+        damoe.fused_moe_stage(self.dl.layer, stage, self.x, self.w if w is None else w, T, self.perm,
+                              self.inv_perm, self.variant, force_variant, self.y, self.ws, stream)
+
+    def ctrl(self):
+        lo = damoe.workspace_layout(self.dl.shape.E, self.dl.shape.k, self.dl.shape.H, self.dl.shape.I,
+                                    self.T_max)
+        return self.ws[lo["ctrl"]: lo["ctrl"] + 256].view(torch.int32).cpu().numpy()
+
+    def tiles(self, T: int, cls: int):
+        sh = self.dl.shape
+        lo = damoe.workspace_layout(sh.E, sh.k, sh.H, sh.I, T)
+        off = lo["tiles"][cls]
+        n = int(self.ws[off: off + 4].view(torch.int32).item())
+        ent = self.ws[off + 8: off + 8 + 8 * n].view(torch.int32).cpu().numpy().reshape(n, 2)
+        return ent

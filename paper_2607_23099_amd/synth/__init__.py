@@ -85,9 +85,12 @@ def philox4x32_10(ctr, key) -> np.ndarray:
 
 
 def fill_bf16_host(n: int, *, seed: int, tensor: int, slab0: int = 0, slab_elems: int | None = None,
-                   start: int = 0, sigma: float = 1.0) -> np.ndarray:
+                   start: int = 0, sigma: float = 1.0, out: np.ndarray | None = None) -> np.ndarray:
     """Host bf16 values (as uint16 bit patterns) of elements start..start+n-1."""
-    out = np.empty(int(n), dtype=np.uint16)
+    if out is None:
+        out = np.empty(int(n), dtype=np.uint16)
+    elif out.dtype != np.uint16 or out.size != int(n) or not out.flags.c_contiguous:
+        raise ValueError("out must be a contiguous uint16 array of n elements")
     se = int(slab_elems) if slab_elems else max(int(start) + int(n), 1)
     lib().synth_fill_bf16_host(out.ctypes.data, int(n), int(start), se, int(slab0), int(seed),
                                int(tensor), ih_scale(sigma))
@@ -220,14 +223,31 @@ def weight_dims(shape: Shape, name: str):
     return tid, getattr(shape, r), getattr(shape, c)
 
 
-def expert_weights_host(shape: Shape, e: int):
-    """bf16 bit patterns (uint16) of expert e: (W1 [I][H], W3 [I][H], W2 [H][I])."""
-    out = []
-    for name in ("w1", "w3", "w2"):
+def expert_weights_host(shape: Shape, e: int, out=None):
+    """bf16 bit patterns (uint16) of expert e: (W1 [I][H], W3 [I][H], W2 [H][I]).
+
+    ``out`` may be a previous result to refill in place (avoids first-touch cost)."""
+    res = []
+    for i, name in enumerate(("w1", "w3", "w2")):
         tid, r, c = weight_dims(shape, name)
-        out.append(fill_bf16_host(r * c, seed=shape.weight_seed, tensor=tid, slab0=e,
-                                  slab_elems=r * c, sigma=shape.w_sigma).reshape(r, c))
-    return tuple(out)
+        buf = None if out is None else out[i].reshape(-1)
+        res.append(fill_bf16_host(r * c, seed=shape.weight_seed, tensor=tid, slab0=e,
+                                  slab_elems=r * c, sigma=shape.w_sigma, out=buf).reshape(r, c))
+    return tuple(res)
+
+
+class ExpertWeightSource:
+    """Callable e -> expert e's host weights, refilling one set of buffers."""
+
+    def __init__(self, shape: Shape):
+        self.shape = shape
+        self.buf = None
+
+    def __call__(self, e: int):
+        if self.shape.wdtype == "fp8":
+            return expert_weights_fp8_host(self.shape, e)
+        self.buf = expert_weights_host(self.shape, e, self.buf)
+        return self.buf
 
 
 def expert_weights_fp8_host(shape: Shape, e: int):

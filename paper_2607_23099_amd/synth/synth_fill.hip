@@ -206,9 +206,14 @@ void synth_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t 
 void synth_fill_bf16_host(uint16_t* out, uint64_t n, uint64_t start, uint64_t slab_elems,
                           uint32_t slab0, uint64_t seed, uint32_t tensor, float scale) {
   parallel_for(n, [&](uint64_t b, uint64_t e) {
+    uint32_t slab = slab0 + (uint32_t)((start + b) / slab_elems);
+    uint64_t idx = (start + b) % slab_elems;
     for (uint64_t j = b; j < e; ++j) {
-      const uint64_t g = start + j;
-      out[j] = synth_bf16(seed, tensor, slab0 + (uint32_t)(g / slab_elems), g % slab_elems, scale);
+      out[j] = synth_bf16(seed, tensor, slab, idx, scale);
+      if (++idx == slab_elems) {
+        idx = 0;
+        ++slab;
+      }
     }
   });
 }
@@ -233,23 +238,24 @@ int synth_fill_fp8_b128_host(uint8_t* q, float* s, uint32_t rows, uint32_t cols,
   const uint32_t rb_n = rows / 128, cb_n = cols / 128;
   const uint64_t nblk = (uint64_t)n_slabs * rb_n * cb_n;
   parallel_for(nblk, [&](uint64_t b, uint64_t e) {
+    std::vector<float> w(128 * 128);
     for (uint64_t blk = b; blk < e; ++blk) {
       const uint32_t sl = (uint32_t)(blk / ((uint64_t)rb_n * cb_n));
       const uint32_t rem = (uint32_t)(blk % ((uint64_t)rb_n * cb_n));
       const uint32_t rb = rem / cb_n, cb = rem % cb_n;
+      for (uint32_t i = 0; i < 128; ++i) {
+        const uint64_t row0 = (uint64_t)(rb * 128 + i) * cols + cb * 128;
+        for (uint32_t j = 0; j < 128; ++j)
+          w[i * 128 + j] = bf16_to_f32(synth_bf16(seed, tensor, slab0 + sl, row0 + j, scale));
+      }
       float amax = 0.f;
-      for (uint32_t r = rb * 128; r < rb * 128 + 128; ++r)
-        for (uint32_t c = cb * 128; c < cb * 128 + 128; ++c) {
-          const float w = bf16_to_f32(synth_bf16(seed, tensor, slab0 + sl, (uint64_t)r * cols + c, scale));
-          amax = std::max(amax, std::fabs(w));
-        }
+      for (float v : w) amax = std::max(amax, std::fabs(v));
       const float sc = amax > 0.f ? amax / 448.0f : 1.0f;
       const uint64_t base = (uint64_t)sl * rows * cols;
-      for (uint32_t r = rb * 128; r < rb * 128 + 128; ++r)
-        for (uint32_t c = cb * 128; c < cb * 128 + 128; ++c) {
-          const float w = bf16_to_f32(synth_bf16(seed, tensor, slab0 + sl, (uint64_t)r * cols + c, scale));
-          q[base + (uint64_t)r * cols + c] = f32_to_e4m3_rne_sat(w / sc);
-        }
+      for (uint32_t i = 0; i < 128; ++i) {
+        const uint64_t row0 = base + (uint64_t)(rb * 128 + i) * cols + cb * 128;
+        for (uint32_t j = 0; j < 128; ++j) q[row0 + j] = f32_to_e4m3_rne_sat(w[i * 128 + j] / sc);
+      }
       s[(uint64_t)sl * rb_n * cb_n + rem] = sc;
     }
   });

@@ -1,0 +1,158 @@
+"""C-ABI checks that need no GPU: exports, argument validation, layout, host-side math."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_23099_amd import damoe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    if not os.path.exists(damoe.LIB_PATH):
+        from paper_2607_23099_amd import build
+        build.build_damoe()
+    oracle.build()
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "damoe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(damoe_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 18
+    L = ctypes.CDLL(damoe.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(damoe.EXPORTED)
+
+
+def test_status_strings_and_registry():
+    L = damoe.lib()
+    for code in damoe.STATUS:
+        assert L.damoe_status_string(code)
+    nv = damoe.num_variants()
+    assert nv >= 3
+    names = [damoe.variant_name(v) for v in range(nv)]
+    assert len(set(names)) == nv and all(names)
+    assert damoe.variant_name(nv) == "" and damoe.variant_tile_m(-1) == 0
+    assert all(damoe.variant_tile_m(v) in (16, 32, 64, 128, 256) for v in range(nv))
+    assert all(damoe.variant_supports(v, damoe.W_BF16) for v in range(nv))
+    assert not damoe.variant_supports(0, 7)
+
+
+def test_workspace_layout():
+    for (E, k, H, I, T) in [(8, 2, 256, 512, 64), (256, 8, 7168, 2048, 128), (384, 8, 7168, 2048, 8192),
+                            (256, 8, 7168, 2048, 0)]:
+        lo = damoe.workspace_layout(E, k, H, I, T)
+        A = T * k
+        regions = [(lo["ctrl"], 256)] + [(o, 8 + 8 * lo["tiles_cap"]) for o in lo["tiles"]] + \
+                  [(lo["h"], A * I * 2), (lo["out"], A * H * 4)]
+        for off, size in regions:
+            assert off % 256 == 0 and off + size <= lo["total"]
+        ends = sorted(regions)
+        assert all(a[0] + a[1] <= b[0] for a, b in zip(ends, ends[1:]))
+        # Enough tile slots for the worst case of every tile size.
+        assert lo["tiles_cap"] >= A // 16 + min(E, A)
+    L = damoe.lib()
+    bad = damoe.WsLayout()
+    assert L.damoe_workspace_layout(0, 1, 128, 128, 4, ctypes.byref(bad)) == -1
+    assert L.damoe_workspace_layout(8, 9, 128, 128, 4, ctypes.byref(bad)) == -1
+    assert L.damoe_workspace_layout(2048, 8, 128, 128, 4, ctypes.byref(bad)) == -1
+    assert L.damoe_workspace_layout(8, 2, 128, 128, -1, ctypes.byref(bad)) == -1
+
+
+def _fake_layer(**kw):
+    d = dict(E=8, k=2, H=256, I=512, wdtype=0, w1=0x1000, w3=0x2000, w2=0x3000, s1=0, s3=0, s2=0)
+    d.update(kw)
+    return damoe.Layer(d["E"], d["k"], d["H"], d["I"], d["wdtype"], d["w1"], d["w3"], d["w2"], d["s1"],
+                       d["s3"], d["s2"])
+
+
+def test_validation_before_launch():
+    L = damoe.lib()
+    P = 0x10000  # never dereferenced: every call below must fail validation first
+    ws_ok = 1 << 30
+    # route_histogram
+    assert L.damoe_route_histogram(P, 4, 3, 2, P, P, P, P, P, P, P, ws_ok, None) == -1  # k > E
+    assert L.damoe_route_histogram(P, -1, 2, 8, P, P, P, P, P, P, P, ws_ok, None) == -1
+    assert L.damoe_route_histogram(P, 4, 2, 8, None, P, P, P, P, P, P, ws_ok, None) == -1
+    assert L.damoe_route_histogram(None, 4, 2, 8, P, P, P, P, P, P, P, ws_ok, None) == -1
+    assert L.damoe_route_histogram(P, 4, 2, 8, P, P, P, P, P, P, P, 16, None) == -3
+    assert L.damoe_route_histogram(P, 4, 2, 4096, P, P, P, P, P, P, P, ws_ok, None) == -1
+    # fused_moe
+    fm = L.damoe_fused_moe
+    lay = _fake_layer()
+    assert fm(None, P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(_fake_layer(H=200)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
+    assert fm(ctypes.byref(_fake_layer(w2=0)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(_fake_layer(wdtype=1)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -1  # no scales
+    assert fm(ctypes.byref(_fake_layer(wdtype=1, s1=P, s3=P, s2=P)), P, P, 4, P, P, P, -1, P, P, ws_ok,
+              None) == -2  # fp8 needs H, I multiples of 512
+    assert fm(ctypes.byref(_fake_layer(wdtype=5)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, damoe.num_variants(), P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, None, -1, P, P, ws_ok, None) == -1  # no variant id
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, -1, P, P, 1024, None) == -3
+    assert fm(ctypes.byref(lay), P, P, -2, P, P, P, -1, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(lay), None, None, 0, None, None, None, 0, None, None, 0, None) == 0  # T = 0 no-op
+    # dispatch
+    assert L.damoe_dispatch(None, P, 4, P, P, ws_ok, None) == -1
+    # workspace size of an invalid layer is 0
+    assert damoe.workspace_size(_fake_layer(k=0), 4) == 0
+    assert damoe.workspace_size(_fake_layer(), 64) == damoe.workspace_layout(8, 2, 256, 512, 64)["total"]
+
+
+def test_alpha_search_matches_oracle_and_closed_form():
+    # Both sides implement Alg. 1 over the same counter-based random numbers.
+    for E, m in [(256, 128.0), (256, 13.0), (384, 200.0), (8, 4.0)]:
+        a_lib = damoe.alpha_search(E, m, 32, 60, 5)
+        a_or = oracle.alpha_search(E, m, S=32, iters=60, seed=5)
+        assert a_lib == pytest.approx(a_or, rel=1e-9)
+    a = damoe.alpha_search(256, 128.0, 64, 60, 0)
+    assert a == pytest.approx(127.0 / 128.0, rel=0.05)
+
+
+def test_table_roundtrip_host(tmp_path):
+    rng = np.random.default_rng(0)
+    E = 16
+    nv = damoe.num_variants()
+    td = damoe.TableData(E=E, k=2, H=256, I=512, wdtype=0, bucket_T=np.array([1, 4, 16]),
+                         n_ex=np.array([2, 3, 1]), Q=rng.integers(0, 32768, (6, E)),
+                         kid=rng.integers(0, nv, 6), noda=np.array([0, 1, 2]) % nv)
+    t = damoe.Table.create(td)
+    got = t.data(E)
+    np.testing.assert_array_equal(got.bucket_T, td.bucket_T)
+    np.testing.assert_array_equal(got.n_ex, td.n_ex)
+    np.testing.assert_array_equal(got.Q, td.Q)
+    np.testing.assert_array_equal(got.kid, td.kid)
+    np.testing.assert_array_equal(got.noda, td.noda)
+    p = str(tmp_path / "t.damoe")
+    t.save(p)
+    t2 = damoe.Table.load(p)
+    g2 = t2.data(E)
+    np.testing.assert_array_equal(g2.Q, td.Q)
+    np.testing.assert_array_equal(g2.kid, td.kid)
+    # A file written for another variant set is rejected.
+    txt = open(p).read().split("\n")
+    txt[0] = "damoe-table 1 2,other,set"
+    open(p, "w").write("\n".join(txt))
+    with pytest.raises(damoe.DamoeError) as ei:
+        damoe.Table.load(p)
+    assert ei.value.code == -4
+    with pytest.raises(damoe.DamoeError) as ei:
+        damoe.Table.load(str(tmp_path / "missing"))
+    assert ei.value.code == -7
+    # Invalid descriptions.
+    for bad in (dict(bucket_T=np.array([4, 1, 16])), dict(n_ex=np.array([0, 3, 3])),
+                dict(kid=np.full(6, nv)), dict(noda=np.array([0, 0, -1]))):
+        d = damoe.TableData(**{**td.__dict__, **bad})
+        with pytest.raises(damoe.DamoeError):
+            damoe.Table.create(d)

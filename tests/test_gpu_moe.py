@@ -1,0 +1,179 @@
+"""GPU parity of a6-a8: the fused MoE layer of every variant against the CPU oracle."""
+import numpy as np
+import pytest
+
+from paper_2607_23099_amd import damoe, synth
+from tests.gpu_common import TOL, bf16_rows, log, oracle_rows, row_err, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _variants():
+    return list(range(damoe.num_variants()))
+
+
+def _run(path, r, x_tag, variant=None, table=None):
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import Path  # noqa: F401
+    path.set_routing(r)
+    path.fill_x(r.T, x_tag)
+    path.y.fill_(float("nan"))
+    path.route(r.T)
+    if table is not None:
+        path.dispatch(table, r.T)
+        path.fused(r.T, -1)
+    else:
+        path.fused(r.T, variant)
+    torch.cuda.synchronize()
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    dl = DeviceLayer(synth.TINY)
+    yield dl, Path(dl, 256)
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T,alpha,seed", [(64, 1.0, 0), (1, 1.0, 1), (37, 0.05, 2), (200, 10.0, 3)])
+def test_tiny_every_variant(tiny, T, alpha, seed):
+    dl, path = tiny
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, alpha, [seed] if seed else 0)
+    ref = oracle_rows(sh, r, seed, np.arange(T))
+    for v in _variants():
+        log(f"tiny T={T} alpha={alpha} variant={damoe.variant_name(v)}")
+        _run(path, r, seed, v)
+        err = row_err(bf16_rows(path.y, np.arange(T)), ref)
+        assert err <= TOL["bf16"], (v, err)
+        assert path.ctrl()[4] == v
+
+
+def test_tiny_adaptive_uses_device_variant(tiny):
+    torch = torch_cuda()
+    dl, path = tiny
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, 64, 1.0, 0)
+    nv = damoe.num_variants()
+    for target in range(nv):
+        q = np.full((1, sh.E), int(round(2 ** 15 / np.sqrt(sh.E))), np.int32)
+        td = damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0, bucket_T=np.array([1 << 20]),
+                             n_ex=np.array([1]), Q=q, kid=np.array([target]), noda=np.array([0]))
+        table = damoe.Table.create(td)
+        _run(path, r, 0, table=table)
+        assert int(path.variant.item()) == target and path.ctrl()[4] == target
+        y_adaptive = path.y[:64].clone()
+        _run(path, r, 0, variant=target)
+        assert torch.equal(y_adaptive, path.y[:64])
+
+
+def test_tiny_zero_tokens_is_noop(tiny):
+    torch = torch_cuda()
+    dl, path = tiny
+    path.y.fill_(3.0)
+    r = synth.routing(dl.shape.E, dl.shape.k, 0, 1.0, 0)
+    path.route(0)
+    path.fused(0, 0)
+    torch.cuda.synchronize()
+    assert bool((path.y == 3.0).all())
+
+
+def test_cold_experts_are_never_read():
+    # Experts without tokens hold NaN weights; the output must not see them.
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    sh = synth.Shape("tiny-cold", E=16, k=2, H=256, I=512, shape_id=0)
+    dl = DeviceLayer(sh)
+    path = Path(dl, 64)
+    r = synth.routing(sh.E, sh.k, 64, 0.05, [21])
+    cold = sorted(set(range(sh.E)) - set(np.unique(r.ids).tolist()))
+    assert cold, "routing should leave some experts cold"
+    for name in ("w1", "w3", "w2"):
+        dl.w[name][cold] = float("nan")
+    ref = oracle_rows(sh, r, 21, np.arange(64))
+    for v in _variants():
+        _run(path, r, 21, v)
+        y = bf16_rows(path.y, np.arange(64))
+        assert np.all(np.isfinite(y))
+        assert row_err(y, ref) <= TOL["bf16"]
+
+
+@pytest.fixture(scope="module")
+def ds():
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    log("filling DeepSeek-V3-shaped bf16 layer (22.5 GB)")
+    dl = DeviceLayer(synth.DS)
+    torch.cuda.synchronize()
+    yield dl, Path(dl, 128), synth.ExpertWeightSource(synth.DS)
+    del dl
+    torch.cuda.empty_cache()
+
+
+DS_CASES = [(1, 0.3), (8, 0.05), (8, 10.0), (32, 1.0), (128, 0.05), (128, 10.0)]
+
+
+@pytest.mark.parametrize("T,alpha", DS_CASES)
+def test_ds_decode_every_variant(ds, T, alpha):
+    dl, path, src = ds
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, alpha, synth.seed_decode(T, alpha, 0))
+    rows = np.arange(T) if T <= 4 else np.sort(np.random.default_rng(T).choice(T, 4, replace=False))
+    log(f"ds decode T={T} alpha={alpha}: oracle on rows {rows.tolist()}")
+    ref = oracle_rows(sh, r, 100 + T, rows, src)
+    for v in _variants():
+        log(f"ds decode T={T} alpha={alpha} variant={damoe.variant_name(v)}")
+        _run(path, r, 100 + T, v)
+        err = row_err(bf16_rows(path.y, rows), ref)
+        assert err <= TOL["bf16"], (v, err)
+
+
+@pytest.fixture(scope="module")
+def kimi():
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    log("filling Kimi-K2-shaped bf16 layer (33.8 GB)")
+    dl = DeviceLayer(synth.KIMI)
+    torch.cuda.synchronize()
+    yield dl, Path(dl, 2048), synth.ExpertWeightSource(synth.KIMI)
+    del dl
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T", [16, 256, 2048])
+def test_kimi_hot_experts(kimi, T):
+    dl, path, src = kimi
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, 0.05, synth.seed_kimi(T, 0), n_hot=4)
+    rows = np.sort(np.random.default_rng(T).choice(T, 3, replace=False))
+    ref = oracle_rows(sh, r, 300 + T, rows, src)
+    for v in _variants():
+        log(f"kimi T={T} variant={damoe.variant_name(v)}")
+        _run(path, r, 300 + T, v)
+        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["bf16"]
+
+
+@pytest.fixture(scope="module")
+def ds_fp8():
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    log("filling DeepSeek-V3-shaped fp8 block-128 layer")
+    dl = DeviceLayer(synth.DS_FP8)
+    torch.cuda.synchronize()
+    yield dl, Path(dl, 4096), synth.ExpertWeightSource(synth.DS_FP8)
+    del dl
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T,alpha", [(1024, 0.05), (1024, 10.0), (4096, 0.3)])
+def test_ds_prefill_fp8(ds_fp8, T, alpha):
+    dl, path, src = ds_fp8
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, alpha, synth.seed_prefill(T, alpha, 0))
+    rows = np.sort(np.random.default_rng(T).choice(T, 2, replace=False))
+    ref = oracle_rows(sh, r, 200 + T, rows, src)
+    for v in _variants():
+        log(f"ds fp8 prefill T={T} alpha={alpha} variant={damoe.variant_name(v)}")
+        _run(path, r, 200 + T, v)
+        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["fp8"]
