@@ -137,9 +137,10 @@ def main():
         ids, w = ids_d[T, a, rep], w_d[T, a, rep]
         if events:
             events[0].record(stream)
-        path.route(T, ids=ids)
         if force < 0:
-            path.dispatch(table, T)
+            path.route_dispatch(table, T, ids=ids)
+        else:
+            path.route(T, ids=ids)
         if events:
             events[1].record(stream)
         path.fused_stage(0, T, force, w=w)

@@ -175,6 +175,17 @@ damoe_status damoe_table_load(const char* path, damoe_table** out);
 damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int32_t T,
                             int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* a2-a5 in one launch: exactly damoe_route_histogram followed by damoe_dispatch on
+ * its counts (same outputs, same workspace contents), with the histogram, the
+ * exemplar match and the permutation sharing one workgroup's LDS.  This is the
+ * paper's online step 5 (Sec. IV-B): histogram, sort, match, kernel id, all on
+ * the device.  The table must be built for this E and k. */
+damoe_status damoe_route_dispatch(const damoe_table* table, const int32_t* topk_ids, int32_t T,
+                                  int32_t k, int32_t E, int32_t* counts, int32_t* offsets,
+                                  int32_t* perm, int32_t* inv_perm, uint64_t* effexp_numden,
+                                  int32_t* effexp_bucket, int32_t* variant_id, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
 /* a6-a8: the fused expert computation.
  *   x          bf16 [T][H] token activations
  *   topk_w     fp32 [T][k] gate of each (token, slot)

@@ -137,24 +137,66 @@ size_t damoe_workspace_size(const damoe_layer* L, int32_t T_max) {
   return lo.total;
 }
 
+static damoe_status check_route(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
+                                int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
+                                int32_t* bucket, void* ws, size_t ws_bytes, damoe_ws_layout* lo) {
+  if (!shape_ok(E, k) || T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
+  if (!counts || !offsets || !numden || !bucket || !ws) return DAMOE_ERR_INVALID_ARG;
+  if (T > 0 && (!topk_ids || !perm || !inv_perm)) return DAMOE_ERR_INVALID_ARG;
+  layout(E, k, 0, 0, T, lo);
+  if (ws_bytes < lo->h) return DAMOE_ERR_WORKSPACE;
+  return DAMOE_OK;
+}
+
+// Bucket of the paper's online path: the smallest tuned token count >= T, else the last.
+static int32_t table_bucket(const damoe_table* t, int32_t T) {
+  const int32_t nb = (int32_t)t->bucket_T.size();
+  for (int32_t i = 0; i < nb; ++i)
+    if (T <= t->bucket_T[i]) return i;
+  return nb - 1;
+}
+
+static DispatchArgs table_args(const damoe_table* t, int32_t T, int32_t* variant_id) {
+  const int32_t b = table_bucket(t, T);
+  return DispatchArgs{t->d_Q + (size_t)t->ex_begin[b] * t->E, t->d_kid + t->ex_begin[b], t->n_ex[b],
+                      t->noda[b], variant_id};
+}
+
+static damoe_status route_impl(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
+                               int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
+                               int32_t* bucket, void* ws, size_t ws_bytes, const DispatchArgs* d,
+                               hipStream_t stream) {
+  damoe_ws_layout lo;
+  const damoe_status st =
+      check_route(topk_ids, T, k, E, counts, offsets, perm, inv_perm, numden, bucket, ws, ws_bytes, &lo);
+  if (st != DAMOE_OK) return st;
+  char* base = static_cast<char*>(ws);
+  int32_t* lists[DAMOE_N_TILE_SIZES];
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) lists[c] = reinterpret_cast<int32_t*>(base + lo.tiles[c]);
+  const hipError_t e = launch_route(topk_ids, T, k, E, counts, offsets, perm, inv_perm, numden, bucket,
+                                    reinterpret_cast<int32_t*>(base + lo.ctrl), lists, d, stream);
+  return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+}
+
 damoe_status damoe_route_histogram(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
                                    int32_t* counts, int32_t* offsets, int32_t* perm,
                                    int32_t* inv_perm, uint64_t* effexp_numden,
                                    int32_t* effexp_bucket, void* ws, size_t ws_bytes,
                                    hipStream_t stream) {
-  if (!shape_ok(E, k) || T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
-  if (!counts || !offsets || !effexp_numden || !effexp_bucket || !ws) return DAMOE_ERR_INVALID_ARG;
-  if (T > 0 && (!topk_ids || !perm || !inv_perm)) return DAMOE_ERR_INVALID_ARG;
-  damoe_ws_layout lo;
-  layout(E, k, 0, 0, T, &lo);
-  if (ws_bytes < lo.h) return DAMOE_ERR_WORKSPACE;
-  char* base = static_cast<char*>(ws);
-  int32_t* lists[DAMOE_N_TILE_SIZES];
-  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) lists[c] = reinterpret_cast<int32_t*>(base + lo.tiles[c]);
-  const hipError_t e = launch_route(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden,
-                                    effexp_bucket, reinterpret_cast<int32_t*>(base + lo.ctrl), lists,
-                                    stream);
-  return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+  return route_impl(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden, effexp_bucket, ws,
+                    ws_bytes, nullptr, stream);
+}
+
+damoe_status damoe_route_dispatch(const damoe_table* t, const int32_t* topk_ids, int32_t T, int32_t k,
+                                  int32_t E, int32_t* counts, int32_t* offsets, int32_t* perm,
+                                  int32_t* inv_perm, uint64_t* effexp_numden, int32_t* effexp_bucket,
+                                  int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!t || !variant_id) return DAMOE_ERR_INVALID_ARG;
+  if (t->E != E || t->k != k) return DAMOE_ERR_TABLE_MISMATCH;
+  if (!t->d_Q) return DAMOE_ERR_HIP;  // table built without a device
+  const DispatchArgs d = table_args(t, T, variant_id);
+  return route_impl(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden, effexp_bucket, ws,
+                    ws_bytes, &d, stream);
 }
 
 damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t T,
@@ -162,16 +204,8 @@ damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t
   if (!t || !counts || !variant_id || !ws || T < 0) return DAMOE_ERR_INVALID_ARG;
   if (ws_bytes < kCtrlWords * sizeof(int32_t)) return DAMOE_ERR_WORKSPACE;
   if (!t->d_Q) return DAMOE_ERR_HIP;  // table built without a device
-  const int32_t nb = (int32_t)t->bucket_T.size();
-  int32_t b = nb - 1;
-  for (int32_t i = 0; i < nb; ++i)
-    if (T <= t->bucket_T[i]) {
-      b = i;
-      break;
-    }
-  const hipError_t e = launch_dispatch(counts, t->E, t->d_Q + (size_t)t->ex_begin[b] * t->E,
-                                       t->d_kid + t->ex_begin[b], t->n_ex[b], t->noda[b], variant_id,
-                                       reinterpret_cast<int32_t*>(ws), stream);
+  const hipError_t e =
+      launch_dispatch(counts, t->E, table_args(t, T, variant_id), reinterpret_cast<int32_t*>(ws), stream);
   return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
 }
 

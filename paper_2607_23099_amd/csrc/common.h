@@ -74,13 +74,22 @@ struct ReduceArgs {
   int32_t T, k, H;
 };
 
-// Launchers (return hipError_t of the launch).
+// Exemplars of the selected token-count bucket (device arrays) and where the choice goes.
+struct DispatchArgs {
+  const int32_t* Q;    // [n_ex][E]
+  const int32_t* kid;  // [n_ex]
+  int32_t n_ex;
+  int32_t noda;
+  int32_t* variant_id;
+};
+
+// Launchers (return hipError_t of the launch).  launch_route with a non-null dispatch runs
+// the exemplar match in the same kernel.
 hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
                         int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                         int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
-                        hipStream_t stream);
-hipError_t launch_dispatch(const int32_t* counts, int32_t E, const int32_t* Q, const int32_t* kid,
-                           int32_t n_ex, int32_t noda, int32_t* variant_id, int32_t* ctrl,
+                        const DispatchArgs* dispatch, hipStream_t stream);
+hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
                            hipStream_t stream);
 hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream);

@@ -28,29 +28,51 @@ namespace {
 
 constexpr int LDS_PAD = 1;
 
-// Register-ring depth (k-steps in flight per wave) of a stream variant.
-__host__ __device__ constexpr int stream_depth(int bm) { return bm <= 16 ? 4 : (bm <= 32 ? 3 : 2); }
 
-// e4m3fn byte -> bf16 bits (exact: every e4m3 value is a bf16 value).
-__device__ __forceinline__ uint32_t e4m3_to_bf16(uint32_t b) {
-  const uint32_t sign = (b & 0x80u) << 8;
-  const uint32_t ex = (b >> 3) & 15u, man = b & 7u;
-  uint32_t mag;
-  if (ex) {
-    mag = ((b & 0x7Fu) << 4) + (120u << 7);  // exponent ex - 7 + 127, mantissa man << 4
-  } else {
-    mag = __float_as_uint((float)man * 0.001953125f) >> 16;  // man * 2^-9, exact
-  }
-  return sign | mag;
+// fp8 weights: eight OCP e4m3fn codes -> bf16 MFMA operand with the 128x128 block scale
+// folded in.  A code's 7 magnitude bits placed at fp32 bit 20 form the fp32 number
+// value * 2^-120 (exponent bias 127 vs 7; e4m3 subnormals land on fp32 subnormals, which the
+// kernels keep), so one multiply by s * 2^120 yields q * s with a single rounding, and the
+// packed convert rounds it to bf16 (nearest even).
+__device__ __forceinline__ float e4m3_times(uint32_t b, float s120) {
+  return __uint_as_float(((b & 0x7Fu) << 20) | ((b & 0x80u) << 24)) * s120;
 }
 
-__device__ __forceinline__ uint4 fp8x8_to_bf16x8(uint2 q) {
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 r;
+  r[0] = (__bf16)lo;
+  r[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ uint4 fp8x8_to_bf16x8(uint2 q, float s120) {
   uint4 r;
-  r.x = e4m3_to_bf16(q.x & 0xFF) | (e4m3_to_bf16((q.x >> 8) & 0xFF) << 16);
-  r.y = e4m3_to_bf16((q.x >> 16) & 0xFF) | (e4m3_to_bf16(q.x >> 24) << 16);
-  r.z = e4m3_to_bf16(q.y & 0xFF) | (e4m3_to_bf16((q.y >> 8) & 0xFF) << 16);
-  r.w = e4m3_to_bf16((q.y >> 16) & 0xFF) | (e4m3_to_bf16(q.y >> 24) << 16);
+  r.x = pack_bf16x2(e4m3_times(q.x, s120), e4m3_times(q.x >> 8, s120));
+  r.y = pack_bf16x2(e4m3_times(q.x >> 16, s120), e4m3_times(q.x >> 24, s120));
+  r.z = pack_bf16x2(e4m3_times(q.y, s120), e4m3_times(q.y >> 8, s120));
+  r.w = pack_bf16x2(e4m3_times(q.y >> 16, s120), e4m3_times(q.y >> 24, s120));
   return r;
+}
+
+// Raw buffer loads: the slab base lives in a scalar resource descriptor, each lane keeps a
+// 32-bit byte offset and the k-step advances the scalar offset, so an operand fragment costs
+// one VGPR of addressing instead of a 64-bit pointer.  Offsets at or beyond the descriptor's
+// size read as zero (used for the padding rows of a token tile).
+constexpr uint32_t kOobOffset = 0x80000000u;
+constexpr int kAuxNontemporal = 2;  // cache-policy bit: streamed, not retained
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+template <class T, int AUX>
+__device__ __forceinline__ T buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  if constexpr (sizeof(T) == 16) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX));
+  } else {
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
+  }
 }
 
 template <bool FP8>
@@ -66,10 +88,14 @@ struct WFrag<true> {
   static constexpr int kBytesPerElem = 1;
 };
 
-template <int BM, int BN, bool GLU, bool FP8>
+// IL: the waves take interleaved 32-wide k-steps (wave w reads k-steps w, w+4, ...), so the
+//     4 waves of a workgroup read 256 contiguous bytes of every weight row at a time;
+//     otherwise each wave reads one contiguous quarter of the row.
+// NT: weight loads carry the nontemporal hint (streamed once, not worth caching).
+// D:  register-ring depth, k-steps in flight per wave.
+template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D>
 __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __restrict__ list,
                                             float* __restrict__ red) {
-  constexpr int D = stream_depth(BM);
   constexpr int NX = BM / 16;
   constexpr int NR = (GLU ? 2 : 1) * BN / 16;
   constexpr int LDR = BM + LDS_PAD;
@@ -80,9 +106,10 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
   const int K = a.K, N = a.N;
   const int n_fb = N / BN;
   const long long n_items = (long long)n_tiles * n_fb;
-  const int kw = K >> 2;  // K-slice of this wave
-  const int nks = kw >> 5;
-  const int kcol = wave * kw + (lane >> 4) * 8;
+  const int kw = K >> 2;  // elements of K per wave
+  const int nks = kw >> 5;  // k-steps per wave
+  constexpr int KSTEP = IL ? 128 : 32;  // element distance between a wave's k-steps
+  const int kcol = (IL ? wave * 32 : wave * kw) + (lane >> 4) * 8;
   const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
   const uint8_t* __restrict__ wb = reinterpret_cast<const uint8_t*>(a.wb);
   constexpr int EB = WFrag<FP8>::kBytesPerElem;
@@ -98,25 +125,34 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
       continue;
     }
 
-    const uint16_t* xp[NX];
-    bool xv[NX];
+    // Token operand: GEMM1 gathers rows perm[p] / k of x, GEMM2 reads the tile's rows of h.
+    __amdgpu_buffer_rsrc_t rx;
+    uint32_t xo[NX];
+    if (GLU) {
+      rx = make_rsrc(a.x, (uint32_t)((size_t)(a.A / a.k) * K * 2));
+    } else {
+      rx = make_rsrc(a.x + (size_t)p0 * K, (uint32_t)((size_t)rows * K * 2));
+    }
 #pragma unroll
     for (int s = 0; s < NX; ++s) {
       const int r = s * 16 + (lane & 15);
-      xv[s] = r < rows;
-      long long row;
-      if (GLU) row = xv[s] ? a.perm[p0 + r] / a.k : 0;
-      else row = p0 + (xv[s] ? r : 0);
-      xp[s] = a.x + row * K + kcol;
+      if (r < rows) {
+        const uint32_t row = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) : (uint32_t)r;
+        xo[s] = (row * (uint32_t)K + kcol) * 2u;
+      } else {
+        xo[s] = kOobOffset;
+      }
     }
-    const uint8_t* wp[NR];
+    // Weight operand: rows f of W1 (gate) and W3 (up) for GEMM1, of W2 for GEMM2.
+    const size_t slab = (size_t)N * K * EB;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(wa + (size_t)e * slab, (uint32_t)slab);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc((GLU ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
+    uint32_t wo[NR];
 #pragma unroll
     for (int b = 0; b < NR; ++b) {
-      const bool up = GLU && b >= NR / 2;
-      const int rb = GLU ? (b % (NR / 2)) : b;
-      const int f = fb * BN + rb * 16 + (lane & 15);
-      const uint8_t* base = up ? wb : wa;
-      wp[b] = base + (((size_t)e * N + f) * K + kcol) * EB;
+      const int rb_ = GLU ? (b % (NR / 2)) : b;
+      const int f = fb * BN + rb_ * 16 + (lane & 15);
+      wo[b] = ((uint32_t)f * (uint32_t)K + kcol) * EB;
     }
     const float* sa = a.sa;
     const float* sb = a.sb;
@@ -133,27 +169,24 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
     WT wf[D][NR];
     uint4 xf[D][NX];
     auto load = [&](int ks, int st) __attribute__((always_inline)) {
+      const uint32_t sw = (uint32_t)ks * KSTEP * EB;
 #pragma unroll
       for (int b = 0; b < NR; ++b)
-        wf[st][b] = *reinterpret_cast<const WT*>(wp[b] + (size_t)ks * 32 * EB);
+        wf[st][b] = buf_load<WT, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b], sw);
+      const uint32_t sx = (uint32_t)ks * KSTEP * 2;
 #pragma unroll
-      for (int s = 0; s < NX; ++s)
-        xf[st][s] = xv[s] ? *reinterpret_cast<const uint4*>(xp[s] + ks * 32) : make_uint4(0, 0, 0, 0);
+      for (int s = 0; s < NX; ++s) xf[st][s] = buf_load<uint4, 0>(rx, xo[s], sx);
     };
     auto compute = [&](int ks, int st) __attribute__((always_inline)) {
       if constexpr (FP8) {
-        const int kb = (wave * kw + ks * 32) >> 7;
-        const float s_g = sa[sbase + kb];
-        const float s_u = GLU ? sb[sbase + kb] : 0.f;
+        const int kb = (IL ? ks * 128 + wave * 32 : wave * kw + ks * 32) >> 7;
+        const float s_g = sa[sbase + kb] * 0x1p120f;
+        const float s_u = GLU ? sb[sbase + kb] * 0x1p120f : 0.f;
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
-          const uint4 wv = fp8x8_to_bf16x8(wf[st][b]);
-          const float sc = (GLU && b >= NR / 2) ? s_u : s_g;
+          const uint4 wv = fp8x8_to_bf16x8(wf[st][b], (GLU && b >= NR / 2) ? s_u : s_g);
 #pragma unroll
-          for (int s = 0; s < NX; ++s) {
-            const floatx4 t = mfma16x16x32(wv, xf[st][s], floatx4{0.f, 0.f, 0.f, 0.f});
-            acc[b][s] += sc * t;
-          }
+          for (int s = 0; s < NX; ++s) acc[b][s] = mfma16x16x32(wv, xf[st][s], acc[b][s]);
         }
       } else {
 #pragma unroll
@@ -163,17 +196,22 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
       }
     };
 
+    // Register ring: k-step s lives in slot s % D and is loaded D - 1 steps before its MFMAs.
+    // The steady-state loop is branch-free so the compiler can wait for exactly the oldest
+    // step's loads; loads past the last step are clamped to it (redundant, never computed).
 #pragma unroll
-    for (int d = 0; d < D - 1; ++d)
-      if (d < nks) load(d, d);
-    for (int ks = 0; ks < nks; ks += D) {
+    for (int d = 0; d < D - 1; ++d) load(min(d, nks - 1), d);
+    int ks = 0;
+    for (; ks + D <= nks; ks += D) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
-        const int kl = ks + d + D - 1;
-        if (kl < nks) load(kl, (d + D - 1) % D);
-        if (ks + d < nks) compute(ks + d, d);
+        load(min(ks + d + D - 1, nks - 1), (d + D - 1) % D);
+        compute(ks + d, d);
       }
     }
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d)
+      if (ks + d < nks) compute(ks + d, d);
 
     // Partial tiles of the 4 waves -> LDS, rows = output features, columns = tokens.
 #pragma unroll
@@ -209,24 +247,27 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
   }
 }
 
-// The registry.  Indices are the public variant ids.
-#define DAMOE_STREAM_VARIANTS(X) \
-  X(0, "stream_bm16", 16, 32, 64) \
-  X(1, "stream_bm32", 32, 32, 64) \
-  X(2, "stream_bm64", 64, 32, 64)
+// The registry.  Indices are the public variant ids: (id, name, BM, BN1, BN2, IL, NT, D).
+#define DAMOE_STREAM_VARIANTS(X)                         \
+  X(0, "stream_bm16", 16, 32, 32, true, false, 6)        \
+  X(1, "stream_bm32", 32, 32, 64, false, false, 3)       \
+  X(2, "stream_bm64", 64, 32, 64, false, false, 2)       \
+  X(3, "stream_bm16_n16", 16, 32, 16, true, false, 6)    \
+  X(4, "stream_bm32_n32", 32, 32, 32, false, false, 3)   \
+  X(5, "stream_bm32_il", 32, 32, 64, true, false, 4)
 
-template <bool GLU>
+constexpr int tile_class(int bm) { return bm == 16 ? 0 : bm == 32 ? 1 : bm == 64 ? 2 : bm == 128 ? 3 : 4; }
+
+template <bool GLU, bool FP8>
 __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   extern __shared__ float smem[];
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
   if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
   switch (v) {
-#define DAMOE_CASE(ID, NAME, BM, BN1, BN2)                                                     \
+#define DAMOE_CASE(ID, NAME, BM, BN1, BN2, IL, NT, D)                                          \
   case ID: {                                                                                   \
     constexpr int BN = GLU ? BN1 : BN2;                                                        \
-    constexpr int CLS = BM == 16 ? 0 : BM == 32 ? 1 : BM == 64 ? 2 : BM == 128 ? 3 : 4;        \
-    if (a.fp8) stream_body<BM, BN, GLU, true>(a, a.tiles.list[CLS], smem);                     \
-    else stream_body<BM, BN, GLU, false>(a, a.tiles.list[CLS], smem);                          \
+    stream_body<BM, BN, GLU, FP8, IL, NT, D>(a, a.tiles.list[tile_class(BM)], smem);          \
     break;                                                                                     \
   }
     DAMOE_STREAM_VARIANTS(DAMOE_CASE)
@@ -237,41 +278,48 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
 }
 
 // a8: y[t] = sum_j w[t][j] out[inv_perm[t*k+j]], summed in slot order in fp32.
+// Grid (T, H / 1024): each thread owns 4 consecutive features of one token and issues the
+// loads of all k slots before summing them.
 __global__ void __launch_bounds__(256) k_reduce(ReduceArgs a) {
   const int t = blockIdx.x;
-  int pos[DAMOE_MAX_K];
-  float gw[DAMOE_MAX_K];
-  for (int j = 0; j < a.k; ++j) {
-    pos[j] = a.inv_perm[(size_t)t * a.k + j];
-    gw[j] = a.w[(size_t)t * a.k + j];
-  }
-  for (int n = threadIdx.x * 4; n < a.H; n += 256 * 4) {
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j = 0; j < a.k; ++j) {
-      if (pos[j] < 0) continue;
-      const float4 o = *reinterpret_cast<const float4*>(a.out + (size_t)pos[j] * a.H + n);
-      s.x += gw[j] * o.x;
-      s.y += gw[j] * o.y;
-      s.z += gw[j] * o.z;
-      s.w += gw[j] * o.w;
+  const int n = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (n >= a.H) return;
+  float4 o[DAMOE_MAX_K];
+  float g[DAMOE_MAX_K];
+#pragma unroll
+  for (int j = 0; j < DAMOE_MAX_K; ++j) {
+    if (j < a.k) {
+      const int p = a.inv_perm[(size_t)t * a.k + j];
+      g[j] = p >= 0 ? a.w[(size_t)t * a.k + j] : 0.f;
+      o[j] = *reinterpret_cast<const float4*>(a.out + (size_t)(p >= 0 ? p : 0) * a.H + n);
+      if (p < 0) o[j] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    uint2 pk;
-    pk.x = f32_to_bf16(s.x) | ((uint32_t)f32_to_bf16(s.y) << 16);
-    pk.y = f32_to_bf16(s.z) | ((uint32_t)f32_to_bf16(s.w) << 16);
-    *reinterpret_cast<uint2*>(a.y + (size_t)t * a.H + n) = pk;
   }
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int j = 0; j < DAMOE_MAX_K; ++j) {
+    if (j < a.k) {
+      s.x += g[j] * o[j].x;
+      s.y += g[j] * o[j].y;
+      s.z += g[j] * o[j].z;
+      s.w += g[j] * o[j].w;
+    }
+  }
+  uint2 pk;
+  pk.x = f32_to_bf16(s.x) | ((uint32_t)f32_to_bf16(s.y) << 16);
+  pk.y = f32_to_bf16(s.z) | ((uint32_t)f32_to_bf16(s.w) << 16);
+  *reinterpret_cast<uint2*>(a.y + (size_t)t * a.H + n) = pk;
 }
 
 const VariantDesc kVariants[] = {
-#define DAMOE_DESC(ID, NAME, BM, BN1, BN2) \
-  {NAME, kStream, BM, BN1, BN2, BM == 16 ? 0 : BM == 32 ? 1 : BM == 64 ? 2 : BM == 128 ? 3 : 4},
+#define DAMOE_DESC(ID, NAME, BM, BN1, BN2, IL, NT, D) {NAME, kStream, BM, BN1, BN2, tile_class(BM)},
     DAMOE_STREAM_VARIANTS(DAMOE_DESC)
 #undef DAMOE_DESC
 };
 
 constexpr size_t max_lds() {
   size_t m = 0;
-#define DAMOE_LDS(ID, NAME, BM, BN1, BN2)                                              \
+#define DAMOE_LDS(ID, NAME, BM, BN1, BN2, IL, NT, D)                                    \
   m = m > (size_t)4 * 2 * BN1 * (BM + LDS_PAD) * 4 ? m : (size_t)4 * 2 * BN1 * (BM + LDS_PAD) * 4; \
   m = m > (size_t)4 * BN2 * (BM + LDS_PAD) * 4 ? m : (size_t)4 * BN2 * (BM + LDS_PAD) * 4;
   DAMOE_STREAM_VARIANTS(DAMOE_LDS)
@@ -286,26 +334,36 @@ const VariantDesc& variant(int32_t v) { return kVariants[v]; }
 size_t gemm_lds_bytes() { return max_lds(); }
 
 hipError_t gemm_set_lds_limits() {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<true>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)gemm_lds_bytes());
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm<false>),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)gemm_lds_bytes());
+  const void* fns[] = {reinterpret_cast<const void*>(&k_gemm<true, false>),
+                       reinterpret_cast<const void*>(&k_gemm<false, false>),
+                       reinterpret_cast<const void*>(&k_gemm<true, true>),
+                       reinterpret_cast<const void*>(&k_gemm<false, true>)};
+  for (const void* f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)gemm_lds_bytes());
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL(k_gemm<true>, dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
+  if (a.fp8)
+    hipLaunchKernelGGL((k_gemm<true, true>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
+  else
+    hipLaunchKernelGGL((k_gemm<true, false>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL(k_gemm<false>, dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
+  if (a.fp8)
+    hipLaunchKernelGGL((k_gemm<false, true>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
+  else
+    hipLaunchKernelGGL((k_gemm<false, false>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_reduce, dim3(a.T), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(k_reduce, dim3(a.T, (a.H + 1023) / 1024), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -1,15 +1,16 @@
-// Routing histogram, Effective Experts, stable expert permutation, token tiles (a2-a4)
-// and the exemplar-matching dispatch kernel (a5).
+// Routing histogram, Effective Experts, stable expert permutation and token tiles (a2-a4),
+// and the exemplar-matching dispatch (a5), either as separate kernels or fused in one.
 //
-// Both kernels run as one 1024-thread workgroup: the inputs are at most a few
-// hundred KB, so a single workgroup that keeps every intermediate in LDS beats
-// a multi-kernel pipeline that would round-trip through HBM between launches.
+// Every kernel here is one 1024-thread workgroup: the inputs are at most a few hundred KB,
+// so a single workgroup that keeps every intermediate in LDS beats a chain of kernels that
+// would round-trip through HBM and pay a launch each.
 #include "common.h"
 
 namespace damoe {
 namespace {
 
 constexpr int kNW = kRouteThreads / kWave;  // 16 waves
+constexpr int kMaxExemplarRegs = 8;  // exemplar entries prefetched per lane (E <= 512)
 
 // ddist:X thresholds of the Effective Experts bucket, X = XN / XD.
 __constant__ uint32_t c_xn[13] = {11, 13, 3, 17, 2, 5, 4, 6, 8, 12, 16, 24, 32};
@@ -20,107 +21,234 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Exclusive scan of one int per thread over the 1024-thread block; returns the exclusive
-// prefix and writes the block total to *total.  `tmp` holds kNW ints.
-__device__ int block_exclusive_scan(int v, int* tmp, int* total) {
+// Exclusive scans of N ints per thread over the 1024-thread block, in one pass: a wave-level
+// shuffle scan, then every thread adds the totals of the waves before it.  `tmp` holds
+// N * kNW ints.  Returns the block totals in tot[].
+template <int N>
+__device__ void block_scan(const int (&v)[N], int (&ex)[N], int (&tot)[N], int* tmp) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int inc = v;
+  int inc[N];
+#pragma unroll
+  for (int c = 0; c < N; ++c) inc[c] = v[c];
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) tmp[w] = inc;
-  __syncthreads();
-  if (w == 0) {
-    int t = lane < kNW ? tmp[lane] : 0;
 #pragma unroll
-    for (int o = 1; o < kNW; o <<= 1) {
-      const int y = __shfl_up(t, o, 64);
-      if (lane >= o) t += y;
+    for (int c = 0; c < N; ++c) {
+      const int y = __shfl_up(inc[c], o, 64);
+      if (lane >= o) inc[c] += y;
     }
-    if (lane < kNW) tmp[lane] = t;  // inclusive wave totals
+  }
+  if (lane == 63)
+#pragma unroll
+    for (int c = 0; c < N; ++c) tmp[c * kNW + w] = inc[c];
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < N; ++c) {
+    int before = 0, all = 0;
+    for (int u = 0; u < kNW; ++u) {
+      const int t = tmp[c * kNW + u];
+      before += u < w ? t : 0;
+      all += t;
+    }
+    ex[c] = before + inc[c] - v[c];
+    tot[c] = all;
   }
   __syncthreads();
-  const int before = w ? tmp[w - 1] : 0;
-  *total = tmp[kNW - 1];
-  __syncthreads();
-  return before + inc - v;
 }
 
-__device__ uint64_t block_sum_u64(uint64_t v, uint64_t* tmp) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+__device__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const uint32_t lo = __shfl_xor((uint32_t)v, o, 64);
     const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
     v += ((uint64_t)hi << 32) | lo;
   }
-  if (lane == 0) tmp[w] = v;
-  __syncthreads();
-  uint64_t s = 0;
-  for (int i = 0; i < kNW; ++i) s += tmp[i];
-  __syncthreads();
-  return s;
+  return v;
 }
 
 struct TileOut {
   int32_t* list[DAMOE_N_TILE_SIZES];
 };
 
-__global__ void __launch_bounds__(kRouteThreads)
-k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, int32_t* __restrict__ counts,
-        int32_t* __restrict__ offsets, int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
-        uint64_t* __restrict__ numden, int32_t* __restrict__ bucket, int32_t* __restrict__ ctrl,
-        TileOut tiles) {
-  __shared__ int s_cnt[DAMOE_MAX_E];
-  __shared__ int s_base[DAMOE_MAX_E];
-  __shared__ uint16_t s_wc[kNW][DAMOE_MAX_E];
-  __shared__ int s_tmp[kNW];
-  __shared__ uint64_t s_tmp64[kNW];
-  __shared__ int s_bad;
+struct DispatchIn {
+  const int32_t* Q;    // [n_ex][E] exemplars of the selected bucket
+  const int32_t* kid;  // [n_ex]
+  int32_t n_ex;
+  int32_t noda;
+  int32_t* variant_id;
+};
 
+struct RouteOut {
+  int32_t* counts;
+  int32_t* offsets;
+  int32_t* perm;
+  int32_t* inv_perm;
+  uint64_t* numden;
+  int32_t* bucket;
+  int32_t* ctrl;
+  TileOut tiles;
+};
+
+struct Smem {
+  int cnt[DAMOE_MAX_E];
+  int base[DAMOE_MAX_E];
+  int sorted[DAMOE_MAX_E];
+  uint16_t wc[kNW][DAMOE_MAX_E];
+  int tmp[(1 + DAMOE_N_TILE_SIZES) * kNW];
+  int qpre[kNW][64 * kMaxExemplarRegs];  // first exemplar of each wave
+  uint64_t tmp64[kNW];
+  long long score[256];
+  int bad;
+};
+
+// a5 on counts already in LDS: rank-sort the histogram in descending order with R threads per
+// expert, score every exemplar as an exact int64 dot product with the sorted vector, and pick
+// the first maximum.  `qpre` holds this wave's first exemplar, prefetched by the caller.
+__device__ void dispatch_core(Smem& sm, int E, int total, const DispatchIn& d, int32_t* ctrl) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int e = tid; e < DAMOE_MAX_E; e += kRouteThreads) s_cnt[e] = 0;
-  for (int i = tid; i < kNW * DAMOE_MAX_E; i += kRouteThreads) (&s_wc[0][0])[i] = 0;
-  if (tid == 0) s_bad = 0;
+  int epad = 64;
+  while (epad < E) epad <<= 1;
+  const int R = kRouteThreads / epad;  // threads per expert, a power of two <= 16
+  const int i = tid / R, j = tid % R;
+  int rank = 0, ci = 0;
+  if (i < E) {
+    ci = sm.cnt[i];
+    for (int q = j; q < E; q += R) {
+      const int cq = sm.cnt[q];
+      rank += (cq > ci) || (cq == ci && q < i);
+    }
+  }
+  for (int o = 1; o < R; o <<= 1) rank += __shfl_xor(rank, o, 64);
+  if (i < E && j == 0) sm.sorted[rank] = ci;
+  __syncthreads();
+  for (int x = w; x < d.n_ex; x += kNW) {
+    long long acc = 0;
+    if (x == w) {
+#pragma unroll
+      for (int m = 0; m < kMaxExemplarRegs; ++m) {
+        const int r = lane + 64 * m;
+        if (r < E) acc += (long long)sm.sorted[r] * sm.qpre[w][r];
+      }
+      const int32_t* q = d.Q + (size_t)x * E;
+      for (int r = lane + 64 * kMaxExemplarRegs; r < E; r += 64) acc += (long long)sm.sorted[r] * q[r];
+    } else {
+      const int32_t* q = d.Q + (size_t)x * E;
+      for (int r = lane; r < E; r += 64) acc += (long long)sm.sorted[r] * q[r];
+    }
+    acc = (long long)wave_sum_u64((uint64_t)acc);
+    if (lane == 0) sm.score[x] = acc;
+  }
+  __syncthreads();
+  if (w == 0) {
+    long long best = 0;
+    int bi = -1;
+    for (int x = lane; x < d.n_ex; x += 64)
+      if (bi < 0 || sm.score[x] > best) {
+        best = sm.score[x];
+        bi = x;
+      }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t lo = __shfl_xor((uint32_t)(unsigned long long)best, o, 64);
+      const uint32_t hi = __shfl_xor((uint32_t)((unsigned long long)best >> 32), o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      const long long ob = (long long)(((unsigned long long)hi << 32) | lo);
+      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+        best = ob;
+        bi = oi;
+      }
+    }
+    if (lane == 0) {
+      *d.variant_id = total == 0 ? d.noda : d.kid[bi];
+      ctrl[1] = total == 0 ? -1 : bi;
+      const long long sc = total == 0 ? 0 : best;
+      ctrl[2] = (int32_t)(uint32_t)((unsigned long long)sc);
+      ctrl[3] = (int32_t)(uint32_t)((unsigned long long)sc >> 32);
+    }
+  }
+}
+
+template <bool DISPATCH>
+__global__ void __launch_bounds__(kRouteThreads)
+k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, DispatchIn d) {
+  __shared__ Smem sm;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+
+  // The wave's first exemplar is fetched before anything else so its latency hides behind
+  // the histogram; it moves to LDS once the histogram is done.
+  int qpre[kMaxExemplarRegs];
+#pragma unroll
+  for (int m = 0; m < kMaxExemplarRegs; ++m) {
+    const int r = lane + 64 * m;
+    qpre[m] = (DISPATCH && w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
+  }
+  for (int e = tid; e < E; e += kRouteThreads) sm.cnt[e] = 0;
+  if (A > 0)
+    for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wc[x / E][x % E] = 0;
+  if (tid == 0) sm.bad = 0;
   __syncthreads();
 
   // a2: histogram.
   int bad = 0;
   for (int a = tid; a < A; a += kRouteThreads) {
     const int e = ids[a];
-    if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+    if (e >= 0 && e < E) atomicAdd(&sm.cnt[e], 1);
     else ++bad;
   }
-  if (bad) atomicAdd(&s_bad, bad);
+  if (bad) atomicAdd(&sm.bad, bad);
+  if (DISPATCH)
+#pragma unroll
+    for (int m = 0; m < kMaxExemplarRegs; ++m) sm.qpre[w][lane + 64 * m] = qpre[m];
   __syncthreads();
 
-  // Offsets (exclusive scan) and the Effective Experts numerator / denominator.
-  const int c = tid < E ? s_cnt[tid] : 0;
-  int total;
-  const int off = block_exclusive_scan(c, s_tmp, &total);
+  // Offsets, Effective Experts numerator / denominator (a3), and the token-tile counts of
+  // every tile size, all in one scan.
+  const int c = tid < E ? sm.cnt[tid] : 0;
+  int v[1 + DAMOE_N_TILE_SIZES], ex[1 + DAMOE_N_TILE_SIZES], tot[1 + DAMOE_N_TILE_SIZES];
+  v[0] = c;
+#pragma unroll
+  for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) v[1 + cls] = (c + (16 << cls) - 1) / (16 << cls);
+  const uint64_t sq = wave_sum_u64((uint64_t)c * (uint64_t)c);
+  if (lane == 0) sm.tmp64[w] = sq;
+  block_scan<1 + DAMOE_N_TILE_SIZES>(v, ex, tot, sm.tmp);
+  const int off = ex[0], total = tot[0];
   if (tid < E) {
-    counts[tid] = c;
-    offsets[tid] = off;
-    s_base[tid] = off;
+    o.counts[tid] = c;
+    o.offsets[tid] = off;
+    sm.base[tid] = off;
   }
-  if (tid == 0) offsets[E] = total;
-  const uint64_t sq = block_sum_u64((uint64_t)c * (uint64_t)c, s_tmp64);
   if (tid == 0) {
+    o.offsets[E] = total;
+    uint64_t den = 0;
+    for (int u = 0; u < kNW; ++u) den += sm.tmp64[u];
     const uint64_t num = (uint64_t)total * (uint64_t)total;
-    numden[0] = num;
-    numden[1] = sq;
+    o.numden[0] = num;
+    o.numden[1] = den;
     int b = -1;
-    if (sq != 0) {
+    if (den != 0) {
       b = 0;
-      for (int j = 0; j < 13; ++j)
-        if (num * c_xn[j] <= (uint64_t)E * c_xd[j] * sq) ++b;
+      for (int jx = 0; jx < 13; ++jx)
+        if (num * c_xn[jx] <= (uint64_t)E * c_xd[jx] * den) ++b;
     }
-    *bucket = b;
-    if (s_bad) atomicOr(&ctrl[0], DAMOE_DEVERR_EXPERT_ID);
+    *o.bucket = b;
+    if (sm.bad) atomicOr(&o.ctrl[0], DAMOE_DEVERR_EXPERT_ID);
   }
-  __syncthreads();
+#pragma unroll
+  for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
+    const int bm = 16 << cls;
+    int32_t* list = o.tiles.list[cls];
+    if (tid == 0) {
+      list[0] = tot[1 + cls];
+      list[1] = 0;
+    }
+    int2* ent = reinterpret_cast<int2*>(list + 2);
+    for (int jt = 0; jt < v[1 + cls]; ++jt) {
+      const int rows = min(bm, c - jt * bm);
+      ent[ex[1 + cls] + jt] = make_int2(off + jt * bm, tid | (rows << 16));
+    }
+  }
+
+  if (DISPATCH) dispatch_core(sm, E, total, d, o.ctrl);
 
   // a4: stable scatter, one 1024-assignment chunk at a time.  Within a wave the rank among
   // equal experts comes from ballot-based multisplit; across waves from per-wave counts.
@@ -131,100 +259,51 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, int32_t* __restri
     const int e = a < A ? ids[a] : -1;
     const bool valid = e >= 0 && e < E;
     uint64_t peers = __ballot(valid);
-    for (int b = 0; b < nbits; ++b) {
-      const uint64_t m = __ballot(valid && ((e >> b) & 1));
-      peers &= ((e >> b) & 1) ? m : ~m;
+    for (int bt = 0; bt < nbits; ++bt) {
+      const uint64_t m = __ballot(valid && ((e >> bt) & 1));
+      peers &= ((e >> bt) & 1) ? m : ~m;
     }
     const int rank = __popcll(peers & lanemask_lt());
-    if (valid && rank == 0) s_wc[w][e] = (uint16_t)__popcll(peers);
+    if (valid && rank == 0) sm.wc[w][e] = (uint16_t)__popcll(peers);
     __syncthreads();
     if (valid) {
-      int p = s_base[e] + rank;
-      for (int v = 0; v < w; ++v) p += s_wc[v][e];
-      perm[p] = a;
-      inv_perm[a] = p;
+      int p = sm.base[e] + rank;
+      for (int u = 0; u < w; ++u) p += sm.wc[u][e];
+      o.perm[p] = a;
+      o.inv_perm[a] = p;
     } else if (a < A) {
-      inv_perm[a] = -1;
+      o.inv_perm[a] = -1;
     }
-    __syncthreads();
-    if (tid < E) {
-      int s = 0;
-      for (int v = 0; v < kNW; ++v) {
-        s += s_wc[v][tid];
-        s_wc[v][tid] = 0;
+    if (a0 + kRouteThreads < A) {
+      __syncthreads();
+      if (tid < E) {
+        int s = 0;
+        for (int u = 0; u < kNW; ++u) {
+          s += sm.wc[u][tid];
+          sm.wc[u][tid] = 0;
+        }
+        sm.base[tid] += s;
       }
-      s_base[tid] += s;
-    }
-    __syncthreads();
-  }
-
-  // Token tiles of every tile size: expert-major, ceil(t_e / BM) tiles per expert.
-  for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
-    const int bm = 16 << cls;
-    const int nt = (c + bm - 1) / bm;
-    int ntot;
-    const int t0 = block_exclusive_scan(nt, s_tmp, &ntot);
-    int32_t* list = tiles.list[cls];
-    if (tid == 0) {
-      list[0] = ntot;
-      list[1] = 0;
-    }
-    int2* ent = reinterpret_cast<int2*>(list + 2);
-    for (int j = 0; j < nt; ++j) {
-      const int rows = min(bm, c - j * bm);
-      ent[t0 + j] = make_int2(off + j * bm, tid | (rows << 16));
+      __syncthreads();
     }
   }
 }
 
-// a5: sort the histogram (descending), score every exemplar of the bucket by its exact integer
-// dot product with the sorted histogram, and write the variant of the first best exemplar.
+// a5 on its own: counts from device memory.
 __global__ void __launch_bounds__(kRouteThreads)
-k_dispatch(const int32_t* __restrict__ counts, int32_t E, const int32_t* __restrict__ Q,
-           const int32_t* __restrict__ kid, int32_t n_ex, int32_t noda,
-           int32_t* __restrict__ variant_id, int32_t* __restrict__ ctrl) {
-  __shared__ int s_c[DAMOE_MAX_E];
-  __shared__ int s_sorted[DAMOE_MAX_E];
-  __shared__ long long s_score[256];
-  __shared__ int s_tmp[kNW];
+k_dispatch(const int32_t* __restrict__ counts, int32_t E, DispatchIn d, int32_t* __restrict__ ctrl) {
+  __shared__ Smem sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c = tid < E ? counts[tid] : 0;
-  if (tid < E) s_c[tid] = c;
-  int total;
-  block_exclusive_scan(c, s_tmp, &total);  // also a barrier for s_c
-  if (tid < E) {
-    // Rank in descending order; ties keep index order (any order gives the same sorted vector).
-    int r = 0;
-    for (int j = 0; j < E; ++j) {
-      const int cj = s_c[j];
-      r += (cj > c) || (cj == c && j < tid);
-    }
-    s_sorted[r] = c;
-  }
-  __syncthreads();
-  for (int i = w; i < n_ex; i += kNW) {
-    const int32_t* q = Q + (size_t)i * E;
-    long long acc = 0;
-    for (int r = lane; r < E; r += 64) acc += (long long)s_sorted[r] * q[r];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint32_t lo = __shfl_xor((uint32_t)acc, o, 64);
-      const uint32_t hi = __shfl_xor((uint32_t)((unsigned long long)acc >> 32), o, 64);
-      acc += (long long)(((unsigned long long)hi << 32) | lo);
-    }
-    if (lane == 0) s_score[i] = acc;
+  for (int m = 0; m < kMaxExemplarRegs; ++m) {
+    const int r = lane + 64 * m;
+    sm.qpre[w][r] = (w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
   }
-  __syncthreads();
-  if (tid == 0) {
-    int best = 0;
-    for (int i = 1; i < n_ex; ++i)
-      if (s_score[i] > s_score[best]) best = i;
-    *variant_id = total == 0 ? noda : kid[best];
-    ctrl[1] = total == 0 ? -1 : best;
-    const long long sc = total == 0 ? 0 : s_score[best];
-    ctrl[2] = (int32_t)(uint32_t)((unsigned long long)sc);
-    ctrl[3] = (int32_t)(uint32_t)((unsigned long long)sc >> 32);
-  }
+  const int c = tid < E ? counts[tid] : 0;
+  if (tid < E) sm.cnt[tid] = c;
+  int v[1] = {c}, ex[1], tot[1];
+  block_scan<1>(v, ex, tot, sm.tmp);
+  dispatch_core(sm, E, tot[0], d, ctrl);
 }
 
 }  // namespace
@@ -232,19 +311,24 @@ k_dispatch(const int32_t* __restrict__ counts, int32_t E, const int32_t* __restr
 hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
                         int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                         int32_t* bucket, int32_t* ctrl,
-                        int32_t* const tile_lists[DAMOE_N_TILE_SIZES], hipStream_t stream) {
-  TileOut t;
-  for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) t.list[i] = tile_lists[i];
-  hipLaunchKernelGGL(k_route, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, counts,
-                     offsets, perm, inv_perm, numden, bucket, ctrl, t);
+                        int32_t* const tile_lists[DAMOE_N_TILE_SIZES], const DispatchArgs* dispatch,
+                        hipStream_t stream) {
+  RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}};
+  for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) o.tiles.list[i] = tile_lists[i];
+  if (dispatch) {
+    DispatchIn d{dispatch->Q, dispatch->kid, dispatch->n_ex, dispatch->noda, dispatch->variant_id};
+    hipLaunchKernelGGL(k_route<true>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
+  } else {
+    hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o,
+                       DispatchIn{});
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_dispatch(const int32_t* counts, int32_t E, const int32_t* Q, const int32_t* kid,
-                           int32_t n_ex, int32_t noda, int32_t* variant_id, int32_t* ctrl,
+hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
                            hipStream_t stream) {
-  hipLaunchKernelGGL(k_dispatch, dim3(1), dim3(kRouteThreads), 0, stream, counts, E, Q, kid, n_ex,
-                     noda, variant_id, ctrl);
+  DispatchIn d{dispatch.Q, dispatch.kid, dispatch.n_ex, dispatch.noda, dispatch.variant_id};
+  hipLaunchKernelGGL(k_dispatch, dim3(1), dim3(kRouteThreads), 0, stream, counts, E, d, ctrl);
   return hipGetLastError();
 }
 

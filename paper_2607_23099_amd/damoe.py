@@ -27,7 +27,7 @@ EXPORTED = [
     "damoe_table_create", "damoe_table_destroy", "damoe_table_info", "damoe_table_save",
     "damoe_table_load", "damoe_dispatch", "damoe_fused_moe", "damoe_num_variants", "damoe_variant_name",
     "damoe_variant_tile_m", "damoe_variant_supports", "damoe_tune", "damoe_alpha_search",
-    "damoe_read_device_error", "damoe_fused_moe_stage",
+    "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch",
 ]
 
 
@@ -88,6 +88,7 @@ def lib() -> ctypes.CDLL:
             "damoe_table_save": ([vp, ctypes.c_char_p], i32),
             "damoe_table_load": ([ctypes.c_char_p, vp], i32),
             "damoe_dispatch": ([vp, vp, i32, vp, vp, sz, vp], i32),
+            "damoe_route_dispatch": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
             "damoe_fused_moe": ([vp, vp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
             "damoe_fused_moe_stage": ([vp, i32, vp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
             "damoe_num_variants": ([], i32),
@@ -173,6 +174,13 @@ def route_histogram(ids, T, k, E, counts, offsets, perm, inv_perm, numden, bucke
     _check("damoe_route_histogram", lib().damoe_route_histogram(
         _p(ids), T, k, E, _p(counts), _p(offsets), _p(perm), _p(inv_perm), _p(numden), _p(bucket),
         _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def route_dispatch(table: "Table", ids, T, k, E, counts, offsets, perm, inv_perm, numden, bucket,
+                   variant_id, ws, stream=None):
+    _check("damoe_route_dispatch", lib().damoe_route_dispatch(
+        table.handle, _p(ids), T, k, E, _p(counts), _p(offsets), _p(perm), _p(inv_perm), _p(numden),
+        _p(bucket), _p(variant_id), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def dispatch(table: "Table", counts, T, variant_id, ws, stream=None):

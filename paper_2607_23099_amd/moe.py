@@ -84,6 +84,11 @@ class Path:
         damoe.route_histogram(self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
                               self.perm, self.inv_perm, self.numden, self.bucket, self.ws, stream)
 
+    def route_dispatch(self, table: damoe.Table, T: int, ids=None, stream=None):
+        sh = self.dl.shape
+        damoe.route_dispatch(table, self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
+                             self.perm, self.inv_perm, self.numden, self.bucket, self.variant, self.ws, stream)
+
     def dispatch(self, table: damoe.Table, T: int, stream=None):
         damoe.dispatch(table, self.counts, T, self.variant, self.ws, stream)
 

@@ -13,16 +13,16 @@ def _variants():
 
 
 def _run(path, r, x_tag, variant=None, table=None):
+    """One layer call: route (+ dispatch when a table is given) and the fused computation."""
     torch = torch_cuda()
-    from paper_2607_23099_amd.moe import Path  # noqa: F401
     path.set_routing(r)
     path.fill_x(r.T, x_tag)
     path.y.fill_(float("nan"))
-    path.route(r.T)
     if table is not None:
-        path.dispatch(table, r.T)
+        path.route_dispatch(table, r.T)
         path.fused(r.T, -1)
     else:
+        path.route(r.T)
         path.fused(r.T, variant)
     torch.cuda.synchronize()
 

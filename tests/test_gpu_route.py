@@ -160,6 +160,24 @@ def test_dispatch_matches_oracle(E):
         ctrl = ws[:16].view(torch.int32).cpu().numpy()
         assert ctrl[1] == i
         assert int(np.array(ctrl[2:4], np.int32).view(np.int64)[0]) == scores[i]
+    # The fused route + dispatch call gives the same histogram, permutation and choice.
+    for step in range(20):
+        T = int(np.floor(np.exp(rng.uniform(0, np.log(4096)))))
+        alpha = float(np.exp(rng.uniform(np.log(0.03), np.log(10))))
+        r = synth.routing(E, 8, T, alpha, [79, step])
+        b = RouteBufs(torch, E, 8, T)
+        b.ids.copy_(torch.from_numpy(r.ids.ravel().copy()))
+        vid2 = torch.full((1,), -9, dtype=torch.int32, device="cuda")
+        damoe.route_dispatch(table, b.ids, T, 8, E, b.counts, b.offsets, b.perm, b.inv, b.nd, b.bucket, vid2,
+                             b.ws)
+        torch.cuda.synchronize()
+        _check_route(b, r.ids)
+        c = oracle.histogram(r.ids, E)
+        rows = td.bucket_rows(oracle.select_bucket(td.bucket_T, T))
+        i, scores = oracle.match(c, td.Q[rows])
+        assert int(vid2.item()) == int(td.kid[rows][i]), (step, T)
+        ctrl = b.ws[:16].view(torch.int32).cpu().numpy()
+        assert ctrl[1] == i and int(np.array(ctrl[2:4], np.int32).view(np.int64)[0]) == scores[i]
     # No tokens -> the bucket's noda variant.
     counts.zero_()
     damoe.dispatch(table, counts, 0, vid, ws)
