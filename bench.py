@@ -72,7 +72,7 @@ def cpu_baseline(shape, T, alpha):
                       "weight generation excluded"}
 
 
-def load_or_tune_table(dl, x, quick):
+def load_or_tune_table(dl, x, quick, buckets=DECODE_T):
     from paper_2607_23099_amd import damoe
     path = os.path.join(TABLE_DIR, f"{dl.shape.name}.damoe")
     if os.path.exists(path) and not quick:
@@ -81,9 +81,111 @@ def load_or_tune_table(dl, x, quick):
         except damoe.DamoeError as e:
             log(f"table {path} unusable ({e}); tuning a quick one")
     t0 = time.perf_counter()
-    table = damoe.tune(dl.layer, list(DECODE_T), EXTENDED_SKEWS, x, samples=3, reps=3, alpha_samples=32,
+    table = damoe.tune(dl.layer, list(buckets), EXTENDED_SKEWS, x, samples=3, reps=3, alpha_samples=32,
                        alpha_iters=50, seed=0x7AB1E)
     return table, f"quick-tuned at start-up in {time.perf_counter() - t0:.1f} s (S=3, reps=3)"
+
+
+def run_trace(args):
+    """Dispatch trace on the Kimi-K2 shape: adaptive vs per-step best vs static buckets."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+
+    shape = synth.KIMI
+    T_MAX = 8192
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    dl = DeviceLayer(shape)
+    path = Path(dl, T_MAX)
+    path.fill_x(T_MAX, 4)
+    torch.cuda.synchronize()
+    table, note = load_or_tune_table(dl, path.x, args.quick_tune, [2 ** i for i in range(14)])
+    log(f"dispatch table: {note}")
+    td = table.data(shape.E)
+    nv = damoe.num_variants()
+    V = [v for v in range(nv) if damoe.variant_supports(v, dl.wdtype)]
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    steps = []
+    t_start = time.perf_counter()
+    for s in range(args.trace_steps):
+        T, alpha = synth.trace_step_params(s, T_MAX)
+        r = synth.routing(shape.E, shape.k, T, alpha, synth.seed_trace_step(s))
+        path.set_routing(r)
+        # one untimed pass of every configuration, then reps timed passes
+        runs = {}
+        for rep in range(args.trace_reps + 1):
+            for v in V + [-1]:
+                e0, e1 = ev(), ev()
+                e0.record(stream)
+                if v < 0:
+                    path.route_dispatch(table, T)
+                else:
+                    path.route(T)
+                path.fused(T, v)
+                e1.record(stream)
+                if rep:
+                    runs.setdefault(v, []).append((e0, e1))
+        torch.cuda.synchronize()
+        lat = {v: float(np.median([a.elapsed_time(b) for a, b in runs[v]])) * 1e3 for v in runs}
+        chosen = int(path.variant.item())
+        b = next((i for i, bt in enumerate(td.bucket_T) if T <= bt), len(td.bucket_T) - 1)
+        steps.append({"T": T, "alpha": alpha, "bucket": b, "chosen": chosen,
+                      "adaptive": lat[-1], "lat": [lat[v] for v in V]})
+        if (s + 1) % 50 == 0:
+            log(f"trace step {s + 1}/{args.trace_steps} ({time.perf_counter() - t_start:.0f} s)")
+    # Derived baselines from the one latency matrix.
+    L = np.array([st["lat"] for st in steps])            # [steps][variants]
+    A = np.array([st["adaptive"] for st in steps])
+    B = np.array([st["bucket"] for st in steps])
+    step_best = L.min(axis=1)
+    noda = np.array([L[i, V.index(int(td.noda[B[i]]))] for i in range(len(steps))])
+    static = np.zeros(len(steps))
+    static_choice = {}
+    for b in sorted(set(B.tolist())):
+        idx = np.where(B == b)[0]
+        gm = [np.exp(np.mean(np.log(L[idx, j]))) for j in range(len(V))]
+        j = int(np.argmin(gm))
+        static_choice[int(td.bucket_T[b])] = damoe.variant_name(V[j])
+        static[idx] = L[idx, j]
+    g = lambda x: float(np.exp(np.mean(np.log(x))))
+    per_bucket = {}
+    for b in sorted(set(B.tolist())):
+        idx = np.where(B == b)[0]
+        per_bucket[int(td.bucket_T[b])] = {
+            "steps": int(len(idx)),
+            "adaptive_pct_of_step_best": round(100 * g(A[idx] / step_best[idx]), 1),
+            "best_static_pct_of_step_best": round(100 * g(static[idx] / step_best[idx]), 1),
+            "noda_pct_of_step_best": round(100 * g(noda[idx] / step_best[idx]), 1),
+        }
+    picked_best = float(np.mean([V[int(np.argmin(st["lat"]))] == st["chosen"] for st in steps]))
+    out = {
+        "metric": "geomean dispatch speedup over the best static token-count bucket (Kimi-K2 trace)",
+        "value": round(g(static / A), 4),
+        "unit": "x",
+        "n_gpus": 1,
+        "steps": len(steps),
+        "warmup": 1,
+        "ms_per_step": round(float(np.mean(A)) / 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"kimi-k2 dispatch trace: E=384 top-8 H=7168 I=2048 bf16, {len(steps)} steps, "
+                               "T log-uniform in [1,8192], Dirichlet alpha log-uniform in [0.03,10]",
+                   "table": note, "variants": [damoe.variant_name(v) for v in V]},
+        "speedup_vs_noda": round(g(noda / A), 4),
+        "adaptive_over_step_best": round(g(A / step_best), 4),
+        "best_static_over_step_best": round(g(static / step_best), 4),
+        "chose_step_best_fraction": round(picked_best, 3),
+        "best_static_choice": static_choice,
+        "per_bucket": per_bucket,
+    }
+    with open(os.path.join(ROOT, "gpurun_out", "trace_steps.json") if os.path.isdir(os.path.join(ROOT, "gpurun_out"))
+              else os.devnull, "w") as f:
+        json.dump(steps, f)
+    print(json.dumps(out), flush=True)
 
 
 def main():
@@ -94,6 +196,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
+    ap.add_argument("--workload", choices=["decode-sweep", "trace"], default="decode-sweep")
+    ap.add_argument("--trace-steps", type=int, default=1000)
+    ap.add_argument("--trace-reps", type=int, default=3)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -109,6 +214,8 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a ROCm GPU")
     damoe.lib()  # fails loudly if the HIP library is not built
+    if args.workload == "trace":
+        return run_trace(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")

@@ -76,7 +76,7 @@ typedef enum damoe_wdtype {
  * (Sec. II-A).  Weights of expert e are contiguous slabs:
  *   w1, w3: [E][I][H]   w2: [E][H][I]   (bf16, or e4m3 bytes for DAMOE_W_FP8_B128)
  *   s1, s3: [E][I/128][H/128]  s2: [E][H/128][I/128]  fp32 block scales (fp8 only,
- *   NULL otherwise).  H and I must be multiples of 128. */
+ *   NULL otherwise).  H and I must be multiples of 128 (of 512 for fp8 weights). */
 typedef struct damoe_layer {
   int32_t E, k, H, I;
   int32_t wdtype; /* damoe_wdtype */

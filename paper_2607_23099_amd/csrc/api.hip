@@ -50,7 +50,7 @@ damoe_status check_layer(const damoe_layer* L) {
   if (!L) return DAMOE_ERR_INVALID_ARG;
   if (!shape_ok(L->E, L->k)) return DAMOE_ERR_INVALID_ARG;
   if (L->H <= 0 || L->I <= 0) return DAMOE_ERR_INVALID_ARG;
-  if (L->H % 128 || L->I % 128) return DAMOE_ERR_UNSUPPORTED;
+  if (L->H % 128 || L->I % 128) return DAMOE_ERR_UNSUPPORTED;  // whole feature blocks of every variant
   if (!L->w1 || !L->w3 || !L->w2) return DAMOE_ERR_INVALID_ARG;
   if (L->wdtype == DAMOE_W_BF16) return DAMOE_OK;
   if (L->wdtype == DAMOE_W_FP8_B128) {

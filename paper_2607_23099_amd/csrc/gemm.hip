@@ -247,6 +247,204 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
   }
 }
 
+
+// Tiled variants (large token counts): the 4 waves split the output features.  Each wave
+// streams NRW row blocks of 16 weight rows straight from memory into MFMA A-operands, as the
+// stream variants do, while the item's BM = 128 gathered token rows are staged in LDS in
+// 128-wide K stages (double-buffered, the next stage moving in two halves during the current
+// one) and shared by the 4 waves.  With NRW = 2 a wave reads 1/32 B of LDS per FLOP.  The
+// token tile in LDS is row-major, 256 B per row, with its 16-byte chunks XOR-swizzled by
+// (row & 15) so that both the cooperative stores and the MFMA operand reads hit 64 distinct
+// banks.  Item = (tile of up to 128 tokens of one expert, 64 features of GEMM1 / 128 rows of
+// GEMM2).
+constexpr int kTiledBM = 128;
+constexpr int kTiledBK = 128;
+constexpr int kTiledNRW = 2;
+constexpr size_t kTiledLds = 2 * (size_t)kTiledBM * kTiledBK * 2;  // 64 KB
+
+template <bool GLU, bool FP8, int D>
+__device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __restrict__ list,
+                                           uint8_t* __restrict__ lds) {
+  constexpr int BM = kTiledBM, NRW = kTiledNRW, NX = BM / 16;
+  constexpr int ROWS_PER_ITEM = 4 * NRW * 16;               // weight rows per workgroup item
+  constexpr int FEAT = GLU ? ROWS_PER_ITEM / 2 : ROWS_PER_ITEM;  // output features per item
+  static_assert(4 % D == 0, "ring depth must divide the 4 k-steps of a stage");
+  using WT = typename WFrag<FP8>::T;
+  constexpr int EB = WFrag<FP8>::kBytesPerElem;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n_tiles = list[0];
+  const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
+  const int K = a.K, N = a.N;
+  const int n_fb = N / FEAT;
+  const long long n_items = (long long)n_tiles * n_fb;
+  const int nst = K / kTiledBK;  // K stages
+  const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
+  const uint8_t* __restrict__ wb = reinterpret_cast<const uint8_t*>(a.wb);
+  // Cooperative token staging: thread t moves chunk (t & 15) of rows (t >> 4) + 16 i.
+  const int sc = tid & 15, sr = tid >> 4;
+  // MFMA operand read: lane l reads row s*16 + (l & 15), logical chunk kk*4 + (l >> 4).
+  const int rl = lane & 15, gl = lane >> 4;
+
+  for (long long it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int tile = (int)(it / n_fb);
+    const int fb = (int)(it - (long long)tile * n_fb);
+    const int2 en = ent[tile];
+    const int p0 = en.x, e = en.y & 0xFFFF, rows = en.y >> 16;
+    if (p0 < 0 || rows <= 0 || rows > BM || p0 + rows > a.A || e >= a.E) {
+      if (tid == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
+      continue;
+    }
+    // Token rows this thread stages (byte offsets in x / h; padding rows read as zero).
+    __amdgpu_buffer_rsrc_t rx;
+    if (GLU) rx = make_rsrc(a.x, (uint32_t)((size_t)(a.A / a.k) * K * 2));
+    else rx = make_rsrc(a.x + (size_t)p0 * K, (uint32_t)((size_t)rows * K * 2));
+    uint32_t xo[NX];
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const int r = sr + 16 * i;
+      if (r < rows) {
+        const uint32_t row = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) : (uint32_t)r;
+        xo[i] = row * (uint32_t)K * 2u + sc * 16u;
+      } else {
+        xo[i] = kOobOffset;
+      }
+    }
+    // Weight rows of this wave.
+    const size_t slab = (size_t)N * K * EB;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(wa + (size_t)e * slab, (uint32_t)slab);
+    const __amdgpu_buffer_rsrc_t rbk = make_rsrc((GLU ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
+    uint32_t wo[NRW];
+#pragma unroll
+    for (int b = 0; b < NRW; ++b) {
+      int f;
+      if (GLU) f = fb * FEAT + wave * (NRW / 2) * 16 + (b % (NRW / 2)) * 16 + rl;
+      else f = fb * FEAT + wave * NRW * 16 + b * 16 + rl;
+      wo[b] = ((uint32_t)f * (uint32_t)K + gl * 8) * EB;
+    }
+    const int sk = K / 128;
+    const int srow = (fb * FEAT + (GLU ? 0 : wave * NRW * 16)) / 128;
+    const size_t sbase = ((size_t)e * (N / 128) + srow) * sk;
+
+    floatx4 acc[NRW][NX];
+#pragma unroll
+    for (int b = 0; b < NRW; ++b)
+#pragma unroll
+      for (int s = 0; s < NX; ++s) acc[b][s] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    // The next K stage moves in two halves of NX/2 rows per thread, loaded during the
+    // current stage's k-steps 0 and 2 and stored at k-steps 2 and the stage's end.
+    constexpr int NH = NX / 2;
+    auto stage_load = [&](int st, int half, uint4 (&buf)[NH]) __attribute__((always_inline)) {
+      const uint32_t soff = (uint32_t)st * kTiledBK * 2;
+#pragma unroll
+      for (int i = 0; i < NH; ++i) buf[i] = buf_load<uint4, 0>(rx, xo[half * NH + i], soff);
+    };
+    auto stage_store = [&](int slot, int half, const uint4 (&buf)[NH]) __attribute__((always_inline)) {
+      uint8_t* base = lds + (size_t)slot * BM * kTiledBK * 2;
+#pragma unroll
+      for (int i = 0; i < NH; ++i) {
+        const int r = sr + 16 * (half * NH + i);
+        *reinterpret_cast<uint4*>(base + r * 256 + ((sc ^ (r & 15)) * 16)) = buf[i];
+      }
+    };
+    WT wf[D][NRW];
+    auto wload = [&](int ks, int slot) __attribute__((always_inline)) {
+      const uint32_t sw = (uint32_t)ks * 32 * EB;
+#pragma unroll
+      for (int b = 0; b < NRW; ++b)
+        wf[slot][b] = buf_load<WT, 0>((GLU && b >= NRW / 2) ? rbk : ra, wo[b], sw);
+    };
+
+    // Prologue: token stage 0 into LDS slot 0, weight k-steps 0 .. D-2 in flight.
+    {
+      uint4 buf[NH];
+      stage_load(0, 0, buf);
+      stage_store(0, 0, buf);
+      stage_load(0, 1, buf);
+      stage_store(0, 1, buf);
+    }
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) wload(min(d, 4 * nst - 1), d);
+    __syncthreads();
+
+    for (int st = 0; st < nst; ++st) {
+      uint4 nbuf[NH];
+      const bool more = st + 1 < nst;
+      const uint8_t* cur = lds + (size_t)(st & 1) * BM * kTiledBK * 2;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int ks = st * 4 + kk;
+        if (more && kk == 0) stage_load(st + 1, 0, nbuf);
+        if (more && kk == 2) {
+          stage_store((st + 1) & 1, 0, nbuf);
+          stage_load(st + 1, 1, nbuf);
+        }
+        wload(min(ks + D - 1, 4 * nst - 1), (kk + D - 1) % D);
+        uint4 wv[NRW];
+        if constexpr (FP8) {
+          const int kb = ks >> 2;
+          const float s_g = a.sa[sbase + kb] * 0x1p120f;
+          const float s_u = GLU ? a.sb[sbase + kb] * 0x1p120f : 0.f;
+          float s_r[NRW];
+          if (!GLU) {
+            // GEMM2: a wave's 64 rows lie in one 128-row scale block.
+#pragma unroll
+            for (int b = 0; b < NRW; ++b) s_r[b] = s_g;
+          }
+#pragma unroll
+          for (int b = 0; b < NRW; ++b)
+            wv[b] = fp8x8_to_bf16x8(wf[kk % D][b], GLU ? ((b >= NRW / 2) ? s_u : s_g) : s_r[b]);
+        } else {
+#pragma unroll
+          for (int b = 0; b < NRW; ++b) wv[b] = wf[kk % D][b];
+        }
+#pragma unroll
+        for (int s = 0; s < NX; ++s) {
+          const int r = s * 16 + rl;
+          const uint4 tf =
+              *reinterpret_cast<const uint4*>(cur + r * 256 + (((kk * 4 + gl) ^ rl) * 16));
+#pragma unroll
+          for (int b = 0; b < NRW; ++b) acc[b][s] = mfma16x16x32(wv[b], tf, acc[b][s]);
+        }
+      }
+      if (more) stage_store((st + 1) & 1, 1, nbuf);
+      __syncthreads();
+    }
+
+    // Epilogue straight from the accumulators: lane (l) holds features 4*(l/16) .. +3 of
+    // token l%16 in every 16x16 block.
+#pragma unroll
+    for (int s = 0; s < NX; ++s) {
+      const int i = s * 16 + rl;
+      if (i >= rows) continue;
+      const size_t orow = (size_t)(p0 + i) * N;
+      if (GLU) {
+#pragma unroll
+        for (int b = 0; b < NRW / 2; ++b) {
+          const int f = fb * FEAT + wave * (NRW / 2) * 16 + b * 16 + 4 * gl;
+          float hv[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float g = acc[b][s][r], u = acc[b + NRW / 2][s][r];
+            hv[r] = g / (1.0f + __expf(-g)) * u;
+          }
+          uint2 pk;
+          pk.x = pack_bf16x2(hv[0], hv[1]);
+          pk.y = pack_bf16x2(hv[2], hv[3]);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < NRW; ++b) {
+          const int f = fb * FEAT + wave * NRW * 16 + b * 16 + 4 * gl;
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
+              make_float4(acc[b][s][0], acc[b][s][1], acc[b][s][2], acc[b][s][3]);
+        }
+      }
+    }
+  }
+}
+
 // The registry.  Indices are the public variant ids: (id, name, BM, BN1, BN2, IL, NT, D).
 #define DAMOE_STREAM_VARIANTS(X)                         \
   X(0, "stream_bm16", 16, 32, 32, true, false, 6)        \
@@ -255,6 +453,10 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
   X(3, "stream_bm16_n16", 16, 32, 16, true, false, 6)    \
   X(4, "stream_bm32_n32", 32, 32, 32, false, false, 3)   \
   X(5, "stream_bm32_il", 32, 32, 64, true, false, 4)
+
+// Tiled variants: (id, name, ring depth D); token tile BM = 128.
+#define DAMOE_TILED_VARIANTS(X) \
+  X(6, "tiled_bm128", 2)
 
 constexpr int tile_class(int bm) { return bm == 16 ? 0 : bm == 32 ? 1 : bm == 64 ? 2 : bm == 128 ? 3 : 4; }
 
@@ -272,6 +474,12 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   }
     DAMOE_STREAM_VARIANTS(DAMOE_CASE)
 #undef DAMOE_CASE
+#define DAMOE_TCASE(ID, NAME, D)                                                               \
+  case ID:                                                                                     \
+    tiled_body<GLU, FP8, D>(a, a.tiles.list[tile_class(kTiledBM)], reinterpret_cast<uint8_t*>(smem)); \
+    break;
+    DAMOE_TILED_VARIANTS(DAMOE_TCASE)
+#undef DAMOE_TCASE
     default:
       break;
   }
@@ -315,6 +523,9 @@ const VariantDesc kVariants[] = {
 #define DAMOE_DESC(ID, NAME, BM, BN1, BN2, IL, NT, D) {NAME, kStream, BM, BN1, BN2, tile_class(BM)},
     DAMOE_STREAM_VARIANTS(DAMOE_DESC)
 #undef DAMOE_DESC
+#define DAMOE_TDESC(ID, NAME, D) {NAME, kTiled, kTiledBM, kTiledNRW * 16 * 2, kTiledNRW * 16 * 4, tile_class(kTiledBM)},
+    DAMOE_TILED_VARIANTS(DAMOE_TDESC)
+#undef DAMOE_TDESC
 };
 
 constexpr size_t max_lds() {
@@ -324,6 +535,7 @@ constexpr size_t max_lds() {
   m = m > (size_t)4 * BN2 * (BM + LDS_PAD) * 4 ? m : (size_t)4 * BN2 * (BM + LDS_PAD) * 4;
   DAMOE_STREAM_VARIANTS(DAMOE_LDS)
 #undef DAMOE_LDS
+  m = m > kTiledLds ? m : kTiledLds;
   return m;
 }
 

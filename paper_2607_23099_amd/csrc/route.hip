@@ -11,6 +11,7 @@ namespace {
 
 constexpr int kNW = kRouteThreads / kWave;  // 16 waves
 constexpr int kMaxExemplarRegs = 8;  // exemplar entries prefetched per lane (E <= 512)
+constexpr int kValueBins = 4096;     // counting sort of the histogram when every count is smaller
 
 // ddist:X thresholds of the Effective Experts bucket, X = XN / XD.
 __constant__ uint32_t c_xn[13] = {11, 13, 3, 17, 2, 5, 4, 6, 8, 12, 16, 24, 32};
@@ -98,28 +99,66 @@ struct Smem {
   int qpre[kNW][64 * kMaxExemplarRegs];  // first exemplar of each wave
   uint64_t tmp64[kNW];
   long long score[256];
+  int vh[kValueBins];  // value histogram of the counts, then start positions
   int bad;
 };
 
-// a5 on counts already in LDS: rank-sort the histogram in descending order with R threads per
-// expert, score every exemplar as an exact int64 dot product with the sorted vector, and pick
-// the first maximum.  `qpre` holds this wave's first exemplar, prefetched by the caller.
+// a5 on counts already in LDS: sort the histogram in descending order, score every exemplar
+// as an exact int64 dot product with the sorted vector, and pick the first maximum.
+// The sort is a counting sort over count values (every count < kValueBins, always the case
+// for T < kValueBins): value histogram, descending exclusive scan -> start of each value,
+// then each expert takes a slot of its value.  Equal counts may land in either order, which
+// leaves the sorted vector unchanged.  Larger counts fall back to an O(E^2 / 1024) rank count.
 __device__ void dispatch_core(Smem& sm, int E, int total, const DispatchIn& d, int32_t* ctrl) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  int epad = 64;
-  while (epad < E) epad <<= 1;
-  const int R = kRouteThreads / epad;  // threads per expert, a power of two <= 16
-  const int i = tid / R, j = tid % R;
-  int rank = 0, ci = 0;
-  if (i < E) {
-    ci = sm.cnt[i];
-    for (int q = j; q < E; q += R) {
-      const int cq = sm.cnt[q];
-      rank += (cq > ci) || (cq == ci && q < i);
+  const int ci = tid < E ? sm.cnt[tid] : 0;
+  int cmax = ci;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) cmax = max(cmax, __shfl_xor(cmax, o, 64));
+  if (lane == 0) sm.tmp[w] = cmax;
+  __syncthreads();
+  cmax = 0;
+  for (int u = 0; u < kNW; ++u) cmax = max(cmax, sm.tmp[u]);
+  if (cmax < kValueBins) {
+    for (int v = tid; v <= cmax; v += kRouteThreads) sm.vh[v] = 0;
+    __syncthreads();
+    if (tid < E) atomicAdd(&sm.vh[ci], 1);
+    __syncthreads();
+    // Thread t owns the values cmax - 4t .. cmax - 4t - 3 (descending order of values).
+    int h[4], local = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int v = cmax - 4 * tid - q;
+      h[q] = v >= 0 ? sm.vh[v] : 0;
+      local += h[q];
     }
+    int sv[1] = {local}, ex[1], tot[1];
+    block_scan<1>(sv, ex, tot, sm.tmp);  // its barriers also order the reads above
+    int start = ex[0];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int v = cmax - 4 * tid - q;
+      if (v >= 0) sm.vh[v] = start;
+      start += h[q];
+    }
+    __syncthreads();
+    if (tid < E) sm.sorted[atomicAdd(&sm.vh[ci], 1)] = ci;
+  } else {
+    int epad = 64;
+    while (epad < E) epad <<= 1;
+    const int R = kRouteThreads / epad;  // threads per expert, a power of two <= 16
+    const int i = tid / R, j = tid % R;
+    int rank = 0, c2 = 0;
+    if (i < E) {
+      c2 = sm.cnt[i];
+      for (int q = j; q < E; q += R) {
+        const int cq = sm.cnt[q];
+        rank += (cq > c2) || (cq == c2 && q < i);
+      }
+    }
+    for (int o = 1; o < R; o <<= 1) rank += __shfl_xor(rank, o, 64);
+    if (i < E && j == 0) sm.sorted[rank] = c2;
   }
-  for (int o = 1; o < R; o <<= 1) rank += __shfl_xor(rank, o, 64);
-  if (i < E && j == 0) sm.sorted[rank] = ci;
   __syncthreads();
   for (int x = w; x < d.n_ex; x += kNW) {
     long long acc = 0;

@@ -276,6 +276,8 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
 
     t_bucket.push_back(T);
     int32_t n_added = 0;
+    const size_t first_ex = t_kid.size();
+    std::vector<std::vector<double>> skew_mean;  // [skew][variant] mean latency over the samples
     for (int32_t j = 0; j < cfg->n_skews; ++j) {
       std::vector<std::vector<int32_t>> cs;
       std::vector<double> mean(nv, 0.0), lat;
@@ -294,12 +296,33 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
       t_kid.push_back(best);
       t_Q.resize(t_Q.size() + E);
       exemplar(cs, E, t_Q.data() + t_Q.size() - E);
+      skew_mean.push_back(mean);
       ++n_added;
       if (cfg->verbose)
         std::fprintf(stderr, "damoe_tune: T=%d ddist:%.2f -> %s (%.1f us)\n", T, cfg->skew_X[j],
                      damoe_variant_name(best), mean[best] * 1e3);
     }
     t_nex.push_back(n_added);
+    // Skews whose exemplars quantise to the same vector are the same distribution to the
+    // dispatcher (it can only ever pick the first of them): they share one kernel, the one
+    // with the fastest mean over all of their samples.
+    for (int32_t j = 0; j < n_added; ++j) {
+      std::vector<double> pooled(nv, 0.0);
+      int32_t members = 0;
+      for (int32_t u = 0; u < n_added; ++u) {
+        if (!std::equal(t_Q.begin() + (first_ex + j) * E, t_Q.begin() + (first_ex + j + 1) * E,
+                        t_Q.begin() + (first_ex + u) * E))
+          continue;
+        for (int32_t v = 0; v < nv; ++v) pooled[v] += skew_mean[u][v];
+        ++members;
+      }
+      if (members > 1) {
+        int32_t best = 0;
+        for (int32_t v = 1; v < nv; ++v)
+          if (pooled[v] < pooled[best]) best = v;
+        t_kid[first_ex + j] = best;
+      }
+    }
     // Distribution-unaware baseline: the fastest variant under uniform routing.
     {
       std::vector<double> mean(nv, 0.0), lat;

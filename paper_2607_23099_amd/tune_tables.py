@@ -1,0 +1,61 @@
+"""Offline auto-tuning of dispatch tables (Sec. IV-A) for the named layer shapes.
+
+    python -m paper_2607_23099_amd.tune_tables dsv3 --max-T 128 --out tables/dsv3.damoe
+
+For each power-of-two token bucket up to --max-T, each ddist:X skew of the
+grid (the paper's {1.1 ... 4.0} extended to 32) and S routing samples, every
+variant is timed by the library's tuner; the table maps each skew's exemplar
+to its fastest variant, plus the uniform-routing (NoDA) choice per bucket.
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import sys
+import time
+
+PAPER_SKEWS = [1.1, 1.3, 1.5, 1.7, 2.0, 2.5, 4.0]
+EXTENDED_SKEWS = PAPER_SKEWS + [6.0, 8.0, 12.0, 16.0, 24.0, 32.0]
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, verbose: bool = True,
+               dl=None):
+    import torch
+    from . import damoe, synth
+    from .moe import DeviceLayer
+    shapes = {"dsv3": synth.DS, "dsv3-fp8": synth.DS_FP8, "kimi-k2": synth.KIMI, "tiny": synth.TINY}
+    shape = shapes[shape_name]
+    if dl is None:
+        dl = DeviceLayer(shape)
+    buckets = []
+    t = 1
+    while t <= max_T:
+        buckets.append(t)
+        t *= 2
+    x = torch.empty((max_T, shape.H), dtype=torch.bfloat16, device="cuda")
+    synth.fill_bf16_device(x.data_ptr(), x.numel(), seed=synth.x_seed(999), tensor=synth.T_X,
+                           slab_elems=x.numel(), sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
+    t0 = time.perf_counter()
+    table = damoe.tune(dl.layer, buckets, EXTENDED_SKEWS, x, samples=samples, reps=reps, seed=seed,
+                       verbose=verbose)
+    return table, time.perf_counter() - t0, buckets, dl
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("shape", choices=["dsv3", "dsv3-fp8", "kimi-k2", "tiny"])
+    ap.add_argument("--max-T", type=int, default=128)
+    ap.add_argument("--samples", type=int, default=10)
+    ap.add_argument("--reps", type=int, default=5)
+    ap.add_argument("--seed", type=int, default=0x7AB1E)
+    ap.add_argument("--out", required=True)
+    args = ap.parse_args()
+    table, secs, buckets, _ = tune_shape(args.shape, args.max_T, args.samples, args.reps, args.seed)
+    table.save(args.out)
+    print(f"tuned {args.shape}: buckets {buckets}, {len(EXTENDED_SKEWS)} skews, S={args.samples}, "
+          f"reps={args.reps} in {secs:.1f} s -> {args.out}", file=sys.stderr, flush=True)
+
+
+if __name__ == "__main__":
+    main()
