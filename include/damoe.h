@@ -72,14 +72,28 @@ typedef enum damoe_wdtype {
   DAMOE_W_FP8_B128 = 1  /* OCP e4m3fn weights, one fp32 scale per 128x128 block         */
 } damoe_wdtype;
 
+/* Weight layouts.  Row-major is the interchange layout; the fragment-packed
+ * layout stores every 16-row x 32-column block of a matrix as one contiguous
+ * MFMA operand fragment (64 lanes x 8 elements, lane l holding row l % 16,
+ * columns 8 (l / 16) .. 8 (l / 16) + 7), blocks ordered row-block-major, so a
+ * wavefront loads a whole fragment (1 KB bf16 / 512 B fp8) in one contiguous
+ * access.  damoe_pack_weights converts once, at load time. */
+typedef enum damoe_wlayout {
+  DAMOE_LAYOUT_ROWMAJOR = 0,
+  DAMOE_LAYOUT_FRAG16 = 1
+} damoe_wlayout;
+
 /* One MoE layer of E SwiGLU experts, FFN_e(x) = W2_e (silu(W1_e x) * (W3_e x))
  * (Sec. II-A).  Weights of expert e are contiguous slabs:
- *   w1, w3: [E][I][H]   w2: [E][H][I]   (bf16, or e4m3 bytes for DAMOE_W_FP8_B128)
+ *   w1, w3: [E][I][H]   w2: [E][H][I]   (bf16, or e4m3 bytes for DAMOE_W_FP8_B128),
+ *   row-major or fragment-packed (`layout`), the same size either way;
  *   s1, s3: [E][I/128][H/128]  s2: [E][H/128][I/128]  fp32 block scales (fp8 only,
- *   NULL otherwise).  H and I must be multiples of 128 (of 512 for fp8 weights). */
+ *   NULL otherwise), always row-major.  H and I must be multiples of 128 (of 512
+ *   for fp8 weights). */
 typedef struct damoe_layer {
   int32_t E, k, H, I;
   int32_t wdtype; /* damoe_wdtype */
+  int32_t layout; /* damoe_wlayout */
   const void* w1;
   const void* w3;
   const void* w2;
@@ -179,7 +193,9 @@ damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int
  * its counts (same outputs, same workspace contents), with the histogram, the
  * exemplar match and the permutation sharing one workgroup's LDS.  This is the
  * paper's online step 5 (Sec. IV-B): histogram, sort, match, kernel id, all on
- * the device.  The table must be built for this E and k. */
+ * the device.  The table must be built for this E and k.  When every exemplar
+ * of the bucket maps to the same variant, that variant is written without
+ * scoring (the match cannot change it) and control word [1] is -2. */
 damoe_status damoe_route_dispatch(const damoe_table* table, const int32_t* topk_ids, int32_t T,
                                   int32_t k, int32_t E, int32_t* counts, int32_t* offsets,
                                   int32_t* perm, int32_t* inv_perm, uint64_t* effexp_numden,
@@ -213,6 +229,14 @@ damoe_status damoe_fused_moe_stage(const damoe_layer* layer /* host */, int32_t 
                                    const int32_t* perm, const int32_t* inv_perm,
                                    const int32_t* variant_id, int32_t force_variant, uint16_t* y,
                                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Converts the row-major weights of `src` (layout must be DAMOE_LAYOUT_ROWMAJOR)
+ * into the fragment-packed layout, written to w1, w3, w2 (device buffers of the
+ * same sizes, not overlapping the sources).  Scales are not touched.  A layer
+ * descriptor with layout = DAMOE_LAYOUT_FRAG16 and these pointers then runs the
+ * same computation.  Stream-ordered. */
+damoe_status damoe_pack_weights(const damoe_layer* src /* host */, void* w1, void* w3, void* w2,
+                                hipStream_t stream);
 
 /* Variant registry.  Variant v computes with token tiles of
  * damoe_variant_tile_m(v) rows. */

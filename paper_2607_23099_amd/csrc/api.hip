@@ -52,6 +52,7 @@ damoe_status check_layer(const damoe_layer* L) {
   if (L->H <= 0 || L->I <= 0) return DAMOE_ERR_INVALID_ARG;
   if (L->H % 128 || L->I % 128) return DAMOE_ERR_UNSUPPORTED;  // whole feature blocks of every variant
   if (!L->w1 || !L->w3 || !L->w2) return DAMOE_ERR_INVALID_ARG;
+  if (L->layout != DAMOE_LAYOUT_ROWMAJOR && L->layout != DAMOE_LAYOUT_FRAG16) return DAMOE_ERR_UNSUPPORTED;
   if (L->wdtype == DAMOE_W_BF16) return DAMOE_OK;
   if (L->wdtype == DAMOE_W_FP8_B128) {
     if (!L->s1 || !L->s3 || !L->s2) return DAMOE_ERR_INVALID_ARG;
@@ -156,10 +157,16 @@ static int32_t table_bucket(const damoe_table* t, int32_t T) {
   return nb - 1;
 }
 
+// When every exemplar of the bucket maps to the same variant the match cannot change the
+// outcome, so the kernel writes that variant without scoring (noda when there are no tokens).
 static DispatchArgs table_args(const damoe_table* t, int32_t T, int32_t* variant_id) {
   const int32_t b = table_bucket(t, T);
+  const int32_t* kid = t->kid.data() + t->ex_begin[b];
+  bool same = true;
+  for (int32_t i = 1; i < t->n_ex[b]; ++i) same = same && kid[i] == kid[0];
+  const int32_t fixed = T == 0 ? t->noda[b] : (same ? kid[0] : -1);
   return DispatchArgs{t->d_Q + (size_t)t->ex_begin[b] * t->E, t->d_kid + t->ex_begin[b], t->n_ex[b],
-                      t->noda[b], variant_id};
+                      t->noda[b], variant_id, fixed};
 }
 
 static damoe_status route_impl(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
@@ -248,6 +255,7 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g1.K = L->H;
   g1.N = L->I;
   g1.fp8 = L->wdtype == DAMOE_W_FP8_B128;
+  g1.packed = L->layout == DAMOE_LAYOUT_FRAG16;
 
   GemmArgs g2 = g1;
   g2.x = reinterpret_cast<const uint16_t*>(base + lo.h);
@@ -284,6 +292,27 @@ damoe_status damoe_fused_moe_stage(const damoe_layer* L, int32_t stage, const ui
   if (stage < 0 || stage > 2) return DAMOE_ERR_INVALID_ARG;
   return fused_impl(L, 1 << stage, x, topk_w, T, perm, inv_perm, variant_id, force_variant, y, ws,
                     ws_bytes, stream);
+}
+
+damoe_status damoe_pack_weights(const damoe_layer* L, void* w1, void* w3, void* w2, hipStream_t stream) {
+  const damoe_status st = check_layer(L);
+  if (st != DAMOE_OK) return st;
+  if (L->layout != DAMOE_LAYOUT_ROWMAJOR || !w1 || !w3 || !w2) return DAMOE_ERR_INVALID_ARG;
+  const int eb = L->wdtype == DAMOE_W_FP8_B128 ? 1 : 2;
+  const size_t bytes = (size_t)L->E * L->H * L->I * eb;
+  const void* src[3] = {L->w1, L->w3, L->w2};
+  void* dst[3] = {w1, w3, w2};
+  for (int m = 0; m < 3; ++m)
+    for (int n = 0; n < 3; ++n) {  // no destination may overlap any source
+      const char* s0 = static_cast<const char*>(src[n]);
+      const char* d0 = static_cast<const char*>(dst[m]);
+      if (d0 < s0 + bytes && s0 < d0 + bytes) return DAMOE_ERR_INVALID_ARG;
+    }
+  if (launch_pack(L->w1, w1, L->E, L->I, L->H, eb, stream) != hipSuccess ||
+      launch_pack(L->w3, w3, L->E, L->I, L->H, eb, stream) != hipSuccess ||
+      launch_pack(L->w2, w2, L->E, L->H, L->I, eb, stream) != hipSuccess)
+    return DAMOE_ERR_HIP;
+  return DAMOE_OK;
 }
 
 damoe_status damoe_read_device_error(void* ws, int32_t* code, hipStream_t stream) {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "damoe.h"
 
 namespace damoe {
@@ -64,6 +66,7 @@ struct GemmArgs {
   int32_t K;           // reduction length: H for GEMM1, I for GEMM2
   int32_t N;           // output features: I for GEMM1, H for GEMM2
   int32_t fp8;
+  int32_t packed;      // weights in the fragment-packed layout
 };
 
 struct ReduceArgs {
@@ -81,6 +84,7 @@ struct DispatchArgs {
   int32_t n_ex;
   int32_t noda;
   int32_t* variant_id;
+  int32_t fixed;       // >= 0: every exemplar of the bucket maps to this variant (no match needed)
 };
 
 // Launchers (return hipError_t of the launch).  launch_route with a non-null dispatch runs
@@ -95,6 +99,8 @@ hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream);
 hipError_t gemm_set_lds_limits();
+hipError_t launch_pack(const void* src, void* dst, int32_t slabs, int32_t rows, int32_t cols, int32_t elem_bytes,
+                       hipStream_t stream);
 
 // Dynamic LDS bytes the GEMM kernels are launched with.
 size_t gemm_lds_bytes();

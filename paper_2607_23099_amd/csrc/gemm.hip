@@ -93,7 +93,9 @@ struct WFrag<true> {
 //     otherwise each wave reads one contiguous quarter of the row.
 // NT: weight loads carry the nontemporal hint (streamed once, not worth caching).
 // D:  register-ring depth, k-steps in flight per wave.
-template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D>
+// PK: weights in the fragment-packed layout (block (rb, kb) of 16 rows x 32 columns is one
+//     contiguous 64-lane fragment); otherwise row-major.
+template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D, bool PK>
 __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __restrict__ list,
                                             float* __restrict__ red) {
   constexpr int NX = BM / 16;
@@ -151,8 +153,14 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
 #pragma unroll
     for (int b = 0; b < NR; ++b) {
       const int rb_ = GLU ? (b % (NR / 2)) : b;
-      const int f = fb * BN + rb_ * 16 + (lane & 15);
-      wo[b] = ((uint32_t)f * (uint32_t)K + kcol) * EB;
+      if (PK) {
+        const uint32_t rblk = (uint32_t)(fb * BN) / 16 + rb_;
+        const uint32_t kb0 = IL ? wave : wave * nks;  // this wave's first 32-column block
+        wo[b] = ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 8u * EB;
+      } else {
+        const int f = fb * BN + rb_ * 16 + (lane & 15);
+        wo[b] = ((uint32_t)f * (uint32_t)K + kcol) * EB;
+      }
     }
     const float* sa = a.sa;
     const float* sb = a.sb;
@@ -169,7 +177,7 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
     WT wf[D][NR];
     uint4 xf[D][NX];
     auto load = [&](int ks, int st) __attribute__((always_inline)) {
-      const uint32_t sw = (uint32_t)ks * KSTEP * EB;
+      const uint32_t sw = PK ? (uint32_t)ks * (KSTEP / 32) * 512u * EB : (uint32_t)ks * KSTEP * EB;
 #pragma unroll
       for (int b = 0; b < NR; ++b)
         wf[st][b] = buf_load<WT, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b], sw);
@@ -262,7 +270,7 @@ constexpr int kTiledBK = 128;
 constexpr int kTiledNRW = 2;
 constexpr size_t kTiledLds = 2 * (size_t)kTiledBM * kTiledBK * 2;  // 64 KB
 
-template <bool GLU, bool FP8, int D>
+template <bool GLU, bool FP8, int D, bool PK>
 __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __restrict__ list,
                                            uint8_t* __restrict__ lds) {
   constexpr int BM = kTiledBM, NRW = kTiledNRW, NX = BM / 16;
@@ -316,10 +324,11 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
     uint32_t wo[NRW];
 #pragma unroll
     for (int b = 0; b < NRW; ++b) {
-      int f;
-      if (GLU) f = fb * FEAT + wave * (NRW / 2) * 16 + (b % (NRW / 2)) * 16 + rl;
-      else f = fb * FEAT + wave * NRW * 16 + b * 16 + rl;
-      wo[b] = ((uint32_t)f * (uint32_t)K + gl * 8) * EB;
+      int f0;  // first row of the block
+      if (GLU) f0 = fb * FEAT + wave * (NRW / 2) * 16 + (b % (NRW / 2)) * 16;
+      else f0 = fb * FEAT + wave * NRW * 16 + b * 16;
+      if (PK) wo[b] = ((uint32_t)(f0 / 16) * (uint32_t)(K / 32) * 64u + lane) * 8u * EB;
+      else wo[b] = ((uint32_t)(f0 + rl) * (uint32_t)K + gl * 8) * EB;
     }
     const int sk = K / 128;
     const int srow = (fb * FEAT + (GLU ? 0 : wave * NRW * 16)) / 128;
@@ -349,7 +358,7 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
     };
     WT wf[D][NRW];
     auto wload = [&](int ks, int slot) __attribute__((always_inline)) {
-      const uint32_t sw = (uint32_t)ks * 32 * EB;
+      const uint32_t sw = (uint32_t)ks * (PK ? 512u : 32u) * EB;
 #pragma unroll
       for (int b = 0; b < NRW; ++b)
         wf[slot][b] = buf_load<WT, 0>((GLU && b >= NRW / 2) ? rbk : ra, wo[b], sw);
@@ -460,7 +469,7 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
 
 constexpr int tile_class(int bm) { return bm == 16 ? 0 : bm == 32 ? 1 : bm == 64 ? 2 : bm == 128 ? 3 : 4; }
 
-template <bool GLU, bool FP8>
+template <bool GLU, bool FP8, bool PK>
 __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   extern __shared__ float smem[];
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
@@ -469,14 +478,14 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
 #define DAMOE_CASE(ID, NAME, BM, BN1, BN2, IL, NT, D)                                          \
   case ID: {                                                                                   \
     constexpr int BN = GLU ? BN1 : BN2;                                                        \
-    stream_body<BM, BN, GLU, FP8, IL, NT, D>(a, a.tiles.list[tile_class(BM)], smem);          \
+    stream_body<BM, BN, GLU, FP8, IL, NT, D, PK>(a, a.tiles.list[tile_class(BM)], smem);      \
     break;                                                                                     \
   }
     DAMOE_STREAM_VARIANTS(DAMOE_CASE)
 #undef DAMOE_CASE
 #define DAMOE_TCASE(ID, NAME, D)                                                               \
   case ID:                                                                                     \
-    tiled_body<GLU, FP8, D>(a, a.tiles.list[tile_class(kTiledBM)], reinterpret_cast<uint8_t*>(smem)); \
+    tiled_body<GLU, FP8, D, PK>(a, a.tiles.list[tile_class(kTiledBM)], reinterpret_cast<uint8_t*>(smem)); \
     break;
     DAMOE_TILED_VARIANTS(DAMOE_TCASE)
 #undef DAMOE_TCASE
@@ -545,11 +554,25 @@ int32_t num_variants() { return (int32_t)(sizeof(kVariants) / sizeof(kVariants[0
 const VariantDesc& variant(int32_t v) { return kVariants[v]; }
 size_t gemm_lds_bytes() { return max_lds(); }
 
+template <bool GLU>
+static hipError_t launch_stage(const GemmArgs& a, int grid, hipStream_t stream) {
+  const size_t lds = gemm_lds_bytes();
+  if (a.fp8) {
+    if (a.packed) hipLaunchKernelGGL((k_gemm<GLU, true, true>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
+    else hipLaunchKernelGGL((k_gemm<GLU, true, false>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
+  } else {
+    if (a.packed) hipLaunchKernelGGL((k_gemm<GLU, false, true>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
+    else hipLaunchKernelGGL((k_gemm<GLU, false, false>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
+  }
+  return hipGetLastError();
+}
+
 hipError_t gemm_set_lds_limits() {
-  const void* fns[] = {reinterpret_cast<const void*>(&k_gemm<true, false>),
-                       reinterpret_cast<const void*>(&k_gemm<false, false>),
-                       reinterpret_cast<const void*>(&k_gemm<true, true>),
-                       reinterpret_cast<const void*>(&k_gemm<false, true>)};
+  const void* fns[] = {
+      reinterpret_cast<const void*>(&k_gemm<true, false, false>), reinterpret_cast<const void*>(&k_gemm<false, false, false>),
+      reinterpret_cast<const void*>(&k_gemm<true, true, false>), reinterpret_cast<const void*>(&k_gemm<false, true, false>),
+      reinterpret_cast<const void*>(&k_gemm<true, false, true>), reinterpret_cast<const void*>(&k_gemm<false, false, true>),
+      reinterpret_cast<const void*>(&k_gemm<true, true, true>), reinterpret_cast<const void*>(&k_gemm<false, true, true>)};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)gemm_lds_bytes());
     if (e != hipSuccess) return e;
@@ -557,21 +580,9 @@ hipError_t gemm_set_lds_limits() {
   return hipSuccess;
 }
 
-hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream) {
-  if (a.fp8)
-    hipLaunchKernelGGL((k_gemm<true, true>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
-  else
-    hipLaunchKernelGGL((k_gemm<true, false>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
-  return hipGetLastError();
-}
+hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream) { return launch_stage<true>(a, grid, stream); }
 
-hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream) {
-  if (a.fp8)
-    hipLaunchKernelGGL((k_gemm<false, true>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
-  else
-    hipLaunchKernelGGL((k_gemm<false, false>), dim3(grid), dim3(kGemmThreads), gemm_lds_bytes(), stream, a);
-  return hipGetLastError();
-}
+hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream) { return launch_stage<false>(a, grid, stream); }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;

@@ -77,6 +77,7 @@ struct DispatchIn {
   int32_t n_ex;
   int32_t noda;
   int32_t* variant_id;
+  int32_t fixed;       // >= 0: the bucket has one variant; write it without scoring
 };
 
 struct RouteOut {
@@ -288,6 +289,12 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   }
 
   if (DISPATCH) dispatch_core(sm, E, total, d, o.ctrl);
+  if (!DISPATCH && d.fixed >= 0 && tid == 0) {
+    *d.variant_id = total == 0 ? d.noda : d.fixed;
+    o.ctrl[1] = total == 0 ? -1 : -2;  // single-variant bucket: no exemplar scored
+    o.ctrl[2] = 0;
+    o.ctrl[3] = 0;
+  }
 
   // a4: stable scatter, one 1024-assignment chunk at a time.  Within a wave the rank among
   // equal experts comes from ballot-based multisplit; across waves from per-wave counts.
@@ -354,19 +361,20 @@ hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int
                         hipStream_t stream) {
   RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}};
   for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) o.tiles.list[i] = tile_lists[i];
-  if (dispatch) {
-    DispatchIn d{dispatch->Q, dispatch->kid, dispatch->n_ex, dispatch->noda, dispatch->variant_id};
+  if (dispatch && dispatch->fixed < 0) {
+    DispatchIn d{dispatch->Q, dispatch->kid, dispatch->n_ex, dispatch->noda, dispatch->variant_id, -1};
     hipLaunchKernelGGL(k_route<true>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
   } else {
-    hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o,
-                       DispatchIn{});
+    DispatchIn d{nullptr, nullptr, 0, dispatch ? dispatch->noda : 0, dispatch ? dispatch->variant_id : nullptr,
+                 dispatch ? dispatch->fixed : -1};
+    hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
                            hipStream_t stream) {
-  DispatchIn d{dispatch.Q, dispatch.kid, dispatch.n_ex, dispatch.noda, dispatch.variant_id};
+  DispatchIn d{dispatch.Q, dispatch.kid, dispatch.n_ex, dispatch.noda, dispatch.variant_id, -1};
   hipLaunchKernelGGL(k_dispatch, dim3(1), dim3(kRouteThreads), 0, stream, counts, E, d, ctrl);
   return hipGetLastError();
 }

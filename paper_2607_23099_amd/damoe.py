@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdamoe.so")
 
 N_TILE_SIZES = 5
 W_BF16, W_FP8_B128 = 0, 1
+LAYOUT_ROWMAJOR, LAYOUT_FRAG16 = 0, 1
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
           -4: "table mismatch", -5: "hip error", -6: "out of memory", -7: "io error"}
@@ -27,7 +28,7 @@ EXPORTED = [
     "damoe_table_create", "damoe_table_destroy", "damoe_table_info", "damoe_table_save",
     "damoe_table_load", "damoe_dispatch", "damoe_fused_moe", "damoe_num_variants", "damoe_variant_name",
     "damoe_variant_tile_m", "damoe_variant_supports", "damoe_tune", "damoe_alpha_search",
-    "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch",
+    "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch", "damoe_pack_weights",
 ]
 
 
@@ -39,7 +40,8 @@ class DamoeError(RuntimeError):
 
 class Layer(ctypes.Structure):
     _fields_ = [("E", ctypes.c_int32), ("k", ctypes.c_int32), ("H", ctypes.c_int32),
-                ("I", ctypes.c_int32), ("wdtype", ctypes.c_int32), ("w1", ctypes.c_void_p),
+                ("I", ctypes.c_int32), ("wdtype", ctypes.c_int32), ("layout", ctypes.c_int32),
+                ("w1", ctypes.c_void_p),
                 ("w3", ctypes.c_void_p), ("w2", ctypes.c_void_p), ("s1", ctypes.c_void_p),
                 ("s3", ctypes.c_void_p), ("s2", ctypes.c_void_p)]
 
@@ -98,6 +100,7 @@ def lib() -> ctypes.CDLL:
             "damoe_tune": ([vp, vp, vp, vp], i32),
             "damoe_alpha_search": ([i32, f64, i32, i32, u64], f64),
             "damoe_read_device_error": ([vp, vp, vp], i32),
+            "damoe_pack_weights": ([vp, vp, vp, vp, vp], i32),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -156,8 +159,13 @@ def workspace_layout(E: int, k: int, H: int, I: int, T: int) -> dict:
             "h": lo.h, "out": lo.out}
 
 
-def make_layer(E, k, H, I, wdtype, w1, w3, w2, s1=None, s3=None, s2=None) -> Layer:
-    return Layer(E, k, H, I, wdtype, _p(w1), _p(w3), _p(w2), _p(s1), _p(s3), _p(s2))
+def make_layer(E, k, H, I, wdtype, w1, w3, w2, s1=None, s3=None, s2=None, layout=LAYOUT_ROWMAJOR) -> Layer:
+    return Layer(E, k, H, I, wdtype, layout, _p(w1), _p(w3), _p(w2), _p(s1), _p(s3), _p(s2))
+
+
+def pack_weights(layer: Layer, w1, w3, w2, stream=None):
+    _check("damoe_pack_weights", lib().damoe_pack_weights(ctypes.byref(layer), _p(w1), _p(w3), _p(w2),
+                                                          _stream(stream)))
 
 
 def workspace_size(layer: Layer, T_max: int) -> int:

@@ -14,7 +14,10 @@ from . import damoe, synth
 
 
 class DeviceLayer:
-    def __init__(self, shape: synth.Shape, device: str = "cuda"):
+    """One layer's weights in HBM.  ``packed`` converts them to the fragment-packed layout
+    (the fast path) after the row-major fill; the row-major copy is released."""
+
+    def __init__(self, shape: synth.Shape, device: str = "cuda", packed: bool = True):
         self.shape = shape
         E, H, I = shape.E, shape.H, shape.I
         self.wdtype = damoe.W_FP8_B128 if shape.wdtype == "fp8" else damoe.W_BF16
@@ -35,6 +38,15 @@ class DeviceLayer:
                 self.w[name], self.s[name] = q, s
         self.layer = damoe.make_layer(E, shape.k, H, I, self.wdtype, self.w["w1"], self.w["w3"],
                                       self.w["w2"], self.s.get("w1"), self.s.get("w3"), self.s.get("w2"))
+        self.packed = packed
+        if packed:
+            dst = {n: torch.empty_like(t) for n, t in self.w.items()}
+            damoe.pack_weights(self.layer, dst["w1"], dst["w3"], dst["w2"])
+            torch.cuda.synchronize()
+            self.w = dst
+            self.layer = damoe.make_layer(E, shape.k, H, I, self.wdtype, dst["w1"], dst["w3"], dst["w2"],
+                                          self.s.get("w1"), self.s.get("w3"), self.s.get("w2"),
+                                          layout=damoe.LAYOUT_FRAG16)
 
     @property
     def weight_bytes_per_expert(self) -> int:

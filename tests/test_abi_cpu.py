@@ -71,10 +71,10 @@ def test_workspace_layout():
 
 
 def _fake_layer(**kw):
-    d = dict(E=8, k=2, H=256, I=512, wdtype=0, w1=0x1000, w3=0x2000, w2=0x3000, s1=0, s3=0, s2=0)
+    d = dict(E=8, k=2, H=256, I=512, wdtype=0, layout=0, w1=0x1000, w3=0x2000, w2=0x3000, s1=0, s3=0, s2=0)
     d.update(kw)
-    return damoe.Layer(d["E"], d["k"], d["H"], d["I"], d["wdtype"], d["w1"], d["w3"], d["w2"], d["s1"],
-                       d["s3"], d["s2"])
+    return damoe.Layer(d["E"], d["k"], d["H"], d["I"], d["wdtype"], d["layout"], d["w1"], d["w3"], d["w2"],
+                       d["s1"], d["s3"], d["s2"])
 
 
 def test_validation_before_launch():
@@ -98,6 +98,12 @@ def test_validation_before_launch():
     assert fm(ctypes.byref(_fake_layer(wdtype=1, s1=P, s3=P, s2=P)), P, P, 4, P, P, P, -1, P, P, ws_ok,
               None) == -2  # fp8 needs H, I multiples of 512
     assert fm(ctypes.byref(_fake_layer(wdtype=5)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
+    assert fm(ctypes.byref(_fake_layer(layout=2)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
+    # pack_weights: the source must be row-major and the destinations must not overlap it
+    pk = L.damoe_pack_weights
+    assert pk(ctypes.byref(_fake_layer(layout=1)), P, P, P, None) == -1
+    assert pk(ctypes.byref(_fake_layer()), 0x1000, 0x900000, 0xA00000, None) == -1  # w1 dst == w1 src
+    assert pk(ctypes.byref(_fake_layer()), None, P, P, None) == -1
     assert fm(ctypes.byref(lay), P, P, 4, P, P, P, damoe.num_variants(), P, P, ws_ok, None) == -1
     assert fm(ctypes.byref(lay), P, P, 4, P, P, None, -1, P, P, ws_ok, None) == -1  # no variant id
     assert fm(ctypes.byref(lay), P, P, 4, P, P, P, -1, P, P, 1024, None) == -3

@@ -27,11 +27,11 @@ def _run(path, r, x_tag, variant=None, table=None):
     torch.cuda.synchronize()
 
 
-@pytest.fixture(scope="module")
-def tiny():
+@pytest.fixture(scope="module", params=[False, True], ids=["rowmajor", "packed"])
+def tiny(request):
     torch = torch_cuda()
     from paper_2607_23099_amd.moe import DeviceLayer, Path
-    dl = DeviceLayer(synth.TINY)
+    dl = DeviceLayer(synth.TINY, packed=request.param)
     yield dl, Path(dl, 256)
     torch.cuda.empty_cache()
 

@@ -177,7 +177,10 @@ def test_dispatch_matches_oracle(E):
         i, scores = oracle.match(c, td.Q[rows])
         assert int(vid2.item()) == int(td.kid[rows][i]), (step, T)
         ctrl = b.ws[:16].view(torch.int32).cpu().numpy()
-        assert ctrl[1] == i and int(np.array(ctrl[2:4], np.int32).view(np.int64)[0]) == scores[i]
+        if np.all(td.kid[rows] == td.kid[rows][0]):
+            assert ctrl[1] == -2  # single-variant bucket: written without scoring
+        else:
+            assert ctrl[1] == i and int(np.array(ctrl[2:4], np.int32).view(np.int64)[0]) == scores[i]
     # No tokens -> the bucket's noda variant.
     counts.zero_()
     damoe.dispatch(table, counts, 0, vid, ws)
@@ -223,3 +226,29 @@ def test_device_fill_equals_host_fill():
     qh, sh_ = synth.fill_fp8_host(256, 384, 2, seed=9, tensor=synth.T_W2, slab0=3)
     np.testing.assert_array_equal(q.cpu().numpy(), qh)
     np.testing.assert_array_equal(s.cpu().numpy(), sh_)
+
+
+def test_route_dispatch_single_variant_bucket():
+    torch = torch_cuda()
+    E, k, T = 64, 8, 40
+    nv = damoe.num_variants()
+    rng = np.random.default_rng(5)
+    Q = rng.integers(0, 20000, (3, E)).astype(np.int32)
+    td = damoe.TableData(E=E, k=k, H=256, I=256, wdtype=0, bucket_T=np.array([16, 64], np.int32),
+                         n_ex=np.array([1, 2], np.int32), Q=Q, kid=np.array([0, 2, 2], np.int32) % nv,
+                         noda=np.array([1, 1], np.int32) % nv)
+    table = damoe.Table.create(td)
+    r = synth.routing(E, k, T, 0.5, [80])
+    b = RouteBufs(torch, E, k, T)
+    b.ids.copy_(torch.from_numpy(r.ids.ravel().copy()))
+    vid = torch.full((1,), -9, dtype=torch.int32, device="cuda")
+    damoe.route_dispatch(table, b.ids, T, k, E, b.counts, b.offsets, b.perm, b.inv, b.nd, b.bucket, vid, b.ws)
+    torch.cuda.synchronize()
+    _check_route(b, r.ids)
+    assert int(vid.item()) == 2 % nv and b.ws[:16].view(torch.int32).cpu().numpy()[1] == -2
+    # No tokens: the bucket's noda variant.
+    b0 = RouteBufs(torch, E, k, 0)
+    damoe.route_dispatch(table, b0.ids, 0, k, E, b0.counts, b0.offsets, b0.perm, b0.inv, b0.nd, b0.bucket,
+                         vid, b0.ws)
+    torch.cuda.synchronize()
+    assert int(vid.item()) == 1 % nv
