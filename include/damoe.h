@@ -66,6 +66,7 @@ typedef enum damoe_status {
 #define DAMOE_DEVERR_NONE 0
 #define DAMOE_DEVERR_EXPERT_ID 1 /* an id outside [0, E) was dropped                       */
 #define DAMOE_DEVERR_TILES 2     /* fused_moe found tile lists of another T; items skipped */
+#define DAMOE_DEVERR_VARIANT 4   /* the dispatched id was outside fused_moe's candidates  */
 
 typedef enum damoe_wdtype {
   DAMOE_W_BF16 = 0,     /* bf16 weights                                                */
@@ -186,6 +187,12 @@ damoe_status damoe_table_load(const char* path, damoe_table** out);
  * kid[i] to *variant_id (device int32).  With no tokens (all counts 0) the
  * bucket's noda variant is written.  The chosen exemplar and its score land in
  * the workspace control words.  Stream-ordered; no host sync. */
+/* Host bit mask of the variant ids that dispatch may write for a call with T
+ * tokens: the kid of every exemplar of T's bucket and the bucket's noda variant
+ * (the paper keeps one graph per bucket holding exactly these kernels, Sec. IV).
+ * Pass it to damoe_fused_moe.  0 for a null table or T < 0. */
+uint32_t damoe_table_candidates(const damoe_table* table, int32_t T);
+
 damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int32_t T,
                             int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -211,13 +218,24 @@ damoe_status damoe_route_dispatch(const damoe_table* table, const int32_t* topk_
  *              kernels on the device (no host round trip)
  *   force_variant  host int: -1 uses *variant_id; >= 0 runs that variant
  *              (benchmarking, tuning, per-step best)
+ *   candidates host bit mask of the variant ids *variant_id may hold (bit v),
+ *              e.g. damoe_table_candidates(table, T); 0 = every variant.  Only
+ *              the kernel classes holding a candidate are launched (the big-tile
+ *              class is a kernel of its own, the others share one), so a decode
+ *              bucket whose table row never names the big-tile variant costs no
+ *              launch of it.  A dispatched id outside the mask runs no expert
+ *              GEMM and sets DAMOE_DEVERR_VARIANT (y is then unspecified).
+ *              Ignored when force_variant >= 0;
+ *              bits beyond damoe_num_variants() are DAMOE_ERR_INVALID_ARG.
  *   y          bf16 [T][H] output, y[t] = sum_j topk_w[t][j] FFN_{ids[t][j]}(x[t])
- * Only experts with at least one token are read.  Stream-ordered. */
+ * Only experts with at least one token are read.  Stream-ordered.  T * H * 2
+ * must stay below 2^31 (32-bit row offsets), else DAMOE_ERR_UNSUPPORTED; so must
+ * H and I of fp8 layers stay <= 16384 when the big-tile variant may run. */
 damoe_status damoe_fused_moe(const damoe_layer* layer /* host */, const uint16_t* x,
                              const float* topk_w, int32_t T, const int32_t* perm,
                              const int32_t* inv_perm, const int32_t* variant_id,
-                             int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
-                             hipStream_t stream);
+                             int32_t force_variant, uint32_t candidates, uint16_t* y, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
 
 /* The same computation as damoe_fused_moe, one stage at a time, so a caller can
  * bracket each kernel with events:  stage 0 = grouped GEMM1 + SwiGLU (writes h
@@ -227,8 +245,9 @@ damoe_status damoe_fused_moe(const damoe_layer* layer /* host */, const uint16_t
 damoe_status damoe_fused_moe_stage(const damoe_layer* layer /* host */, int32_t stage,
                                    const uint16_t* x, const float* topk_w, int32_t T,
                                    const int32_t* perm, const int32_t* inv_perm,
-                                   const int32_t* variant_id, int32_t force_variant, uint16_t* y,
-                                   void* ws, size_t ws_bytes, hipStream_t stream);
+                                   const int32_t* variant_id, int32_t force_variant,
+                                   uint32_t candidates, uint16_t* y, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
 
 /* Converts the row-major weights of `src` (layout must be DAMOE_LAYOUT_ROWMAJOR)
  * into the fragment-packed layout, written to w1, w3, w2 (device buffers of the

@@ -36,7 +36,7 @@ damoe_status device_info(DeviceInfo** out) {
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus <= 0)
       return DAMOE_ERR_HIP;
-    if (gemm_set_lds_limits() != hipSuccess) return DAMOE_ERR_HIP;
+    if (gemm_set_lds_limits() != hipSuccess || big_set_lds_limits() != hipSuccess) return DAMOE_ERR_HIP;
     d.cus = cus;
     d.ready = true;
   }
@@ -206,6 +206,14 @@ damoe_status damoe_route_dispatch(const damoe_table* t, const int32_t* topk_ids,
                     ws_bytes, &d, stream);
 }
 
+uint32_t damoe_table_candidates(const damoe_table* t, int32_t T) {
+  if (!t || T < 0) return 0;
+  const int32_t b = table_bucket(t, T);
+  uint32_t m = 1u << t->noda[b];
+  for (int32_t i = 0; i < t->n_ex[b]; ++i) m |= 1u << t->kid[t->ex_begin[b] + i];
+  return m;
+}
+
 damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t T,
                             int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!t || !counts || !variant_id || !ws || T < 0) return DAMOE_ERR_INVALID_ARG;
@@ -219,14 +227,19 @@ damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t
 static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const uint16_t* x,
                                const float* topk_w, int32_t T, const int32_t* perm,
                                const int32_t* inv_perm, const int32_t* variant_id,
-                               int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
-                               hipStream_t stream) {
+                               int32_t force_variant, uint32_t candidates, uint16_t* y, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
   damoe_status st = check_layer(L);
   if (st != DAMOE_OK) return st;
   if (T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
   if (force_variant >= num_variants() || force_variant < -1) return DAMOE_ERR_INVALID_ARG;
   if (force_variant >= 0 && !damoe_variant_supports(force_variant, L->wdtype)) return DAMOE_ERR_UNSUPPORTED;
+  const uint32_t all = (uint32_t)((1ull << num_variants()) - 1);
+  if (candidates & ~all) return DAMOE_ERR_INVALID_ARG;
+  if (candidates == 0) candidates = all;
   if (T == 0) return DAMOE_OK;
+  // 32-bit buffer offsets address the gathered token rows.
+  if ((size_t)T * L->H * 2 >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
   if (!x || !topk_w || !perm || !inv_perm || !y || !ws) return DAMOE_ERR_INVALID_ARG;
   if (force_variant < 0 && !variant_id) return DAMOE_ERR_INVALID_ARG;
   damoe_ws_layout lo;
@@ -248,6 +261,7 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
     g1.tiles.list[c] = reinterpret_cast<const int32_t*>(base + lo.tiles[c]);
   g1.variant_id = variant_id;
   g1.force_variant = force_variant;
+  g1.candidates = candidates;
   g1.ctrl = reinterpret_cast<int32_t*>(base + lo.ctrl);
   g1.k = L->k;
   g1.A = T * L->k;
@@ -268,9 +282,22 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g2.K = L->I;
   g2.N = L->H;
 
+  // Kernel classes to launch: the forced variant's, else every class holding a candidate.  The
+  // launches of a class whose variant the device did not choose return at once.
+  const uint32_t big_bit = 1u << kBigVariant;
+  const bool big = force_variant >= 0 ? force_variant == kBigVariant : (candidates & big_bit) != 0;
+  const bool mega = force_variant >= 0 ? force_variant != kBigVariant : (candidates & ~big_bit) != 0;
+  // The big-tile kernel holds an item's fp8 scale rows in LDS: at most 128 scale columns.
+  if (big && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128) return DAMOE_ERR_UNSUPPORTED;
   const int grid = dev->cus * 2;
-  if ((stage_mask & 1) && launch_gemm1(g1, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
-  if ((stage_mask & 2) && launch_gemm2(g2, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  if (stage_mask & 1) {
+    if (mega && launch_gemm1(g1, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if (big && launch_big_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  }
+  if (stage_mask & 2) {
+    if (mega && launch_gemm2(g2, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if (big && launch_big_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
+  }
   ReduceArgs r{reinterpret_cast<const float*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};
   if ((stage_mask & 4) && launch_reduce(r, stream) != hipSuccess) return DAMOE_ERR_HIP;
   return DAMOE_OK;
@@ -278,20 +305,20 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
 
 damoe_status damoe_fused_moe(const damoe_layer* L, const uint16_t* x, const float* topk_w, int32_t T,
                              const int32_t* perm, const int32_t* inv_perm, const int32_t* variant_id,
-                             int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
-                             hipStream_t stream) {
-  return fused_impl(L, 7, x, topk_w, T, perm, inv_perm, variant_id, force_variant, y, ws, ws_bytes,
-                    stream);
+                             int32_t force_variant, uint32_t candidates, uint16_t* y, void* ws,
+                             size_t ws_bytes, hipStream_t stream) {
+  return fused_impl(L, 7, x, topk_w, T, perm, inv_perm, variant_id, force_variant, candidates, y, ws,
+                    ws_bytes, stream);
 }
 
 damoe_status damoe_fused_moe_stage(const damoe_layer* L, int32_t stage, const uint16_t* x,
                                    const float* topk_w, int32_t T, const int32_t* perm,
                                    const int32_t* inv_perm, const int32_t* variant_id,
-                                   int32_t force_variant, uint16_t* y, void* ws, size_t ws_bytes,
-                                   hipStream_t stream) {
+                                   int32_t force_variant, uint32_t candidates, uint16_t* y, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
   if (stage < 0 || stage > 2) return DAMOE_ERR_INVALID_ARG;
-  return fused_impl(L, 1 << stage, x, topk_w, T, perm, inv_perm, variant_id, force_variant, y, ws,
-                    ws_bytes, stream);
+  return fused_impl(L, 1 << stage, x, topk_w, T, perm, inv_perm, variant_id, force_variant, candidates,
+                    y, ws, ws_bytes, stream);
 }
 
 damoe_status damoe_pack_weights(const damoe_layer* L, void* w1, void* w3, void* w2, hipStream_t stream) {

@@ -26,8 +26,12 @@ constexpr int kCtrlWords = 64;
 // ---------------------------------------------------------------------------------------------
 enum VariantKind : int32_t {
   kStream = 0,  // split-K over the 4 waves, weights streamed straight from HBM into registers
-  kTiled = 1,   // LDS-staged token and weight tiles, waves tile the output
+  kTiled = 1,   // LDS-staged token tile, weights streamed per wave, waves tile the output
+  kBig = 2,     // own kernel, one workgroup per CU: both operands DMA'd into LDS, 256 x 256 items
 };
+
+// Id of the big-tile variant (its kernel is launched separately from the others).
+constexpr int32_t kBigVariant = 7;
 
 struct VariantDesc {
   const char* name;
@@ -59,6 +63,7 @@ struct GemmArgs {
   TileLists tiles;
   const int32_t* variant_id;
   int32_t force_variant;
+  uint32_t candidates;  // variant ids the device-side id may hold (bit v); others are flagged
   int32_t* ctrl;
   int32_t k;
   int32_t A;           // assignments T * k
@@ -97,6 +102,9 @@ hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs&
                            hipStream_t stream);
 hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t launch_big_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t big_set_lds_limits();
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream);
 hipError_t gemm_set_lds_limits();
 hipError_t launch_pack(const void* src, void* dst, int32_t slabs, int32_t rows, int32_t cols, int32_t elem_bytes,
@@ -118,8 +126,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Device-side variant check of a fused launch: a forced variant is trusted (validated on the
+// host); a dispatched id outside the candidate set of this launch is flagged and runs nothing.
+__device__ __forceinline__ bool variant_admitted(int32_t v, int32_t force, uint32_t candidates) {
+  return force >= 0 || ((uint32_t)v < 32u && ((candidates >> v) & 1u));
+}
+
 __device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, const floatx4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ floatx16 mfma32x32x16(const uint4& a, const uint4& b, const floatx16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 

@@ -22,71 +22,13 @@
 // The weights of a (tile, feature block) are read exactly once; a larger BM
 // reads them once for more tokens at the price of padded MFMA rows.
 #include "common.h"
+#include "device.h"
 
 namespace damoe {
 namespace {
 
 constexpr int LDS_PAD = 1;
 
-
-// fp8 weights: eight OCP e4m3fn codes -> bf16 MFMA operand with the 128x128 block scale
-// folded in.  A code's 7 magnitude bits placed at fp32 bit 20 form the fp32 number
-// value * 2^-120 (exponent bias 127 vs 7; e4m3 subnormals land on fp32 subnormals, which the
-// kernels keep), so one multiply by s * 2^120 yields q * s with a single rounding, and the
-// packed convert rounds it to bf16 (nearest even).
-__device__ __forceinline__ float e4m3_times(uint32_t b, float s120) {
-  return __uint_as_float(((b & 0x7Fu) << 20) | ((b & 0x80u) << 24)) * s120;
-}
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  bf16x2 r;
-  r[0] = (__bf16)lo;
-  r[1] = (__bf16)hi;
-  return __builtin_bit_cast(uint32_t, r);
-}
-
-__device__ __forceinline__ uint4 fp8x8_to_bf16x8(uint2 q, float s120) {
-  uint4 r;
-  r.x = pack_bf16x2(e4m3_times(q.x, s120), e4m3_times(q.x >> 8, s120));
-  r.y = pack_bf16x2(e4m3_times(q.x >> 16, s120), e4m3_times(q.x >> 24, s120));
-  r.z = pack_bf16x2(e4m3_times(q.y, s120), e4m3_times(q.y >> 8, s120));
-  r.w = pack_bf16x2(e4m3_times(q.y >> 16, s120), e4m3_times(q.y >> 24, s120));
-  return r;
-}
-
-// Raw buffer loads: the slab base lives in a scalar resource descriptor, each lane keeps a
-// 32-bit byte offset and the k-step advances the scalar offset, so an operand fragment costs
-// one VGPR of addressing instead of a 64-bit pointer.  Offsets at or beyond the descriptor's
-// size read as zero (used for the padding rows of a token tile).
-constexpr uint32_t kOobOffset = 0x80000000u;
-constexpr int kAuxNontemporal = 2;  // cache-policy bit: streamed, not retained
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-}
-
-template <class T, int AUX>
-__device__ __forceinline__ T buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  if constexpr (sizeof(T) == 16) {
-    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX));
-  } else {
-    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
-  }
-}
-
-template <bool FP8>
-struct WFrag;
-template <>
-struct WFrag<false> {
-  using T = uint4;
-  static constexpr int kBytesPerElem = 2;
-};
-template <>
-struct WFrag<true> {
-  using T = uint2;
-  static constexpr int kBytesPerElem = 1;
-};
 
 // IL: the waves take interleaved 32-wide k-steps (wave w reads k-steps w, w+4, ...), so the
 //     4 waves of a workgroup read 256 contiguous bytes of every weight row at a time;
@@ -474,6 +416,10 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   extern __shared__ float smem[];
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
   if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
+  if (!variant_admitted(v, a.force_variant, a.candidates)) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
+    return;
+  }
   switch (v) {
 #define DAMOE_CASE(ID, NAME, BM, BN1, BN2, IL, NT, D)                                          \
   case ID: {                                                                                   \
@@ -535,7 +481,9 @@ const VariantDesc kVariants[] = {
 #define DAMOE_TDESC(ID, NAME, D) {NAME, kTiled, kTiledBM, kTiledNRW * 16 * 2, kTiledNRW * 16 * 4, tile_class(kTiledBM)},
     DAMOE_TILED_VARIANTS(DAMOE_TDESC)
 #undef DAMOE_TDESC
+    {"big_bm256", kBig, 256, 128, 256, tile_class(256)},  // k_gemm_big, id kBigVariant
 };
+static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kBigVariant + 1, "big variant id");
 
 constexpr size_t max_lds() {
   size_t m = 0;

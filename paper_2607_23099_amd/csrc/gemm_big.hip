@@ -1,0 +1,399 @@
+// Big-tile class of the grouped expert GEMMs (a6, a7) for prefill-sized token counts, where the
+// work is bound by the matrix cores rather than by the weight stream.
+//
+// One workgroup of 4 waves per CU.  A work item is (tile of up to 256 tokens of one expert,
+// 256 weight rows): for GEMM1 the rows are 128 features of W1 (gate) and the same 128 of W3
+// (up), so the SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.
+//
+// Each K stage of 64 columns moves the item's token rows and weight rows into LDS with direct
+// buffer -> LDS loads (no registers on the way), double-buffered so that stage s + 1 is in
+// flight while stage s is multiplied.  Both operands land in LDS in MFMA fragment order: a
+// fragment (16 rows x 32 columns of bf16, 1 KB) holds lane l's 16 bytes at l * 16.  For
+// fragment-packed weights that is a plain contiguous copy; for token rows (and row-major
+// weights) lane l gathers row l % 16, columns 8 (l / 16) .. + 7, which is the same order.
+// Every operand read is then one linear, conflict-free 16-byte LDS read per lane.
+//
+// The 4 waves tile the 256 x 256 output 2 x 2: wave (wt, wr) owns 128 tokens x 128 weight rows,
+// 4 x 4 MFMA blocks of 32 x 32 (32x32x16 bf16, 256 fp32 accumulators per lane).  Per 16-column
+// k-step a wave reads 8 KB of LDS for 16 MFMAs, i.e. 1/64 B of LDS per FLOP.
+#include <type_traits>
+
+#include "common.h"
+#include "device.h"
+
+namespace damoe {
+namespace {
+
+constexpr int kBigBM = 256;    // tokens per tile
+constexpr int kBigRows = 256;  // weight rows per item
+constexpr int kBigBK = 32;     // K columns per stage: one fragment column
+constexpr uint32_t kFrag = 1024;                              // one bf16 fragment
+constexpr uint32_t kBigTokBytes = kBigBM / 16 * kFrag;        // 16 KB of token fragments
+constexpr int kBigMaxSk = 128;  // fp8 scale columns per row held in LDS (K <= 16384)
+
+// LDS ring: as many stages as fit in the 160 KB of a CU, so the DMAs run kBufs - 1 stages
+// (3 to 4 us of MFMA work) ahead of the reads.  A stage is 16 KB of token fragments plus
+// 16 KB of bf16 (8 KB of fp8) weight fragments; fp8 adds the per-wave scale rows.
+template <bool FP8>
+struct BigCfg {
+  static constexpr int kBufs = FP8 ? 6 : 5;
+  static constexpr uint32_t kStage = kBigTokBytes + kBigRows / 16 * kFrag / (FP8 ? 2 : 1);
+  static constexpr size_t kScaleOff = kBufs * (size_t)kStage;
+  static constexpr size_t kLds = kScaleOff + (FP8 ? 4 * 2 * kBigMaxSk * 4 : 0);
+  static_assert(kLds <= 160 * 1024, "LDS of one CU");
+};
+constexpr int kXcds = 8;
+
+typedef __attribute__((address_space(3))) uint8_t lds_t;
+typedef __attribute__((address_space(3))) float lds_f32;
+
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_t* dst, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, soff, 0, 0);
+}
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 lds_read16(const lds_t* p) {
+  return __builtin_bit_cast(uint4, *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p));
+}
+
+__device__ __forceinline__ uint2 lds_read8(const lds_t* p) {
+  return __builtin_bit_cast(uint2, *reinterpret_cast<const __attribute__((address_space(3))) u32x2*>(p));
+}
+
+// s_waitcnt vmcnt(VM) lgkmcnt(LGKM) (gfx9 encoding; expcnt left alone).
+template <int VM, int LGKM>
+__device__ __forceinline__ void wait_cnt() {
+  static_assert(VM >= 0 && VM < 64 && LGKM >= 0 && LGKM < 16, "counter range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (LGKM << 8) | ((VM >> 4) << 14));
+}
+
+// Item order.  Workgroup b runs on XCD b % 8 (round-robin placement), so the items one XCD
+// holds at a time are those with equal slot index mod 8 in one round of gridDim.x slots.
+// They form a block of tg token tiles x fg feature blocks (tg * fg = gridDim.x / 8), which
+// shares the XCD's L2 between tg token tiles and fg weight blocks instead of spreading every
+// token tile over all XCDs.  Slots of a partial block are idle.
+struct ItemMap {
+  bool xcd;
+  int fg, tg, n_fg;
+  long long n_slots;
+
+  __device__ ItemMap(int n_tiles, int n_fb) {
+    const int per_xcd = gridDim.x / kXcds;
+    xcd = gridDim.x % kXcds == 0 && per_xcd > 0;
+    fg = n_fb % 4 == 0 ? 4 : n_fb % 2 == 0 ? 2 : 1;
+    if (fg > per_xcd) fg = 1;
+    tg = xcd ? per_xcd / fg : 1;
+    n_fg = n_fb / fg;
+    if (xcd) {
+      const long long chunks = (long long)((n_tiles + tg - 1) / tg) * n_fg;
+      n_slots = (chunks + kXcds - 1) / kXcds * gridDim.x;
+    } else {
+      n_slots = (long long)n_tiles * n_fb;
+    }
+  }
+
+  __device__ bool item(long long it, int n_tiles, int n_fb, int& tile, int& fb) const {
+    if (!xcd) {
+      tile = (int)(it / n_fb);
+      fb = (int)(it - (long long)tile * n_fb);
+      return tile < n_tiles;
+    }
+    const long long round = it / gridDim.x;
+    const int slot = (int)(it - round * gridDim.x);
+    const long long chunk = round * kXcds + slot % kXcds;
+    const int local = slot / kXcds;
+    if (local >= tg * fg) return false;
+    const long long tgroup = chunk / n_fg;
+    tile = (int)(tgroup * tg + local / fg);
+    fb = (int)(chunk - tgroup * n_fg) * fg + local % fg;
+    return tile < n_tiles;
+  }
+};
+
+template <bool GLU, bool FP8, bool PK>
+__device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
+  constexpr int FEAT = GLU ? kBigRows / 2 : kBigRows;  // output features per item
+  constexpr int EB = FP8 ? 1 : 2;
+  constexpr int NWDMA = FP8 ? 2 : 4;                   // weight DMAs per wave per stage
+  constexpr int D = 4 + NWDMA;                         // vector-memory ops per pipeline iteration
+  using Cfg = BigCfg<FP8>;
+  constexpr int NB = Cfg::kBufs;
+  constexpr uint32_t SB = Cfg::kStage;
+  using WRaw = typename std::conditional<FP8, uint2, uint4>::type;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wt = wave >> 1, wr = wave & 1;  // token half, weight-row half of the output
+  const int32_t* __restrict__ list = a.tiles.list[4];
+  const int n_tiles = list[0];
+  const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
+  const int K = a.K, N = a.N;
+  const int n_fb = (N + FEAT - 1) / FEAT;
+  const int nst = K / kBigBK;
+  const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
+  const uint8_t* __restrict__ wb = reinterpret_cast<const uint8_t*>(a.wb);
+  const int lr = lane & 15, lg = lane >> 4, l32 = lane & 31, lh = lane >> 5;
+  const ItemMap map(n_tiles, n_fb);
+
+  for (long long it = blockIdx.x; it < map.n_slots; it += gridDim.x) {
+    int tile, fb;
+    if (!map.item(it, n_tiles, n_fb, tile, fb)) continue;
+    const int2 en = ent[tile];
+    const int p0 = en.x, e = en.y & 0xFFFF, rows = en.y >> 16;
+    if (p0 < 0 || rows <= 0 || rows > kBigBM || p0 + rows > a.A || e >= a.E) {
+      if (tid == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
+      continue;
+    }
+    // Token fragments this wave moves: row blocks 4 * wave + j of the tile; lane l gathers
+    // row l % 16, columns 8 (l / 16) .. + 7 (padding rows read as zero).
+    __amdgpu_buffer_rsrc_t rx;
+    if (GLU) rx = make_rsrc(a.x, (uint32_t)((size_t)(a.A / a.k) * K * 2));
+    else rx = make_rsrc(a.x + (size_t)p0 * K, (uint32_t)((size_t)rows * K * 2));
+    uint32_t xo[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = (4 * wave + j) * 16 + lr;
+      if (r < rows) {
+        const uint32_t row = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) : (uint32_t)r;
+        xo[j] = row * (uint32_t)K * 2u + lg * 16u;
+      } else {
+        xo[j] = kOobOffset;
+      }
+    }
+    // Weight fragments this wave moves: item row blocks 4 * wave .. + 3.  GEMM1: item blocks
+    // 0..7 are W1 features fb * 128 + 16 b, blocks 8..15 the same features of W3.  An fp8
+    // fragment is 512 B, so one move carries two row blocks (lanes 0..31 and 32..63).
+    const size_t slab = (size_t)N * K * EB;
+    const __amdgpu_buffer_rsrc_t rw =
+        make_rsrc(((GLU && wave >= 2) ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
+    const uint32_t rb0 = GLU ? (uint32_t)fb * 8u + (wave & 1) * 4u : (uint32_t)fb * 16u + wave * 4u;
+    uint32_t wo[NWDMA];
+#pragma unroll
+    for (int j = 0; j < NWDMA; ++j) {
+      if (FP8) {
+        const uint32_t rbg = rb0 + 2 * j + lh;
+        if (PK) wo[j] = rbg * (uint32_t)(K / 32) * 512u + l32 * 16u;
+        else wo[j] = (rbg * 16u + lr) * (uint32_t)K + (lg & 1) * 16u;
+      } else {
+        const uint32_t rbg = rb0 + j;
+        if (PK) wo[j] = (rbg * (uint32_t)(K / 32) * 64u + lane) * 16u;
+        else wo[j] = ((rbg * 16u + lr) * (uint32_t)K + lg * 8u) * 2u;
+      }
+    }
+    auto dma_stage = [&](int st, lds_t* sb) __attribute__((always_inline)) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dma16(rx, sb + (4 * wave + j) * kFrag, xo[j], (uint32_t)st * 64u);
+#pragma unroll
+      for (int j = 0; j < NWDMA; ++j) {
+        const uint32_t so = FP8 ? (PK ? (uint32_t)st * 512u : (uint32_t)st * 32u)
+                                : (PK ? (uint32_t)st * 1024u : (uint32_t)st * 64u);
+        dma16(rw, sb + kBigTokBytes + (NWDMA * wave + j) * kFrag, wo[j], so);
+      }
+    };
+
+    // fp8 block scales of this wave's rows (one 128-row block per matrix): the item's row of
+    // scale columns is staged in LDS, K stage st reads column st / 4 with its operands.
+    lds_f32* sc_lds = nullptr;
+    if constexpr (FP8) {
+      const int sk = K / 128;
+      const int srow = GLU ? fb : fb * 2 + wr;
+      const bool srow_ok = srow < N / 128;
+      const size_t sbase = ((size_t)e * (N / 128) + (srow_ok ? srow : 0)) * sk;
+      lds_f32* wsc = reinterpret_cast<lds_f32*>(lds + Cfg::kScaleOff) + wave * 2 * kBigMaxSk;
+#pragma unroll
+      for (int h = 0; h < kBigMaxSk / 64; ++h) {
+        const int i = h * 64 + lane;
+        if (i < sk) {
+          wsc[i] = srow_ok ? a.sa[sbase + i] * 0x1p120f : 0.f;
+          if (GLU) wsc[kBigMaxSk + i] = srow_ok ? a.sb[sbase + i] * 0x1p120f : 0.f;
+        }
+      }
+      sc_lds = wsc;
+    }
+
+    // Wave (wt, wr) accumulates 4 x 4 MFMA blocks of 32 x 32: block (m, n) = weight rows
+    // 32 m .. + 31 of the wave's 128 (GEMM1: m = 0, 1 gate features, m = 2, 3 the same up
+    // features) x tokens wt * 128 + 32 n .. + 31.
+    floatx16 acc[4][4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int n = 0; n < 4; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
+
+    // Operands of one 16-column k-step (ks = 0, 1 of a stage).  A 32x32x16 operand lane l
+    // takes row l % 32 (fragment row block (l % 32) / 16, row l % 16 in it) and the 8-column
+    // chunk 2 ks + l / 32 of the 32-column fragment.
+    struct Ops {
+      WRaw w[4];
+      uint4 t[4];
+      float sg, su;  // fp8: block scales of the stage (times 2^120)
+    };
+    auto read_ops = [&](int ks, int st, const lds_t* cur, Ops& o) __attribute__((always_inline)) {
+      const int c = 2 * ks + lh;
+      if constexpr (FP8) {
+        o.sg = sc_lds[st >> 2];
+        if (GLU) o.su = sc_lds[kBigMaxSk + (st >> 2)];
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const int wrb = (GLU ? (m < 2 ? wr * 4 + 2 * m : 8 + wr * 4 + 2 * (m - 2)) : wr * 8 + 2 * m) + (l32 >> 4);
+        if constexpr (FP8) {
+          const lds_t* blk = cur + kBigTokBytes + (wrb >> 1) * kFrag + (wrb & 1) * 512;
+          if (PK) o.w[m] = lds_read8(blk + (lr + 16 * c) * 8);
+          else o.w[m] = lds_read8(blk + (ks * 16 + lr) * 16 + 8 * lh);
+        } else {
+          o.w[m] = lds_read16(cur + kBigTokBytes + wrb * kFrag + (lr + 16 * c) * 16);
+        }
+      }
+#pragma unroll
+      for (int n = 0; n < 4; ++n)
+        o.t[n] = lds_read16(cur + (wt * 8 + 2 * n + (l32 >> 4)) * kFrag + (lr + 16 * c) * 16);
+    };
+    auto mma = [&](const Ops& o) __attribute__((always_inline)) {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        uint4 wv;
+        if constexpr (FP8) wv = fp8x8_to_bf16x8(o.w[m], (GLU && m >= 2) ? o.su : o.sg);
+        else wv = o.w[m];
+#pragma unroll
+        for (int n = 0; n < 4; ++n) acc[m][n] = mfma32x32x16(wv, o.t[n], acc[m][n]);
+      }
+    };
+
+    // Software pipeline.  Iteration t (between barriers t - 1 and t): DMA of stage t + NB - 1 into
+    // the buffer stage t - 1 left, operand reads of stage t (k-step 0 then 1) each issued
+    // ahead of the MFMAs of the previous k-step, then wait for this wave's DMAs of stage
+    // t + 1 and its LDS reads, and the barrier that makes stage t + 1 visible to every wave
+    // and frees stage t's buffer.  The barrier is a bare s_barrier: the counter waits before
+    // it are the ordering (a fence would drain the DMAs still ahead).  `dst` and `cur` are
+    // distinct buffers, so the compiler does not hold the reads of `cur` behind the DMA
+    // writes into `dst`.  Stages past the last are re-issued as the last stage into buffers
+    // nobody reads again.
+    Ops A, B;
+    auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto first)
+        __attribute__((always_inline)) {
+      dma_stage(min(t + NB - 1, nst - 1), dst);
+      read_ops(0, t, cur, A);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (!decltype(first)::value) mma(B);
+      __builtin_amdgcn_sched_barrier(0);
+      read_ops(1, t, cur, B);
+      __builtin_amdgcn_sched_barrier(0);
+      mma(A);
+      __builtin_amdgcn_sched_barrier(0);
+      wait_cnt<(NB - 2) * D, 0>();
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+    };
+
+#pragma unroll
+    for (int st = 0; st < NB - 1; ++st) dma_stage(min(st, nst - 1), lds + st * SB);
+    wait_cnt<(NB - 2) * D, 15>();  // this wave's stage-0 moves have landed
+    __syncthreads();        // ... and every wave's (also orders the scale rows in LDS)
+    iter(lds + (NB - 1) * SB, lds, 0, std::true_type{});
+    for (int t = 1; t < nst; ++t)
+      iter(lds + ((t + NB - 1) % NB) * SB, lds + (t % NB) * SB, t, std::false_type{});
+    mma(B);
+    // Moves of re-issued stages may still be in flight: drain before the next item's DMAs.
+    wait_cnt<0, 0>();
+    __syncthreads();
+
+    // Epilogue from the accumulators: in block (m, n) lane l holds token 32 n + l % 32 and, in
+    // registers 4 q .. 4 q + 3, weight rows 8 q + 4 (l / 32) .. + 3.
+#pragma unroll
+    for (int n = 0; n < 4; ++n) {
+      const int i = wt * 128 + n * 32 + l32;
+      if (i >= rows) continue;
+      const size_t orow = (size_t)(p0 + i) * N;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (GLU) {
+#pragma unroll
+          for (int m = 0; m < 2; ++m) {
+            const int f = fb * FEAT + wr * 64 + m * 32 + 8 * q + 4 * lh;
+            if (f >= N) continue;
+            float hv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float g = acc[m][n][4 * q + r], u = acc[m + 2][n][4 * q + r];
+              hv[r] = g / (1.0f + __expf(-g)) * u;
+            }
+            uint2 pk;
+            pk.x = pack_bf16x2(hv[0], hv[1]);
+            pk.y = pack_bf16x2(hv[2], hv[3]);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
+          }
+        } else {
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const int f = fb * FEAT + wr * 128 + m * 32 + 8 * q + 4 * lh;
+            if (f >= N) continue;
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
+                make_float4(acc[m][n][4 * q], acc[m][n][4 * q + 1], acc[m][n][4 * q + 2], acc[m][n][4 * q + 3]);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <bool GLU, bool FP8, bool PK>
+__global__ void __launch_bounds__(kGemmThreads, 1) k_gemm_big(GemmArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t big_smem[];
+  const int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
+  if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
+  if (!variant_admitted(v, a.force_variant, a.candidates)) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
+    return;
+  }
+  if (v != kBigVariant) return;  // the device chose a variant of the other kernel class
+  big_body<GLU, FP8, PK>(a, (lds_t*)big_smem);
+}
+
+template <bool GLU>
+hipError_t launch_big_stage(const GemmArgs& a, int grid, hipStream_t stream) {
+  if (a.fp8) {
+    if (a.packed) hipLaunchKernelGGL((k_gemm_big<GLU, true, true>), dim3(grid), dim3(kGemmThreads), BigCfg<true>::kLds, stream, a);
+    else hipLaunchKernelGGL((k_gemm_big<GLU, true, false>), dim3(grid), dim3(kGemmThreads), BigCfg<true>::kLds, stream, a);
+  } else {
+    if (a.packed) hipLaunchKernelGGL((k_gemm_big<GLU, false, true>), dim3(grid), dim3(kGemmThreads), BigCfg<false>::kLds, stream, a);
+    else hipLaunchKernelGGL((k_gemm_big<GLU, false, false>), dim3(grid), dim3(kGemmThreads), BigCfg<false>::kLds, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t big_set_lds_limits() {
+  struct Fn {
+    const void* f;
+    size_t lds;
+  };
+  const Fn fns[] = {
+      {reinterpret_cast<const void*>(&k_gemm_big<true, false, false>), BigCfg<false>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<false, false, false>), BigCfg<false>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<true, true, false>), BigCfg<true>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<false, true, false>), BigCfg<true>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<true, false, true>), BigCfg<false>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<false, false, true>), BigCfg<false>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<true, true, true>), BigCfg<true>::kLds},
+      {reinterpret_cast<const void*>(&k_gemm_big<false, true, true>), BigCfg<true>::kLds}};
+  for (const Fn& f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f.f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)f.lds);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_big_gemm1(const GemmArgs& a, int grid, hipStream_t stream) {
+  return launch_big_stage<true>(a, grid, stream);
+}
+
+hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream) {
+  return launch_big_stage<false>(a, grid, stream);
+}
+
+}  // namespace damoe

@@ -209,6 +209,7 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   float* d_w = nullptr;
   uint64_t* d_nd = nullptr;
   uint16_t* d_y = nullptr;
+  int32_t* d_vid = nullptr;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   std::vector<int32_t> t_bucket, t_nex, t_noda, t_kid, t_Q;
   std::vector<double> alphas(cfg->n_skews);
@@ -227,6 +228,7 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   TRY_HIP(hipMalloc(&d_nd, sizeof(uint64_t) * 2));
   TRY_HIP(hipMalloc(&d_bucket, sizeof(int32_t)));
   TRY_HIP(hipMalloc(&d_y, sizeof(uint16_t) * (size_t)T_max * H));
+  TRY_HIP(hipMalloc(&d_vid, sizeof(int32_t)));
   TRY_HIP(hipMemset(ws, 0, ws_bytes));
   TRY_HIP(hipEventCreate(&e0));
   TRY_HIP(hipEventCreate(&e1));
@@ -257,11 +259,11 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
       for (int32_t v = 0; v < nv; ++v) {
         if (!damoe_variant_supports(v, L->wdtype)) continue;
         // warm-up
-        s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, d_y, ws, ws_bytes, stream);
+        s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, 0u, d_y, ws, ws_bytes, stream);
         if (s2 != DAMOE_OK) return s2;
         for (int32_t r = 0; r < cfg->reps; ++r) {
           if (hipEventRecord(e0, stream)) return DAMOE_ERR_HIP;
-          s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, d_y, ws, ws_bytes, stream);
+          s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, 0u, d_y, ws, ws_bytes, stream);
           if (s2 != DAMOE_OK) return s2;
           if (hipEventRecord(e1, stream) || hipEventSynchronize(e1)) return DAMOE_ERR_HIP;
           float ms = 0.f;
@@ -323,6 +325,68 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
         t_kid[first_ex + j] = best;
       }
     }
+    // Cost of the exemplar match itself: route + match on a one-bucket table of this bucket's
+    // exemplars whose kernels differ (so every call scores them), minus route alone, both on
+    // the last routing timed above.  The per-exemplar choice is kept only when its mean over
+    // the bucket's samples, charged this cost, beats the best single variant; otherwise every
+    // exemplar maps to that variant and the online step skips the match.
+    {
+      std::vector<int32_t> kid_probe(n_added), noda_probe(1, 0), bt(1, T), nex(1, n_added);
+      for (int32_t j = 0; j < n_added; ++j) kid_probe[j] = j & 1;
+      damoe_table_desc pd{};
+      pd.E = E;
+      pd.k = k;
+      pd.H = L->H;
+      pd.I = L->I;
+      pd.wdtype = L->wdtype;
+      pd.n_buckets = 1;
+      pd.bucket_T = bt.data();
+      pd.n_ex = nex.data();
+      pd.Q = t_Q.data() + first_ex * E;
+      pd.kid = kid_probe.data();
+      pd.noda = noda_probe.data();
+      damoe_table* probe = nullptr;
+      TRY(damoe_table_create(&pd, &probe));
+      const int32_t nrep = 2 * cfg->reps + 1;
+      std::vector<float> t_route(nrep), t_match(nrep);
+      damoe_status s3 = DAMOE_OK;
+      for (int32_t r = 0; r < nrep && s3 == DAMOE_OK; ++r) {
+        for (int32_t m = 0; m < 2 && s3 == DAMOE_OK; ++m) {
+          if (hipEventRecord(e0, stream)) s3 = DAMOE_ERR_HIP;
+          if (s3 == DAMOE_OK)
+            s3 = m == 0 ? damoe_route_histogram(d_ids, T, k, E, d_counts, d_off, d_perm, d_inv, d_nd, d_bucket,
+                                                ws, ws_bytes, stream)
+                        : damoe_route_dispatch(probe, d_ids, T, k, E, d_counts, d_off, d_perm, d_inv, d_nd,
+                                               d_bucket, d_vid, ws, ws_bytes, stream);
+          float ms = 0.f;
+          if (s3 == DAMOE_OK && (hipEventRecord(e1, stream) || hipEventSynchronize(e1) ||
+                                 hipEventElapsedTime(&ms, e0, e1)))
+            s3 = DAMOE_ERR_HIP;
+          (m == 0 ? t_route : t_match)[r] = ms;
+        }
+      }
+      damoe_table_destroy(probe);
+      TRY(s3);
+      std::nth_element(t_route.begin(), t_route.begin() + nrep / 2, t_route.end());
+      std::nth_element(t_match.begin(), t_match.begin() + nrep / 2, t_match.end());
+      const double match_cost = std::max(0.0, (double)t_match[nrep / 2] - (double)t_route[nrep / 2]);
+      double adaptive = match_cost;
+      std::vector<double> single(nv, 0.0);
+      for (int32_t j = 0; j < n_added; ++j) {
+        adaptive += skew_mean[j][t_kid[first_ex + j]] / n_added;
+        for (int32_t v = 0; v < nv; ++v) single[v] += skew_mean[j][v] / n_added;
+      }
+      int32_t best = 0;
+      for (int32_t v = 1; v < nv; ++v)
+        if (single[v] < single[best]) best = v;
+      const bool collapse = adaptive >= single[best];
+      if (collapse)
+        for (int32_t j = 0; j < n_added; ++j) t_kid[first_ex + j] = best;
+      if (cfg->verbose)
+        std::fprintf(stderr, "damoe_tune: T=%d match %.1f us; adaptive %.1f us vs %s %.1f us%s\n", T,
+                     match_cost * 1e3, adaptive * 1e3, damoe_variant_name(best), single[best] * 1e3,
+                     collapse ? " -> single variant" : "");
+    }
     // Distribution-unaware baseline: the fastest variant under uniform routing.
     {
       std::vector<double> mean(nv, 0.0), lat;
@@ -369,6 +433,7 @@ done:
   (void)hipFree(d_nd);
   (void)hipFree(d_bucket);
   (void)hipFree(d_y);
+  (void)hipFree(d_vid);
   return st;
 }
 

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdamoe.so")
 
 N_TILE_SIZES = 5
 W_BF16, W_FP8_B128 = 0, 1
+DEVERR_EXPERT_ID, DEVERR_TILES, DEVERR_VARIANT = 1, 2, 4
 LAYOUT_ROWMAJOR, LAYOUT_FRAG16 = 0, 1
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",
@@ -29,6 +30,7 @@ EXPORTED = [
     "damoe_table_load", "damoe_dispatch", "damoe_fused_moe", "damoe_num_variants", "damoe_variant_name",
     "damoe_variant_tile_m", "damoe_variant_supports", "damoe_tune", "damoe_alpha_search",
     "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch", "damoe_pack_weights",
+    "damoe_table_candidates",
 ]
 
 
@@ -77,8 +79,8 @@ def lib() -> ctypes.CDLL:
             raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
                                "(the fused-MoE path has no fallback)")
         L = ctypes.CDLL(LIB_PATH)
-        vp, i32, u64, sz, f64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t,
-                                 ctypes.c_double)
+        vp, i32, u32, u64, sz, f64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64,
+                                      ctypes.c_size_t, ctypes.c_double)
         sigs = {
             "damoe_status_string": ([i32], ctypes.c_char_p),
             "damoe_workspace_layout": ([i32, i32, i32, i32, i32, vp], i32),
@@ -91,8 +93,9 @@ def lib() -> ctypes.CDLL:
             "damoe_table_load": ([ctypes.c_char_p, vp], i32),
             "damoe_dispatch": ([vp, vp, i32, vp, vp, sz, vp], i32),
             "damoe_route_dispatch": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
-            "damoe_fused_moe": ([vp, vp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
-            "damoe_fused_moe_stage": ([vp, i32, vp, vp, i32, vp, vp, vp, i32, vp, vp, sz, vp], i32),
+            "damoe_fused_moe": ([vp, vp, vp, i32, vp, vp, vp, i32, u32, vp, vp, sz, vp], i32),
+            "damoe_fused_moe_stage": ([vp, i32, vp, vp, i32, vp, vp, vp, i32, u32, vp, vp, sz, vp], i32),
+            "damoe_table_candidates": ([vp, i32], u32),
             "damoe_num_variants": ([], i32),
             "damoe_variant_name": ([i32], ctypes.c_char_p),
             "damoe_variant_tile_m": ([i32], i32),
@@ -196,17 +199,20 @@ def dispatch(table: "Table", counts, T, variant_id, ws, stream=None):
                                                   ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def fused_moe(layer: Layer, x, w, T, perm, inv_perm, variant_id, force_variant, y, ws, stream=None):
+def fused_moe(layer: Layer, x, w, T, perm, inv_perm, variant_id, force_variant, y, ws, stream=None,
+              candidates: int = 0):
+    """candidates: bit mask of the variant ids *variant_id may hold (Table.candidates(T)); 0 = all."""
     _check("damoe_fused_moe", lib().damoe_fused_moe(
         ctypes.byref(layer), _p(x), _p(w), T, _p(perm), _p(inv_perm), _p(variant_id), int(force_variant),
-        _p(y), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
+        int(candidates), _p(y), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def fused_moe_stage(layer: Layer, stage, x, w, T, perm, inv_perm, variant_id, force_variant, y, ws,
-                    stream=None):
+                    stream=None, candidates: int = 0):
     _check("damoe_fused_moe_stage", lib().damoe_fused_moe_stage(
         ctypes.byref(layer), int(stage), _p(x), _p(w), T, _p(perm), _p(inv_perm), _p(variant_id),
-        int(force_variant), _p(y), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
+        int(force_variant), int(candidates), _p(y), _p(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
 
 
 def read_device_error(ws, stream=None) -> int:
@@ -254,6 +260,10 @@ class Table:
         h = ctypes.c_void_p()
         _check("damoe_table_load", lib().damoe_table_load(path.encode(), ctypes.byref(h)))
         return cls(h.value)
+
+    def candidates(self, T: int) -> int:
+        """Bit mask of the variants dispatch may choose for T tokens (T's bucket row + noda)."""
+        return int(lib().damoe_table_candidates(self.handle, int(T)))
 
     def save(self, path: str):
         _check("damoe_table_save", lib().damoe_table_save(self.handle, path.encode()))

@@ -76,6 +76,7 @@ class Path:
         self.x = torch.zeros((max(T_max, 1), sh.H), dtype=torch.bfloat16, device=device)
         self.y = torch.zeros((max(T_max, 1), sh.H), dtype=torch.bfloat16, device=device)
         self.ws = torch.zeros(damoe.workspace_size(dl.layer, T_max), dtype=torch.uint8, device=device)
+        self.candidates = 0  # variants the last dispatch could choose (0 = all)
 
     def set_routing(self, r: synth.Routing):
         T = r.T
@@ -98,19 +99,22 @@ class Path:
 
     def route_dispatch(self, table: damoe.Table, T: int, ids=None, stream=None):
         sh = self.dl.shape
+        self.candidates = table.candidates(T)
         damoe.route_dispatch(table, self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
                              self.perm, self.inv_perm, self.numden, self.bucket, self.variant, self.ws, stream)
 
     def dispatch(self, table: damoe.Table, T: int, stream=None):
+        self.candidates = table.candidates(T)
         damoe.dispatch(table, self.counts, T, self.variant, self.ws, stream)
 
     def fused(self, T: int, force_variant: int = -1, w=None, stream=None):
         damoe.fused_moe(self.dl.layer, self.x, self.w if w is None else w, T, self.perm, self.inv_perm,
-                        self.variant, force_variant, self.y, self.ws, stream)
+                        self.variant, force_variant, self.y, self.ws, stream, candidates=self.candidates)
 
     def fused_stage(self, stage: int, T: int, force_variant: int = -1, w=None, stream=None):
         damoe.fused_moe_stage(self.dl.layer, stage, self.x, self.w if w is None else w, T, self.perm,
-                              self.inv_perm, self.variant, force_variant, self.y, self.ws, stream)
+                              self.inv_perm, self.variant, force_variant, self.y, self.ws, stream,
+                              candidates=self.candidates)
 
     def ctrl(self):
         lo = damoe.workspace_layout(self.dl.shape.E, self.dl.shape.k, self.dl.shape.H, self.dl.shape.I,

@@ -91,24 +91,28 @@ def test_validation_before_launch():
     # fused_moe
     fm = L.damoe_fused_moe
     lay = _fake_layer()
-    assert fm(None, P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -1
-    assert fm(ctypes.byref(_fake_layer(H=200)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
-    assert fm(ctypes.byref(_fake_layer(w2=0)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -1
-    assert fm(ctypes.byref(_fake_layer(wdtype=1)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -1  # no scales
-    assert fm(ctypes.byref(_fake_layer(wdtype=1, s1=P, s3=P, s2=P)), P, P, 4, P, P, P, -1, P, P, ws_ok,
+    assert fm(None, P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(_fake_layer(H=200)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -2
+    assert fm(ctypes.byref(_fake_layer(w2=0)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(_fake_layer(wdtype=1)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -1  # no scales
+    assert fm(ctypes.byref(_fake_layer(wdtype=1, s1=P, s3=P, s2=P)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok,
               None) == -2  # fp8 needs H, I multiples of 512
-    assert fm(ctypes.byref(_fake_layer(wdtype=5)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
-    assert fm(ctypes.byref(_fake_layer(layout=2)), P, P, 4, P, P, P, -1, P, P, ws_ok, None) == -2
+    assert fm(ctypes.byref(_fake_layer(wdtype=5)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -2
+    assert fm(ctypes.byref(_fake_layer(layout=2)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -2
     # pack_weights: the source must be row-major and the destinations must not overlap it
     pk = L.damoe_pack_weights
     assert pk(ctypes.byref(_fake_layer(layout=1)), P, P, P, None) == -1
     assert pk(ctypes.byref(_fake_layer()), 0x1000, 0x900000, 0xA00000, None) == -1  # w1 dst == w1 src
     assert pk(ctypes.byref(_fake_layer()), None, P, P, None) == -1
-    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, damoe.num_variants(), P, P, ws_ok, None) == -1
-    assert fm(ctypes.byref(lay), P, P, 4, P, P, None, -1, P, P, ws_ok, None) == -1  # no variant id
-    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, -1, P, P, 1024, None) == -3
-    assert fm(ctypes.byref(lay), P, P, -2, P, P, P, -1, P, P, ws_ok, None) == -1
-    assert fm(ctypes.byref(lay), None, None, 0, None, None, None, 0, None, None, 0, None) == 0  # T = 0 no-op
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, damoe.num_variants(), 0, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, None, -1, 0, P, P, ws_ok, None) == -1  # no variant id
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, -1, 0, P, P, 1024, None) == -3
+    assert fm(ctypes.byref(lay), P, P, -2, P, P, P, -1, 0, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(lay), None, None, 0, None, None, None, 0, 0, None, None, 0, None) == 0  # T = 0 no-op
+    # candidates: bits beyond the registry are rejected; T * H * 2 must fit 31 bits
+    nv = damoe.num_variants()
+    assert fm(ctypes.byref(lay), P, P, 4, P, P, P, -1, 1 << nv, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(_fake_layer(H=7168)), P, P, 150000, P, P, P, -1, 0, P, P, 1 << 50, None) == -2
     # dispatch
     assert L.damoe_dispatch(None, P, 4, P, P, ws_ok, None) == -1
     # workspace size of an invalid layer is 0

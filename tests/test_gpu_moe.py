@@ -50,7 +50,10 @@ def test_tiny_every_variant(tiny, T, alpha, seed):
         assert path.ctrl()[4] == v
 
 
-def test_tiny_adaptive_uses_device_variant(tiny):
+@pytest.mark.parametrize("noda_same", [False, True], ids=["two-classes", "one-class"])
+def test_tiny_adaptive_uses_device_variant(tiny, noda_same):
+    # The device-side id picks the variant; with noda == kid the candidate mask holds one
+    # variant, so only that variant's kernel class is launched.
     torch = torch_cuda()
     dl, path = tiny
     sh = dl.shape
@@ -58,14 +61,68 @@ def test_tiny_adaptive_uses_device_variant(tiny):
     nv = damoe.num_variants()
     for target in range(nv):
         q = np.full((1, sh.E), int(round(2 ** 15 / np.sqrt(sh.E))), np.int32)
+        noda = target if noda_same else 0
         td = damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0, bucket_T=np.array([1 << 20]),
-                             n_ex=np.array([1]), Q=q, kid=np.array([target]), noda=np.array([0]))
+                             n_ex=np.array([1]), Q=q, kid=np.array([target]), noda=np.array([noda]))
         table = damoe.Table.create(td)
+        assert table.candidates(64) == (1 << target) | (1 << noda)
         _run(path, r, 0, table=table)
         assert int(path.variant.item()) == target and path.ctrl()[4] == target
         y_adaptive = path.y[:64].clone()
         _run(path, r, 0, variant=target)
         assert torch.equal(y_adaptive, path.y[:64])
+    assert damoe.read_device_error(path.ws) == 0
+
+
+def test_tiny_dispatch_outside_candidates_is_flagged(tiny):
+    # A dispatched id that the caller's candidate mask does not hold runs no expert GEMM and
+    # sets the sticky device error, whichever kernel class holds it (y is then unspecified).
+    torch = torch_cuda()
+    dl, path = tiny
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, 64, 1.0, 0)
+    nv = damoe.num_variants()
+    for target, cand in [(3, 1 << 0), (nv - 1, 1 << 0), (0, 1 << (nv - 1))]:
+        q = np.full((1, sh.E), 1000, np.int32)
+        td = damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0, bucket_T=np.array([1 << 20]),
+                             n_ex=np.array([1]), Q=q, kid=np.array([target]), noda=np.array([target]))
+        table = damoe.Table.create(td)
+        path.set_routing(r)
+        path.fill_x(64, 0)
+        path.y.fill_(float("nan"))
+        path.route_dispatch(table, 64)
+        path.candidates = cand
+        path.fused(64, -1)
+        torch.cuda.synchronize()
+        assert int(path.variant.item()) == target
+        assert damoe.read_device_error(path.ws) == damoe.DEVERR_VARIANT
+
+
+SMALL_FP8 = synth.Shape("small-fp8", E=8, k=2, H=512, I=1024, shape_id=5, wdtype="fp8")
+
+
+@pytest.fixture(scope="module", params=[False, True], ids=["rowmajor", "packed"])
+def small_fp8(request):
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    dl = DeviceLayer(SMALL_FP8, packed=request.param)
+    yield dl, Path(dl, 512), synth.ExpertWeightSource(SMALL_FP8)
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T,alpha,seed", [(64, 1.0, 4), (300, 0.05, 5), (3, 10.0, 6)])
+def test_small_fp8_every_variant(small_fp8, T, alpha, seed):
+    # fp8 block-128 weights in both layouts, tiles of every size incl. two 256-token tiles.
+    dl, path, src = small_fp8
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, alpha, [seed])
+    rows = np.arange(T) if T <= 64 else np.sort(np.random.default_rng(T).choice(T, 48, replace=False))
+    ref = oracle_rows(sh, r, seed, rows, src)
+    for v in _variants():
+        log(f"small fp8 T={T} alpha={alpha} variant={damoe.variant_name(v)}")
+        _run(path, r, seed, v)
+        err = row_err(bf16_rows(path.y, rows), ref)
+        assert err <= TOL["fp8"], (v, err)
 
 
 def test_tiny_zero_tokens_is_noop(tiny):
