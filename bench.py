@@ -188,6 +188,119 @@ def run_trace(args):
     print(json.dumps(out), flush=True)
 
 
+def run_dispatch(args):
+    """Dispatch mechanisms on the DeepSeek-V3 decode shape (the analog of the paper's table of
+    conditional-graph costs, Sec. V-C): the whole a2-a8 call, host wall clock from an idle
+    stream to the end of the call, for
+      host      route + match, the variant id copied to the host, then the forced variant
+      device    route + match, the kernels read the id in device memory (this build)
+      single    route with a one-variant table (no match) + device id
+      fixed     route without any dispatch + the forced variant
+      graph-*   the device and fixed sequences captured once in a HIP graph and replayed."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+
+    shape = synth.DS
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    dl = DeviceLayer(shape)
+    path = Path(dl, max(DECODE_T))
+    path.fill_x(max(DECODE_T), 1)
+    torch.cuda.synchronize()
+    tuned, note = load_or_tune_table(dl, path.x, args.quick_tune)
+    td = tuned.data(shape.E)
+    alpha, n = 0.3, args.dispatch_reps
+    rows = {}
+    for T in DECODE_T:
+        b = next((i for i, bt in enumerate(td.bucket_T) if T <= bt), len(td.bucket_T) - 1)
+        sl = td.bucket_rows(b)
+        q = td.Q[sl]
+        best = int(np.bincount(td.kid[sl]).argmax())
+        other = 1 if best != 1 else 0
+        kid = np.full(len(q), best)
+        kid[-1] = other  # two kernels in the row: every call scores the exemplars
+        mk = lambda k_: damoe.Table.create(damoe.TableData(E=shape.E, k=shape.k, H=shape.H, I=shape.I, wdtype=0,
+                                                           bucket_T=np.array([T]), n_ex=np.array([len(q)]), Q=q,
+                                                           kid=k_, noda=np.array([best])))
+        match_t, single_t = mk(kid), mk(np.full(len(q), best))
+        r = synth.routing(shape.E, shape.k, T, alpha, synth.seed_decode(T, alpha, 0))
+        path.set_routing(r)
+        path.route_dispatch(match_t, T)
+        torch.cuda.synchronize()
+        v = int(path.variant.item())
+
+        def host():
+            path.route_dispatch(match_t, T)
+            path.fused(T, int(path.variant.item()))
+
+        def device():
+            path.route_dispatch(match_t, T)
+            path.fused(T, -1)
+
+        def single():
+            path.route_dispatch(single_t, T)
+            path.fused(T, -1)
+
+        def fixed():
+            path.route(T)
+            path.fused(T, v)
+
+        graphs = {}
+        for name, fn in (("graph-device", device), ("graph-fixed", fixed)):
+            s_ = torch.cuda.Stream()
+            s_.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s_):
+                fn()
+            torch.cuda.current_stream().wait_stream(s_)
+            torch.cuda.synchronize()
+            g_ = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_, stream=s_):
+                fn()
+            torch.cuda.synchronize()
+            graphs[name] = g_
+        mech = {"host": host, "device": device, "single": single, "fixed": fixed,
+                "graph-device": graphs["graph-device"].replay, "graph-fixed": graphs["graph-fixed"].replay}
+        res = {}
+        for name, fn in mech.items():
+            for _ in range(5):
+                fn()
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(n):
+                t0 = time.perf_counter()
+                fn()
+                torch.cuda.synchronize()
+                ts.append((time.perf_counter() - t0) * 1e6)
+            res[name] = round(float(np.median(ts)), 1)
+        res["variant"] = damoe.variant_name(v)
+        rows[f"T{T}"] = res
+        log(f"dispatch T={T}: {res}")
+    over = lambda name: [rows[k][name] - rows[k]["fixed"] for k in rows]
+    out = {
+        "metric": "device-side dispatch overhead over a fixed kernel (DeepSeek-V3 decode, median over T)",
+        "value": round(float(np.median(over("device"))), 1),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": n,
+        "warmup": 5,
+        "ms_per_step": round(float(np.mean([rows[k]["device"] for k in rows])) / 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dsv3 dispatch mechanisms: E=256 top-8 H=7168 I=2048 bf16, T in {1,8,32,128}, "
+                               "alpha=0.3, host wall clock per layer call (idle stream to completion)",
+                   "table": note},
+        "host_copyback_overhead_us": round(float(np.median(over("host"))), 1),
+        "single_variant_overhead_us": round(float(np.median(over("single"))), 1),
+        "graph_device_over_graph_fixed_us": round(float(np.median(
+            [rows[k]["graph-device"] - rows[k]["graph-fixed"] for k in rows])), 1),
+        "per_T_us": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -196,7 +309,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
-    ap.add_argument("--workload", choices=["decode-sweep", "trace"], default="decode-sweep")
+    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch"], default="decode-sweep")
+    ap.add_argument("--dispatch-reps", type=int, default=200)
     ap.add_argument("--trace-steps", type=int, default=1000)
     ap.add_argument("--trace-reps", type=int, default=3)
     args = ap.parse_args()
@@ -216,6 +330,8 @@ def main():
     damoe.lib()  # fails loudly if the HIP library is not built
     if args.workload == "trace":
         return run_trace(args)
+    if args.workload == "dispatch":
+        return run_dispatch(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")

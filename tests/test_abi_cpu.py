@@ -166,3 +166,24 @@ def test_table_roundtrip_host(tmp_path):
         d = damoe.TableData(**{**td.__dict__, **bad})
         with pytest.raises(damoe.DamoeError):
             damoe.Table.create(d)
+
+
+def test_committed_tables_match_the_variant_registry():
+    # bench.py loads these; a table written for another variant set would be rejected and
+    # silently replaced by a quick start-up tune.
+    tdir = os.path.join(ROOT, "paper_2607_23099_amd", "tables")
+    names = sorted(f for f in os.listdir(tdir) if f.endswith(".damoe"))
+    assert {"dsv3.damoe", "kimi-k2.damoe"} <= set(names)
+    nv = damoe.num_variants()
+    for f in names:
+        t = damoe.Table.load(os.path.join(tdir, f))
+        E = 256 if f.startswith("dsv3") else 384
+        td = t.data(E)
+        assert td.kid.min() >= 0 and td.kid.max() < nv and td.noda.max() < nv
+        assert np.all(np.diff(td.bucket_T) > 0)
+        # every bucket's candidate mask holds exactly its kernels and its noda kernel
+        for b, T in enumerate(td.bucket_T):
+            want = (1 << int(td.noda[b]))
+            for v in td.kid[td.bucket_rows(b)]:
+                want |= 1 << int(v)
+            assert t.candidates(int(T)) == want
