@@ -126,6 +126,37 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Kernel arguments are read with scalar loads where first used, and each such load waits a
+// full memory latency (the argument block is written by the launch, so it is never cached).
+// pin() makes the value live in scalar registers at the point of the call, so that all the
+// fields pinned at kernel entry are fetched together, with one wait; later uses of the same
+// (invariant) argument fields reuse those registers.
+template <class T>
+__device__ __forceinline__ void pin(const T& v) {
+  asm volatile("" ::"s"(v));
+}
+
+__device__ __forceinline__ void pin_gemm_args(const GemmArgs& a) {
+  pin(a.x);
+  pin(a.wa);
+  pin(a.wb);
+  pin(a.sa);
+  pin(a.sb);
+  pin(a.perm);
+  pin(a.out);
+#pragma unroll
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) pin(a.tiles.list[c]);
+  pin(a.variant_id);
+  pin(a.force_variant);
+  pin(a.candidates);
+  pin(a.ctrl);
+  pin(a.k);
+  pin(a.A);
+  pin(a.E);
+  pin(a.K);
+  pin(a.N);
+}
+
 // Device-side variant check of a fused launch: a forced variant is trusted (validated on the
 // host); a dispatched id outside the candidate set of this launch is flagged and runs nothing.
 __device__ __forceinline__ bool variant_admitted(int32_t v, int32_t force, uint32_t candidates) {

@@ -414,6 +414,7 @@ constexpr int tile_class(int bm) { return bm == 16 ? 0 : bm == 32 ? 1 : bm == 64
 template <bool GLU, bool FP8, bool PK>
 __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   extern __shared__ float smem[];
+  pin_gemm_args(a);
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
   if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
   if (!variant_admitted(v, a.force_variant, a.candidates)) {
@@ -441,21 +442,33 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
 }
 
 // a8: y[t] = sum_j w[t][j] out[inv_perm[t*k+j]], summed in slot order in fp32.
-// Grid (T, H / 1024): each thread owns 4 consecutive features of one token and issues the
-// loads of all k slots before summing them.
+// Grid (T, H / 1024): each thread owns 4 consecutive features of one token.  The k slot
+// indices and gates arrive with one lane-parallel load (lane j holds slot j) and are
+// broadcast to the wave, then the loads of all k output rows are issued before the sum.
 __global__ void __launch_bounds__(256) k_reduce(ReduceArgs a) {
-  const int t = blockIdx.x;
+  pin(a.out);
+  pin(a.w);
+  pin(a.inv_perm);
+  pin(a.y);
+  pin(a.k);
+  pin(a.H);
+  const int t = blockIdx.x, lane = threadIdx.x & 63;
   const int n = (blockIdx.y * 256 + threadIdx.x) * 4;
+  int p_l = -1;
+  float g_l = 0.f;
+  if (lane < a.k) {
+    p_l = a.inv_perm[(size_t)t * a.k + lane];
+    g_l = a.w[(size_t)t * a.k + lane];
+  }
   if (n >= a.H) return;
   float4 o[DAMOE_MAX_K];
   float g[DAMOE_MAX_K];
 #pragma unroll
   for (int j = 0; j < DAMOE_MAX_K; ++j) {
     if (j < a.k) {
-      const int p = a.inv_perm[(size_t)t * a.k + j];
-      g[j] = p >= 0 ? a.w[(size_t)t * a.k + j] : 0.f;
-      o[j] = *reinterpret_cast<const float4*>(a.out + (size_t)(p >= 0 ? p : 0) * a.H + n);
-      if (p < 0) o[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      const int p = __builtin_amdgcn_readlane(p_l, j);
+      g[j] = p >= 0 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g_l), j)) : 0.f;
+      o[j] = p >= 0 ? *reinterpret_cast<const float4*>(a.out + (size_t)p * a.H + n) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);

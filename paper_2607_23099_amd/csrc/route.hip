@@ -12,59 +12,109 @@ namespace {
 constexpr int kNW = kRouteThreads / kWave;  // 16 waves
 constexpr int kMaxExemplarRegs = 8;  // exemplar entries prefetched per lane (E <= 512)
 constexpr int kValueBins = 4096;     // counting sort of the histogram when every count is smaller
+constexpr int kIdBatch = 16;         // 64-id chunks loaded together per wave
 
-// ddist:X thresholds of the Effective Experts bucket, X = XN / XD.
-__constant__ uint32_t c_xn[13] = {11, 13, 3, 17, 2, 5, 4, 6, 8, 12, 16, 24, 32};
-__constant__ uint32_t c_xd[13] = {10, 10, 2, 10, 1, 2, 1, 1, 1, 1, 1, 1, 1};
+// The Effective Experts bucket: the number of ddist:X thresholds X = XN / XD with
+// eff <= E / X, decided exactly as num * XN <= E * XD * den in uint64 (the thresholds are
+// immediates: a table in memory would cost one dependent load each).
+__device__ __forceinline__ int effexp_bucket(uint64_t num, uint64_t den, uint64_t E) {
+  constexpr uint32_t xn[13] = {11, 13, 3, 17, 2, 5, 4, 6, 8, 12, 16, 24, 32};
+  constexpr uint32_t xd[13] = {10, 10, 2, 10, 1, 2, 1, 1, 1, 1, 1, 1, 1};
+  if (den == 0) return -1;
+  int b = 0;
+#pragma unroll
+  for (int j = 0; j < 13; ++j) b += num * xn[j] <= E * xd[j] * den ? 1 : 0;
+  return b;
+}
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = threadIdx.x & 63;
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Exclusive scans of N ints per thread over the 1024-thread block, in one pass: a wave-level
-// shuffle scan, then every thread adds the totals of the waves before it.  `tmp` holds
-// N * kNW ints.  Returns the block totals in tot[].
+// Wave-level scans with DPP row operations (gfx9): row_shr 1, 2, 4, 8 scan each row of 16
+// lanes, row_bcast 15 and 31 carry the row totals across the rows.  Each step is one VALU op,
+// where a shuffle through the LDS crossbar would cost a round trip.  Lanes a step cannot
+// source keep 0 (bound_ctrl off, old value 0).
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ int dpp(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROW_MASK, 0xF, false);
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += dpp<0x111>(x);       // row_shr:1
+  x += dpp<0x112>(x);       // row_shr:2
+  x += dpp<0x114>(x);       // row_shr:4
+  x += dpp<0x118>(x);       // row_shr:8
+  x += dpp<0x142, 0xA>(x);  // row_bcast:15 into rows 1, 3
+  x += dpp<0x143, 0xC>(x);  // row_bcast:31 into rows 2, 3
+  return x;
+}
+
+// Inclusive scan of row 0 only (lanes 0..15).
+__device__ __forceinline__ int row16_incl_scan(int x) {
+  x += dpp<0x111>(x);
+  x += dpp<0x112>(x);
+  x += dpp<0x114>(x);
+  x += dpp<0x118>(x);
+  return x;
+}
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const uint32_t lo = (uint32_t)dpp<CTRL, ROW_MASK>((int)(uint32_t)x);
+  const uint32_t hi = (uint32_t)dpp<CTRL, ROW_MASK>((int)(uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Sum over the wave, returned to every lane.
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
+  x += dpp_u64<0x111>(x);
+  x += dpp_u64<0x112>(x);
+  x += dpp_u64<0x114>(x);
+  x += dpp_u64<0x118>(x);
+  x += dpp_u64<0x142, 0xA>(x);
+  x += dpp_u64<0x143, 0xC>(x);
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)x, 63);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Exclusive scans of N ints per thread over the 1024-thread block: a DPP wave scan; the 16
+// wave totals go through LDS, and every wave scans them itself (one LDS read per lane of row
+// 0, a 16-lane DPP scan, two lane reads).  `tmp` holds N * kNW ints.  Returns the block
+// totals in tot[].  Ends with a barrier, so `tmp` may be reused at once.
 template <int N>
 __device__ void block_scan(const int (&v)[N], int (&ex)[N], int (&tot)[N], int* tmp) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int inc[N];
 #pragma unroll
-  for (int c = 0; c < N; ++c) inc[c] = v[c];
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-#pragma unroll
-    for (int c = 0; c < N; ++c) {
-      const int y = __shfl_up(inc[c], o, 64);
-      if (lane >= o) inc[c] += y;
-    }
-  }
+  for (int c = 0; c < N; ++c) inc[c] = wave_incl_scan(v[c]);
   if (lane == 63)
 #pragma unroll
     for (int c = 0; c < N; ++c) tmp[c * kNW + w] = inc[c];
   __syncthreads();
+  int t[N];
+#pragma unroll
+  for (int c = 0; c < N; ++c) t[c] = lane < kNW ? tmp[c * kNW + lane] : 0;
 #pragma unroll
   for (int c = 0; c < N; ++c) {
-    int before = 0, all = 0;
-    for (int u = 0; u < kNW; ++u) {
-      const int t = tmp[c * kNW + u];
-      before += u < w ? t : 0;
-      all += t;
-    }
+    const int s16 = row16_incl_scan(t[c]);
+    const int before = w ? __builtin_amdgcn_readlane(s16, w - 1) : 0;
     ex[c] = before + inc[c] - v[c];
-    tot[c] = all;
+    tot[c] = __builtin_amdgcn_readlane(s16, kNW - 1);
   }
   __syncthreads();
 }
 
-__device__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t lo = __shfl_xor((uint32_t)v, o, 64);
-    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), o, 64);
-    v += ((uint64_t)hi << 32) | lo;
+// Lanes of the wave holding the same expert id (ballot multisplit over the id's bits).
+__device__ __forceinline__ uint64_t same_expert(int e, bool valid, int nbits) {
+  uint64_t peers = __ballot(valid);
+  for (int bt = 0; bt < nbits; ++bt) {
+    const uint64_t m = __ballot(valid && ((e >> bt) & 1));
+    peers &= ((e >> bt) & 1) ? m : ~m;
   }
-  return v;
+  return peers;
 }
 
 struct TileOut {
@@ -95,42 +145,33 @@ struct Smem {
   int cnt[DAMOE_MAX_E];
   int base[DAMOE_MAX_E];
   int sorted[DAMOE_MAX_E];
-  uint16_t wc[kNW][DAMOE_MAX_E];
+  uint32_t wcnt[kNW][DAMOE_MAX_E];  // per-wave counts, then per-wave running offsets
   int tmp[(1 + DAMOE_N_TILE_SIZES) * kNW];
   int qpre[kNW][64 * kMaxExemplarRegs];  // first exemplar of each wave
   uint64_t tmp64[kNW];
   long long score[256];
   int vh[kValueBins];  // value histogram of the counts, then start positions
   int bad;
+  int big;             // some count >= kValueBins
 };
 
-// a5 on counts already in LDS: sort the histogram in descending order, score every exemplar
-// as an exact int64 dot product with the sorted vector, and pick the first maximum.
-// The sort is a counting sort over count values (every count < kValueBins, always the case
-// for T < kValueBins): value histogram, descending exclusive scan -> start of each value,
-// then each expert takes a slot of its value.  Equal counts may land in either order, which
-// leaves the sorted vector unchanged.  Larger counts fall back to an O(E^2 / 1024) rank count.
-__device__ void dispatch_core(Smem& sm, int E, int total, const DispatchIn& d, int32_t* ctrl) {
+// a5 on counts already in LDS (and `ci`, this thread's count): sort the histogram in
+// descending order, score every exemplar as an exact int64 dot product with the sorted
+// vector, and pick the first maximum.  The sort is a counting sort over count values when
+// every count is below kValueBins: value histogram (zeroed by the caller), descending
+// exclusive scan -> start of each value, then each expert takes a slot of its value.  Equal
+// counts may land in either order, which leaves the sorted vector unchanged.  Larger counts
+// fall back to an O(E^2 / 1024) rank count.  sm.big must be visible to every thread.
+__device__ void dispatch_core(Smem& sm, int E, int total, int ci, const DispatchIn& d, int32_t* ctrl) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int ci = tid < E ? sm.cnt[tid] : 0;
-  int cmax = ci;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) cmax = max(cmax, __shfl_xor(cmax, o, 64));
-  if (lane == 0) sm.tmp[w] = cmax;
-  __syncthreads();
-  cmax = 0;
-  for (int u = 0; u < kNW; ++u) cmax = max(cmax, sm.tmp[u]);
-  if (cmax < kValueBins) {
-    for (int v = tid; v <= cmax; v += kRouteThreads) sm.vh[v] = 0;
-    __syncthreads();
+  if (!sm.big) {
     if (tid < E) atomicAdd(&sm.vh[ci], 1);
     __syncthreads();
-    // Thread t owns the values cmax - 4t .. cmax - 4t - 3 (descending order of values).
+    // Thread t owns the values kValueBins - 1 - 4t .. - 3 (descending order of values).
     int h[4], local = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int v = cmax - 4 * tid - q;
-      h[q] = v >= 0 ? sm.vh[v] : 0;
+      h[q] = sm.vh[kValueBins - 1 - 4 * tid - q];
       local += h[q];
     }
     int sv[1] = {local}, ex[1], tot[1];
@@ -138,8 +179,7 @@ __device__ void dispatch_core(Smem& sm, int E, int total, const DispatchIn& d, i
     int start = ex[0];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int v = cmax - 4 * tid - q;
-      if (v >= 0) sm.vh[v] = start;
+      sm.vh[kValueBins - 1 - 4 * tid - q] = start;
       start += h[q];
     }
     __syncthreads();
@@ -180,22 +220,14 @@ __device__ void dispatch_core(Smem& sm, int E, int total, const DispatchIn& d, i
   }
   __syncthreads();
   if (w == 0) {
+    // First maximum over the exemplars, in index order.
     long long best = 0;
     int bi = -1;
-    for (int x = lane; x < d.n_ex; x += 64)
-      if (bi < 0 || sm.score[x] > best) {
-        best = sm.score[x];
+    for (int x = 0; x < d.n_ex; ++x) {
+      const long long sc = sm.score[x];
+      if (bi < 0 || sc > best) {
+        best = sc;
         bi = x;
-      }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint32_t lo = __shfl_xor((uint32_t)(unsigned long long)best, o, 64);
-      const uint32_t hi = __shfl_xor((uint32_t)((unsigned long long)best >> 32), o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      const long long ob = (long long)(((unsigned long long)hi << 32) | lo);
-      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
-        best = ob;
-        bi = oi;
       }
     }
     if (lane == 0) {
@@ -208,11 +240,36 @@ __device__ void dispatch_core(Smem& sm, int E, int total, const DispatchIn& d, i
   }
 }
 
+// a2-a4 (and a5 when DISPATCH) in one 1024-thread workgroup.  Wave w owns the contiguous
+// range of assignments [w R, w R + R) (R a multiple of 64), so the histogram and the stable
+// scatter run per wave with no block barrier inside their loops: 64 assignments at a time,
+// the lanes holding the same expert found by ballot multisplit, the first of them updating
+// the wave's counter of that expert.  Per expert, an exclusive scan of the 16 wave counts
+// gives each wave's starting offset in the expert's segment, so the order inside a segment
+// is the flat order a = t k + j.
 template <bool DISPATCH>
 __global__ void __launch_bounds__(kRouteThreads)
 k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, DispatchIn d) {
   __shared__ Smem sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  pin(ids);
+  pin(A);
+  pin(E);
+  pin(o.counts);
+  pin(o.offsets);
+  pin(o.perm);
+  pin(o.inv_perm);
+  pin(o.numden);
+  pin(o.bucket);
+  pin(o.ctrl);
+#pragma unroll
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) pin(o.tiles.list[c]);
+  pin(d.Q);
+  pin(d.kid);
+  pin(d.n_ex);
+  pin(d.noda);
+  pin(d.variant_id);
+  pin(d.fixed);
 
   // The wave's first exemplar is fetched before anything else so its latency hides behind
   // the histogram; it moves to LDS once the histogram is done.
@@ -222,18 +279,41 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     const int r = lane + 64 * m;
     qpre[m] = (DISPATCH && w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
   }
-  for (int e = tid; e < E; e += kRouteThreads) sm.cnt[e] = 0;
-  if (A > 0)
-    for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wc[x / E][x % E] = 0;
-  if (tid == 0) sm.bad = 0;
+  for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wcnt[x / E][x % E] = 0;
+  if (DISPATCH)
+    for (int v = tid; v < kValueBins; v += kRouteThreads) sm.vh[v] = 0;
+  if (tid == 0) {
+    sm.bad = 0;
+    sm.big = 0;
+  }
   __syncthreads();
 
-  // a2: histogram.
+  // a2: per-wave histogram.  Ids move in batches of kIdBatch chunks (one memory latency per
+  // batch); a range of at most one batch keeps its ids in registers for the scatter.
+  int nbits = 1;
+  while ((1 << nbits) < E) ++nbits;
+  const int R = (A + kNW * 64 - 1) / (kNW * 64) * 64;
+  const int a_lo = w * R, a_hi = min(A, a_lo + R);
+  const bool one_batch = R <= 64 * kIdBatch;
   int bad = 0;
-  for (int a = tid; a < A; a += kRouteThreads) {
-    const int e = ids[a];
-    if (e >= 0 && e < E) atomicAdd(&sm.cnt[e], 1);
-    else ++bad;
+  int eb[kIdBatch];
+  for (int a0 = a_lo; a0 < a_hi; a0 += 64 * kIdBatch) {
+    // Unconditional loads (index clamped into the range) so the batch issues back to back.
+#pragma unroll
+    for (int q = 0; q < kIdBatch; ++q) eb[q] = ids[min(a0 + 64 * q + lane, a_hi - 1)];
+#pragma unroll
+    for (int q = 0; q < kIdBatch; ++q) {
+      const int a = a0 + 64 * q + lane;
+      if (a >= a_hi) eb[q] = -1;
+      bad += (a < a_hi && !(eb[q] >= 0 && eb[q] < E)) ? 1 : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < kIdBatch; ++q) {
+      if (a0 + 64 * q >= a_hi) break;
+      const bool valid = eb[q] >= 0 && eb[q] < E;
+      const uint64_t peers = same_expert(eb[q], valid, nbits);
+      if (valid && (peers & lanemask_lt()) == 0) sm.wcnt[w][eb[q]] += (uint32_t)__popcll(peers);
+    }
   }
   if (bad) atomicAdd(&sm.bad, bad);
   if (DISPATCH)
@@ -241,9 +321,22 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     for (int m = 0; m < kMaxExemplarRegs; ++m) sm.qpre[w][lane + 64 * m] = qpre[m];
   __syncthreads();
 
+  // Per expert: the wave counts become each wave's starting offset inside the segment.
+  int c = 0;
+  if (tid < E) {
+#pragma unroll
+    for (int u = 0; u < kNW; ++u) {
+      const uint32_t t = sm.wcnt[u][tid];
+      sm.wcnt[u][tid] = (uint32_t)c;
+      c += (int)t;
+    }
+    sm.cnt[tid] = c;
+    if (c >= kValueBins) sm.big = 1;
+  }
+
   // Offsets, Effective Experts numerator / denominator (a3), and the token-tile counts of
-  // every tile size, all in one scan.
-  const int c = tid < E ? sm.cnt[tid] : 0;
+  // every tile size, all in one scan (whose barriers also publish cnt, big and the wave
+  // offsets).
   int v[1 + DAMOE_N_TILE_SIZES], ex[1 + DAMOE_N_TILE_SIZES], tot[1 + DAMOE_N_TILE_SIZES];
   v[0] = c;
 #pragma unroll
@@ -264,13 +357,7 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     const uint64_t num = (uint64_t)total * (uint64_t)total;
     o.numden[0] = num;
     o.numden[1] = den;
-    int b = -1;
-    if (den != 0) {
-      b = 0;
-      for (int jx = 0; jx < 13; ++jx)
-        if (num * c_xn[jx] <= (uint64_t)E * c_xd[jx] * den) ++b;
-    }
-    *o.bucket = b;
+    *o.bucket = effexp_bucket(num, den, (uint64_t)E);
     if (sm.bad) atomicOr(&o.ctrl[0], DAMOE_DEVERR_EXPERT_ID);
   }
 #pragma unroll
@@ -288,49 +375,39 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     }
   }
 
-  if (DISPATCH) dispatch_core(sm, E, total, d, o.ctrl);
+  if (DISPATCH) dispatch_core(sm, E, total, c, d, o.ctrl);
   if (!DISPATCH && d.fixed >= 0 && tid == 0) {
     *d.variant_id = total == 0 ? d.noda : d.fixed;
     o.ctrl[1] = total == 0 ? -1 : -2;  // single-variant bucket: no exemplar scored
     o.ctrl[2] = 0;
     o.ctrl[3] = 0;
   }
+  __syncthreads();  // segment bases
 
-  // a4: stable scatter, one 1024-assignment chunk at a time.  Within a wave the rank among
-  // equal experts comes from ballot-based multisplit; across waves from per-wave counts.
-  int nbits = 1;
-  while ((1 << nbits) < E) ++nbits;
-  for (int a0 = 0; a0 < A; a0 += kRouteThreads) {
-    const int a = a0 + tid;
-    const int e = a < A ? ids[a] : -1;
-    const bool valid = e >= 0 && e < E;
-    uint64_t peers = __ballot(valid);
-    for (int bt = 0; bt < nbits; ++bt) {
-      const uint64_t m = __ballot(valid && ((e >> bt) & 1));
-      peers &= ((e >> bt) & 1) ? m : ~m;
+  // a4: stable scatter, per wave over its own range.
+  for (int a0 = a_lo; a0 < a_hi; a0 += 64 * kIdBatch) {
+    if (!one_batch) {
+#pragma unroll
+      for (int q = 0; q < kIdBatch; ++q) eb[q] = ids[min(a0 + 64 * q + lane, a_hi - 1)];
+#pragma unroll
+      for (int q = 0; q < kIdBatch; ++q)
+        if (a0 + 64 * q + lane >= a_hi) eb[q] = -1;
     }
-    const int rank = __popcll(peers & lanemask_lt());
-    if (valid && rank == 0) sm.wc[w][e] = (uint16_t)__popcll(peers);
-    __syncthreads();
-    if (valid) {
-      int p = sm.base[e] + rank;
-      for (int u = 0; u < w; ++u) p += sm.wc[u][e];
-      o.perm[p] = a;
-      o.inv_perm[a] = p;
-    } else if (a < A) {
-      o.inv_perm[a] = -1;
-    }
-    if (a0 + kRouteThreads < A) {
-      __syncthreads();
-      if (tid < E) {
-        int s = 0;
-        for (int u = 0; u < kNW; ++u) {
-          s += sm.wc[u][tid];
-          sm.wc[u][tid] = 0;
-        }
-        sm.base[tid] += s;
+#pragma unroll
+    for (int q = 0; q < kIdBatch; ++q) {
+      if (a0 + 64 * q >= a_hi) break;
+      const int a = a0 + 64 * q + lane, e = eb[q];
+      const bool valid = e >= 0 && e < E;
+      const uint64_t peers = same_expert(e, valid, nbits);
+      const int rank = __popcll(peers & lanemask_lt());
+      if (valid) {
+        const int p = sm.base[e] + (int)sm.wcnt[w][e] + rank;
+        o.perm[p] = a;
+        o.inv_perm[a] = p;
+      } else if (a < a_hi) {
+        o.inv_perm[a] = -1;
       }
-      __syncthreads();
+      if (valid && rank == 0) sm.wcnt[w][e] += (uint32_t)__popcll(peers);
     }
   }
 }
@@ -340,16 +417,30 @@ __global__ void __launch_bounds__(kRouteThreads)
 k_dispatch(const int32_t* __restrict__ counts, int32_t E, DispatchIn d, int32_t* __restrict__ ctrl) {
   __shared__ Smem sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  pin(counts);
+  pin(E);
+  pin(ctrl);
+  pin(d.Q);
+  pin(d.kid);
+  pin(d.n_ex);
+  pin(d.noda);
+  pin(d.variant_id);
 #pragma unroll
   for (int m = 0; m < kMaxExemplarRegs; ++m) {
     const int r = lane + 64 * m;
     sm.qpre[w][r] = (w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
   }
+  for (int v = tid; v < kValueBins; v += kRouteThreads) sm.vh[v] = 0;
+  if (tid == 0) sm.big = 0;
+  __syncthreads();
   const int c = tid < E ? counts[tid] : 0;
-  if (tid < E) sm.cnt[tid] = c;
+  if (tid < E) {
+    sm.cnt[tid] = c;
+    if (c >= kValueBins) sm.big = 1;
+  }
   int v[1] = {c}, ex[1], tot[1];
-  block_scan<1>(v, ex, tot, sm.tmp);
-  dispatch_core(sm, E, tot[0], d, ctrl);
+  block_scan<1>(v, ex, tot, sm.tmp);  // also publishes cnt and big
+  dispatch_core(sm, E, tot[0], c, d, ctrl);
 }
 
 }  // namespace
