@@ -188,9 +188,11 @@ damoe_status damoe_table_load(const char* path, damoe_table** out);
  * bucket's noda variant is written.  The chosen exemplar and its score land in
  * the workspace control words.  Stream-ordered; no host sync. */
 /* Host bit mask of the variant ids that dispatch may write for a call with T
- * tokens: the kid of every exemplar of T's bucket and the bucket's noda variant
- * (the paper keeps one graph per bucket holding exactly these kernels, Sec. IV).
- * Pass it to damoe_fused_moe.  0 for a null table or T < 0. */
+ * tokens: the kid of every exemplar of T's bucket, plus the bucket's noda
+ * variant when the bucket names several kernels (or T == 0); a bucket whose
+ * exemplars all map to one kernel writes that kernel in every case.  The paper
+ * keeps one graph per bucket holding exactly these kernels (Sec. IV).  Pass it
+ * to damoe_fused_moe.  0 for a null table or T < 0. */
 uint32_t damoe_table_candidates(const damoe_table* table, int32_t T);
 
 damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int32_t T,
@@ -202,7 +204,8 @@ damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int
  * paper's online step 5 (Sec. IV-B): histogram, sort, match, kernel id, all on
  * the device.  The table must be built for this E and k.  When every exemplar
  * of the bucket maps to the same variant, that variant is written without
- * scoring (the match cannot change it) and control word [1] is -2. */
+ * scoring (the match cannot change it), also when T > 0 but no assignment is
+ * valid, and control word [1] is -2 (-1 with no valid assignment). */
 damoe_status damoe_route_dispatch(const damoe_table* table, const int32_t* topk_ids, int32_t T,
                                   int32_t k, int32_t E, int32_t* counts, int32_t* offsets,
                                   int32_t* perm, int32_t* inv_perm, uint64_t* effexp_numden,
@@ -223,9 +226,11 @@ damoe_status damoe_route_dispatch(const damoe_table* table, const int32_t* topk_
  *              the kernel classes holding a candidate are launched (the big-tile
  *              class is a kernel of its own, the others share one), so a decode
  *              bucket whose table row never names the big-tile variant costs no
- *              launch of it.  A dispatched id outside the mask runs no expert
- *              GEMM and sets DAMOE_DEVERR_VARIANT (y is then unspecified).
- *              Ignored when force_variant >= 0;
+ *              launch of it.  A mask with one bit runs that variant without
+ *              reading *variant_id (a one-kernel bucket leaves nothing to decide
+ *              on the device).  A dispatched id outside a mask of several bits
+ *              runs no expert GEMM and sets DAMOE_DEVERR_VARIANT (y is then
+ *              unspecified).  Ignored when force_variant >= 0;
  *              bits beyond damoe_num_variants() are DAMOE_ERR_INVALID_ARG.
  *   y          bf16 [T][H] output, y[t] = sum_j topk_w[t][j] FFN_{ids[t][j]}(x[t])
  * Only experts with at least one token are read.  Stream-ordered.  T * H * 2

@@ -209,8 +209,11 @@ damoe_status damoe_route_dispatch(const damoe_table* t, const int32_t* topk_ids,
 uint32_t damoe_table_candidates(const damoe_table* t, int32_t T) {
   if (!t || T < 0) return 0;
   const int32_t b = table_bucket(t, T);
-  uint32_t m = 1u << t->noda[b];
+  uint32_t m = 0;
   for (int32_t i = 0; i < t->n_ex[b]; ++i) m |= 1u << t->kid[t->ex_begin[b] + i];
+  // A bucket with several kernels writes its noda variant when no assignment is valid; a
+  // one-kernel bucket writes that kernel in every case.
+  if (__builtin_popcount(m) > 1 || T == 0) m |= 1u << t->noda[b];
   return m;
 }
 
@@ -237,6 +240,12 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   const uint32_t all = (uint32_t)((1ull << num_variants()) - 1);
   if (candidates & ~all) return DAMOE_ERR_INVALID_ARG;
   if (candidates == 0) candidates = all;
+  // One candidate: the launch names it, and the kernels need not read the device-side id
+  // (a bucket with a single kernel has no decision left to take on the device).
+  if (force_variant < 0 && __builtin_popcount(candidates) == 1) {
+    force_variant = __builtin_ctz(candidates);
+    if (!damoe_variant_supports(force_variant, L->wdtype)) return DAMOE_ERR_UNSUPPORTED;
+  }
   if (T == 0) return DAMOE_OK;
   // 32-bit buffer offsets address the gathered token rows.
   if ((size_t)T * L->H * 2 >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;

@@ -377,7 +377,9 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
 
   if (DISPATCH) dispatch_core(sm, E, total, c, d, o.ctrl);
   if (!DISPATCH && d.fixed >= 0 && tid == 0) {
-    *d.variant_id = total == 0 ? d.noda : d.fixed;
+    // The host's choice (the bucket's one kernel, or noda when T = 0), also when no
+    // assignment is valid (nothing to compute then): the candidate set stays one variant.
+    *d.variant_id = d.fixed;
     o.ctrl[1] = total == 0 ? -1 : -2;  // single-variant bucket: no exemplar scored
     o.ctrl[2] = 0;
     o.ctrl[3] = 0;

@@ -50,10 +50,10 @@ def test_tiny_every_variant(tiny, T, alpha, seed):
         assert path.ctrl()[4] == v
 
 
-@pytest.mark.parametrize("noda_same", [False, True], ids=["two-classes", "one-class"])
+@pytest.mark.parametrize("noda_same", [False, True], ids=["noda-other", "noda-same"])
 def test_tiny_adaptive_uses_device_variant(tiny, noda_same):
-    # The device-side id picks the variant; with noda == kid the candidate mask holds one
-    # variant, so only that variant's kernel class is launched.
+    # A one-kernel bucket: its candidate mask is that kernel alone, whatever noda is, and
+    # the launch runs it directly; the device-side id still records it.
     torch = torch_cuda()
     dl, path = tiny
     sh = dl.shape
@@ -65,7 +65,7 @@ def test_tiny_adaptive_uses_device_variant(tiny, noda_same):
         td = damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0, bucket_T=np.array([1 << 20]),
                              n_ex=np.array([1]), Q=q, kid=np.array([target]), noda=np.array([noda]))
         table = damoe.Table.create(td)
-        assert table.candidates(64) == (1 << target) | (1 << noda)
+        assert table.candidates(64) == 1 << target  # one exemplar: one kernel, no noda
         _run(path, r, 0, table=table)
         assert int(path.variant.item()) == target and path.ctrl()[4] == target
         y_adaptive = path.y[:64].clone()
@@ -82,7 +82,8 @@ def test_tiny_dispatch_outside_candidates_is_flagged(tiny):
     sh = dl.shape
     r = synth.routing(sh.E, sh.k, 64, 1.0, 0)
     nv = damoe.num_variants()
-    for target, cand in [(3, 1 << 0), (nv - 1, 1 << 0), (0, 1 << (nv - 1))]:
+    # masks of two variants, so the launches still read the device-side id
+    for target, cand in [(3, 0b11), (nv - 1, 0b11), (0, (1 << (nv - 1)) | (1 << (nv - 2)))]:
         q = np.full((1, sh.E), 1000, np.int32)
         td = damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0, bucket_T=np.array([1 << 20]),
                              n_ex=np.array([1]), Q=q, kid=np.array([target]), noda=np.array([target]))
