@@ -44,6 +44,68 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemm_glu_decode_sweep_traffic.txt")
+GEMM_SOURCES = ("csrc/gemm.hip", "csrc/device.h", "csrc/common.h")
+
+
+def gemm_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2607_23099_amd", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per GEMM1 launch from the committed counter summary, or None when it is missing
+    or was taken on other kernel sources."""
+    try:
+        kv = dict(l.split(":", 1) for l in open(TRAFFIC_FILE).read().splitlines() if ":" in l)
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("source_digest") != gemm_source_digest():
+        return None
+    return int(float(kv["hbm_bytes_per_launch"]))
+
+
+def summarize_traffic(pmc_dir: str):
+    """Write TRAFFIC_FILE from four rocprofv3 --pmc runs under pmc_dir (subfolders fetch/,
+    write/: the decode sweep; copy_fetch/, copy_write/: `--workload copy`).  Counters are in KiB
+    per dispatch; each is scaled by what it reads for the plain copy of known size."""
+    import csv
+    import glob
+
+    def values(sub, counter, match):
+        f = glob.glob(os.path.join(pmc_dir, sub, "**", "*counter_collection.csv"), recursive=True)[0]
+        return [float(r["Counter_Value"]) * 1024 for r in csv.DictReader(open(f))
+                if r["Counter_Name"] == counter and match(r["Kernel_Name"])]
+
+    is_glu = lambda n: "k_gemm<true" in n
+    is_copy = lambda n: "copy" in n.lower() or "elementwise" in n.lower()
+    n_copy = 4 << 30
+    fcal = max(values("copy_fetch", "FETCH_SIZE", is_copy)) / n_copy
+    wcal = max(values("copy_write", "WRITE_SIZE", is_copy)) / n_copy
+    fetch = values("fetch", "FETCH_SIZE", is_glu)
+    write = values("write", "WRITE_SIZE", is_glu)
+    per_launch = float(np.mean(fetch)) / fcal + float(np.mean(write)) / wcal
+    with open(TRAFFIC_FILE, "w") as f:
+        f.write("# HBM traffic of k_gemm<GEMM1+SwiGLU> over the DeepSeek-V3 decode sweep\n")
+        f.write("# rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv -d <dir>/fetch -- "
+                "python3 -u bench.py --steps 2 --warmup 1 --no-cpu-baseline\n")
+        f.write("# calibration: the same counters on python3 -u bench.py --workload copy --steps 3 "
+                "(4 GiB read + 4 GiB written per call)\n")
+        f.write(f"source_digest: {gemm_source_digest()}\n")
+        f.write(f"launches: {len(fetch)}\n")
+        f.write(f"fetch_calibration: {fcal:.4f}\n")
+        f.write(f"write_calibration: {wcal:.4f}\n")
+        f.write(f"fetch_bytes_per_launch: {np.mean(fetch) / fcal:.0f}\n")
+        f.write(f"write_bytes_per_launch: {np.mean(write) / wcal:.0f}\n")
+        f.write(f"hbm_bytes_per_launch: {per_launch:.0f}\n")
+    print(open(TRAFFIC_FILE).read())
+
+
 def geomean(v):
     v = [x for x in v if x > 0]
     return math.exp(sum(math.log(x) for x in v) / len(v)) if v else 0.0
@@ -301,6 +363,108 @@ def run_dispatch(args):
     print(json.dumps(out), flush=True)
 
 
+def run_prefill(args):
+    """Per-variant GEMM times at the MFMA-bound prefill points: Kimi-K2 (bf16, 40% of the mass
+    on 4 hot experts) at T = 2048 and 8192, and DeepSeek-V3 with fp8 block-128 weights at
+    T = 4096 and 16384 (alpha 0.05 and 1).  Reports algorithmic and padded TFLOP/s per stage."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+
+    V = [int(v) for v in args.variants.split(",")] if args.variants else \
+        [v for v in range(damoe.num_variants()) if damoe.variant_tile_m(v) >= 128]
+    rows = {}
+    best = None
+    for shape, Ts, alphas, hot in ((synth.KIMI, (2048, 8192), (0.05,), 4),
+                                   (synth.DS_FP8, (4096, 16384), (0.05, 1.0), 0)):
+        log(f"filling {shape.name} weights")
+        dl = DeviceLayer(shape)
+        path = Path(dl, max(Ts))
+        path.fill_x(max(Ts), 5)
+        for T in Ts:
+            for a in alphas:
+                r = synth.routing(shape.E, shape.k, T, a, synth.seed_prefill(T, a, 0) if not hot else
+                                  synth.seed_kimi(T, 0), n_hot=hot)
+                path.set_routing(r)
+                A = T * shape.k
+                counts = np.bincount(r.ids.ravel(), minlength=shape.E)
+                f1, f2 = 4.0 * A * shape.H * shape.I, 2.0 * A * shape.H * shape.I
+                for v in V:
+                    if not damoe.variant_supports(v, dl.wdtype):
+                        continue
+                    bm = damoe.variant_tile_m(v)
+                    pad = float(np.sum(-(-counts // bm) * bm)) / A
+                    t1, t2 = [], []
+                    for rep in range(args.steps + 1):
+                        path.route(T)
+                        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                        e[0].record()
+                        path.fused_stage(0, T, v)
+                        e[1].record()
+                        path.fused_stage(1, T, v)
+                        e[2].record()
+                        path.fused_stage(2, T, v)
+                        torch.cuda.synchronize()
+                        if rep:
+                            t1.append(e[0].elapsed_time(e[1]))
+                            t2.append(e[1].elapsed_time(e[2]))
+                    m1, m2 = float(np.median(t1)), float(np.median(t2))
+                    key = f"{shape.name}_T{T}_a{a}_{damoe.variant_name(v)}"
+                    rows[key] = {"gemm1_us": round(m1 * 1e3, 1), "gemm2_us": round(m2 * 1e3, 1),
+                                 "gemm1_tflops": round(f1 / m1 / 1e9, 1), "gemm2_tflops": round(f2 / m2 / 1e9, 1),
+                                 "padded_gemm1_tflops": round(f1 * pad / m1 / 1e9, 1),
+                                 "touched_experts": int((counts > 0).sum())}
+                    log(f"{key}: {rows[key]}")
+                    if shape is synth.KIMI and T == 8192 and (best is None or m1 < best[1]):
+                        best = (key, m1, f1)
+        del dl, path
+        torch.cuda.empty_cache()
+    peak = 2500.0
+    out = {
+        "metric": "grouped GEMM1 + SwiGLU TFLOP/s, Kimi-K2 prefill T=8192 (best variant)",
+        "value": round(best[2] / best[1] / 1e9, 1),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": 1,
+        "ms_per_step": round(best[1], 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "prefill points: kimi-k2 E=384 top-8 H=7168 I=2048 bf16 T in {2048, 8192} "
+                               "(alpha 0.05 + 4 hot experts); dsv3 fp8 block-128 T in {4096, 16384}, alpha in "
+                               "{0.05, 1}", "best": best[0]},
+        "roofline": {"bound": "mfma", "achieved": round(best[2] / best[1] / 1e9, 1), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(best[2] / best[1] / 1e9 / peak, 4), "traffic": None},
+        "per_point": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_copy(args):
+    """A plain device copy of known size (4 GiB read + 4 GiB written per call), the reference
+    for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = 4 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.steps
+    print(json.dumps({"metric": "device copy bandwidth (counter calibration)", "value": round(2 * n / dt / 1e9, 1),
+                      "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": 0,
+                      "ms_per_step": round(dt * 1e3, 3), "higher_is_better": True, "scaling": "weak",
+                      "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+                      "config": {"workload": "torch copy_ of 4 GiB", "bytes_read_per_call": n,
+                                 "bytes_written_per_call": n}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -309,11 +473,17 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
-    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch"], default="decode-sweep")
+    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy"],
+                    default="decode-sweep")
+    ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
     ap.add_argument("--dispatch-reps", type=int, default=200)
     ap.add_argument("--trace-steps", type=int, default=1000)
     ap.add_argument("--trace-reps", type=int, default=3)
+    ap.add_argument("--summarize-traffic", default="", metavar="PMC_DIR",
+                    help="write the GEMM1 traffic summary from rocprofv3 --pmc runs (no GPU needed)")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        return summarize_traffic(args.summarize_traffic)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -332,6 +502,10 @@ def main():
         return run_trace(args)
     if args.workload == "dispatch":
         return run_dispatch(args)
+    if args.workload == "prefill":
+        return run_prefill(args)
+    if args.workload == "copy":
+        return run_copy(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
@@ -437,7 +611,8 @@ def main():
                    "points": len(points), "table": table_note},
         "roofline": {"bound": "hbm", "kernel": "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic(),
+                     "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1))},
         "per_point": per_point,
     }
     if not args.no_cpu_baseline:
