@@ -245,6 +245,7 @@ class TableData:
 class Table:
     def __init__(self, handle: int):
         self.handle = ctypes.c_void_p(handle)
+        self._candidates = {}  # T -> mask; tables are immutable, so the lookup is cached
 
     @classmethod
     def create(cls, td: TableData) -> "Table":
@@ -262,8 +263,11 @@ class Table:
         return cls(h.value)
 
     def candidates(self, T: int) -> int:
-        """Bit mask of the variants dispatch may choose for T tokens (T's bucket row + noda)."""
-        return int(lib().damoe_table_candidates(self.handle, int(T)))
+        """Bit mask of the variants dispatch may choose for T tokens (see damoe_table_candidates)."""
+        m = self._candidates.get(T)
+        if m is None:
+            m = self._candidates[T] = int(lib().damoe_table_candidates(self.handle, int(T)))
+        return m
 
     def save(self, path: str):
         _check("damoe_table_save", lib().damoe_table_save(self.handle, path.encode()))

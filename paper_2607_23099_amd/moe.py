@@ -77,7 +77,6 @@ class Path:
         self.y = torch.zeros((max(T_max, 1), sh.H), dtype=torch.bfloat16, device=device)
         self.ws = torch.zeros(damoe.workspace_size(dl.layer, T_max), dtype=torch.uint8, device=device)
         self.candidates = 0  # variants the last dispatch could choose (0 = all)
-        self._cand_cache = {}  # (table handle, T) -> mask: a host lookup, kept off the issue path
 
     def set_routing(self, r: synth.Routing):
         T = r.T
@@ -98,21 +97,14 @@ class Path:
         damoe.route_histogram(self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
                               self.perm, self.inv_perm, self.numden, self.bucket, self.ws, stream)
 
-    def _candidates(self, table: damoe.Table, T: int) -> int:
-        key = (table.handle.value, T)
-        m = self._cand_cache.get(key)
-        if m is None:
-            m = self._cand_cache[key] = table.candidates(T)
-        return m
-
     def route_dispatch(self, table: damoe.Table, T: int, ids=None, stream=None):
         sh = self.dl.shape
-        self.candidates = self._candidates(table, T)
+        self.candidates = table.candidates(T)
         damoe.route_dispatch(table, self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
                              self.perm, self.inv_perm, self.numden, self.bucket, self.variant, self.ws, stream)
 
     def dispatch(self, table: damoe.Table, T: int, stream=None):
-        self.candidates = self._candidates(table, T)
+        self.candidates = table.candidates(T)
         damoe.dispatch(table, self.counts, T, self.variant, self.ws, stream)
 
     def fused(self, T: int, force_variant: int = -1, w=None, stream=None):
