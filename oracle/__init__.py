@@ -61,6 +61,7 @@ def lib() -> ctypes.CDLL:
             "oracle_exemplar": ([vp, i32, i32, vp], None),
             "oracle_fastest_mean": ([vp, i32, i32], i32),
             "oracle_dirichlet_logp": ([i32, f64, ctypes.c_uint32, u64, vp], None),
+            "oracle_router": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp], None),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -182,3 +183,19 @@ def dirichlet_logp(E: int, alpha: float, s: int, seed: int = 0) -> np.ndarray:
     out = np.zeros(E, np.float64)
     lib().oracle_dirichlet_logp(E, float(alpha), int(s), int(seed), out.ctypes.data)
     return out
+
+
+def router(x_bf16, wg_bf16, k: int, bias=None):
+    """Gating logits (fp64), top-k ids (descending, ties to the lower id) and softmax gates over
+    the k chosen logits.  x_bf16 [T][H] and wg_bf16 [E][H] are uint16 bf16 bit patterns."""
+    x = _c(x_bf16, np.uint16)
+    wg = _c(wg_bf16, np.uint16)
+    T, H = x.shape
+    E = wg.shape[0]
+    b = None if bias is None else _c(bias, np.float32)
+    logits = np.zeros((T, E), np.float64)
+    ids = np.zeros((T, k), np.int32)
+    w = np.zeros((T, k), np.float64)
+    lib().oracle_router(x.ctypes.data, wg.ctypes.data, None if b is None else b.ctypes.data, T, H, E, k,
+                        logits.ctypes.data, ids.ctypes.data, w.ctypes.data)
+    return logits, ids, w

@@ -461,3 +461,79 @@ def test_exemplar_normalises_each_sample_before_the_centroid():
     u = np.array([3, 1, 1, 1]) / 4 / (math.sqrt(3) / 2)
     np.testing.assert_array_equal(Q, np.rint(u * 2 ** 15))
     assert list(Q) == [28378, 9459, 9459, 9459]
+
+
+# ---------------------------------------------------------------- router (the gate in front of a1)
+
+def _router_inputs(T, H, E, seed, sigma_w=None):
+    rng = np.random.default_rng(seed)
+    x = synth.f32_to_bf16_bits(rng.normal(0, 1, (T, H)))
+    wg = synth.f32_to_bf16_bits(rng.normal(0, sigma_w or 1 / math.sqrt(H), (E, H)))
+    return x, wg
+
+
+def test_router_logits_are_the_matmul():
+    x, wg = _router_inputs(9, 96, 12, 30)
+    bias = np.random.default_rng(31).normal(0, 1, 12).astype(np.float32)
+    logits, _, _ = oracle.router(x, wg, 3, bias)
+    want = synth.bf16_to_f64(x) @ synth.bf16_to_f64(wg).T + bias.astype(np.float64)
+    np.testing.assert_allclose(logits, want, rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("T,H,E,k", [(17, 64, 8, 2), (5, 128, 256, 8), (3, 32, 5, 5), (4, 64, 9, 1)])
+def test_router_topk_is_stable_argsort(T, H, E, k):
+    x, wg = _router_inputs(T, H, E, T * E)
+    logits, ids, _ = oracle.router(x, wg, k)
+    want = np.argsort(-logits, axis=1, kind="stable")[:, :k]
+    np.testing.assert_array_equal(ids, want)
+
+
+def test_router_brute_force_subsets_and_gates():
+    # The chosen set maximises the sum of logits over all k-subsets (distinct logits), and
+    # the gate of a slot is exp(l) over the sum of exp over the set.
+    import itertools
+    x, wg = _router_inputs(6, 64, 7, 33)
+    for k in (1, 2, 3):
+        logits, ids, w = oracle.router(x, wg, k)
+        for t in range(6):
+            best = max(itertools.combinations(range(7), k), key=lambda s: sum(logits[t, list(s)]))
+            assert set(ids[t].tolist()) == set(best)
+            z = sum(math.exp(logits[t, e]) for e in best)
+            for j in range(k):
+                assert w[t, j] == pytest.approx(math.exp(logits[t, ids[t, j]]) / z, rel=1e-12)
+            assert all(logits[t, ids[t, j]] >= logits[t, ids[t, j + 1]] for j in range(k - 1))
+
+
+def test_router_gates_closed_forms_and_shift_invariance():
+    x, wg = _router_inputs(8, 64, 16, 34)
+    logits, ids, w = oracle.router(x, wg, 1)
+    assert np.all(w == 1.0)
+    logits, ids, w = oracle.router(x, wg, 2)
+    d = logits[np.arange(8), ids[:, 0]] - logits[np.arange(8), ids[:, 1]]
+    np.testing.assert_allclose(w[:, 0], 1 / (1 + np.exp(-d)), rtol=1e-13)
+    np.testing.assert_allclose(w.sum(axis=1), 1.0, rtol=1e-14)
+    # A common bias moves every logit alike: same slots, same gates.
+    _, ids2, w2 = oracle.router(x, wg, 2, np.full(16, 5.0, np.float32))
+    np.testing.assert_array_equal(ids2, ids)
+    np.testing.assert_allclose(w2, w, rtol=1e-12)
+    # A large bias on one expert puts it first in every row.
+    b = np.zeros(16, np.float32)
+    b[11] = 1000.0
+    _, ids3, _ = oracle.router(x, wg, 2, b)
+    assert np.all(ids3[:, 0] == 11)
+
+
+def test_router_ties_go_to_the_lower_id():
+    # Experts 2, 5, 6 share one gate row, and all-zero tokens tie every expert.
+    x, wg = _router_inputs(4, 64, 8, 35)
+    wg[5] = wg[2]
+    wg[6] = wg[2]
+    x[3] = 0
+    b = np.zeros(8, np.float32)
+    b[[2, 5, 6]] = 100.0
+    _, ids, w = oracle.router(x, wg, 3, b)
+    np.testing.assert_array_equal(ids[:3], [[2, 5, 6]] * 3)
+    np.testing.assert_allclose(w[:3], 1 / 3, rtol=1e-14)
+    _, ids, w = oracle.router(x[3:], wg, 4)
+    np.testing.assert_array_equal(ids, [[0, 1, 2, 3]])
+    np.testing.assert_allclose(w, 0.25, rtol=1e-14)
