@@ -14,6 +14,8 @@
  *                          SwiGLU, GEMM2, gate-weighted unpermute-reduce, as a
  *                          family of token-tile variants selected on the
  *                          device by the variant id (Sec. II-A, II-C)
+ *   damoe_router           gating logits, top-k experts and softmax gates of
+ *                          each token: the routing input above (Sec. II-A)
  *   damoe_tune             offline auto-tuning: Alg. 1, ddist:X sweep,
  *                          benchmark every variant, exemplar centroids
  *                          (Sec. III-A, IV-A)
@@ -293,6 +295,28 @@ typedef struct damoe_tune_config {
  * only call that allocates device memory on its own. */
 damoe_status damoe_tune(const damoe_layer* layer /* host */, const damoe_tune_config* cfg,
                         damoe_table** out, hipStream_t stream);
+
+/* Router: the gate in front of a1 (Sec. II-A), part of the end-to-end layer
+ * that Sec. V-C times inside one graph.  For each token t:
+ *   logits[t][e] = sum_h x[t][h] * wg[e][h] + bias[e]   (fp32 accumulation)
+ *   topk_ids[t]  = the k largest logits, in descending order; equal logits are
+ *                  taken lowest expert id first (NaN logits give valid,
+ *                  distinct but otherwise unspecified ids)
+ *   topk_w[t][j] = exp(l_j - l_0) / sum_i exp(l_i - l_0) over the k chosen
+ *                  logits (softmax over the chosen slots)
+ * so its outputs are exactly the topk_ids / topk_w inputs of route_histogram.
+ *   x       bf16 [T][H] tokens;  wg  bf16 [E][H] gate weights
+ *   bias    fp32 [E] or NULL;    logits fp32 [T][E] output, or NULL
+ *   topk_ids int32 [T][k], topk_w fp32 [T][k] outputs
+ *   ws      scratch of at least damoe_router_workspace_size(E, H, T) bytes
+ *           (partial sums); no contents are kept between calls
+ * H must be a multiple of 64 and T*H*2, E*H*2 below 2^31 (32-bit offsets),
+ * else DAMOE_ERR_UNSUPPORTED.  T = 0 is a no-op.  Deterministic (fixed
+ * summation order); stream-ordered, allocates nothing, capturable. */
+size_t damoe_router_workspace_size(int32_t E, int32_t H, int32_t T_max);
+damoe_status damoe_router(const uint16_t* x, const uint16_t* wg, const float* bias, int32_t T,
+                          int32_t H, int32_t E, int32_t k, float* logits, int32_t* topk_ids,
+                          float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Alg. 1 (Sec. III-A): bisection over alpha in [1e-6, 1e6] for the Dirichlet
  * concentration whose mean sampled Effective Experts over `samples` draws

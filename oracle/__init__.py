@@ -62,6 +62,7 @@ def lib() -> ctypes.CDLL:
             "oracle_fastest_mean": ([vp, i32, i32], i32),
             "oracle_dirichlet_logp": ([i32, f64, ctypes.c_uint32, u64, vp], None),
             "oracle_router": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp], None),
+            "oracle_topk_softmax": ([vp, i32, i32, i32, vp, vp], None),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -199,3 +200,14 @@ def router(x_bf16, wg_bf16, k: int, bias=None):
     lib().oracle_router(x.ctypes.data, wg.ctypes.data, None if b is None else b.ctypes.data, T, H, E, k,
                         logits.ctypes.data, ids.ctypes.data, w.ctypes.data)
     return logits, ids, w
+
+
+def topk_softmax(logits, k: int):
+    """Top-k ids (descending, ties to the lower id) and softmax gates over the chosen slots of
+    the given logits [T][E] (taken as fp64)."""
+    l = _c(logits, np.float64)
+    T, E = l.shape
+    ids = np.zeros((T, k), np.int32)
+    w = np.zeros((T, k), np.float64)
+    lib().oracle_topk_softmax(l.ctypes.data, T, E, k, ids.ctypes.data, w.ctypes.data)
+    return ids, w

@@ -458,36 +458,42 @@ void oracle_dirichlet_logp(int32_t E, double alpha, uint32_t s, uint64_t seed, d
 /* Router (the gating step in front of the path)                              */
 /* ------------------------------------------------------------------------- */
 
-/* Sec. II-A: the gating network scores every expert for each token and the
- * token goes to the k best.  Here the gate is a linear layer:
- *   logits[t][e] = sum_h x[t][h] * wg[e][h] + bias[e]
- * in fp64 from the bf16 x [T][H] and wg [E][H] (bias fp32 [E], or NULL).  The
- * token's slots are its k largest logits in descending order, equal logits
- * taken lowest expert id first; the gates are the softmax over those k logits
- * (the reading of the gate form taken for this build). */
-void oracle_router(const uint16_t* x, const uint16_t* wg, const float* bias, int32_t T, int32_t H,
-                   int32_t E, int32_t k, double* logits, int32_t* ids, double* w) {
+/* Sec. II-A, selection and gates from given logits [T][E] (fp64): the token's slots are its
+ * k largest logits in descending order, equal logits taken lowest expert id first; the gates
+ * are the softmax over those k logits (the reading of the gate form taken for this build). */
+void oracle_topk_softmax(const double* logits, int32_t T, int32_t E, int32_t k, int32_t* ids, double* w) {
   for (int32_t t = 0; t < T; ++t) {
-    double* l = logits + (int64_t)t * E;
-    for (int32_t e = 0; e < E; ++e) {
-      double s = 0.0;
-      for (int32_t h = 0; h < H; ++h)
-        s += bf16_value(x[(int64_t)t * H + h]) * bf16_value(wg[(int64_t)e * H + h]);
-      l[e] = s + (bias ? (double)bias[e] : 0.0);
-    }
+    const double* l = logits + (int64_t)t * E;
+    int32_t* id = ids + (int64_t)t * k;
     for (int32_t j = 0; j < k; ++j) {
       int32_t best = -1;
       for (int32_t e = 0; e < E; ++e) {
         int taken = 0;
-        for (int32_t q = 0; q < j; ++q) taken |= ids[(int64_t)t * k + q] == e;
+        for (int32_t q = 0; q < j; ++q) taken |= id[q] == e;
         if (taken) continue;
         if (best < 0 || l[e] > l[best]) best = e;
       }
-      ids[(int64_t)t * k + j] = best;
+      id[j] = best;
     }
     double z = 0.0;
-    const double top = l[ids[(int64_t)t * k]];
-    for (int32_t j = 0; j < k; ++j) z += exp(l[ids[(int64_t)t * k + j]] - top);
-    for (int32_t j = 0; j < k; ++j) w[(int64_t)t * k + j] = exp(l[ids[(int64_t)t * k + j]] - top) / z;
+    for (int32_t j = 0; j < k; ++j) z += exp(l[id[j]] - l[id[0]]);
+    for (int32_t j = 0; j < k; ++j) w[(int64_t)t * k + j] = exp(l[id[j]] - l[id[0]]) / z;
   }
+}
+
+/* Sec. II-A: the gating network scores every expert for each token and the token goes to the
+ * k best.  Here the gate is a linear layer,
+ *   logits[t][e] = sum_h x[t][h] * wg[e][h] + bias[e],
+ * in fp64 from the bf16 x [T][H] and wg [E][H] (bias fp32 [E], or NULL), followed by the
+ * selection and gates above. */
+void oracle_router(const uint16_t* x, const uint16_t* wg, const float* bias, int32_t T, int32_t H,
+                   int32_t E, int32_t k, double* logits, int32_t* ids, double* w) {
+  for (int32_t t = 0; t < T; ++t)
+    for (int32_t e = 0; e < E; ++e) {
+      double s = 0.0;
+      for (int32_t h = 0; h < H; ++h)
+        s += bf16_value(x[(int64_t)t * H + h]) * bf16_value(wg[(int64_t)e * H + h]);
+      logits[(int64_t)t * E + e] = s + (bias ? (double)bias[e] : 0.0);
+    }
+  oracle_topk_softmax(logits, T, E, k, ids, w);
 }

@@ -30,7 +30,7 @@ EXPORTED = [
     "damoe_table_load", "damoe_dispatch", "damoe_fused_moe", "damoe_num_variants", "damoe_variant_name",
     "damoe_variant_tile_m", "damoe_variant_supports", "damoe_tune", "damoe_alpha_search",
     "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch", "damoe_pack_weights",
-    "damoe_table_candidates",
+    "damoe_table_candidates", "damoe_router", "damoe_router_workspace_size",
 ]
 
 
@@ -104,6 +104,8 @@ def lib() -> ctypes.CDLL:
             "damoe_alpha_search": ([i32, f64, i32, i32, u64], f64),
             "damoe_read_device_error": ([vp, vp, vp], i32),
             "damoe_pack_weights": ([vp, vp, vp, vp, vp], i32),
+            "damoe_router": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp], i32),
+            "damoe_router_workspace_size": ([i32, i32, i32], sz),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -213,6 +215,15 @@ def fused_moe_stage(layer: Layer, stage, x, w, T, perm, inv_perm, variant_id, fo
         ctypes.byref(layer), int(stage), _p(x), _p(w), T, _p(perm), _p(inv_perm), _p(variant_id),
         int(force_variant), int(candidates), _p(y), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def router_workspace_size(E: int, H: int, T_max: int) -> int:
+    return int(lib().damoe_router_workspace_size(E, H, T_max))
+
+
+def router(x, wg, bias, T, H, E, k, logits, ids, w, ws, stream=None):
+    _check("damoe_router", lib().damoe_router(_p(x), _p(wg), _p(bias), T, H, E, k, _p(logits), _p(ids), _p(w),
+                                              _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def read_device_error(ws, stream=None) -> int:

@@ -2,8 +2,8 @@
 
 ``DeviceLayer`` holds one MoE layer's expert weights in HBM (filled on the
 device by the seeded generator), ``Path`` owns every buffer one call sequence
-needs (routing, histogram, permutation, variant id, activations, output,
-workspace).  Both only allocate at construction; the per-step methods call
+needs (router output, routing, histogram, permutation, variant id, activations,
+output, workspaces).  Both only allocate at construction; the per-step methods call
 the library and nothing else.
 """
 from __future__ import annotations
@@ -56,6 +56,22 @@ class DeviceLayer:
         return 3 * sh.H * sh.I + 3 * (sh.H // 128) * (sh.I // 128) * 4
 
 
+class Gate:
+    """The router's weights in HBM: Wg [E][H] bf16 from the seeded generator and a per-expert
+    fp32 bias (zeros unless set)."""
+
+    def __init__(self, shape: synth.Shape, device: str = "cuda"):
+        self.shape = shape
+        n = shape.E * shape.H
+        self.wg = torch.empty((shape.E, shape.H), dtype=torch.bfloat16, device=device)
+        synth.fill_bf16_device(self.wg.data_ptr(), n, seed=shape.weight_seed, tensor=synth.T_WG, slab_elems=n,
+                               sigma=synth.gate_sigma(shape.H), stream=torch.cuda.current_stream(device).cuda_stream)
+        self.bias = torch.zeros(shape.E, dtype=torch.float32, device=device)
+
+    def set_bias(self, bias):
+        self.bias.copy_(torch.as_tensor(bias, dtype=torch.float32))
+
+
 class Path:
     """Buffers for calls with up to T_max tokens on one layer."""
 
@@ -77,6 +93,9 @@ class Path:
         self.y = torch.zeros((max(T_max, 1), sh.H), dtype=torch.bfloat16, device=device)
         self.ws = torch.zeros(damoe.workspace_size(dl.layer, T_max), dtype=torch.uint8, device=device)
         self.candidates = 0  # variants the last dispatch could choose (0 = all)
+        self.logits = torch.zeros((max(T_max, 1), sh.E), dtype=torch.float32, device=device)
+        self.router_ws = torch.zeros(damoe.router_workspace_size(sh.E, sh.H, T_max), dtype=torch.uint8,
+                                     device=device)
 
     def set_routing(self, r: synth.Routing):
         T = r.T
@@ -91,6 +110,12 @@ class Path:
             synth.fill_bf16_device(self.x.data_ptr(), T * self.dl.shape.H, seed=synth.x_seed(tag),
                                    tensor=synth.T_X, slab_elems=T * self.dl.shape.H, sigma=1.0,
                                    stream=torch.cuda.current_stream().cuda_stream)
+
+    def router(self, gate: Gate, T: int, logits: bool = True, stream=None):
+        """Gating logits, top-k ids and gates of the first T tokens of x into ids / w."""
+        sh = self.dl.shape
+        damoe.router(self.x, gate.wg, gate.bias, T, sh.H, sh.E, sh.k, self.logits if logits else None, self.ids,
+                     self.w, self.router_ws, stream)
 
     def route(self, T: int, ids=None, stream=None):
         sh = self.dl.shape

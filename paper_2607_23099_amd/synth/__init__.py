@@ -42,7 +42,7 @@ LIB_PATH = os.path.join(_HERE, "libdamoe_synth.so")
 IH8_STD = math.sqrt(8.0 * (65536.0 ** 2 - 1.0) / 12.0)
 
 # Tensor ids of the counter-based generator.
-T_X, T_W1, T_W2, T_W3 = 0, 1, 2, 3
+T_X, T_W1, T_W2, T_W3, T_WG = 0, 1, 2, 3, 4
 
 
 def ih_scale(sigma: float) -> float:
@@ -258,6 +258,28 @@ def expert_weights_fp8_host(shape: Shape, e: int):
         q, s = fill_fp8_host(r, c, 1, seed=shape.weight_seed, tensor=tid, slab0=e, sigma=shape.w_sigma)
         out.append((q[0], s[0]))
     return tuple(out)
+
+
+def gate_sigma(H: int) -> float:
+    """Gate weights N(0, 1/H): the logits of N(0, 1) tokens then have unit variance."""
+    return 1.0 / math.sqrt(H)
+
+
+def gate_weights_host(shape: Shape) -> np.ndarray:
+    """bf16 gate weights Wg [E][H] (uint16) of the shape's router."""
+    n = shape.E * shape.H
+    return fill_bf16_host(n, seed=shape.weight_seed, tensor=T_WG, slab_elems=n,
+                          sigma=gate_sigma(shape.H)).reshape(shape.E, shape.H)
+
+
+def gate_bias(E: int, alpha: float | None, seed) -> np.ndarray:
+    """Per-expert gate bias: log p of one Dirichlet(alpha) draw (float32), or zeros for None.
+
+    Added to unit-variance logits it skews the router's choices towards the high-p experts,
+    the more the smaller alpha, like the routing model above."""
+    if alpha is None:
+        return np.zeros(E, np.float32)
+    return dirichlet_logp(np.random.default_rng(seed), E, float(alpha)).astype(np.float32)
 
 
 def x_seed(tag: int) -> int:

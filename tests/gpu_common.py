@@ -2,7 +2,7 @@
 import numpy as np
 
 import oracle
-from paper_2607_23099_amd import synth
+from paper_2607_23099_amd import damoe, synth
 
 # Tolerances on y, row-normalised max error (bf16 / fp8 weights, fp32 accumulation).
 TOL = {"bf16": 2e-2, "fp8": 6e-2}
@@ -49,3 +49,12 @@ def tiles_expected(counts, bm):
     t = oracle.tiles(counts, bm)
     return np.stack([t[:, 0], t[:, 1] | (t[:, 2] << 16)], axis=1).astype(np.int64) if len(t) else \
         np.zeros((0, 2), np.int64)
+
+
+def one_bucket_table(sh, kids, noda):
+    """A one-bucket dispatch table whose exemplars map to `kids` (scored on every call)."""
+    rng = np.random.default_rng(7)
+    q = -np.sort(-rng.integers(0, 1 << 15, (len(kids), sh.E)), axis=1).astype(np.int32)
+    return damoe.Table.create(damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0,
+                                              bucket_T=np.array([1 << 20]), n_ex=np.array([len(kids)]),
+                                              Q=q, kid=np.asarray(kids), noda=np.array([noda])))

@@ -190,3 +190,33 @@ def test_committed_tables_match_the_variant_registry():
             if bin(want).count("1") > 1:
                 want |= 1 << int(td.noda[b])
             assert t.candidates(int(T)) == want
+
+
+def test_router_validation_and_workspace_bound():
+    L = damoe.lib()
+    P = 0x10000  # never dereferenced: every call below stops in validation
+    big = 1 << 40
+    r = L.damoe_router
+    assert r(P, P, None, 4, 256, 8, 9, None, P, P, P, big, None) == -1      # k > E
+    assert r(P, P, None, 4, 256, 2048, 8, None, P, P, P, big, None) == -1   # E beyond the limit
+    assert r(P, P, None, 4, 256, 8, 0, None, P, P, P, big, None) == -1      # k = 0
+    assert r(P, P, None, -1, 256, 8, 2, None, P, P, P, big, None) == -1
+    assert r(P, P, None, 4, 0, 8, 2, None, P, P, P, big, None) == -1
+    assert r(P, P, None, 4, 100, 8, 2, None, P, P, P, big, None) == -2      # H not a multiple of 64
+    assert r(P, P, None, 150000, 7168, 8, 2, None, P, P, P, big, None) == -2  # T*H*2 >= 2^31
+    assert r(None, None, None, 0, 256, 8, 2, None, None, None, None, 0, None) == 0  # T = 0: no-op
+    assert r(P, P, None, 4, 256, 8, 2, None, P, P, P, 0, None) == -3
+    assert r(P, P, None, 4, 256, 8, 2, None, None, P, P, big, None) == -1    # no ids
+    assert r(P, P, None, 4, 256, 8, 2, None, P, P, None, big, None) == -1    # no workspace
+    assert damoe.router_workspace_size(0, 256, 4) == 0
+    assert damoe.router_workspace_size(8, 100, 4) == 0
+    # The size for T_max covers every T <= T_max (the split count, and with it S * T, is not
+    # monotone in T): a call with that many bytes passes the workspace check and stops at the
+    # missing activations instead.
+    rng = np.random.default_rng(0)
+    for E, H, T_max in [(8, 256, 600), (256, 7168, 4096), (384, 7168, 3000), (1000, 64, 300)]:
+        ws = damoe.router_workspace_size(E, H, T_max)
+        assert ws >= T_max * E * 4
+        for T in np.unique(np.r_[1, T_max, rng.integers(1, T_max + 1, 300), np.arange(1, min(T_max, 300))]):
+            assert r(None, P, None, int(T), H, E, 1, None, P, P, P, ws, None) == -1, (E, H, T)
+            assert r(None, P, None, int(T), H, E, 1, None, P, P, P, 16, None) == -3

@@ -7,18 +7,9 @@ import numpy as np
 import pytest
 
 from paper_2607_23099_amd import damoe, synth
-from tests.gpu_common import TOL, bf16_rows, log, oracle_rows, row_err, torch_cuda
+from tests.gpu_common import TOL, bf16_rows, log, one_bucket_table, oracle_rows, row_err, torch_cuda
 
 pytestmark = pytest.mark.gpu
-
-
-def _table(sh, kids, noda):
-    """A one-bucket table whose exemplars map to `kids` (scored on every call)."""
-    rng = np.random.default_rng(7)
-    q = -np.sort(-rng.integers(0, 1 << 15, (len(kids), sh.E)), axis=1).astype(np.int32)
-    return damoe.Table.create(damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0,
-                                              bucket_T=np.array([1 << 20]), n_ex=np.array([len(kids)]),
-                                              Q=q, kid=np.asarray(kids), noda=np.array([noda])))
 
 
 @pytest.mark.parametrize("kids,noda", [([0, 1, 3], 0), ([6, 7, 6], 7), ([2], 2)],
@@ -29,7 +20,7 @@ def test_graph_replays_match_eager(kids, noda):
     sh = synth.TINY
     dl = DeviceLayer(sh, packed=True)
     path = Path(dl, 256)
-    table = _table(sh, kids, noda)
+    table = one_bucket_table(sh, kids, noda)
     T = 96
     routings = [synth.routing(sh.E, sh.k, T, a, [40 + i]) for i, a in enumerate((1.0, 0.05, 10.0, 0.3))]
 

@@ -1,0 +1,243 @@
+"""GPU parity of the router (gating logits, top-k, softmax gates) against the CPU oracle, and
+of the end-to-end layer (router -> routing metadata -> dispatch -> fused experts) captured in
+one HIP graph (Sec. II-A; Sec. V-C times this whole sequence as one graph).
+
+Checks, per call:
+  * logits: |l_gpu - l_exact| <= gamma * (sum_h |x_h w_h| + |b|) with gamma = (H + H/256 + 8) u,
+    u = 2^-24: the recursive-summation bound for the H products (exact in fp32), the partial
+    sums of the K split (at most H/256 of them), the in-block adds and the bias;
+  * ids and gates: the selection is an integer decision taken on floating point, so the
+    oracle takes it on the GPU's own fp32 logits; the ids must match bit for bit, the gates
+    to fp32 rounding of the softmax (expf and one division).
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_23099_amd import damoe, synth
+from tests.gpu_common import TOL, bf16_rows, log, one_bucket_table, oracle_rows, row_err, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -24
+
+
+def _dev_bf16(u16):
+    torch = torch_cuda()
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def _router(x, wg, bias, T, H, E, k, logits=True):
+    """Runs damoe_router on device tensors; returns (logits or None, ids, w) on the host."""
+    torch = torch_cuda()
+    lg = torch.full((max(T, 1), E), float("nan"), dtype=torch.float32, device="cuda") if logits else None
+    ids = torch.full((max(T, 1), k), -7, dtype=torch.int32, device="cuda")
+    w = torch.full((max(T, 1), k), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.empty(damoe.router_workspace_size(E, H, T), dtype=torch.uint8, device="cuda")
+    ws.fill_(0xFF)  # partial sums must all be written by the call
+    damoe.router(x, wg, bias, T, H, E, k, lg, ids, w, ws)
+    torch.cuda.synchronize()
+    return (None if lg is None else lg[:T].cpu().numpy()), ids[:T].cpu().numpy(), w[:T].cpu().numpy()
+
+
+def _check_logits(lg, x_rows_u16, wg_u16, bias, H):
+    xr, wr = synth.bf16_to_f64(x_rows_u16), synth.bf16_to_f64(wg_u16)
+    exact = xr @ wr.T + (0.0 if bias is None else bias.astype(np.float64))
+    mag = np.abs(xr) @ np.abs(wr).T + (0.0 if bias is None else np.abs(bias.astype(np.float64)))
+    gamma = (H + H // 256 + 8) * U
+    err = np.abs(lg.astype(np.float64) - exact)
+    assert np.all(err <= gamma * mag + 1e-30), float(np.max(err / (gamma * mag + 1e-30)))
+    return float(err.max())
+
+
+def _check_selection(lg, ids, w, k):
+    want_ids, want_w = oracle.topk_softmax(lg.astype(np.float64), k)
+    np.testing.assert_array_equal(ids, want_ids)
+    np.testing.assert_allclose(w, want_w, rtol=4 * k * U * 8, atol=1e-7)
+
+
+def _host_case(T, H, E, seed, bias_alpha):
+    rng = np.random.default_rng(seed)
+    x = synth.f32_to_bf16_bits(rng.normal(0, 1, (T, H)))
+    wg = synth.f32_to_bf16_bits(rng.normal(0, 1 / math.sqrt(H), (E, H)))
+    bias = None if bias_alpha is None else synth.gate_bias(E, bias_alpha, seed)
+    return x, wg, bias
+
+
+@pytest.mark.parametrize("T,H,E,k,bias_alpha", [
+    (1, 256, 8, 2, None), (37, 256, 8, 2, 1.0), (200, 256, 8, 2, None),
+    (65, 128, 100, 6, 0.3),      # E not a multiple of the 64-expert tile, ragged token tile
+    (5, 64, 3, 3, None),         # k = E, one K step
+    (300, 512, 1024, 16, 0.05),  # largest E and k
+    (1000, 192, 40, 4, None),    # many token tiles, three K steps
+])
+def test_router_small_shapes(T, H, E, k, bias_alpha):
+    torch = torch_cuda()
+    x, wg, bias = _host_case(T, H, E, T * 1000 + E, bias_alpha)
+    log(f"router T={T} H={H} E={E} k={k} bias={bias_alpha}")
+    b = None if bias is None else torch.from_numpy(bias).cuda()
+    lg, ids, w = _router(_dev_bf16(x), _dev_bf16(wg), b, T, H, E, k)
+    err = _check_logits(lg, x, wg, bias, H)
+    _check_selection(lg, ids, w, k)
+    # Against the fp64 selection: equal wherever the exact logits leave room for the error.
+    o_logits, o_ids, _ = oracle.router(x, wg, k, bias)
+    same = np.all(ids == o_ids, axis=1)
+    srt = -np.sort(-o_logits, axis=1)[:, :min(k + 1, E)]
+    clear = np.all(np.diff(-srt, axis=1) > 4 * max(err, 1e-6), axis=1)
+    assert np.all(same[clear])
+    log(f"  max logit error {err:.2e}; ids equal to the fp64 selection on {same.mean():.3f} of tokens")
+    # Without the logits output the selection is the same.
+    _, ids2, w2 = _router(_dev_bf16(x), _dev_bf16(wg), b, T, H, E, k, logits=False)
+    np.testing.assert_array_equal(ids2, ids)
+    np.testing.assert_array_equal(w2, w)
+
+
+FULL = [("dsv3", synth.DS, 1, None), ("dsv3", synth.DS, 128, 0.3), ("dsv3", synth.DS, 1000, None),
+        ("dsv3", synth.DS, 4096, 0.05), ("kimi", synth.KIMI, 16, 1.0), ("kimi", synth.KIMI, 2048, None),
+        ("kimi", synth.KIMI, 8192, 0.1)]
+
+
+@pytest.mark.parametrize("name,sh,T,bias_alpha", FULL, ids=[f"{f[0]}-T{f[2]}" for f in FULL])
+def test_router_full_shapes(name, sh, T, bias_alpha):
+    # The shapes of the layers (gate weights from the seeded generator, tokens filled on the
+    # device): logits checked on sampled rows, the selection on every row.
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import Gate
+    gate = Gate(sh)
+    bias = synth.gate_bias(sh.E, bias_alpha, [7, T]) if bias_alpha is not None else None
+    if bias is not None:
+        gate.set_bias(bias)
+    x = torch.empty((T, sh.H), dtype=torch.bfloat16, device="cuda")
+    synth.fill_bf16_device(x.data_ptr(), T * sh.H, seed=synth.x_seed(500 + T), tensor=synth.T_X,
+                           slab_elems=T * sh.H, sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
+    log(f"router {name} T={T} bias={bias_alpha}")
+    lg, ids, w = _router(x, gate.wg, gate.bias, T, sh.H, sh.E, sh.k)
+    rows = np.unique(np.r_[0, T - 1, np.random.default_rng(T).choice(T, min(T, 6), replace=False)])
+    xr = synth.activations_host(T, sh.H, 500 + T, rows)
+    _check_logits(lg[rows], xr, synth.gate_weights_host(sh), bias, sh.H)
+    _check_selection(lg, ids, w, sh.k)
+    # The device weights are the generator's.
+    np.testing.assert_array_equal(gate.wg[:2].view(torch.int16).cpu().numpy().view(np.uint16),
+                                  synth.gate_weights_host(sh)[:2])
+
+
+def test_router_ties_and_zero_tokens():
+    # Duplicate gate rows give equal logits bit for bit; all-zero tokens give +0 for every
+    # expert: both resolve to the lower ids, as in the oracle.
+    torch = torch_cuda()
+    T, H, E, k = 70, 256, 130, 5
+    x, wg, _ = _host_case(T, H, E, 41, None)
+    for dup in (77, 129):
+        wg[dup] = wg[3]
+    x[[0, 33, 69]] = 0
+    bias = np.zeros(E, np.float32)
+    bias[[3, 77, 129]] = 50.0
+    lg, ids, w = _router(_dev_bf16(x), _dev_bf16(wg), torch.from_numpy(bias).cuda(), T, H, E, k)
+    np.testing.assert_array_equal(ids[:, :3], np.tile([3, 77, 129], (T, 1)))
+    _check_selection(lg, ids, w, k)
+    lg, ids, w = _router(_dev_bf16(x), _dev_bf16(wg), None, T, H, E, k)
+    for t in (0, 33, 69):
+        np.testing.assert_array_equal(ids[t], np.arange(k))
+        np.testing.assert_allclose(w[t], 1.0 / k, rtol=1e-6)
+    _check_selection(lg, ids, w, k)
+
+
+def test_router_deterministic_and_empty():
+    torch = torch_cuda()
+    T, H, E, k = 96, 7168, 256, 8
+    x, wg, bias = _host_case(T, H, E, 43, 0.5)
+    xd, wd, bd = _dev_bf16(x), _dev_bf16(wg), torch.from_numpy(bias).cuda()
+    a = _router(xd, wd, bd, T, H, E, k)
+    b = _router(xd, wd, bd, T, H, E, k)
+    for u, v in zip(a, b):
+        np.testing.assert_array_equal(u, v)
+    # T = 0 writes nothing.
+    ids = torch.full((4, k), -7, dtype=torch.int32, device="cuda")
+    ws = torch.empty(256, dtype=torch.uint8, device="cuda")
+    damoe.router(xd, wd, bd, 0, H, E, k, None, ids, ids.float(), ws)
+    torch.cuda.synchronize()
+    assert bool((ids == -7).all())
+
+
+def test_router_bias_skews_the_routing():
+    # A Dirichlet log-p bias concentrates the router's choices (fewer Effective Experts).
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import Gate
+    sh = synth.DS
+    gate = Gate(sh)
+    T = 512
+    x = torch.empty((T, sh.H), dtype=torch.bfloat16, device="cuda")
+    synth.fill_bf16_device(x.data_ptr(), T * sh.H, seed=synth.x_seed(900), tensor=synth.T_X,
+                           slab_elems=T * sh.H, sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
+    eff = []
+    for alpha in (None, 1.0, 0.05):
+        gate.set_bias(synth.gate_bias(sh.E, alpha, 5))
+        _, ids, _ = _router(x, gate.wg, gate.bias, T, sh.H, sh.E, sh.k, logits=False)
+        eff.append(oracle.effexp(oracle.histogram(ids, sh.E))[2])
+    log(f"Effective Experts with bias None / 1.0 / 0.05: {eff}")
+    assert eff[0] > eff[1] > eff[2]
+    assert eff[0] > 0.8 * sh.E and eff[2] < 0.25 * sh.E
+
+
+@pytest.mark.parametrize("kids,noda", [([0, 1, 3], 0), ([6, 7, 6], 7)], ids=["stream-variants", "tiled-and-big"])
+def test_end_to_end_layer_in_one_graph(kids, noda):
+    # router -> histogram / permutation / match -> fused experts, captured once and replayed
+    # on new tokens; every replay equals the eager sequence, and the eager output equals the
+    # oracle layer on the router's (validated) ids and gates.
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Gate, Path
+    sh = synth.TINY
+    dl = DeviceLayer(sh, packed=True)
+    gate = Gate(sh)
+    path = Path(dl, 256)
+    table = one_bucket_table(sh, kids, noda)
+    T = 150
+
+    def step():
+        path.router(gate, T)
+        path.route_dispatch(table, T)
+        path.fused(T, -1)
+
+    eager = []
+    for i, alpha in enumerate((None, 0.3, 0.05)):
+        gate.set_bias(synth.gate_bias(sh.E, alpha, i))
+        path.fill_x(T, 60 + i)
+        step()
+        torch.cuda.synchronize()
+        eager.append((path.y[:T].clone(), path.ids[:T * sh.k].clone(), path.w[:T * sh.k].clone(),
+                      int(path.variant.item())))
+    # Parity of the eager layer on the last bias with the oracle.
+    y, ids, w, _ = eager[2]
+    ids = ids.cpu().numpy().reshape(T, sh.k)
+    w = w.cpu().numpy().reshape(T, sh.k)
+    _check_selection(path.logits[:T].cpu().numpy(), ids, w, sh.k)
+    r = synth.Routing(ids, w, None, sh.E, sh.k, None)
+    rows = np.arange(0, T, 7)
+    assert row_err(bf16_rows(y, rows), oracle_rows(sh, r, 62, rows)) <= TOL["bf16"]
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for i, alpha in enumerate((None, 0.3, 0.05)):
+            gate.set_bias(synth.gate_bias(sh.E, alpha, i))
+            path.fill_x(T, 60 + i)
+            path.y.fill_(float("nan"))
+            path.ids.fill_(-1)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(path.ids[:T * sh.k], eager[i][1]), (rep, i)
+            assert torch.equal(path.w[:T * sh.k], eager[i][2]), (rep, i)
+            assert int(path.variant.item()) == eager[i][3]
+            assert torch.equal(path.y[:T], eager[i][0]), (rep, i)
+    assert damoe.read_device_error(path.ws) == 0

@@ -537,3 +537,16 @@ def test_router_ties_go_to_the_lower_id():
     _, ids, w = oracle.router(x[3:], wg, 4)
     np.testing.assert_array_equal(ids, [[0, 1, 2, 3]])
     np.testing.assert_allclose(w, 0.25, rtol=1e-14)
+
+
+def test_topk_softmax_on_given_logits():
+    # Selection on given values (as the GPU checks feed it fp32 logits): heavy ties from a
+    # coarse grid, against numpy's stable argsort; gates against scipy's softmax.
+    from scipy.special import softmax
+    rng = np.random.default_rng(36)
+    l = rng.integers(-3, 4, (50, 20)).astype(np.float32) / 4
+    for k in (1, 4, 20):
+        ids, w = oracle.topk_softmax(l, k)
+        np.testing.assert_array_equal(ids, np.argsort(-l.astype(np.float64), axis=1, kind="stable")[:, :k])
+        want = softmax(np.take_along_axis(l.astype(np.float64), ids, axis=1), axis=1)
+        np.testing.assert_allclose(w, want, rtol=1e-13)
