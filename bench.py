@@ -363,6 +363,152 @@ def run_dispatch(args):
     print(json.dumps(out), flush=True)
 
 
+def bucket_of(td, T: int) -> int:
+    return next((i for i, bt in enumerate(td.bucket_T) if T <= bt), len(td.bucket_T) - 1)
+
+
+def router_bytes(shape, T: int) -> int:
+    """Algorithmic HBM bytes of one router call: gate weights and token rows read once, ids and
+    gates written (no logits output)."""
+    return shape.E * shape.H * 2 + T * shape.H * 2 + T * shape.k * 8
+
+
+def run_e2e(args):
+    """End-to-end MoE layer on the DeepSeek-V3 decode shape (the analog of the paper's
+    end-to-end latency figure, Sec. V-C): router (gating logits, top-k, softmax gates), routing
+    metadata, dispatch and the fused experts, captured in one HIP graph per token count and
+    replayed.  DA-MoE (exemplar match, device-side id) against NoDA (route without a match, the
+    bucket's static variant).  The skew comes from the router: a per-expert bias log p,
+    p ~ Dirichlet(alpha), over unit-variance logits; REPS token sets and bias draws per point
+    are rotated between replays."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Gate, Path
+
+    shape = synth.DS
+    log(f"filling {shape.name} weights and gate on the device")
+    dl = DeviceLayer(shape)
+    gate = Gate(shape)
+    Tm = max(DECODE_T)
+    path = Path(dl, Tm)
+    stream = torch.cuda.current_stream()
+    xs = []
+    for rep in range(REPS):
+        t = torch.empty((Tm, shape.H), dtype=torch.bfloat16, device="cuda")
+        synth.fill_bf16_device(t.data_ptr(), Tm * shape.H, seed=synth.x_seed(700 + rep), tensor=synth.T_X,
+                               slab_elems=Tm * shape.H, sigma=1.0, stream=stream.cuda_stream)
+        xs.append(t)
+    biases = {(a, rep): torch.from_numpy(synth.gate_bias(shape.E, a, [8, int(round(1000 * a)), rep])).cuda()
+              for a in DECODE_ALPHA for rep in range(REPS)}
+    path.x.copy_(xs[0])
+    torch.cuda.synchronize()
+    table, note = load_or_tune_table(dl, path.x, args.quick_tune)
+    td = table.data(shape.E)
+
+    def capture(fn):
+        s_ = torch.cuda.Stream()
+        s_.wait_stream(stream)
+        with torch.cuda.stream(s_):
+            fn()
+        stream.wait_stream(s_)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s_):
+            fn()
+        torch.cuda.synchronize()
+        return g
+
+    graphs, noda_v = {}, {}
+    for T in DECODE_T:
+        noda_v[T] = int(td.noda[bucket_of(td, T)])
+
+        def da(T=T):
+            path.router(gate, T, logits=False)
+            path.route_dispatch(table, T)
+            path.fused(T, -1)
+
+        def nd(T=T):
+            path.router(gate, T, logits=False)
+            path.route(T)
+            path.candidates = 0
+            path.fused(T, noda_v[T])
+
+        graphs[T] = {"da": capture(da), "noda": capture(nd),
+                     "router": capture(lambda T=T: path.router(gate, T, logits=False))}
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    # A replay of a short graph is host-bound when the stream is idle: the events would time
+    # the host's launch.  Each timed replay is therefore queued behind a GPU spin of ~100 us,
+    # so the graph's work is already in the queue when the first event fires.
+    e0, e1 = ev(), ev()
+    e0.record(stream)
+    torch.cuda._sleep(1 << 20)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    spin = max(1, int((1 << 20) * 0.1 / max(e0.elapsed_time(e1), 1e-3)))
+    rows, t_wall = {}, time.perf_counter()
+    for T in DECODE_T:
+        for a in DECODE_ALPHA:
+            row = {}
+            chosen, effs = [], []
+            for rep in range(REPS):  # untimed: the variant and skew each rotation leads to
+                path.x[:T].copy_(xs[rep][:T])
+                gate.bias.copy_(biases[a, rep])
+                graphs[T]["da"].replay()
+                torch.cuda.synchronize()
+                chosen.append(damoe.variant_name(int(path.variant.item())))
+                nd_ = path.numden.cpu().numpy()
+                effs.append(float(nd_[0]) / max(float(nd_[1]), 1.0))
+            row["variants"] = chosen
+            row["eff_experts"] = round(float(np.mean(effs)), 1)
+            for mode in ("da", "noda", "router"):
+                g = graphs[T][mode]
+                pairs = []
+                for s in range(args.warmup + args.steps):
+                    rep = s % REPS
+                    path.x[:T].copy_(xs[rep][:T])
+                    gate.bias.copy_(biases[a, rep])
+                    torch.cuda._sleep(spin)
+                    e0, e1 = ev(), ev()
+                    e0.record(stream)
+                    g.replay()
+                    e1.record(stream)
+                    if s >= args.warmup:
+                        pairs.append((e0, e1))
+                torch.cuda.synchronize()
+                row[f"{mode}_us"] = round(float(np.mean([p[0].elapsed_time(p[1]) for p in pairs])) * 1e3, 2)
+            row["noda_variant"] = damoe.variant_name(noda_v[T])
+            row["router_GBs"] = round(router_bytes(shape, T) / (row["router_us"] * 1e-6) / 1e9, 1)
+            rows[f"T{T}_a{a}"] = row
+            log(f"e2e T={T} alpha={a}: {row}")
+    wall = time.perf_counter() - t_wall
+    da_g = geomean([r["da_us"] for r in rows.values()])
+    nd_g = geomean([r["noda_us"] for r in rows.values()])
+    out = {
+        "metric": "end-to-end MoE layer latency in one graph (router + metadata + dispatch + fused experts), "
+                  "geomean over the DeepSeek-V3 decode skew sweep",
+        "value": round(da_g, 2),
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / max(args.steps, 1) * 1e3, 3),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dsv3-e2e: E=256 top-8 H=7168 I=2048 bf16, T in {1,8,32,128} x router bias "
+                               "log Dirichlet(alpha), alpha in {0.05,0.3,1,10}, graph replay",
+                   "table": note},
+        "noda_us": round(nd_g, 2),
+        "speedup_vs_noda": round(nd_g / da_g, 4),
+        "router_us_geomean": round(geomean([r["router_us"] for r in rows.values()]), 2),
+        "per_point": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def run_prefill(args):
     """Per-variant GEMM times at the MFMA-bound prefill points: Kimi-K2 (bf16, 40% of the mass
     on 4 hot experts) at T = 2048 and 8192, and DeepSeek-V3 with fp8 block-128 weights at
@@ -473,7 +619,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
-    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy"],
+    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
     ap.add_argument("--dispatch-reps", type=int, default=200)
@@ -506,6 +652,8 @@ def main():
         return run_prefill(args)
     if args.workload == "copy":
         return run_copy(args)
+    if args.workload == "e2e":
+        return run_e2e(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")

@@ -4,13 +4,16 @@
 //
 // Two kernels, both deterministic:
 //   k_router_logits  bf16 MFMA 32x32x16 over (token tile, 64-expert tile, K split); the waves
-//                    of a block either split the block's K range (few tokens: the gate matrix
-//                    is the traffic, so it is spread over many blocks) or own 32-token slices
-//                    of a 128-token tile (many tokens: the gate tile is shared through L1).
+//                    of a block either split the block's K range four ways (few tokens: the
+//                    gate matrix is the traffic, so it is spread over many blocks) or own
+//                    32-token slices of a 128-token tile, two waves per slice along K (many
+//                    tokens: the gate tile is shared through L1, a 3-deep register ring keeps
+//                    two steps of loads in flight per wave).
 //                    Partial sums go to the workspace as fp32 [S][T][E].
-//   k_router_topk    one wave per token: sums the S partials in a fixed order, adds the bias,
-//                    selects the top k with an order-preserving integer key (ties to the lower
-//                    expert id) and writes ids and softmax gates.
+//   k_router_topk_*  sums the S partials in split order (a block per token when S is large,
+//                    a wave per token otherwise), adds the bias, selects the top k with an
+//                    order-preserving integer key (ties to the lower expert id) and writes ids
+//                    and softmax gates.
 #include "common.h"
 #include "device.h"
 
@@ -21,7 +24,6 @@ constexpr int kTok = 32;           // tokens per wave tile (MFMA rows)
 constexpr int kExpTile = 64;       // experts per block tile (two 32-wide MFMA blocks)
 constexpr int kStepK = 64;         // k per step: 128 contiguous bytes of each row
 constexpr int kTargetBlocks = 256; // blocks the few-token plan aims for (one per compute unit)
-constexpr int kMaxLanesE = DAMOE_MAX_E / kWave;
 
 struct LogitsArgs {
   const uint16_t* x;   // [T][H]
@@ -40,10 +42,10 @@ struct TopkArgs {
   int32_t T, E, k, S;
 };
 
-// WT waves along tokens (32 tokens each) x WK = 4 / WT waves along K.
-template <int WT>
-__global__ __launch_bounds__(256) void k_router_logits(LogitsArgs a) {
-  constexpr int WK = 4 / WT;
+// WT waves along tokens (32 tokens each) x WK waves along K; NB register sets of operands
+// (NB - 1 steps of loads in flight while one multiplies).
+template <int WT, int WK, int NB>
+__global__ __launch_bounds__(kWave * WT * WK) void k_router_logits(LogitsArgs a) {
   pin(a.x);
   pin(a.wg);
   pin(a.part);
@@ -60,7 +62,9 @@ __global__ __launch_bounds__(256) void k_router_logits(LogitsArgs a) {
   const int et = (item / a.tiles_t) % a.tiles_e;
   const int s = item / (a.tiles_t * a.tiles_e);
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // The wave index is uniform within a wave; in a scalar register the K range and the
+  // buffer offsets derived from it stay scalar (no per-lane loop around each buffer load).
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int tw = wave % WT, kw = wave / WT;
   const int r = lane & 31, h = lane >> 5;
   const int t0 = tt * kTok * WT + tw * kTok;
@@ -90,11 +94,11 @@ __global__ __launch_bounds__(256) void k_router_logits(LogitsArgs a) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[c][i] = 0.0f;
 
-  // Two register sets: the loads of the next step are in flight while the current one
-  // multiplies.  The prefetch past the last step re-reads that step (harmless, in bounds).
-  uint4 xa[2][4], wb[2][2][4];
+  // A ring of NB register sets.  Loads beyond the last step re-read that step (in bounds,
+  // unused).
+  uint4 xa[NB][4], wb[NB][2][4];
   auto load = [&](int st, int buf) {
-    const uint32_t soff = (uint32_t)st * (kStepK * 2);
+    const uint32_t soff = (uint32_t)min(st, st1 - 1) * (kStepK * 2);
 #pragma unroll
     for (int i = 0; i < 4; ++i) xa[buf][i] = buf_load<uint4, 0>(rx, vx + 16u * i, soff);
 #pragma unroll
@@ -108,44 +112,57 @@ __global__ __launch_bounds__(256) void k_router_logits(LogitsArgs a) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) acc[c] = mfma32x32x16(xa[buf][i], wb[buf][c][i], acc[c]);
   };
-  if (st0 < st1) load(st0, 0);
-  for (int st = st0; st < st1; st += 2) {
-    load(min(st + 1, st1 - 1), 1);
-    mul(0);
-    if (st + 1 >= st1) break;
-    load(min(st + 2, st1 - 1), 0);
-    mul(1);
+  // Invariant at the top of each group: register set u holds step st + u for u < NB - 1.
+  // Whole groups run without guards (one path, so the compiler's wait counts are exact); the
+  // fewer than NB steps left over are then already in flight and only multiply.
+  if (st0 < st1) {
+#pragma unroll
+    for (int i = 0; i < NB - 1; ++i) load(st0 + i, i);
+    int st = st0;
+    for (; st + NB <= st1; st += NB) {
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        // The scheduler would sink the prefetch below the multiplies; keep the issue order.
+        load(st + u + NB - 1, (u + NB - 1) % NB);
+        __builtin_amdgcn_sched_barrier(0);
+        mul(u);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NB - 1; ++u)
+      if (st + u < st1) mul(u);
   }
 
   // Output element (token 8 (q / 4) + 4 h + q % 4, expert 32 c + r) of accumulator register q.
+  // With WK > 1 the K slices meet in LDS and the first slice's waves add them in slice order.
   float* out = a.part + (size_t)s * a.T * a.E;
-  if constexpr (WK == 1) {
+  if constexpr (WK > 1) {
+    __shared__ float red[WK - 1][WT * kTok][kExpTile + 1];
+    if (kw > 0) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int e = e0 + 32 * c + r;
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int t = t0 + 8 * (q >> 2) + 4 * h + (q & 3);
-        if (t < a.T && e < a.E) out[(size_t)t * a.E + e] = acc[c][q];
-      }
+        for (int q = 0; q < 16; ++q)
+          red[kw - 1][tw * kTok + 8 * (q >> 2) + 4 * h + (q & 3)][32 * c + r] = acc[c][q];
     }
-  } else {
-    // The four K quarters meet in LDS and are added in wave order.
-    __shared__ float red[WK][kTok][kExpTile + 1];
+    __syncthreads();
+    if (kw > 0) return;
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) red[kw][8 * (q >> 2) + 4 * h + (q & 3)][32 * c + r] = acc[c][q];
-    __syncthreads();
+      for (int q = 0; q < 16; ++q)
 #pragma unroll
-    for (int j = 0; j < kTok * kExpTile / 256; ++j) {
-      const int idx = threadIdx.x + 256 * j;
-      const int tr = idx / kExpTile, ec = idx % kExpTile;
-      float v = red[0][tr][ec];
+        for (int w = 0; w < WK - 1; ++w)
+          acc[c][q] += red[w][tw * kTok + 8 * (q >> 2) + 4 * h + (q & 3)][32 * c + r];
+  }
 #pragma unroll
-      for (int w = 1; w < WK; ++w) v += red[w][tr][ec];
-      const int t = t0 + tr, e = e0 + ec;
-      if (t < a.T && e < a.E) out[(size_t)t * a.E + e] = v;
+  for (int c = 0; c < 2; ++c) {
+    const int e = e0 + 32 * c + r;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int t = t0 + 8 * (q >> 2) + 4 * h + (q & 3);
+      if (t < a.T && e < a.E) out[(size_t)t * a.E + e] = acc[c][q];
     }
   }
 }
@@ -161,91 +178,160 @@ __device__ __forceinline__ float key_float(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) {
-    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m);
-    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m);
-    const uint64_t o = ((uint64_t)hi << 32) | lo;
-    v = o > v ? o : v;
-  }
-  return v;
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp0(uint32_t v) {
+  // Lanes of rows outside ROW_MASK read 0, the identity of an unsigned max.
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xF, false);
 }
 
-__global__ __launch_bounds__(256) void k_router_topk(TopkArgs a) {
+// Unsigned max over the wave, returned to every lane: butterflies within quads, 8- and
+// 16-lane mirrors, then row broadcasts into the last row and a read of lane 63.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp0<0xB1, 0xF>(v));   // quad_perm [1,0,3,2]
+  v = max(v, dpp0<0x4E, 0xF>(v));   // quad_perm [2,3,0,1]
+  v = max(v, dpp0<0x141, 0xF>(v));  // row_half_mirror
+  v = max(v, dpp0<0x140, 0xF>(v));  // row_mirror
+  v = max(v, dpp0<0x142, 0xA>(v));  // row_bcast15: rows 1, 3 take rows 0, 2
+  v = max(v, dpp0<0x143, 0xC>(v));  // row_bcast31: rows 2, 3 take row 1
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Top-k selection and gates of token t from the E logits the wave holds (expert lane + 64 j
+// in v[j], bit j of `left` set where that expert exists).  Each round takes the largest key
+// left; among lanes and registers holding it the lowest expert id wins (smallest j, then
+// lowest lane, found with ballots).  The rounds are a loop, not unrolled: the kernel stays
+// small, so a block's first instruction fetches are few.
+template <int NJ>
+__device__ __forceinline__ void select_topk(const float (&v)[NJ], uint32_t left, int lane, int t,
+                                            const TopkArgs& a) {
+  uint32_t key[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) key[j] = float_key(v[j]);
+  int32_t my_id = 0;
+  float my_val = 0.0f, top = 0.0f, z = 0.0f;
+#pragma unroll 1
+  for (int r = 0; r < a.k; ++r) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if ((left >> j) & 1u) m = max(m, key[j]);
+    m = wave_max_u32(m);
+    int32_t e = -1;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      if (e < 0) {
+        const uint64_t hold = __ballot(((left >> j) & 1u) && key[j] == m);
+        if (hold) e = kWave * j + (int32_t)__builtin_ctzll(hold);
+      }
+    }
+    if ((e & (kWave - 1)) == lane) left &= ~(1u << (e / kWave));
+    const float val = key_float(m);
+    if (r == 0) top = val;
+    z += expf(val - top);
+    if (r == lane) {
+      my_id = e;
+      my_val = val;
+    }
+  }
+  if (lane < a.k) {
+    a.ids[(size_t)t * a.k + lane] = my_id;
+    a.w[(size_t)t * a.k + lane] = expf(my_val - top) / z;
+  }
+}
+
+// Few splits (many tokens): one wave per token sums its experts' S partials in split order.
+// NJ = 64-expert groups held per lane (ceil(E / 64) rounded up to a power of two).
+template <int NJ>
+__global__ __launch_bounds__(256) void k_router_topk_wave(TopkArgs a) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= a.T) return;
-  const int nj = (a.E + kWave - 1) / kWave;
-
-  // Sum of the S partials in split order, four splits' loads in flight at a time.
-  float v[kMaxLanesE];
-  uint32_t left = 0;  // bit j: expert lane + 64 j is still selectable
+  float v[NJ];
+  uint32_t left = 0;
 #pragma unroll
-  for (int j = 0; j < kMaxLanesE; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     v[j] = 0.0f;
-    if (j < nj && lane + kWave * j < a.E) left |= 1u << j;
+    if (lane + kWave * j < a.E) left |= 1u << j;
   }
   const float* p = a.part + (size_t)t * a.E + lane;
   const size_t split = (size_t)a.T * a.E;
-  for (int s0 = 0; s0 < a.S; s0 += 4) {
-    float q[4][kMaxLanesE];
+#pragma unroll 1
+  for (int s = 0; s < a.S; ++s) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int j = 0; j < kMaxLanesE; ++j)
-        q[u][j] = (s0 + u < a.S && ((left >> j) & 1u)) ? p[(size_t)(s0 + u) * split + kWave * j] : 0.0f;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int j = 0; j < kMaxLanesE; ++j)
-        if (s0 + u < a.S) v[j] += q[u][j];
+    for (int j = 0; j < NJ; ++j)
+      if ((left >> j) & 1u) v[j] += p[(size_t)s * split + kWave * j];
   }
 #pragma unroll
-  for (int j = 0; j < kMaxLanesE; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     if ((left >> j) & 1u) {
       const int e = lane + kWave * j;
       if (a.bias) v[j] += a.bias[e];
       if (a.logits) a.logits[(size_t)t * a.E + e] = v[j];
     }
   }
+  select_topk<NJ>(v, left, lane, t, a);
+}
 
-  // Slot r: the largest key among the experts left, equal keys to the lower id (the low word
-  // holds ~e, so the larger word is the lower expert).
-  int32_t my_id = 0;
-  float my_val = 0.0f, top = 0.0f;
-  float vals[DAMOE_MAX_K];
+// Many splits (few tokens): a block per token.  Each thread sums MB = NJ / 4 experts over the
+// S partials in split order, 32 / MB splits' loads in flight at a time (the whole sum in one
+// round trip for S <= 32 at E <= 256); the logits meet in LDS and the first wave selects.
+template <int NJ>
+__global__ __launch_bounds__(256) void k_router_topk_block(TopkArgs a) {
+  constexpr int MB = NJ >= 4 ? NJ / 4 : 1;
+  constexpr int B = 32 / MB;
+  __shared__ float lg[NJ * kWave];
+  const int t = blockIdx.x;
+  const float* p = a.part + (size_t)t * a.E + threadIdx.x;
+  const size_t split = (size_t)a.T * a.E;
+  float v[MB];
 #pragma unroll
-  for (int r = 0; r < DAMOE_MAX_K; ++r) {
-    vals[r] = 0.0f;
-    if (r < a.k) {
-      uint64_t best = 0;
+  for (int m = 0; m < MB; ++m) v[m] = 0.0f;
+#pragma unroll 1
+  for (int s0 = 0; s0 < a.S; s0 += B) {
+    float q[B][MB];
 #pragma unroll
-      for (int j = 0; j < kMaxLanesE; ++j) {
-        if ((left >> j) & 1u) {
-          const uint64_t c = ((uint64_t)float_key(v[j]) << 32) | (0xFFFFFFFFu - (uint32_t)(lane + kWave * j));
-          best = c > best ? c : best;
-        }
-      }
-      best = wave_max_u64(best);
-      const int32_t e = (int32_t)(0xFFFFFFFFu - (uint32_t)best);
-      if ((e & (kWave - 1)) == lane) left &= ~(1u << (e / kWave));
-      vals[r] = key_float((uint32_t)(best >> 32));
-      if (r == 0) top = vals[0];
-      if (r == lane) {
-        my_id = e;
-        my_val = vals[r];
-      }
+    for (int u = 0; u < B; ++u)
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+        q[u][m] = (s0 + u < a.S && (int)threadIdx.x + 256 * m < a.E) ? p[(size_t)(s0 + u) * split + 256 * m] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < B; ++u)
+#pragma unroll
+      for (int m = 0; m < MB; ++m)
+        if (s0 + u < a.S) v[m] += q[u][m];
+  }
+#pragma unroll
+  for (int m = 0; m < MB; ++m) {
+    const int e = threadIdx.x + 256 * m;
+    if (e < a.E) {
+      if (a.bias) v[m] += a.bias[e];
+      if (a.logits) a.logits[(size_t)t * a.E + e] = v[m];
+      lg[e] = v[m];
     }
   }
-  float z = 0.0f;
+  __syncthreads();
+  if (threadIdx.x >= kWave) return;
+  const int lane = threadIdx.x;
+  float w[NJ];
+  uint32_t left = 0;
 #pragma unroll
-  for (int r = 0; r < DAMOE_MAX_K; ++r)
-    if (r < a.k) z += expf(vals[r] - top);
-  if (lane < a.k) {
-    a.ids[(size_t)t * a.k + lane] = my_id;
-    a.w[(size_t)t * a.k + lane] = expf(my_val - top) / z;
+  for (int j = 0; j < NJ; ++j) {
+    w[j] = 0.0f;
+    if (lane + kWave * j < a.E) {
+      w[j] = lg[lane + kWave * j];
+      left |= 1u << j;
+    }
   }
+  select_topk<NJ>(w, left, lane, t, a);
+}
+
+template <int NJ>
+hipError_t launch_topk(const TopkArgs& ta, bool per_block, hipStream_t stream) {
+  if (per_block)
+    hipLaunchKernelGGL(k_router_topk_block<NJ>, dim3(ta.T), dim3(256), 0, stream, ta);
+  else
+    hipLaunchKernelGGL(k_router_topk_wave<NJ>, dim3((ta.T + 3) / 4), dim3(256), 0, stream, ta);
+  return hipGetLastError();
 }
 
 struct Plan {
@@ -313,15 +399,21 @@ damoe_status damoe_router(const uint16_t* x, const uint16_t* wg, const float* bi
   if (!x || !wg || !topk_ids || !topk_w || !ws) return DAMOE_ERR_INVALID_ARG;
   const Plan p = plan(T, H, E);
   LogitsArgs la{x, wg, static_cast<float*>(ws), T, H, E, p.S, p.tiles_t, p.tiles_e, p.n_items, p.per_xcd};
-  const dim3 grid(8 * p.per_xcd), block(256);
+  const dim3 grid(8 * p.per_xcd);
   if (p.wt == 4)
-    hipLaunchKernelGGL(k_router_logits<4>, grid, block, 0, stream, la);
+    hipLaunchKernelGGL((k_router_logits<4, 2, 3>), grid, dim3(512), 0, stream, la);
   else
-    hipLaunchKernelGGL(k_router_logits<1>, grid, block, 0, stream, la);
+    hipLaunchKernelGGL((k_router_logits<1, 4, 2>), grid, dim3(256), 0, stream, la);
   if (hipGetLastError() != hipSuccess) return DAMOE_ERR_HIP;
   TopkArgs ta{static_cast<const float*>(ws), bias, logits, topk_ids, topk_w, T, E, k, p.S};
-  hipLaunchKernelGGL(k_router_topk, dim3((T + 3) / 4), block, 0, stream, ta);
-  return hipGetLastError() == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+  const bool per_block = p.S > 2;
+  const int groups = (E + kWave - 1) / kWave;
+  const hipError_t e = groups <= 1   ? launch_topk<1>(ta, per_block, stream)
+                       : groups <= 2 ? launch_topk<2>(ta, per_block, stream)
+                       : groups <= 4 ? launch_topk<4>(ta, per_block, stream)
+                       : groups <= 8 ? launch_topk<8>(ta, per_block, stream)
+                                     : launch_topk<16>(ta, per_block, stream);
+  return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
 }
 
 }  // extern "C"
