@@ -438,14 +438,9 @@ def run_e2e(args):
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
     # A replay of a short graph is host-bound when the stream is idle: the events would time
-    # the host's launch.  Each timed replay is therefore queued behind a GPU spin of ~100 us,
+    # the host's launch.  Each timed replay is therefore queued behind a GPU spin of ~300 us,
     # so the graph's work is already in the queue when the first event fires.
-    e0, e1 = ev(), ev()
-    e0.record(stream)
-    torch.cuda._sleep(1 << 20)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    spin = max(1, int((1 << 20) * 0.1 / max(e0.elapsed_time(e1), 1e-3)))
+    spin = gpu_spin(torch, stream)
     rows, t_wall = {}, time.perf_counter()
     for T in DECODE_T:
         for a in DECODE_ALPHA:
@@ -504,6 +499,97 @@ def run_e2e(args):
         "noda_us": round(nd_g, 2),
         "speedup_vs_noda": round(nd_g / da_g, 4),
         "router_us_geomean": round(geomean([r["router_us"] for r in rows.values()]), 2),
+        "per_point": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
+ROUTER_T = (1, 8, 32, 128, 1024, 4096, 8192)
+MFMA_BF16_PEAK_TFS = 2500.0
+
+
+def gpu_spin(torch, stream, us: float = 300.0):
+    """Cycles of torch's GPU spin that take ~us microseconds: queued before a short timed call,
+    the spin keeps the GPU busy while the host enqueues the call, so events time the GPU."""
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(1 << 16)  # the first call pays its own start-up
+    torch.cuda.synchronize()
+    e0, e1 = ev(), ev()
+    torch.cuda._sleep(1 << 16)  # busy while the events and the measured spin are queued
+    e0.record(stream)
+    torch.cuda._sleep(1 << 22)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return max(1, int((1 << 22) * us * 1e-3 / max(e0.elapsed_time(e1), 1e-3)))
+
+
+def run_router(args):
+    """The router alone (gating logits, top-k, softmax gates) on the DeepSeek-V3 and Kimi-K2
+    gate shapes over decode and prefill token counts: GPU time per call (HIP events behind a
+    spin), algorithmic bytes (gate weights + token rows + ids and gates) and FLOPs, and the
+    fraction of the bounding roofline t_roof = max(bytes / 8 TB/s, flops / 2.5 PFLOP/s)."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import Gate
+
+    stream = torch.cuda.current_stream()
+    spin = gpu_spin(torch, stream)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    rows = {}
+    for sh in (synth.DS, synth.KIMI):
+        gate = Gate(sh)
+        gate.set_bias(synth.gate_bias(sh.E, 0.3, [9, sh.E]))
+        Tm = max(ROUTER_T)
+        x = torch.empty((Tm, sh.H), dtype=torch.bfloat16, device="cuda")
+        synth.fill_bf16_device(x.data_ptr(), Tm * sh.H, seed=synth.x_seed(800), tensor=synth.T_X,
+                               slab_elems=Tm * sh.H, sigma=1.0, stream=stream.cuda_stream)
+        ids = torch.empty((Tm, sh.k), dtype=torch.int32, device="cuda")
+        w = torch.empty((Tm, sh.k), dtype=torch.float32, device="cuda")
+        ws = torch.empty(damoe.router_workspace_size(sh.E, sh.H, Tm), dtype=torch.uint8, device="cuda")
+        for T in ROUTER_T:
+            for _ in range(args.warmup):
+                damoe.router(x, gate.wg, gate.bias, T, sh.H, sh.E, sh.k, None, ids, w, ws)
+            pairs = []
+            for _ in range(args.steps):
+                torch.cuda._sleep(spin)
+                e0, e1 = ev(), ev()
+                e0.record(stream)
+                damoe.router(x, gate.wg, gate.bias, T, sh.H, sh.E, sh.k, None, ids, w, ws)
+                e1.record(stream)
+                pairs.append((e0, e1))
+            torch.cuda.synchronize()
+            us = float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3
+            byts = router_bytes(sh, T)
+            flops = 2.0 * T * sh.H * sh.E
+            t_hbm, t_mfma = byts / (HBM_PEAK_GBS * 1e3), flops / (MFMA_BF16_PEAK_TFS * 1e6)  # us
+            rows[f"{sh.name}_T{T}"] = {"us": round(us, 2), "GBs": round(byts / us / 1e3, 1),
+                                       "TFs": round(flops / us / 1e6, 1),
+                                       "frac": round(max(t_hbm, t_mfma) / us, 4),
+                                       "bound": "hbm" if t_hbm >= t_mfma else "mfma"}
+            log(f"router {sh.name} T={T}: {rows[f'{sh.name}_T{T}']}")
+        del gate, x
+        torch.cuda.empty_cache()
+    big = rows[f"{synth.DS.name}_T{max(ROUTER_T)}"]
+    out = {
+        "metric": "router latency (gating logits + top-k + softmax gates), DeepSeek-V3 gate at T=8192",
+        "value": big["us"],
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(big["us"] / 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "router: E=256 / 384, top-8, H=7168, bf16 x and gate, fp32 bias, "
+                               f"T in {list(ROUTER_T)}"},
+        "roofline": {"bound": big["bound"], "kernel": "k_router_logits + k_router_topk",
+                     "achieved": big["GBs"] if big["bound"] == "hbm" else big["TFs"],
+                     "peak": HBM_PEAK_GBS if big["bound"] == "hbm" else MFMA_BF16_PEAK_TFS,
+                     "unit": "GB/s" if big["bound"] == "hbm" else "TFLOP/s", "frac": big["frac"],
+                     "traffic": None},
         "per_point": rows,
     }
     print(json.dumps(out), flush=True)
@@ -619,7 +705,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
-    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e"],
+    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
     ap.add_argument("--dispatch-reps", type=int, default=200)
@@ -654,6 +740,8 @@ def main():
         return run_copy(args)
     if args.workload == "e2e":
         return run_e2e(args)
+    if args.workload == "router":
+        return run_router(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
