@@ -214,7 +214,11 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
 
     // Wave (wt, wr) accumulates 4 x 4 MFMA blocks of 32 x 32: block (m, n) = weight rows
     // 32 m .. + 31 of the wave's 128 (GEMM1: m = 0, 1 gate features, m = 2, 3 the same up
-    // features) x tokens wt * 128 + 32 n .. + 31.
+    // features) x the 32 tokens of token block 2 n + wt.  Interleaving the token blocks of the
+    // two token waves splits a short tile evenly between them; a wave multiplies only its
+    // first nn blocks, those holding valid rows (rows beyond `rows` are never stored, so the
+    // blocks after them need no MFMA).
+    const int nn = min(4, max(0, ((rows + 31) / 32 - wt + 1) / 2));
     floatx16 acc[4][4];
 #pragma unroll
     for (int m = 0; m < 4; ++m)
@@ -231,7 +235,8 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
       uint4 t[4];
       float sg, su;  // fp8: block scales of the stage (times 2^120)
     };
-    auto read_ops = [&](int ks, int st, const lds_t* cur, Ops& o) __attribute__((always_inline)) {
+    auto read_ops = [&](int ks, int st, const lds_t* cur, Ops& o, auto nn_c) __attribute__((always_inline)) {
+      constexpr int NN = decltype(nn_c)::value;
       const int c = 2 * ks + lh;
       if constexpr (FP8) {
         o.sg = sc_lds[st >> 2];
@@ -249,17 +254,19 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
         }
       }
 #pragma unroll
-      for (int n = 0; n < 4; ++n)
-        o.t[n] = lds_read16(cur + (wt * 8 + 2 * n + (l32 >> 4)) * kFrag + (lr + 16 * c) * 16);
+      for (int n = 0; n < NN; ++n)
+        o.t[n] = lds_read16(cur + (4 * n + 2 * wt + (l32 >> 4)) * kFrag + (lr + 16 * c) * 16);
     };
-    auto mma = [&](const Ops& o) __attribute__((always_inline)) {
+    auto mma = [&](const Ops& o, auto nn_c) __attribute__((always_inline)) {
+      constexpr int NN = decltype(nn_c)::value;
+      if constexpr (NN == 0) return;
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         uint4 wv;
         if constexpr (FP8) wv = fp8x8_to_bf16x8(o.w[m], (GLU && m >= 2) ? o.su : o.sg);
         else wv = o.w[m];
 #pragma unroll
-        for (int n = 0; n < 4; ++n) acc[m][n] = mfma32x32x16(wv, o.t[n], acc[m][n]);
+        for (int n = 0; n < NN; ++n) acc[m][n] = mfma32x32x16(wv, o.t[n], acc[m][n]);
       }
     };
 
@@ -273,69 +280,84 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
     // writes into `dst`.  Stages past the last are re-issued as the last stage into buffers
     // nobody reads again.
     Ops A, B;
-    auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto first)
+    auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto first, auto nn_c)
         __attribute__((always_inline)) {
       dma_stage(min(t + NB - 1, nst - 1), dst);
-      read_ops(0, t, cur, A);
+      read_ops(0, t, cur, A, nn_c);
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (!decltype(first)::value) mma(B);
+      if constexpr (!decltype(first)::value) mma(B, nn_c);
       __builtin_amdgcn_sched_barrier(0);
-      read_ops(1, t, cur, B);
+      read_ops(1, t, cur, B, nn_c);
       __builtin_amdgcn_sched_barrier(0);
-      mma(A);
+      mma(A, nn_c);
       __builtin_amdgcn_sched_barrier(0);
       wait_cnt<(NB - 2) * D, 0>();
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
+    };
+    auto epilogue = [&](auto nn_c) __attribute__((always_inline)) {
+      constexpr int NN = decltype(nn_c)::value;
+      // Epilogue from the accumulators: in block (m, n) lane l holds token 32 (2 n + wt) + l % 32
+      // and, in registers 4 q .. 4 q + 3, weight rows 8 q + 4 (l / 32) .. + 3.
+#pragma unroll
+      for (int n = 0; n < NN; ++n) {
+        const int i = (2 * n + wt) * 32 + l32;
+        if (i >= rows) continue;
+        const size_t orow = (size_t)(p0 + i) * N;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (GLU) {
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+              const int f = fb * FEAT + wr * 64 + m * 32 + 8 * q + 4 * lh;
+              if (f >= N) continue;
+              float hv[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float g = acc[m][n][4 * q + r], u = acc[m + 2][n][4 * q + r];
+                hv[r] = g / (1.0f + __expf(-g)) * u;
+              }
+              uint2 pk;
+              pk.x = pack_bf16x2(hv[0], hv[1]);
+              pk.y = pack_bf16x2(hv[2], hv[3]);
+              *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
+            }
+          } else {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+              const int f = fb * FEAT + wr * 128 + m * 32 + 8 * q + 4 * lh;
+              if (f >= N) continue;
+              *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
+                  make_float4(acc[m][n][4 * q], acc[m][n][4 * q + 1], acc[m][n][4 * q + 2], acc[m][n][4 * q + 3]);
+            }
+          }
+        }
+      }
+    };
+    // The K loop and epilogue, one instance per count of active token blocks (each instance
+    // stores only its own blocks, so no accumulator lives across instances): every wave
+    // issues the same DMAs and meets the same barriers whatever its count.
+    auto k_loop = [&](auto nn_c) __attribute__((always_inline)) {
+      iter(lds + (NB - 1) * SB, lds, 0, std::true_type{}, nn_c);
+      for (int t = 1; t < nst; ++t)
+        iter(lds + ((t + NB - 1) % NB) * SB, lds + (t % NB) * SB, t, std::false_type{}, nn_c);
+      mma(B, nn_c);
+      // Moves of re-issued stages may still be in flight: drain before the next item's DMAs.
+      wait_cnt<0, 0>();
+      __syncthreads();
+      epilogue(nn_c);
     };
 
 #pragma unroll
     for (int st = 0; st < NB - 1; ++st) dma_stage(min(st, nst - 1), lds + st * SB);
     wait_cnt<(NB - 2) * D, 15>();  // this wave's stage-0 moves have landed
     __syncthreads();        // ... and every wave's (also orders the scale rows in LDS)
-    iter(lds + (NB - 1) * SB, lds, 0, std::true_type{});
-    for (int t = 1; t < nst; ++t)
-      iter(lds + ((t + NB - 1) % NB) * SB, lds + (t % NB) * SB, t, std::false_type{});
-    mma(B);
-    // Moves of re-issued stages may still be in flight: drain before the next item's DMAs.
-    wait_cnt<0, 0>();
-    __syncthreads();
-
-    // Epilogue from the accumulators: in block (m, n) lane l holds token 32 n + l % 32 and, in
-    // registers 4 q .. 4 q + 3, weight rows 8 q + 4 (l / 32) .. + 3.
-#pragma unroll
-    for (int n = 0; n < 4; ++n) {
-      const int i = wt * 128 + n * 32 + l32;
-      if (i >= rows) continue;
-      const size_t orow = (size_t)(p0 + i) * N;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (GLU) {
-#pragma unroll
-          for (int m = 0; m < 2; ++m) {
-            const int f = fb * FEAT + wr * 64 + m * 32 + 8 * q + 4 * lh;
-            if (f >= N) continue;
-            float hv[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float g = acc[m][n][4 * q + r], u = acc[m + 2][n][4 * q + r];
-              hv[r] = g / (1.0f + __expf(-g)) * u;
-            }
-            uint2 pk;
-            pk.x = pack_bf16x2(hv[0], hv[1]);
-            pk.y = pack_bf16x2(hv[2], hv[3]);
-            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
-          }
-        } else {
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const int f = fb * FEAT + wr * 128 + m * 32 + 8 * q + 4 * lh;
-            if (f >= N) continue;
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
-                make_float4(acc[m][n][4 * q], acc[m][n][4 * q + 1], acc[m][n][4 * q + 2], acc[m][n][4 * q + 3]);
-          }
-        }
-      }
+    switch (nn) {
+      case 4: k_loop(std::integral_constant<int, 4>{}); break;
+      case 3: k_loop(std::integral_constant<int, 3>{}); break;
+      case 2: k_loop(std::integral_constant<int, 2>{}); break;
+      case 1: k_loop(std::integral_constant<int, 1>{}); break;
+      default: k_loop(std::integral_constant<int, 0>{}); break;
     }
   }
 }
