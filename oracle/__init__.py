@@ -63,6 +63,7 @@ def lib() -> ctypes.CDLL:
             "oracle_dirichlet_logp": ([i32, f64, ctypes.c_uint32, u64, vp], None),
             "oracle_router": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp], None),
             "oracle_topk_softmax": ([vp, i32, i32, i32, vp, vp], None),
+            "oracle_effexp_map": ([vp, vp, i32, i32, i32, vp], None),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -211,3 +212,13 @@ def topk_softmax(logits, k: int):
     w = np.zeros((T, k), np.float64)
     lib().oracle_topk_softmax(l.ctypes.data, T, E, k, ids.ctypes.data, w.ctypes.data)
     return ids, w
+
+
+def effexp_map(Q, kid, noda: int):
+    """Variant per Effective Experts bucket -1..13 (15 entries) of one token bucket's exemplars."""
+    q = _c(Q, np.int32)
+    k = _c(kid, np.int32)
+    n_ex, E = q.shape
+    out = np.zeros(15, np.int32)
+    lib().oracle_effexp_map(q.ctypes.data, k.ctypes.data, n_ex, E, int(noda), out.ctypes.data)
+    return out

@@ -497,3 +497,39 @@ void oracle_router(const uint16_t* x, const uint16_t* wg, const float* bias, int
     }
   oracle_topk_softmax(logits, T, E, k, ids, w);
 }
+
+/* ------------------------------------------------------------------------- */
+/* Effective-Experts-only dispatch (the scalar statistic of Sec. III-A used   */
+/* as the matcher instead of the exemplar match of Sec. IV-B)                 */
+/* ------------------------------------------------------------------------- */
+
+/* Map from the Effective Experts bucket (-1 .. 13, Eq. (2) and the ddist:X grid) to a
+ * variant, derived from one token bucket's exemplar table: each exemplar Q_x (a sorted,
+ * quantised unit vector of counts) has its own Effective Experts (sum Q)^2 / sum Q^2 and so
+ * its own bucket; bucket b maps to the kernel of the first exemplar in b, else to that of
+ * the nearest bucket holding an exemplar (the lower one on a tie); bucket -1 (no tokens)
+ * maps to the NoDA kernel.  map[b + 1], 15 entries (the reading of the cheaper matcher taken
+ * for this build). */
+void oracle_effexp_map(const int32_t* Q, const int32_t* kid, int32_t n_ex, int32_t E, int32_t noda,
+                       int32_t* map) {
+  int32_t first[14];
+  for (int b = 0; b < 14; ++b) first[b] = -1;
+  for (int32_t x = 0; x < n_ex; ++x) {
+    uint64_t s = 0, s2 = 0;
+    for (int32_t e = 0; e < E; ++e) {
+      s += (uint64_t)Q[(int64_t)x * E + e];
+      s2 += (uint64_t)Q[(int64_t)x * E + e] * (uint64_t)Q[(int64_t)x * E + e];
+    }
+    const int32_t b = oracle_effexp_bucket(s * s, s2, E);
+    if (b >= 0 && first[b] < 0) first[b] = x;
+  }
+  map[0] = noda;
+  for (int b = 0; b < 14; ++b) {
+    int32_t pick = -1;
+    for (int d = 0; d < 14 && pick < 0; ++d) {
+      if (b - d >= 0 && first[b - d] >= 0) pick = first[b - d];
+      else if (b + d < 14 && first[b + d] >= 0) pick = first[b + d];
+    }
+    map[b + 1] = pick >= 0 ? kid[pick] : noda;
+  }
+}

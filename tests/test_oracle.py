@@ -550,3 +550,48 @@ def test_topk_softmax_on_given_logits():
         np.testing.assert_array_equal(ids, np.argsort(-l.astype(np.float64), axis=1, kind="stable")[:, :k])
         want = softmax(np.take_along_axis(l.astype(np.float64), ids, axis=1), axis=1)
         np.testing.assert_allclose(w, want, rtol=1e-13)
+
+
+# ---------------------------------------------------------------- Effective-Experts-only dispatch (f4)
+
+def test_effexp_map_hand_worked():
+    # E = 64: the uniform exemplar has Effective Experts 64 (bucket 0), an exemplar with 16
+    # equal entries 16 (X <= 4 pass: bucket 7), a one-hot exemplar 1 (bucket 13).  Empty
+    # buckets take the nearest populated one, the lower on a tie (bucket 10 is 3 from 7 and
+    # from 13); bucket -1 is the NoDA kernel.
+    E = 64
+    uni = np.full(E, 4096)
+    m16 = np.r_[np.full(16, 8192), np.zeros(E - 16)]
+    one = np.r_[32768, np.zeros(E - 1)]
+    Q = np.stack([uni, m16, one]).astype(np.int32)
+    got = oracle.effexp_map(Q, [3, 5, 1], noda=7)
+    want = [7] + [3] * 4 + [5] * 7 + [1] * 3
+    np.testing.assert_array_equal(got, want)
+    # A second exemplar in a bucket loses to the first; scaling an exemplar changes nothing.
+    got = oracle.effexp_map(np.stack([uni, m16, m16 * 2, one]).astype(np.int32), [3, 5, 6, 1], noda=7)
+    np.testing.assert_array_equal(got, want)
+    got = oracle.effexp_map(np.stack([one, uni // 2]).astype(np.int32), [2, 4], noda=0)
+    np.testing.assert_array_equal(got, [0] + [4] * 7 + [2] * 7)
+
+
+def test_effexp_map_brute_force_fractions():
+    # The bucket of each exemplar from exact fractions, then the nearest-populated rule.
+    rng = np.random.default_rng(37)
+    X = [Fraction(11, 10), Fraction(13, 10), Fraction(3, 2), Fraction(17, 10), Fraction(2), Fraction(5, 2),
+         Fraction(4), Fraction(6), Fraction(8), Fraction(12), Fraction(16), Fraction(24), Fraction(32)]
+    for _ in range(60):
+        E = int(rng.integers(2, 80))
+        n_ex = int(rng.integers(1, 9))
+        Q = -np.sort(-rng.integers(0, 30000, (n_ex, E)) * (rng.random((n_ex, E)) < rng.random()), axis=1)
+        Q[:, 0] = np.maximum(Q[:, 0], 1)
+        kid = rng.integers(0, 8, n_ex)
+        first = {}
+        for x in range(n_ex):
+            eff = Fraction(int(Q[x].sum()) ** 2, int((Q[x].astype(object) ** 2).sum()))
+            b = sum(1 for xx in X if eff <= Fraction(E) / xx)
+            first.setdefault(b, x)
+        want = [5]
+        for b in range(14):
+            pops = sorted(first, key=lambda p: (abs(p - b), p))
+            want.append(int(kid[first[pops[0]]]))
+        np.testing.assert_array_equal(oracle.effexp_map(Q.astype(np.int32), kid, noda=5), want)
