@@ -9,7 +9,8 @@
  *                          tiles (Sec. III-A Eq. (2); Sec. IV-B step 5)
  *   damoe_dispatch         token-count bucket, exemplar match by dot product,
  *                          argmax -> variant id written to device memory
- *                          (Sec. IV, IV-B, IV-C)
+ *                          (Sec. IV, IV-B, IV-C); damoe_route_dispatch_effexp
+ *                          picks it from the Effective Experts bucket alone
  *   damoe_fused_moe        the fused expert computation: gathered GEMM1 +
  *                          SwiGLU, GEMM2, gate-weighted unpermute-reduce, as a
  *                          family of token-tile variants selected on the
@@ -213,6 +214,28 @@ damoe_status damoe_route_dispatch(const damoe_table* table, const int32_t* topk_
                                   int32_t* perm, int32_t* inv_perm, uint64_t* effexp_numden,
                                   int32_t* effexp_bucket, int32_t* variant_id, void* ws,
                                   size_t ws_bytes, hipStream_t stream);
+
+/* a2-a5 with the cheaper scalar matcher (the Effective Experts of Sec. III-A Eq. (2)
+ * instead of the exemplar match of Sec. IV-B): exactly damoe_route_histogram, then
+ * *variant_id = map[effexp_bucket + 1], where map is the table's Effective-Experts map for
+ * the bucket of T (damoe_table_effexp_map).  No sort and no dot products.  Same arguments,
+ * errors and workspace as damoe_route_dispatch; ctrl[1] reads -3. */
+damoe_status damoe_route_dispatch_effexp(const damoe_table* table, const int32_t* topk_ids, int32_t T,
+                                         int32_t k, int32_t E, int32_t* counts, int32_t* offsets,
+                                         int32_t* perm, int32_t* inv_perm, uint64_t* effexp_numden,
+                                         int32_t* effexp_bucket, int32_t* variant_id, void* ws,
+                                         size_t ws_bytes, hipStream_t stream);
+
+/* The Effective-Experts map of T's token bucket (host int32[15]): map[b + 1] is the variant
+ * for Effective Experts bucket b = -1 .. 13.  It is derived from the bucket's exemplars when
+ * the table is created: each exemplar's own Effective Experts (sum Q)^2 / sum Q^2 gives its
+ * bucket; bucket b takes the kernel of its first exemplar, else of the populated bucket
+ * nearest to b (the lower of two at equal distance); b = -1 (no tokens) takes noda. */
+damoe_status damoe_table_effexp_map(const damoe_table* table, int32_t T, int32_t* map /* host, 15 */);
+
+/* Variants damoe_route_dispatch_effexp may write for T (bit v): the entries of that map;
+ * the candidates argument of damoe_fused_moe after an Effective-Experts dispatch. */
+uint32_t damoe_table_effexp_candidates(const damoe_table* table, int32_t T);
 
 /* a6-a8: the fused expert computation.
  *   x          bf16 [T][H] token activations

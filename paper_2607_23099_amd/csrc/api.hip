@@ -1,6 +1,7 @@
 // Host side of the C-ABI: argument validation, workspace layout, launches and tables.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -8,6 +9,7 @@
 #include <vector>
 
 #include "common.h"
+#include "route.h"
 
 using namespace damoe;
 
@@ -90,7 +92,41 @@ struct damoe_table {
   std::vector<int32_t> bucket_T, n_ex, ex_begin, Q, kid, noda;
   int32_t* d_Q = nullptr;
   int32_t* d_kid = nullptr;
+  std::vector<int32_t> effmap;  // [n_buckets][kEffMapLen]: variant per Effective Experts bucket
+  int32_t* d_effmap = nullptr;
 };
+
+namespace {
+
+// Effective-Experts-only dispatch map of one token bucket: the bucket of each exemplar's own
+// Effective Experts (sum Q)^2 / sum Q^2; an Effective Experts bucket runs the kernel of its
+// first exemplar, else of the populated bucket at the smallest distance (the lower of two at
+// equal distance); bucket -1 (no tokens) runs the NoDA kernel.
+void derive_effexp_map(const int32_t* Q, const int32_t* kid, int32_t n_ex, int32_t E, int32_t noda,
+                       int32_t* map) {
+  constexpr int kBuckets = kEffMapLen - 1;
+  int32_t owner[kBuckets];
+  std::fill(owner, owner + kBuckets, -1);
+  for (int32_t x = n_ex - 1; x >= 0; --x) {  // the first exemplar of a bucket is written last
+    const int32_t* q = Q + (size_t)x * E;
+    uint64_t s1 = 0, s2 = 0;
+    for (int32_t i = 0; i < E; ++i) {
+      s1 += (uint64_t)q[i];
+      s2 += (uint64_t)q[i] * (uint64_t)q[i];
+    }
+    const int b = effexp_bucket(s1 * s1, s2, (uint64_t)E);
+    if (b >= 0) owner[b] = x;
+  }
+  map[0] = noda;
+  for (int b = 0; b < kBuckets; ++b) {
+    int best = -1;
+    for (int p = 0; p < kBuckets; ++p)
+      if (owner[p] >= 0 && (best < 0 || std::abs(p - b) < std::abs(best - b))) best = p;
+    map[b + 1] = best >= 0 ? kid[owner[best]] : noda;
+  }
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -215,6 +251,42 @@ uint32_t damoe_table_candidates(const damoe_table* t, int32_t T) {
   // one-kernel bucket writes that kernel in every case.
   if (__builtin_popcount(m) > 1 || T == 0) m |= 1u << t->noda[b];
   return m;
+}
+
+damoe_status damoe_route_dispatch_effexp(const damoe_table* t, const int32_t* topk_ids, int32_t T, int32_t k,
+                                         int32_t E, int32_t* counts, int32_t* offsets, int32_t* perm,
+                                         int32_t* inv_perm, uint64_t* effexp_numden, int32_t* effexp_bucket,
+                                         int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!t || !variant_id) return DAMOE_ERR_INVALID_ARG;
+  if (t->E != E || t->k != k) return DAMOE_ERR_TABLE_MISMATCH;
+  if (!t->d_effmap) return DAMOE_ERR_HIP;  // table built without a device
+  damoe_ws_layout lo;
+  const damoe_status st = check_route(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden,
+                                      effexp_bucket, ws, ws_bytes, &lo);
+  if (st != DAMOE_OK) return st;
+  char* base = static_cast<char*>(ws);
+  int32_t* lists[DAMOE_N_TILE_SIZES];
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) lists[c] = reinterpret_cast<int32_t*>(base + lo.tiles[c]);
+  const hipError_t e = launch_route_effexp(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden,
+                                           effexp_bucket, reinterpret_cast<int32_t*>(base + lo.ctrl), lists,
+                                           t->d_effmap + (size_t)table_bucket(t, T) * kEffMapLen, variant_id,
+                                           stream);
+  return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
+}
+
+damoe_status damoe_table_effexp_map(const damoe_table* t, int32_t T, int32_t* map) {
+  if (!t || !map || T < 0) return DAMOE_ERR_INVALID_ARG;
+  const int32_t* m = t->effmap.data() + (size_t)table_bucket(t, T) * kEffMapLen;
+  std::copy(m, m + kEffMapLen, map);
+  return DAMOE_OK;
+}
+
+uint32_t damoe_table_effexp_candidates(const damoe_table* t, int32_t T) {
+  if (!t || T < 0) return 0;
+  const int32_t* m = t->effmap.data() + (size_t)table_bucket(t, T) * kEffMapLen;
+  uint32_t mask = 0;
+  for (int i = 0; i < kEffMapLen; ++i) mask |= 1u << m[i];
+  return mask;
 }
 
 damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t T,
@@ -383,6 +455,10 @@ damoe_status damoe_table_create(const damoe_table_desc* d, damoe_table** out) {
   }
   for (int64_t i = 0; i < total; ++i)
     if (d->kid[i] < 0 || d->kid[i] >= nv) return DAMOE_ERR_INVALID_ARG;
+  // Exemplars are quantised unit vectors (at most 2^15 per entry); the int64 match and the
+  // uint64 Effective Experts of an exemplar stay exact for entries up to 2^16.
+  for (int64_t i = 0; i < total * d->E; ++i)
+    if (d->Q[i] < 0 || d->Q[i] > 65536) return DAMOE_ERR_INVALID_ARG;
   damoe_table* t = new (std::nothrow) damoe_table;
   if (!t) return DAMOE_ERR_NOMEM;
   t->E = d->E;
@@ -401,11 +477,18 @@ damoe_status damoe_table_create(const damoe_table_desc* d, damoe_table** out) {
   }
   t->Q.assign(d->Q, d->Q + (size_t)total * d->E);
   t->kid.assign(d->kid, d->kid + total);
+  t->effmap.resize((size_t)d->n_buckets * kEffMapLen);
+  for (int32_t b = 0; b < d->n_buckets; ++b)
+    derive_effexp_map(t->Q.data() + (size_t)t->ex_begin[b] * t->E, t->kid.data() + t->ex_begin[b], t->n_ex[b],
+                      t->E, t->noda[b], t->effmap.data() + (size_t)b * kEffMapLen);
   // Device copies (skipped when no device is present, e.g. when only inspecting tables).
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) == hipSuccess && ndev > 0) {
     if (hipMalloc(&t->d_Q, sizeof(int32_t) * t->Q.size()) != hipSuccess ||
         hipMalloc(&t->d_kid, sizeof(int32_t) * t->kid.size()) != hipSuccess ||
+        hipMalloc(&t->d_effmap, sizeof(int32_t) * t->effmap.size()) != hipSuccess ||
+        hipMemcpy(t->d_effmap, t->effmap.data(), sizeof(int32_t) * t->effmap.size(), hipMemcpyHostToDevice) !=
+            hipSuccess ||
         hipMemcpy(t->d_Q, t->Q.data(), sizeof(int32_t) * t->Q.size(), hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(t->d_kid, t->kid.data(), sizeof(int32_t) * t->kid.size(), hipMemcpyHostToDevice) !=
             hipSuccess) {
@@ -423,6 +506,7 @@ void damoe_table_destroy(damoe_table* t) {
   if (!t) return;
   if (t->d_Q) (void)hipFree(t->d_Q);
   if (t->d_kid) (void)hipFree(t->d_kid);
+  if (t->d_effmap) (void)hipFree(t->d_effmap);
   delete t;
 }
 

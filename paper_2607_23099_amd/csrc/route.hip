@@ -5,6 +5,7 @@
 // so a single workgroup that keeps every intermediate in LDS beats a chain of kernels that
 // would round-trip through HBM and pay a launch each.
 #include "common.h"
+#include "route.h"
 
 namespace damoe {
 namespace {
@@ -13,19 +14,6 @@ constexpr int kNW = kRouteThreads / kWave;  // 16 waves
 constexpr int kMaxExemplarRegs = 8;  // exemplar entries prefetched per lane (E <= 512)
 constexpr int kValueBins = 4096;     // counting sort of the histogram when every count is smaller
 constexpr int kIdBatch = 16;         // 64-id chunks loaded together per wave
-
-// The Effective Experts bucket: the number of ddist:X thresholds X = XN / XD with
-// eff <= E / X, decided exactly as num * XN <= E * XD * den in uint64 (the thresholds are
-// immediates: a table in memory would cost one dependent load each).
-__device__ __forceinline__ int effexp_bucket(uint64_t num, uint64_t den, uint64_t E) {
-  constexpr uint32_t xn[13] = {11, 13, 3, 17, 2, 5, 4, 6, 8, 12, 16, 24, 32};
-  constexpr uint32_t xd[13] = {10, 10, 2, 10, 1, 2, 1, 1, 1, 1, 1, 1, 1};
-  if (den == 0) return -1;
-  int b = 0;
-#pragma unroll
-  for (int j = 0; j < 13; ++j) b += num * xn[j] <= E * xd[j] * den ? 1 : 0;
-  return b;
-}
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = threadIdx.x & 63;
@@ -128,6 +116,7 @@ struct DispatchIn {
   int32_t noda;
   int32_t* variant_id;
   int32_t fixed;       // >= 0: the bucket has one variant; write it without scoring
+  const int32_t* eff_map;  // non-null: the variant is eff_map[Effective Experts bucket + 1]
 };
 
 struct RouteOut {
@@ -270,6 +259,7 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   pin(d.noda);
   pin(d.variant_id);
   pin(d.fixed);
+  pin(d.eff_map);
 
   // The wave's first exemplar is fetched before anything else so its latency hides behind
   // the histogram; it moves to LDS once the histogram is done.
@@ -357,7 +347,15 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     const uint64_t num = (uint64_t)total * (uint64_t)total;
     o.numden[0] = num;
     o.numden[1] = den;
-    *o.bucket = effexp_bucket(num, den, (uint64_t)E);
+    const int b = effexp_bucket(num, den, (uint64_t)E);
+    *o.bucket = b;
+    if (d.eff_map) {
+      // Effective-Experts-only dispatch: the scalar statistic picks the variant.
+      *d.variant_id = d.eff_map[b + 1];
+      o.ctrl[1] = -3;
+      o.ctrl[2] = 0;
+      o.ctrl[3] = 0;
+    }
     if (sm.bad) atomicOr(&o.ctrl[0], DAMOE_DEVERR_EXPERT_ID);
   }
 #pragma unroll
@@ -455,19 +453,30 @@ hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int
   RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}};
   for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) o.tiles.list[i] = tile_lists[i];
   if (dispatch && dispatch->fixed < 0) {
-    DispatchIn d{dispatch->Q, dispatch->kid, dispatch->n_ex, dispatch->noda, dispatch->variant_id, -1};
+    DispatchIn d{dispatch->Q, dispatch->kid, dispatch->n_ex, dispatch->noda, dispatch->variant_id, -1, nullptr};
     hipLaunchKernelGGL(k_route<true>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
   } else {
     DispatchIn d{nullptr, nullptr, 0, dispatch ? dispatch->noda : 0, dispatch ? dispatch->variant_id : nullptr,
-                 dispatch ? dispatch->fixed : -1};
+                 dispatch ? dispatch->fixed : -1, nullptr};
     hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
   }
   return hipGetLastError();
 }
 
+hipError_t launch_route_effexp(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
+                               int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
+                               int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
+                               const int32_t* eff_map, int32_t* variant_id, hipStream_t stream) {
+  RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}};
+  for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) o.tiles.list[i] = tile_lists[i];
+  DispatchIn d{nullptr, nullptr, 0, 0, variant_id, -1, eff_map};
+  hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
+  return hipGetLastError();
+}
+
 hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
                            hipStream_t stream) {
-  DispatchIn d{dispatch.Q, dispatch.kid, dispatch.n_ex, dispatch.noda, dispatch.variant_id, -1};
+  DispatchIn d{dispatch.Q, dispatch.kid, dispatch.n_ex, dispatch.noda, dispatch.variant_id, -1, nullptr};
   hipLaunchKernelGGL(k_dispatch, dim3(1), dim3(kRouteThreads), 0, stream, counts, E, d, ctrl);
   return hipGetLastError();
 }

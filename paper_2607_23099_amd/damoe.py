@@ -30,7 +30,8 @@ EXPORTED = [
     "damoe_table_load", "damoe_dispatch", "damoe_fused_moe", "damoe_num_variants", "damoe_variant_name",
     "damoe_variant_tile_m", "damoe_variant_supports", "damoe_tune", "damoe_alpha_search",
     "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch", "damoe_pack_weights",
-    "damoe_table_candidates", "damoe_router", "damoe_router_workspace_size",
+    "damoe_table_candidates", "damoe_router", "damoe_router_workspace_size", "damoe_route_dispatch_effexp",
+    "damoe_table_effexp_map", "damoe_table_effexp_candidates",
 ]
 
 
@@ -106,6 +107,9 @@ def lib() -> ctypes.CDLL:
             "damoe_pack_weights": ([vp, vp, vp, vp, vp], i32),
             "damoe_router": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, sz, vp], i32),
             "damoe_router_workspace_size": ([i32, i32, i32], sz),
+            "damoe_route_dispatch_effexp": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
+            "damoe_table_effexp_map": ([vp, i32, vp], i32),
+            "damoe_table_effexp_candidates": ([vp, i32], u32),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -196,6 +200,13 @@ def route_dispatch(table: "Table", ids, T, k, E, counts, offsets, perm, inv_perm
         _p(bucket), _p(variant_id), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
+def route_dispatch_effexp(table: "Table", ids, T, k, E, counts, offsets, perm, inv_perm, numden, bucket,
+                          variant_id, ws, stream=None):
+    _check("damoe_route_dispatch_effexp", lib().damoe_route_dispatch_effexp(
+        table.handle, _p(ids), T, k, E, _p(counts), _p(offsets), _p(perm), _p(inv_perm), _p(numden),
+        _p(bucket), _p(variant_id), _p(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
 def dispatch(table: "Table", counts, T, variant_id, ws, stream=None):
     _check("damoe_dispatch", lib().damoe_dispatch(table.handle, _p(counts), T, _p(variant_id), _p(ws),
                                                   ws.numel() * ws.element_size(), _stream(stream)))
@@ -257,6 +268,7 @@ class Table:
     def __init__(self, handle: int):
         self.handle = ctypes.c_void_p(handle)
         self._candidates = {}  # T -> mask; tables are immutable, so the lookup is cached
+        self._eff_candidates = {}
 
     @classmethod
     def create(cls, td: TableData) -> "Table":
@@ -278,6 +290,19 @@ class Table:
         m = self._candidates.get(T)
         if m is None:
             m = self._candidates[T] = int(lib().damoe_table_candidates(self.handle, int(T)))
+        return m
+
+    def effexp_map(self, T: int) -> np.ndarray:
+        """Variant per Effective Experts bucket -1..13 for T's token bucket."""
+        m = np.zeros(15, np.int32)
+        _check("damoe_table_effexp_map", lib().damoe_table_effexp_map(self.handle, T, m.ctypes.data))
+        return m
+
+    def effexp_candidates(self, T: int) -> int:
+        """Bit mask of the variants the Effective-Experts dispatch may write for T tokens."""
+        m = self._eff_candidates.get(T)
+        if m is None:
+            m = self._eff_candidates[T] = int(lib().damoe_table_effexp_candidates(self.handle, int(T)))
         return m
 
     def save(self, path: str):

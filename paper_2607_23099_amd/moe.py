@@ -128,6 +128,13 @@ class Path:
         damoe.route_dispatch(table, self.ids if ids is None else ids, T, sh.k, sh.E, self.counts, self.offsets,
                              self.perm, self.inv_perm, self.numden, self.bucket, self.variant, self.ws, stream)
 
+    def route_dispatch_effexp(self, table: damoe.Table, T: int, ids=None, stream=None):
+        sh = self.dl.shape
+        self.candidates = table.effexp_candidates(T)
+        damoe.route_dispatch_effexp(table, self.ids if ids is None else ids, T, sh.k, sh.E, self.counts,
+                                    self.offsets, self.perm, self.inv_perm, self.numden, self.bucket, self.variant,
+                                    self.ws, stream)
+
     def dispatch(self, table: damoe.Table, T: int, stream=None):
         self.candidates = table.candidates(T)
         damoe.dispatch(table, self.counts, T, self.variant, self.ws, stream)

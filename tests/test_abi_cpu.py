@@ -220,3 +220,48 @@ def test_router_validation_and_workspace_bound():
         for T in np.unique(np.r_[1, T_max, rng.integers(1, T_max + 1, 300), np.arange(1, min(T_max, 300))]):
             assert r(None, P, None, int(T), H, E, 1, None, P, P, P, ws, None) == -1, (E, H, T)
             assert r(None, P, None, int(T), H, E, 1, None, P, P, P, 16, None) == -3
+
+
+def test_effexp_map_matches_oracle():
+    # The library derives each bucket's Effective-Experts map when a table is created; the
+    # oracle derives it from the same exemplars independently.
+    tdir = os.path.join(ROOT, "paper_2607_23099_amd", "tables")
+    for f in ("dsv3.damoe", "kimi-k2.damoe"):
+        t = damoe.Table.load(os.path.join(tdir, f))
+        E = 256 if f.startswith("dsv3") else 384
+        td = t.data(E)
+        for b, T in enumerate(td.bucket_T):
+            want = oracle.effexp_map(td.Q[td.bucket_rows(b)], td.kid[td.bucket_rows(b)], int(td.noda[b]))
+            np.testing.assert_array_equal(t.effexp_map(int(T)), want)
+            assert t.effexp_candidates(int(T)) == int(np.bitwise_or.reduce(1 << want.astype(np.int64)))
+    rng = np.random.default_rng(3)
+    nv = damoe.num_variants()
+    for _ in range(20):
+        E = int(rng.integers(2, 300))
+        n_ex = rng.integers(1, 9, 3)
+        Q = -np.sort(-(rng.integers(0, 32769, (int(n_ex.sum()), E)) * (rng.random((int(n_ex.sum()), E)) <
+                                                                      rng.random())), axis=1)
+        td = damoe.TableData(E=E, k=1, H=256, I=512, wdtype=0, bucket_T=np.array([4, 16, 64]), n_ex=n_ex,
+                             Q=Q, kid=rng.integers(0, nv, int(n_ex.sum())), noda=rng.integers(0, nv, 3))
+        t = damoe.Table.create(td)
+        for b, T in enumerate((1, 16, 1000)):
+            rows = td.bucket_rows(b)
+            np.testing.assert_array_equal(t.effexp_map(T), oracle.effexp_map(Q[rows], td.kid[rows], int(td.noda[b])))
+
+
+def test_effexp_dispatch_validation():
+    L = damoe.lib()
+    P = 0x10000
+    E = 8
+    td = damoe.TableData(E=E, k=2, H=256, I=512, wdtype=0, bucket_T=np.array([8]), n_ex=np.array([1]),
+                         Q=np.full((1, E), 1000), kid=np.array([1]), noda=np.array([0]))
+    for bad in (np.full((1, E), -1), np.full((1, E), 65537)):
+        with pytest.raises(damoe.DamoeError):
+            damoe.Table.create(damoe.TableData(**{**td.__dict__, "Q": bad}))
+    t = damoe.Table.create(td)
+    rd = L.damoe_route_dispatch_effexp
+    assert rd(None, P, 4, 2, E, P, P, P, P, P, P, P, P, 1 << 30, None) == -1
+    assert rd(t.handle, P, 4, 2, E, P, P, P, P, P, P, None, P, 1 << 30, None) == -1
+    assert rd(t.handle, P, 4, 3, E, P, P, P, P, P, P, P, P, 1 << 30, None) == -4
+    assert L.damoe_table_effexp_map(None, 4, P) == -1
+    assert L.damoe_table_effexp_candidates(None, 4) == 0

@@ -252,3 +252,44 @@ def test_route_dispatch_single_variant_bucket():
                          vid, b0.ws)
     torch.cuda.synchronize()
     assert int(vid.item()) == 1 % nv
+
+
+@pytest.mark.parametrize("E", [16, 256, 384])
+def test_effexp_dispatch_matches_oracle(E):
+    # a2-a5 with the Effective-Experts-only matcher: the same histogram, permutation and tiles
+    # as route_histogram, and the variant of the oracle's map at the oracle's bucket.  The
+    # skews sweep the whole bucket range; T = 0 takes the NoDA kernel.
+    torch = torch_cuda()
+    rng = np.random.default_rng(100 + E)
+    nv = damoe.num_variants()
+    td = _random_table(rng, E, [2 ** i for i in range(14)], nv)
+    table = damoe.Table.create(td)
+    seen = set()
+    for step in range(40):
+        T = int(np.floor(np.exp(rng.uniform(0, np.log(4096)))))
+        alpha = float(np.exp(rng.uniform(np.log(0.01), np.log(10))))
+        r = synth.routing(E, min(8, E), T, alpha, [80, step])
+        b = RouteBufs(torch, E, min(8, E), T)
+        b.ids.copy_(torch.from_numpy(r.ids.ravel().copy()))
+        vid = torch.full((1,), -9, dtype=torch.int32, device="cuda")
+        damoe.route_dispatch_effexp(table, b.ids, T, b.k, E, b.counts, b.offsets, b.perm, b.inv, b.nd, b.bucket,
+                                    vid, b.ws)
+        torch.cuda.synchronize()
+        _check_route(b, r.ids)
+        c = oracle.histogram(r.ids, E)
+        num, den, _ = oracle.effexp(c)
+        eb = oracle.effexp_bucket(num, den, E)
+        bt = oracle.select_bucket(td.bucket_T, T)
+        rows = td.bucket_rows(bt)
+        want = oracle.effexp_map(td.Q[rows], td.kid[rows], int(td.noda[bt]))[eb + 1]
+        assert int(vid.item()) == int(want), (step, T, eb)
+        assert b.ws[:16].view(torch.int32).cpu().numpy()[1] == -3
+        seen.add(eb)
+    log(f"E={E}: Effective Experts buckets seen {sorted(seen)}")
+    assert len(seen) >= 4
+    b = RouteBufs(torch, E, min(8, E), 0)
+    vid = torch.full((1,), -9, dtype=torch.int32, device="cuda")
+    damoe.route_dispatch_effexp(table, b.ids, 0, b.k, E, b.counts, b.offsets, b.perm, b.inv, b.nd, b.bucket, vid,
+                                b.ws)
+    torch.cuda.synchronize()
+    assert int(vid.item()) == int(td.noda[0])
