@@ -595,6 +595,109 @@ def run_router(args):
     print(json.dumps(out), flush=True)
 
 
+IMB_T = (32, 64, 128, 256)
+IMB_F = (0, 10, 20, 50, 100)
+
+
+def run_imbalance(args):
+    """Routing-skew ablation (the analog of the paper's imbalance-factor table, Sec. V-E) on the
+    DeepSeek-V3 decode shape: T in {32, 64, 128, 256} x f in {0, 10, 20, 50, 100}; groups of
+    about f% of the tokens share one routing row (base skew Dirichlet alpha = 1), REPS routings
+    per point.  For each routing, the fused-MoE latency (a6-a8, HIP events behind a GPU spin,
+    median of --steps runs) of every variant; from these the kernel the exemplar match picks
+    (DA-MoE), the kernel the Effective-Experts-only map picks (DA-eff), the bucket's NoDA
+    kernel and the per-routing best.  Speedups over NoDA per point and geomean per f."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+
+    shape = synth.DS
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    dl = DeviceLayer(shape)
+    path = Path(dl, max(IMB_T))
+    path.fill_x(max(IMB_T), 1)
+    torch.cuda.synchronize()
+    table, note = load_or_tune_table(dl, path.x, args.quick_tune)
+    td = table.data(shape.E)
+    stream = torch.cuda.current_stream()
+    spin = gpu_spin(torch, stream, 100.0)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    nv = damoe.num_variants()
+    rows, t0 = {}, time.perf_counter()
+    for T in IMB_T:
+        noda = int(td.noda[bucket_of(td, T)])
+        for f in IMB_F:
+            acc = {"da": [], "eff": [], "noda": [], "best": []}
+            picks, effs = [], []
+            for rep in range(REPS):
+                r = synth.routing_repeated(shape.E, shape.k, T, f, 1.0, synth.seed_imbalance(T, f, rep))
+                path.set_routing(r)
+                path.route_dispatch_effexp(table, T)
+                torch.cuda.synchronize()
+                v_eff = int(path.variant.item())
+                path.route_dispatch(table, T)
+                torch.cuda.synchronize()
+                v_da = int(path.variant.item())
+                nd_ = path.numden.cpu().numpy()
+                effs.append(float(nd_[0]) / max(float(nd_[1]), 1.0))
+                path.candidates = 0
+                lat = []
+                for v in range(nv):
+                    for _ in range(args.warmup):
+                        path.fused(T, v)
+                    pairs = []
+                    for _ in range(args.steps):
+                        torch.cuda._sleep(spin)
+                        e0, e1 = ev(), ev()
+                        e0.record(stream)
+                        path.fused(T, v)
+                        e1.record(stream)
+                        pairs.append((e0, e1))
+                    torch.cuda.synchronize()
+                    lat.append(float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3)
+                acc["da"].append(lat[v_da])
+                acc["eff"].append(lat[v_eff])
+                acc["noda"].append(lat[noda])
+                acc["best"].append(min(lat))
+                picks.append((damoe.variant_name(v_da), damoe.variant_name(v_eff)))
+            m = {k_: float(np.mean(v_)) for k_, v_ in acc.items()}
+            row = {"da_us": round(m["da"], 1), "eff_us": round(m["eff"], 1), "noda_us": round(m["noda"], 1),
+                   "best_us": round(m["best"], 1), "da_speedup": round(m["noda"] / m["da"], 4),
+                   "eff_speedup": round(m["noda"] / m["eff"], 4), "best_speedup": round(m["noda"] / m["best"], 4),
+                   "eff_experts": round(float(np.mean(effs)), 1), "picks_da_eff": picks}
+            rows[f"T{T}_f{f}"] = row
+            log(f"imbalance T={T} f={f}: {row}")
+    wall = time.perf_counter() - t0
+    per_f = {}
+    for f in IMB_F:
+        sel = [rows[f"T{T}_f{f}"] for T in IMB_T]
+        per_f[f"f{f}"] = {k_: round(geomean([r_[k_] for r_ in sel]), 4)
+                          for k_ in ("da_speedup", "eff_speedup", "best_speedup")}
+        log(f"f={f}: geomean {per_f[f'f{f}']}")
+    out = {
+        "metric": "fused-MoE speedup of DA-MoE over NoDA, geomean over the DeepSeek-V3 imbalance sweep",
+        "value": round(geomean([r_["da_speedup"] for r_ in rows.values()]), 4),
+        "unit": "x",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / max(len(rows) * REPS, 1), 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dsv3-imbalance: E=256 top-8 H=7168 I=2048 bf16, T in {32,64,128,256} x imbalance "
+                               "f in {0,10,20,50,100} (repeated routing rows, base Dirichlet alpha = 1)",
+                   "table": note},
+        "eff_only_speedup": round(geomean([r_["eff_speedup"] for r_ in rows.values()]), 4),
+        "best_speedup": round(geomean([r_["best_speedup"] for r_ in rows.values()]), 4),
+        "per_f": per_f,
+        "per_point": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def run_prefill(args):
     """Per-variant GEMM times at the MFMA-bound prefill points: Kimi-K2 (bf16, 40% of the mass
     on 4 hot experts) at T = 2048 and 8192, and DeepSeek-V3 with fp8 block-128 weights at
@@ -705,7 +808,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
-    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router"],
+    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router", "imbalance"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
     ap.add_argument("--dispatch-reps", type=int, default=200)
@@ -742,6 +845,8 @@ def main():
         return run_e2e(args)
     if args.workload == "router":
         return run_router(args)
+    if args.workload == "imbalance":
+        return run_imbalance(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")

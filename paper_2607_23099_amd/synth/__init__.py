@@ -189,6 +189,23 @@ def routing(E: int, k: int, T: int, alpha: float | None, seed, *, n_hot: int = 0
     return Routing(order.astype(np.int32), w.astype(np.float32), logp, E, k, alpha)
 
 
+def routing_repeated(E: int, k: int, T: int, f: int, alpha: float, seed) -> Routing:
+    """Routing of T tokens in groups that repeat one row each: the token analog of the paper's
+    imbalance factor f (Sec. V-E), where groups of about f% of a batch's prompts share one
+    prompt.  f = 0: every token draws its own row; f > 0: groups of max(1, round(f T / 100))
+    consecutive tokens take one row (ids and gates), drawn like `routing` for one token per
+    group from a common Dirichlet(alpha) p; f = 100: one row for the whole batch."""
+    if not 0 <= f <= 100:
+        raise ValueError("f is a percentage")
+    g = 1 if f == 0 else max(1, int(round(f * T / 100.0)))
+    n = -(-T // g) if T else 0
+    base = routing(E, k, n, alpha, seed)
+    if T == 0:
+        return base
+    rows = np.repeat(np.arange(n), g)[:T]
+    return Routing(base.ids[rows].copy(), base.w[rows].copy(), base.logp, E, k, alpha)
+
+
 # ----------------------------------------------------------------------------------------------
 # Named workloads (shapes and seeds)
 # ----------------------------------------------------------------------------------------------
@@ -320,6 +337,10 @@ def seed_prefill(T: int, alpha: float, rep: int):
 
 def seed_kimi(T: int, rep: int):
     return [3, int(T), int(rep)]
+
+
+def seed_imbalance(T: int, f: int, rep: int):
+    return [5, int(T), int(f), int(rep)]
 
 
 def seed_trace_step(step: int):

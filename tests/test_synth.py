@@ -104,3 +104,24 @@ def test_trace_params_ranges():
     assert min(als) >= 0.03 and max(als) <= 10.0
     # log-uniform: median of log T near ln(8192)/2.
     assert abs(np.median(np.log(ts)) - math.log(8192) / 2) < 0.3
+
+
+def test_routing_repeated_groups():
+    for T, f in [(32, 0), (32, 10), (64, 20), (128, 50), (256, 100), (7, 50), (0, 10)]:
+        r = synth.routing_repeated(64, 8, T, f, 1.0, [5, T, f])
+        assert r.ids.shape == (T, 8) and r.w.shape == (T, 8)
+        if T == 0:
+            continue
+        g = 1 if f == 0 else max(1, round(f * T / 100))
+        distinct = {tuple(row) for row in r.ids}
+        assert len(distinct) <= -(-T // g)
+        for t in range(T):  # tokens of one group share the row, ids and gates
+            np.testing.assert_array_equal(r.ids[t], r.ids[(t // g) * g])
+            np.testing.assert_array_equal(r.w[t], r.w[(t // g) * g])
+        assert np.all(np.sort(r.ids, axis=1)[:, 1:] != np.sort(r.ids, axis=1)[:, :-1])
+    # More repetition, fewer Effective Experts (the histogram concentrates).
+    import oracle
+    oracle.build()
+    eff = [oracle.effexp(oracle.histogram(synth.routing_repeated(256, 8, 256, f, 1.0, [5, 256, f, 0]).ids,
+                                          256))[2] for f in (0, 10, 50, 100)]
+    assert eff[0] > eff[1] > eff[2] > eff[3] == 8.0
