@@ -698,6 +698,120 @@ def run_imbalance(args):
     print(json.dumps(out), flush=True)
 
 
+EP_DEGREES = (1, 2, 4, 8)
+EP_T = (32, 64, 128, 256)
+
+
+def run_ep(args):
+    """Expert-parallel ranks on one GPU (the analog of the paper's EP ablation, Sec. V-F):
+    DeepSeek-V3 at EP in {1, 2, 4, 8} and T in {32, 64, 128, 256} global tokens, routing
+    Dirichlet(1) with no repetition.  Rank r holds experts [r E / EP, (r + 1) E / EP) as views
+    into the full layer and runs the fused layer on the tokens with a local slot (remote slots
+    masked), with its own table (tables/dsv3-ep{EP}.damoe; EP = 1 uses dsv3.damoe).  Every rank
+    of every routing is timed for every variant (a6-a8, HIP events behind a GPU spin); the
+    exemplar match's kernel (DA-MoE), the bucket's NoDA kernel and the per-rank best are
+    compared.  Speedup = NoDA / DA-MoE of the mean per-rank latency, geomean over T."""
+    import torch
+    from paper_2607_23099_amd import damoe, synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path, RankLayer
+
+    shape = synth.DS
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    dl = DeviceLayer(shape)
+    stream = torch.cuda.current_stream()
+    spin = gpu_spin(torch, stream, 100.0)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    nv = damoe.num_variants()
+    Tm = max(EP_T)
+    rows, t0 = {}, time.perf_counter()
+    for ep in EP_DEGREES:
+        name = "dsv3.damoe" if ep == 1 else f"dsv3-ep{ep}.damoe"
+        tpath = os.path.join(TABLE_DIR, name)
+        if not os.path.exists(tpath):
+            raise SystemExit(f"{tpath} is missing: python -m paper_2607_23099_amd.tune_tables "
+                             f"dsv3-ep{ep} --max-T {Tm} --out {tpath}")
+        table = damoe.Table.load(tpath)
+        local = shape if ep == 1 else synth.DS_EP[ep]
+        td = table.data(local.E)
+        ranks = [dl if ep == 1 else RankLayer(dl, ep, r_, local) for r_ in range(ep)]
+        paths = [Path(rl, Tm) for rl in ranks]
+        for p_ in paths:
+            p_.fill_x(Tm, 2)
+        for T in EP_T:
+            acc = {"da": [], "noda": [], "best": []}
+            picks, locs = [], []
+            for rep in range(REPS):
+                r = synth.routing(shape.E, shape.k, T, 1.0, synth.seed_ep(T, rep))
+                lat_da, lat_nd, lat_best = [], [], []
+                for rank, path in enumerate(paths):
+                    keep, ids, w = synth.ep_local(r, ep, rank)
+                    tl = len(keep)
+                    locs.append(tl)
+                    if tl == 0:
+                        continue
+                    path.set_routing(synth.Routing(ids, w, None, local.E, shape.k, 1.0))
+                    path.route_dispatch(table, tl)
+                    torch.cuda.synchronize()
+                    v_da = int(path.variant.item())
+                    noda = int(td.noda[bucket_of(td, tl)])
+                    path.candidates = 0
+                    lat = []
+                    for v in range(nv):
+                        for _ in range(args.warmup):
+                            path.fused(tl, v)
+                        pairs = []
+                        for _ in range(args.steps):
+                            torch.cuda._sleep(spin)
+                            e0, e1 = ev(), ev()
+                            e0.record(stream)
+                            path.fused(tl, v)
+                            e1.record(stream)
+                            pairs.append((e0, e1))
+                        torch.cuda.synchronize()
+                        lat.append(float(np.median([a.elapsed_time(b) for a, b in pairs])) * 1e3)
+                    lat_da.append(lat[v_da])
+                    lat_nd.append(lat[noda])
+                    lat_best.append(min(lat))
+                    picks.append(damoe.variant_name(v_da))
+                acc["da"].append(float(np.mean(lat_da)))
+                acc["noda"].append(float(np.mean(lat_nd)))
+                acc["best"].append(float(np.mean(lat_best)))
+            m = {k_: float(np.mean(v_)) for k_, v_ in acc.items()}
+            row = {"local_tokens_mean": round(float(np.mean(locs)), 1), "da_us": round(m["da"], 1),
+                   "noda_us": round(m["noda"], 1), "best_us": round(m["best"], 1),
+                   "da_speedup": round(m["noda"] / m["da"], 4), "best_speedup": round(m["noda"] / m["best"], 4),
+                   "kernels_da": sorted(set(picks))}
+            rows[f"ep{ep}_T{T}"] = row
+            log(f"ep={ep} T={T}: {row}")
+        del paths, ranks
+        torch.cuda.empty_cache()
+    wall = time.perf_counter() - t0
+    per_ep = {f"ep{ep}": {k_: round(geomean([rows[f"ep{ep}_T{T}"][k_] for T in EP_T]), 4)
+                          for k_ in ("da_speedup", "best_speedup")} for ep in EP_DEGREES}
+    for k_, v_ in per_ep.items():
+        log(f"{k_}: geomean {v_}")
+    out = {
+        "metric": "fused-MoE speedup of DA-MoE over NoDA per expert-parallel rank, DeepSeek-V3 at EP = 4 "
+                  "(geomean over T in 32..256)",
+        "value": per_ep["ep4"]["da_speedup"],
+        "unit": "x",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / max(len(rows) * REPS, 1), 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "dsv3-ep: E=256 top-8 H=7168 I=2048 bf16, EP in {1,2,4,8} rank layers on one GPU, "
+                               "T in {32,64,128,256} global tokens, Dirichlet(1) routing, remote slots masked"},
+        "per_ep": per_ep,
+        "per_point": rows,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def run_prefill(args):
     """Per-variant GEMM times at the MFMA-bound prefill points: Kimi-K2 (bf16, 40% of the mass
     on 4 hot experts) at T = 2048 and 8192, and DeepSeek-V3 with fp8 block-128 weights at
@@ -808,7 +922,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick-tune", action="store_true", help="ignore a committed table")
     ap.add_argument("--force-variant", type=int, default=-1, help="time one variant instead of dispatch")
-    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router", "imbalance"],
+    ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router", "imbalance", "ep"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
     ap.add_argument("--dispatch-reps", type=int, default=200)
@@ -847,6 +961,8 @@ def main():
         return run_router(args)
     if args.workload == "imbalance":
         return run_imbalance(args)
+    if args.workload == "ep":
+        return run_ep(args)
 
     shape = synth.DS
     log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")

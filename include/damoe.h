@@ -31,8 +31,9 @@
  *     immutable after creation.
  *   - Argument and shape errors are reported synchronously as a status code,
  *     before any launch.  Data errors found on the device (an expert id
- *     outside [0, E)) set a sticky code in the workspace; the offending slot
- *     is dropped.  damoe_read_device_error() reads and clears it.
+ *     >= E) set a sticky code in the workspace; the offending slot is
+ *     dropped.  damoe_read_device_error() reads and clears it.  Negative ids
+ *     are masked slots (expert parallelism), dropped without an error.
  *   - All calls are thread-safe as long as concurrent calls use distinct
  *     workspaces.
  */
@@ -67,7 +68,7 @@ typedef enum damoe_status {
 
 /* Device error codes (sticky, in the workspace). */
 #define DAMOE_DEVERR_NONE 0
-#define DAMOE_DEVERR_EXPERT_ID 1 /* an id outside [0, E) was dropped                       */
+#define DAMOE_DEVERR_EXPERT_ID 1 /* an id >= E was dropped (negative ids are masked slots) */
 #define DAMOE_DEVERR_TILES 2     /* fused_moe found tile lists of another T; items skipped */
 #define DAMOE_DEVERR_VARIANT 4   /* the dispatched id was outside fused_moe's candidates  */
 
@@ -132,8 +133,10 @@ damoe_status damoe_workspace_layout(int32_t E, int32_t k, int32_t H, int32_t I, 
 size_t damoe_workspace_size(const damoe_layer* layer /* host */, int32_t T_max);
 
 /* a2-a4: routing histogram, Effective Experts and routing metadata.
- *   topk_ids  int32 [T][k], experts of each token (Sec. II-A); ids outside [0, E)
- *             are dropped and flag DAMOE_DEVERR_EXPERT_ID
+ *   topk_ids  int32 [T][k], experts of each token (Sec. II-A).  A negative id is a
+ *             masked slot: with expert parallelism the slot's expert lives on another
+ *             rank, so it is dropped silently (no permutation entry, no contribution to
+ *             y).  Ids >= E are dropped and flag DAMOE_DEVERR_EXPERT_ID
  *   counts    int32 [E]    t_e, tokens routed to expert e (Sec. III-A, Eq. (2))
  *   offsets   int32 [E+1]  exclusive prefix sum of counts
  *   perm      int32 [T*k]  flat assignment index a = t*k + j at each position,
@@ -308,6 +311,10 @@ typedef struct damoe_tune_config {
   uint64_t seed;
   const uint16_t* x;        /* device bf16 [max bucket_T][H] activations to time with */
   int32_t verbose;          /* print progress to stderr                              */
+  int32_t ep;               /* expert parallelism: 0 or 1 = none; ep > 1: the layer is
+                               one rank's E experts of a pool of E * ep, and each sample
+                               keeps the tokens with a slot on the rank, the other slots
+                               masked (-1), up to the bucket's token count              */
 } damoe_tune_config;
 
 /* Builds a table: for each bucket T_b and skew X_j, alpha_j = Alg1(E / X_j);

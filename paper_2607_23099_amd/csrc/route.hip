@@ -295,7 +295,7 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     for (int q = 0; q < kIdBatch; ++q) {
       const int a = a0 + 64 * q + lane;
       if (a >= a_hi) eb[q] = -1;
-      bad += (a < a_hi && !(eb[q] >= 0 && eb[q] < E)) ? 1 : 0;
+      bad += (a < a_hi && eb[q] >= E) ? 1 : 0;  // negative ids are masked slots, not errors
     }
 #pragma unroll
     for (int q = 0; q < kIdBatch; ++q) {

@@ -104,41 +104,68 @@ double mean_effexp(const Philox& g, int32_t E, double alpha, int32_t S, std::vec
   return acc / S;
 }
 
-// Gumbel-top-k routing of T tokens under log p, softmax gates of N(0,1) logits.
-void gumbel_topk(const Philox& g, const std::vector<double>& lp, int32_t T, int32_t k, uint32_t s,
-                 std::vector<int32_t>& ids, std::vector<float>& w) {
+// Gumbel-top-k experts of token t under log p (keys from uniforms tagged 2), softmax gates of
+// N(0,1) logits (tag 3), written to id[0..k) and w[0..k).
+void gumbel_token(const Philox& g, const std::vector<double>& lp, uint32_t t, int32_t k, uint32_t s,
+                  std::vector<double>& key, std::vector<int32_t>& idx, int32_t* id, float* w) {
   const int32_t E = (int32_t)lp.size();
-  ids.resize((size_t)T * k);
-  w.resize((size_t)T * k);
-  std::vector<double> key(E);
-  std::vector<int32_t> idx(E);
-  for (int32_t t = 0; t < T; ++t) {
-    for (int32_t e = 0; e < E; e += 2) {
-      double u0, u1;
-      g.uniforms((uint32_t)t, (uint32_t)e, s, 2, u0, u1);
-      key[e] = lp[e] - std::log(-std::log(u0));
-      if (e + 1 < E) key[e + 1] = lp[e + 1] - std::log(-std::log(u1));
-    }
-    std::iota(idx.begin(), idx.end(), 0);
-    std::partial_sort(idx.begin(), idx.begin() + k, idx.end(), [&](int32_t a, int32_t b) {
-      return key[a] > key[b] || (key[a] == key[b] && a < b);
-    });
-    double zs = 0.0, lg[DAMOE_MAX_K];
-    for (int32_t j = 0; j < k; ++j) {
-      double u0, u1;
-      g.uniforms((uint32_t)t, (uint32_t)j, s, 3, u0, u1);
-      lg[j] = std::sqrt(-2.0 * std::log(u0)) * std::cos(6.283185307179586 * u1);
-    }
-    const double m = *std::max_element(lg, lg + k);
-    for (int32_t j = 0; j < k; ++j) zs += std::exp(lg[j] - m);
-    for (int32_t j = 0; j < k; ++j) {
-      ids[(size_t)t * k + j] = idx[j];
-      w[(size_t)t * k + j] = (float)(std::exp(lg[j] - m) / zs);
-    }
+  for (int32_t e = 0; e < E; e += 2) {
+    double u0, u1;
+    g.uniforms(t, (uint32_t)e, s, 2, u0, u1);
+    key[e] = lp[e] - std::log(-std::log(u0));
+    if (e + 1 < E) key[e + 1] = lp[e + 1] - std::log(-std::log(u1));
+  }
+  std::iota(idx.begin(), idx.end(), 0);
+  std::partial_sort(idx.begin(), idx.begin() + k, idx.end(), [&](int32_t a, int32_t b) {
+    return key[a] > key[b] || (key[a] == key[b] && a < b);
+  });
+  double zs = 0.0, lg[DAMOE_MAX_K];
+  for (int32_t j = 0; j < k; ++j) {
+    double u0, u1;
+    g.uniforms(t, (uint32_t)j, s, 3, u0, u1);
+    lg[j] = std::sqrt(-2.0 * std::log(u0)) * std::cos(6.283185307179586 * u1);
+  }
+  const double m = *std::max_element(lg, lg + k);
+  for (int32_t j = 0; j < k; ++j) zs += std::exp(lg[j] - m);
+  for (int32_t j = 0; j < k; ++j) {
+    id[j] = idx[j];
+    w[j] = (float)(std::exp(lg[j] - m) / zs);
   }
 }
 
-// Exemplar (Sec. IV-A): mean of the sorted, unit-L2 count vectors, renormalised, times 2^15.
+// Routing of T tokens for a layer of E_local experts.  Without expert parallelism (ep <= 1)
+// the tokens are drawn directly (E_local = lp.size()).  With ep > 1, lp is over the global
+// pool of E_local * ep experts and the layer is the rank holding experts [0, E_local): global
+// tokens are drawn in turn, those with at least one local slot are kept with the other slots
+// masked (-1), until T are kept (bounded; rows left over are fully masked).
+void sample_routing(const Philox& g, const std::vector<double>& lp, int32_t T, int32_t k, int32_t E_local,
+                    int32_t ep, uint32_t s, std::vector<int32_t>& ids, std::vector<float>& w) {
+  const int32_t Eg = (int32_t)lp.size();
+  ids.assign((size_t)T * k, -1);
+  w.assign((size_t)T * k, 0.f);
+  std::vector<double> key(Eg);
+  std::vector<int32_t> idx(Eg);
+  if (ep <= 1) {
+    for (int32_t t = 0; t < T; ++t)
+      gumbel_token(g, lp, (uint32_t)t, k, s, key, idx, ids.data() + (size_t)t * k, w.data() + (size_t)t * k);
+    return;
+  }
+  int32_t kept = 0;
+  std::vector<int32_t> id(k);
+  std::vector<float> wt(k);
+  for (uint32_t t = 0; kept < T && t < (uint32_t)T * 1024u; ++t) {
+    gumbel_token(g, lp, t, k, s, key, idx, id.data(), wt.data());
+    bool local = false;
+    for (int32_t j = 0; j < k; ++j) local = local || id[j] < E_local;
+    if (!local) continue;
+    for (int32_t j = 0; j < k; ++j) {
+      ids[(size_t)kept * k + j] = id[j] < E_local ? id[j] : -1;
+      w[(size_t)kept * k + j] = wt[j];
+    }
+    ++kept;
+  }
+}
+
 void exemplar(const std::vector<std::vector<int32_t>>& counts, int32_t E, int32_t* Q) {
   std::vector<double> c(E, 0.0);
   for (const auto& v : counts) {
@@ -198,6 +225,10 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   for (int32_t b = 0; b < cfg->n_buckets; ++b) T_max = std::max(T_max, cfg->bucket_T[b]);
   const size_t ws_bytes = damoe_workspace_size(L, T_max);
   if (ws_bytes == 0) return DAMOE_ERR_INVALID_ARG;
+  // Expert parallelism: the layer is one rank's share of a global pool of E * ep experts.
+  if (cfg->ep < 0 || cfg->ep > 64) return DAMOE_ERR_INVALID_ARG;
+  const int32_t ep = cfg->ep > 1 ? cfg->ep : 1;
+  const int32_t Eg = E * ep;
   const int32_t a_samples = cfg->alpha_samples > 0 ? cfg->alpha_samples : 64;
   const int32_t a_iters = cfg->alpha_iters > 0 ? cfg->alpha_iters : 60;
   const Philox g(cfg->seed);
@@ -235,7 +266,7 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
 
   // Alg. 1 once per skew: the ddist:X target is E / X.
   for (int32_t j = 0; j < cfg->n_skews; ++j) {
-    alphas[j] = damoe_alpha_search(E, (double)E / cfg->skew_X[j], a_samples, a_iters, cfg->seed);
+    alphas[j] = damoe_alpha_search(Eg, (double)Eg / cfg->skew_X[j], a_samples, a_iters, cfg->seed);
     if (cfg->verbose) std::fprintf(stderr, "damoe_tune: ddist:%.2f -> alpha %.5g\n", cfg->skew_X[j], alphas[j]);
   }
 
@@ -285,8 +316,8 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
       std::vector<double> mean(nv, 0.0), lat;
       for (int32_t s = 0; s < cfg->samples; ++s) {
         const uint32_t sid = 0x10000u + ((uint32_t)b << 20) + ((uint32_t)j << 10) + (uint32_t)s;
-        dirichlet_logp(g, alphas[j], E, sid, lp);
-        gumbel_topk(g, lp, T, k, sid, ids, w);
+        dirichlet_logp(g, alphas[j], Eg, sid, lp);
+        sample_routing(g, lp, T, k, E, ep, sid, ids, w);
         std::vector<int32_t> c;
         TRY(time_routing(lat, &c));
         cs.push_back(c);
@@ -390,10 +421,10 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
     // Distribution-unaware baseline: the fastest variant under uniform routing.
     {
       std::vector<double> mean(nv, 0.0), lat;
-      lp.assign(E, -std::log((double)E));
+      lp.assign(Eg, -std::log((double)Eg));
       for (int32_t s = 0; s < cfg->samples; ++s) {
         const uint32_t sid = 0x8000000u + ((uint32_t)b << 10) + (uint32_t)s;
-        gumbel_topk(g, lp, T, k, sid, ids, w);
+        sample_routing(g, lp, T, k, E, ep, sid, ids, w);
         TRY(time_routing(lat, nullptr));
         for (int32_t v = 0; v < nv; ++v) mean[v] += lat[v] / cfg->samples;
       }

@@ -56,6 +56,27 @@ class DeviceLayer:
         return 3 * sh.H * sh.I + 3 * (sh.H // 128) * (sh.I // 128) * 4
 
 
+class RankLayer:
+    """Expert-parallel rank `rank` of `ep`: a layer over the full layer's experts
+    [rank E / ep, (rank + 1) E / ep), as views into its weight tensors (no copy)."""
+
+    def __init__(self, full: DeviceLayer, ep: int, rank: int, shape: synth.Shape):
+        sh = full.shape
+        if sh.E % ep or shape.E != sh.E // ep:
+            raise ValueError("rank shape does not split the layer")
+        self.shape, self.full, self.ep, self.rank = shape, full, ep, rank
+        lo = rank * shape.E
+        self.w = {n: t[lo: lo + shape.E] for n, t in full.w.items()}
+        self.s = {n: t[lo: lo + shape.E] for n, t in full.s.items()}
+        self.wdtype, self.packed = full.wdtype, full.packed
+        self.layer = damoe.make_layer(shape.E, shape.k, shape.H, shape.I, self.wdtype, self.w["w1"], self.w["w3"],
+                                      self.w["w2"], self.s.get("w1"), self.s.get("w3"), self.s.get("w2"),
+                                      layout=damoe.LAYOUT_FRAG16 if full.packed else damoe.LAYOUT_ROWMAJOR)
+
+    def global_expert(self, e: int) -> int:
+        return self.rank * self.shape.E + e
+
+
 class Gate:
     """The router's weights in HBM: Wg [E][H] bf16 from the seeded generator and a per-expert
     fp32 bias (zeros unless set)."""

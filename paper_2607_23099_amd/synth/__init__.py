@@ -206,6 +206,21 @@ def routing_repeated(E: int, k: int, T: int, f: int, alpha: float, seed) -> Rout
     return Routing(base.ids[rows].copy(), base.w[rows].copy(), base.logp, E, k, alpha)
 
 
+def ep_local(r: Routing, ep: int, rank: int):
+    """One expert-parallel rank's share of a routing over E experts: experts
+    [rank E / ep, (rank + 1) E / ep) are local.  Returns (token indices of the tokens with at
+    least one local slot, their local ids [T_l][k] = id - rank E / ep, or -1 for a slot whose
+    expert is on another rank, and their gates, unchanged: the rank computes its partial sum)."""
+    if r.E % ep:
+        raise ValueError("E must split evenly over the ranks")
+    el = r.E // ep
+    lo = rank * el
+    local = (r.ids >= lo) & (r.ids < lo + el)
+    keep = np.nonzero(local.any(axis=1))[0]
+    ids = np.where(local, r.ids - lo, -1)[keep].astype(np.int32)
+    return keep, ids, r.w[keep].copy()
+
+
 # ----------------------------------------------------------------------------------------------
 # Named workloads (shapes and seeds)
 # ----------------------------------------------------------------------------------------------
@@ -230,6 +245,8 @@ TINY = Shape("tiny", E=8, k=2, H=256, I=512, shape_id=0)
 DS = Shape("dsv3", E=256, k=8, H=7168, I=2048, shape_id=1)
 DS_FP8 = Shape("dsv3-fp8", E=256, k=8, H=7168, I=2048, shape_id=1, wdtype="fp8")
 KIMI = Shape("kimi-k2", E=384, k=8, H=7168, I=2048, shape_id=3)
+# One expert-parallel rank's layer of DeepSeek-V3 at EP = 2, 4, 8 (weights of its own experts).
+DS_EP = {ep: Shape(f"dsv3-ep{ep}", E=256 // ep, k=8, H=7168, I=2048, shape_id=1) for ep in (2, 4, 8)}
 
 # Weight matrices of expert e (row-major): W1, W3: [I][H]; W2: [H][I].
 WEIGHT_TENSORS = {"w1": (T_W1, "I", "H"), "w3": (T_W3, "I", "H"), "w2": (T_W2, "H", "I")}
@@ -341,6 +358,10 @@ def seed_kimi(T: int, rep: int):
 
 def seed_imbalance(T: int, f: int, rep: int):
     return [5, int(T), int(f), int(rep)]
+
+
+def seed_ep(T: int, rep: int):
+    return [6, int(T), int(rep)]
 
 
 def seed_trace_step(step: int):

@@ -2,6 +2,10 @@
 
     python -m paper_2607_23099_amd.tune_tables dsv3 --max-T 128 --out tables/dsv3.damoe
 
+The dsv3-ep{2,4,8} shapes are one expert-parallel rank's layer (256 / EP experts); they are
+tuned on the rank's share of routings over the whole pool (remote slots masked), and their
+tables serve the rank layers of the expert-parallel workload.
+
 For each power-of-two token bucket up to --max-T, each ddist:X skew of the
 grid (the paper's {1.1 ... 4.0} extended to 32) and S routing samples, every
 variant is timed by the library's tuner; the table maps each skew's exemplar
@@ -24,7 +28,8 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
     import torch
     from . import damoe, synth
     from .moe import DeviceLayer
-    shapes = {"dsv3": synth.DS, "dsv3-fp8": synth.DS_FP8, "kimi-k2": synth.KIMI, "tiny": synth.TINY}
+    shapes = {"dsv3": synth.DS, "dsv3-fp8": synth.DS_FP8, "kimi-k2": synth.KIMI, "tiny": synth.TINY,
+              **{f"dsv3-ep{ep}": sh for ep, sh in synth.DS_EP.items()}}
     shape = shapes[shape_name]
     if dl is None:
         dl = DeviceLayer(shape)
@@ -37,14 +42,15 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
     synth.fill_bf16_device(x.data_ptr(), x.numel(), seed=synth.x_seed(999), tensor=synth.T_X,
                            slab_elems=x.numel(), sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
     t0 = time.perf_counter()
+    ep = int(shape_name.split("-ep")[1]) if "-ep" in shape_name else 1
     table = damoe.tune(dl.layer, buckets, EXTENDED_SKEWS, x, samples=samples, reps=reps, seed=seed,
-                       verbose=verbose)
+                       verbose=verbose, ep=ep)
     return table, time.perf_counter() - t0, buckets, dl
 
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("shape", choices=["dsv3", "dsv3-fp8", "kimi-k2", "tiny"])
+    ap.add_argument("shape", choices=["dsv3", "dsv3-fp8", "kimi-k2", "tiny", "dsv3-ep2", "dsv3-ep4", "dsv3-ep8"])
     ap.add_argument("--max-T", type=int, default=128)
     ap.add_argument("--samples", type=int, default=10)
     ap.add_argument("--reps", type=int, default=5)

@@ -177,7 +177,7 @@ def test_committed_tables_match_the_variant_registry():
     nv = damoe.num_variants()
     for f in names:
         t = damoe.Table.load(os.path.join(tdir, f))
-        E = 256 if f.startswith("dsv3") else 384
+        E = 384 if f.startswith("kimi") else 256 // (int(f.split("-ep")[1].split(".")[0]) if "-ep" in f else 1)
         td = t.data(E)
         assert td.kid.min() >= 0 and td.kid.max() < nv and td.noda.max() < nv
         assert np.all(np.diff(td.bucket_T) > 0)

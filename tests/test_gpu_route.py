@@ -120,6 +120,21 @@ def test_route_drops_invalid_ids_and_flags_them():
     assert damoe.read_device_error(b.ws) == 0  # read clears it
 
 
+def test_route_masked_slots_are_not_errors():
+    # Expert parallelism: negative ids are slots whose expert lives on another rank; they are
+    # dropped like invalid ids but raise no device error, also when whole tokens are masked.
+    torch = torch_cuda()
+    E, k, T = 64, 8, 300
+    r = synth.routing(256, k, T, 1.0, [12])
+    ids = np.where(r.ids < E, r.ids, -1).astype(np.int32)  # rank 0 of four
+    ids[5] = -1
+    b = RouteBufs(torch, E, k, T)
+    b.run(ids)
+    _check_route(b, ids)
+    assert np.all(b.inv.cpu().numpy()[ids.ravel() < 0] == -1)
+    assert damoe.read_device_error(b.ws) == 0
+
+
 def _random_table(rng, E, buckets, nv):
     n_ex = rng.integers(1, 14, len(buckets))
     Q = []

@@ -50,3 +50,26 @@ def test_tune_tiny_table(tmp_path):
     assert int(path.variant.item()) == int(td.kid[td.bucket_rows(6)][i])
     ref = oracle_rows(sh, r, 31, np.arange(50))
     assert row_err(bf16_rows(path.y, np.arange(50)), ref) <= TOL["bf16"]
+
+
+def test_tune_expert_parallel_rank():
+    # ep > 1: samples are one rank's share of routings over E * ep experts (remote slots
+    # masked); the table is well formed and its exemplars come from the rank's histograms.
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer
+    sh = synth.Shape("small-rank", E=4, k=4, H=256, I=512, shape_id=7)
+    dl = DeviceLayer(sh)
+    x = torch.empty((16, sh.H), dtype=torch.bfloat16, device="cuda")
+    synth.fill_bf16_device(x.data_ptr(), x.numel(), seed=synth.x_seed(3), tensor=synth.T_X, slab_elems=x.numel(),
+                           sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
+    table = damoe.tune(dl.layer, [1, 4, 16], [1.1, 4.0], x, samples=2, reps=1, seed=9, ep=4)
+    td = table.data(sh.E)
+    nv = damoe.num_variants()
+    assert list(td.bucket_T) == [1, 4, 16] and list(td.n_ex) == [2, 2, 2]
+    assert td.kid.min() >= 0 and td.kid.max() < nv and td.noda.max() < nv
+    for q in td.Q:
+        assert np.all(np.diff(q) <= 0) and q[0] > 0
+    with pytest.raises(damoe.DamoeError):
+        damoe.tune(dl.layer, [1], [1.1], x, samples=1, reps=1, ep=-1)
+    del dl
+    torch.cuda.empty_cache()

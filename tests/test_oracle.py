@@ -296,7 +296,7 @@ def _f64_weights_of(shape):
 def _oracle_y(ids, w, x_u16, shape, rows=None):
     T = ids.shape[0]
     rows = np.arange(T) if rows is None else np.asarray(rows)
-    experts = np.unique(ids[rows])
+    experts = np.unique(ids[rows][ids[rows] >= 0])
     return oracle.moe_rows(ids, w, shape.k, rows, x_u16[rows], shape.H, shape.I, experts,
                            lambda e: synth.expert_weights_host(shape, e))
 
@@ -595,3 +595,20 @@ def test_effexp_map_brute_force_fractions():
             pops = sorted(first, key=lambda p: (abs(p - b), p))
             want.append(int(kid[first[pops[0]]]))
         np.testing.assert_array_equal(oracle.effexp_map(Q.astype(np.int32), kid, noda=5), want)
+
+
+def test_moe_masked_slots_equal_zero_gates():
+    # Expert parallelism: a masked slot (negative id) contributes nothing, exactly like a slot
+    # that names any expert with gate 0.
+    sh = synth.TINY
+    r = synth.routing(sh.E, sh.k, 24, 0.3, 13)
+    x = synth.activations_host(24, sh.H, 13)
+    ids_m = r.ids.copy()
+    ids_m[::3, 1] = -1
+    ids_m[5] = -1
+    ids_z, w_z = r.ids.copy(), r.w.copy()
+    w_z[ids_m < 0] = 0.0
+    y_m = _oracle_y(ids_m, r.w, x, sh)
+    y_z = _oracle_y(ids_z, w_z, x, sh)
+    np.testing.assert_array_equal(y_m, y_z)
+    assert np.all(y_m[5] == 0.0)
