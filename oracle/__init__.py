@@ -135,7 +135,8 @@ def moe_rows(ids, w, k: int, rows, x_rows, H: int, I: int, experts, weights_of) 
     ``weights_of(e)`` returns expert e's weights, either bf16 bit patterns
     ``(W1 [I][H], W3 [I][H], W2 [H][I])`` (uint16) or fp8 pairs
     ``((q1, s1), (q3, s3), (q2, s2))``; experts are visited one at a time
-    (expert-major), so only one expert's weights are held at once.
+    (expert-major), so only one expert's weights are held at once.  Slots whose id is not
+    among ``experts`` (masked slots, id < 0) contribute nothing.
     """
     ids = _c(ids, np.int32)
     w = _c(w, np.float32)
@@ -144,6 +145,8 @@ def moe_rows(ids, w, k: int, rows, x_rows, H: int, I: int, experts, weights_of) 
     y = np.zeros((rows.size, H), np.float64)
     L = lib()
     for e in experts:
+        if int(e) < 0:
+            raise ValueError("expert ids are >= 0: a negative id is a masked slot, never an expert")
         wt = weights_of(int(e))
         if isinstance(wt[0], tuple):
             (q1, s1), (q3, s3), (q2, s2) = [(_c(q, np.uint8), _c(s, np.float32)) for q, s in wt]
