@@ -64,6 +64,9 @@ def lib() -> ctypes.CDLL:
             "oracle_router": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp], None),
             "oracle_topk_softmax": ([vp, i32, i32, i32, vp, vp], None),
             "oracle_effexp_map": ([vp, vp, i32, i32, i32, vp], None),
+            "oracle_moe_expert_mxfp4": ([i32, vp, vp, i32, vp, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp, vp],
+                                        ctypes.c_int64),
+            "oracle_mxfp4_value": ([ctypes.c_uint8, ctypes.c_uint8], f64),
         }
         for name, (args, res) in sig.items():
             fn = getattr(L, name)
@@ -133,8 +136,9 @@ def moe_rows(ids, w, k: int, rows, x_rows, H: int, I: int, experts, weights_of) 
     """Layer output y[len(rows)][H] in fp64 for the listed token rows.
 
     ``weights_of(e)`` returns expert e's weights, either bf16 bit patterns
-    ``(W1 [I][H], W3 [I][H], W2 [H][I])`` (uint16) or fp8 pairs
-    ``((q1, s1), (q3, s3), (q2, s2))``; experts are visited one at a time
+    ``(W1 [I][H], W3 [I][H], W2 [H][I])`` (uint16), fp8 pairs ``((q1, s1), (q3, s3), (q2, s2))``
+    with float32 block scales, or MXFP4 pairs of the same form with packed e2m1 codes
+    (uint8 [rows][cols / 2]) and E8M0 scales (uint8 [rows][cols / 32]); experts are visited one at a time
     (expert-major), so only one expert's weights are held at once.  Slots whose id is not
     among ``experts`` (masked slots, id < 0) contribute nothing.
     """
@@ -148,7 +152,13 @@ def moe_rows(ids, w, k: int, rows, x_rows, H: int, I: int, experts, weights_of) 
         if int(e) < 0:
             raise ValueError("expert ids are >= 0: a negative id is a masked slot, never an expert")
         wt = weights_of(int(e))
-        if isinstance(wt[0], tuple):
+        if isinstance(wt[0], tuple) and np.asarray(wt[0][1]).dtype == np.uint8:
+            (q1, s1), (q3, s3), (q2, s2) = [(_c(q, np.uint8), _c(s, np.uint8)) for q, s in wt]
+            L.oracle_moe_expert_mxfp4(int(e), ids.ctypes.data, w.ctypes.data, k, rows.ctypes.data,
+                                      rows.size, x_rows.ctypes.data, H, I, q1.ctypes.data,
+                                      s1.ctypes.data, q3.ctypes.data, s3.ctypes.data, q2.ctypes.data,
+                                      s2.ctypes.data, y.ctypes.data)
+        elif isinstance(wt[0], tuple):
             (q1, s1), (q3, s3), (q2, s2) = [(_c(q, np.uint8), _c(s, np.float32)) for q, s in wt]
             L.oracle_moe_expert_fp8(int(e), ids.ctypes.data, w.ctypes.data, k, rows.ctypes.data,
                                     rows.size, x_rows.ctypes.data, H, I, q1.ctypes.data,
@@ -225,3 +235,8 @@ def effexp_map(Q, kid, noda: int):
     out = np.zeros(15, np.int32)
     lib().oracle_effexp_map(q.ctypes.data, k.ctypes.data, n_ex, E, int(noda), out.ctypes.data)
     return out
+
+
+def mxfp4_value(code: int, scale: int) -> float:
+    """Decoded MXFP4 element: e2m1(code) * 2^(scale - 127)."""
+    return float(lib().oracle_mxfp4_value(code, scale))

@@ -176,19 +176,38 @@ static double e4m3_value(uint8_t q) {
   return sign ? -v : v;
 }
 
+/* OCP MX FP4 (e2m1): 1 sign, 2 exponent (bias 1), 1 mantissa bit; exponent 0 is
+ * subnormal (mant * 0.5).  Magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6. */
+static double e2m1_value(uint8_t c) {
+  const int sign = (c >> 3) & 1, ex = (c >> 1) & 3, man = c & 1;
+  const double v = ex == 0 ? 0.5 * man : (1.0 + 0.5 * man) * ldexp(1.0, ex - 1);
+  return sign ? -v : v;
+}
+
+/* OCP MX E8M0 block scale: 2^(s - 127); 255 is NaN. */
+static double e8m0_value(uint8_t s) { return s == 255 ? NAN : ldexp(1.0, (int)s - 127); }
+
 static double silu(double z) { return z / (1.0 + exp(-z)); }
 
-/* Weight element (row i, column c) of a [rows][cols] expert matrix, either
- * bf16 or fp8 e4m3 with one fp32 scale per 128x128 block. */
+/* Weight element (row i, column c) of a [rows][cols] expert matrix: bf16; fp8 e4m3 with
+ * one fp32 scale per 128x128 block; or MXFP4 (two e2m1 codes per byte, the even column in
+ * the low nibble, [rows][cols / 2]) with one E8M0 scale per 32 consecutive columns of a row
+ * ([rows][cols / 32]). */
 typedef struct {
   const uint16_t* bf16;
   const uint8_t* q;
   const float* s;
   int32_t cols;
+  const uint8_t* q4;
+  const uint8_t* s4;
 } wmat;
 
 static double wval(const wmat* m, int64_t i, int64_t c) {
   if (m->bf16) return bf16_value(m->bf16[i * m->cols + c]);
+  if (m->q4) {
+    const uint8_t byte = m->q4[i * (m->cols / 2) + c / 2];
+    return e2m1_value((uint8_t)(c % 2 ? byte >> 4 : byte & 15)) * e8m0_value(m->s4[i * (m->cols / 32) + c / 32]);
+  }
   return e4m3_value(m->q[i * m->cols + c]) * (double)m->s[(i / 128) * (m->cols / 128) + c / 128];
 }
 
@@ -266,7 +285,7 @@ int64_t oracle_moe_expert_bf16(int32_t e, const int32_t* ids, const float* w, in
                                const int32_t* rows, int32_t n_rows, const uint16_t* x_rows,
                                int32_t H, int32_t I, const uint16_t* w1, const uint16_t* w3,
                                const uint16_t* w2, double* y) {
-  wmat m1 = {w1, 0, 0, H}, m3 = {w3, 0, 0, H}, m2 = {w2, 0, 0, I};
+  wmat m1 = {w1, 0, 0, H, 0, 0}, m3 = {w3, 0, 0, H, 0, 0}, m2 = {w2, 0, 0, I, 0, 0};
   return expert_accumulate(e, ids, w, k, rows, n_rows, x_rows, H, I, &m1, &m3, &m2, y);
 }
 
@@ -277,9 +296,24 @@ int64_t oracle_moe_expert_fp8(int32_t e, const int32_t* ids, const float* w, int
                               int32_t H, int32_t I, const uint8_t* q1, const float* s1,
                               const uint8_t* q3, const float* s3, const uint8_t* q2,
                               const float* s2, double* y) {
-  wmat m1 = {0, q1, s1, H}, m3 = {0, q3, s3, H}, m2 = {0, q2, s2, I};
+  wmat m1 = {0, q1, s1, H, 0, 0}, m3 = {0, q3, s3, H, 0, 0}, m2 = {0, q2, s2, I, 0, 0};
   return expert_accumulate(e, ids, w, k, rows, n_rows, x_rows, H, I, &m1, &m3, &m2, y);
 }
+
+/* MXFP4 weights (OCP Microscaling: e2m1 elements, one E8M0 scale per 32 elements along a
+ * row): the weight value is e2m1(q) * 2^(s - 127) exactly (in fp64).  q1, q3: [I][H / 2];
+ * s1, s3: [I][H / 32]; q2: [H][I / 2]; s2: [H][I / 32]. */
+int64_t oracle_moe_expert_mxfp4(int32_t e, const int32_t* ids, const float* w, int32_t k,
+                                const int32_t* rows, int32_t n_rows, const uint16_t* x_rows,
+                                int32_t H, int32_t I, const uint8_t* q1, const uint8_t* s1,
+                                const uint8_t* q3, const uint8_t* s3, const uint8_t* q2,
+                                const uint8_t* s2, double* y) {
+  wmat m1 = {0, 0, 0, H, q1, s1}, m3 = {0, 0, 0, H, q3, s3}, m2 = {0, 0, 0, I, q2, s2};
+  return expert_accumulate(e, ids, w, k, rows, n_rows, x_rows, H, I, &m1, &m3, &m2, y);
+}
+
+/* Decoded value of one MXFP4 element (tests pin the decode through this). */
+double oracle_mxfp4_value(uint8_t code, uint8_t scale) { return e2m1_value(code & 15) * e8m0_value(scale); }
 
 /* ------------------------------------------------------------------------- */
 /* Offline tuning (Sec. III-A Alg. 1, Sec. IV-A)                              */

@@ -612,3 +612,46 @@ def test_moe_masked_slots_equal_zero_gates():
     y_z = _oracle_y(ids_z, w_z, x, sh)
     np.testing.assert_array_equal(y_m, y_z)
     assert np.all(y_m[5] == 0.0)
+
+
+# ---------------------------------------------------------------- MXFP4 weights (NEXT row f3)
+
+def test_mxfp4_decode_table():
+    # OCP MX FP4 (e2m1): the 16 codes in order, and E8M0 scales 2^(s - 127) (255 is NaN).
+    want = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0]
+    got = [oracle.mxfp4_value(c, 127) for c in range(16)]
+    assert got == want
+    assert oracle.mxfp4_value(2, 0) == 2.0 ** -127 and oracle.mxfp4_value(2, 254) == 2.0 ** 127
+    assert oracle.mxfp4_value(7, 120) == 6.0 * 2.0 ** -7
+    assert math.isnan(oracle.mxfp4_value(2, 255))
+
+
+def test_mxfp4_layer_equals_bf16_layer_on_decoded_values():
+    # Random codes and scales; the bf16 weights hold the decoded values (exact in bf16), so
+    # both layers must agree bit for bit.  A swapped nibble order, a scale indexed by column
+    # block of the wrong width or a transposed scale array would break the equality.
+    rng = np.random.default_rng(40)
+    T, H, I, E, k = 5, 64, 96, 3, 2
+    codes = {m: rng.integers(0, 16, (E, r, c)).astype(np.uint8) for m, (r, c) in
+             {"w1": (I, H), "w3": (I, H), "w2": (H, I)}.items()}
+    scales = {m: rng.integers(118, 131, (E, r, c // 32)).astype(np.uint8) for m, (r, c) in
+              {"w1": (I, H), "w3": (I, H), "w2": (H, I)}.items()}
+    table = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0, -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0])
+
+    def packed(m, e):
+        c = codes[m][e]
+        return (c[:, 0::2] | (c[:, 1::2] << 4)).astype(np.uint8)
+
+    def decoded_bf16(m, e):
+        c, s = codes[m][e], scales[m][e]
+        v = table[c] * np.repeat(2.0 ** (s.astype(np.float64) - 127), 32, axis=1)
+        return synth.f32_to_bf16_bits(v.astype(np.float32))
+
+    r = synth.routing(E, k, T, 1.0, 41)
+    x = synth.f32_to_bf16_bits(rng.normal(0, 1, (T, H)))
+    y4 = oracle.moe_rows(r.ids, r.w, k, np.arange(T), x, H, I, range(E),
+                         lambda e: tuple((packed(m, e), scales[m][e]) for m in ("w1", "w3", "w2")))
+    yb = oracle.moe_rows(r.ids, r.w, k, np.arange(T), x, H, I, range(E),
+                         lambda e: tuple(decoded_bf16(m, e) for m in ("w1", "w3", "w2")))
+    np.testing.assert_array_equal(y4, yb)
+    assert np.abs(y4).max() > 0
