@@ -74,7 +74,13 @@ typedef enum damoe_status {
 
 typedef enum damoe_wdtype {
   DAMOE_W_BF16 = 0,     /* bf16 weights                                                */
-  DAMOE_W_FP8_B128 = 1  /* OCP e4m3fn weights, one fp32 scale per 128x128 block         */
+  DAMOE_W_FP8_B128 = 1, /* OCP e4m3fn weights, one fp32 scale per 128x128 block         */
+  DAMOE_W_MXFP4 = 2     /* OCP MXFP4: e2m1 codes, two per byte (even column in the low
+                           nibble), one E8M0 scale byte 2^(s - 127) per 32 columns of a
+                           row; the s1, s3, s2 pointers carry the uint8 scale arrays
+                           [E][rows][cols / 32], row-major in both layouts.  The fused
+                           layer needs the fragment-packed layout and runs the stream
+                           variants only (damoe_variant_supports)                     */
 } damoe_wdtype;
 
 /* Weight layouts.  Row-major is the interchange layout; the fragment-packed

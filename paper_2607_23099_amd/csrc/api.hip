@@ -61,6 +61,10 @@ damoe_status check_layer(const damoe_layer* L) {
     if (L->H % 512 || L->I % 512) return DAMOE_ERR_UNSUPPORTED;  // 128-blocks per wave slice
     return DAMOE_OK;
   }
+  if (L->wdtype == DAMOE_W_MXFP4) {
+    if (!L->s1 || !L->s3 || !L->s2) return DAMOE_ERR_INVALID_ARG;
+    return DAMOE_OK;
+  }
   return DAMOE_ERR_UNSUPPORTED;
 }
 
@@ -158,6 +162,7 @@ int32_t damoe_variant_tile_m(int32_t v) {
 
 int32_t damoe_variant_supports(int32_t v, int32_t wdtype) {
   if (v < 0 || v >= num_variants()) return 0;
+  if (wdtype == DAMOE_W_MXFP4) return variant(v).kind == kStream;  // the weight-streaming family
   return wdtype == DAMOE_W_BF16 || wdtype == DAMOE_W_FP8_B128;
 }
 
@@ -312,6 +317,16 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   const uint32_t all = (uint32_t)((1ull << num_variants()) - 1);
   if (candidates & ~all) return DAMOE_ERR_INVALID_ARG;
   if (candidates == 0) candidates = all;
+  if (L->wdtype == DAMOE_W_MXFP4) {
+    // MXFP4 runs the stream variants only, fragment-packed: the launch covers just their kernel,
+    // and a dispatched id of another class is flagged by it.
+    if (L->layout != DAMOE_LAYOUT_FRAG16) return DAMOE_ERR_UNSUPPORTED;
+    uint32_t supported = 0;
+    for (int32_t v = 0; v < num_variants(); ++v)
+      if (damoe_variant_supports(v, L->wdtype)) supported |= 1u << v;
+    candidates &= supported;
+    if (candidates == 0) candidates = supported;
+  }
   // One candidate: the launch names it, and the kernels need not read the device-side id
   // (a bucket with a single kernel has no decision left to take on the device).
   if (force_variant < 0 && __builtin_popcount(candidates) == 1) {
@@ -350,6 +365,7 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g1.K = L->H;
   g1.N = L->I;
   g1.fp8 = L->wdtype == DAMOE_W_FP8_B128;
+  g1.fp4 = L->wdtype == DAMOE_W_MXFP4;
   g1.packed = L->layout == DAMOE_LAYOUT_FRAG16;
 
   GemmArgs g2 = g1;
@@ -406,8 +422,10 @@ damoe_status damoe_pack_weights(const damoe_layer* L, void* w1, void* w3, void* 
   const damoe_status st = check_layer(L);
   if (st != DAMOE_OK) return st;
   if (L->layout != DAMOE_LAYOUT_ROWMAJOR || !w1 || !w3 || !w2) return DAMOE_ERR_INVALID_ARG;
-  const int eb = L->wdtype == DAMOE_W_FP8_B128 ? 1 : 2;
-  const size_t bytes = (size_t)L->E * L->H * L->I * eb;
+  // Element bytes for the packer; 0 = MXFP4 codes (half a byte each; the scales keep their
+  // row-major layout).
+  const int eb = L->wdtype == DAMOE_W_FP8_B128 ? 1 : L->wdtype == DAMOE_W_MXFP4 ? 0 : 2;
+  const size_t bytes = eb ? (size_t)L->E * L->H * L->I * eb : (size_t)L->E * L->H * L->I / 2;
   const void* src[3] = {L->w1, L->w3, L->w2};
   void* dst[3] = {w1, w3, w2};
   for (int m = 0; m < 3; ++m)

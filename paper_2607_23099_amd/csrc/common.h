@@ -71,6 +71,7 @@ struct GemmArgs {
   int32_t K;           // reduction length: H for GEMM1, I for GEMM2
   int32_t N;           // output features: I for GEMM1, H for GEMM2
   int32_t fp8;
+  int32_t fp4;         // MXFP4 weights: wa / wb packed e2m1 codes, sa / sb E8M0 scales [E][N][K / 32]
   int32_t packed;      // weights in the fragment-packed layout
 };
 

@@ -1,5 +1,5 @@
-// Device helpers shared by the grouped-GEMM kernels: raw buffer loads, fp8 -> bf16 operand
-// conversion.
+// Device helpers shared by the grouped-GEMM kernels: raw buffer loads, fp8 and MXFP4 -> bf16
+// operand conversion.
 #pragma once
 
 #include "common.h"
@@ -47,9 +47,30 @@ template <class T, int AUX>
 __device__ __forceinline__ T buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
   if constexpr (sizeof(T) == 16) {
     return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX));
-  } else {
+  } else if constexpr (sizeof(T) == 8) {
     return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
+  } else if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
+  } else {
+    return (T)__builtin_amdgcn_raw_buffer_load_b8(r, voff, soff, AUX);
   }
+}
+
+// MXFP4 weights: an E8M0 block scale (2^(s - 127); 255 is NaN) as fp32, built from its bits.
+__device__ __forceinline__ float e8m0_to_f32(uint32_t s) {
+  return __uint_as_float(s == 255u ? 0x7FC00000u : s == 0u ? 0x00400000u : s << 23);
+}
+
+// Eight e2m1 codes of one lane (columns in order, the even column in each byte's low nibble)
+// times the block scale -> bf16 MFMA operand.  The scaled conversion is exact: every e2m1
+// value times a power of two is a bf16 number.
+__device__ __forceinline__ uint4 fp4x8_to_bf16x8(uint32_t q, float scale) {
+  uint4 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(q, scale, 0));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(q, scale, 1));
+  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(q, scale, 2));
+  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(q, scale, 3));
+  return r;
 }
 
 template <bool FP8>

@@ -21,6 +21,8 @@
 // sub-tile of the tile, and the four partial tiles are summed through LDS.
 // The weights of a (tile, feature block) are read exactly once; a larger BM
 // reads them once for more tokens at the price of padded MFMA rows.
+#include <type_traits>
+
 #include "common.h"
 #include "device.h"
 
@@ -37,13 +39,18 @@ constexpr int LDS_PAD = 1;
 // D:  register-ring depth, k-steps in flight per wave.
 // PK: weights in the fragment-packed layout (block (rb, kb) of 16 rows x 32 columns is one
 //     contiguous 64-lane fragment); otherwise row-major.
-template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D, bool PK>
+// FP4: MXFP4 weights (fragment-packed only): a lane's 8 e2m1 codes are 4 bytes of its
+//     fragment, its row's E8M0 scale of the k-step one byte of the row-major scale array; a
+//     k-step moves a quarter of the bf16 bytes, so the ring is twice as deep.
+template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D0, bool PK, bool FP4 = false>
 __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __restrict__ list,
                                             float* __restrict__ red) {
+  static_assert(!FP4 || (PK && !FP8), "MXFP4 weights are fragment-packed");
+  constexpr int D = FP4 ? 2 * D0 : D0;
   constexpr int NX = BM / 16;
   constexpr int NR = (GLU ? 2 : 1) * BN / 16;
   constexpr int LDR = BM + LDS_PAD;
-  using WT = typename WFrag<FP8>::T;
+  using WT = typename std::conditional<FP4, uint32_t, typename WFrag<FP8>::T>::type;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n_tiles = list[0];
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
@@ -88,7 +95,7 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
       }
     }
     // Weight operand: rows f of W1 (gate) and W3 (up) for GEMM1, of W2 for GEMM2.
-    const size_t slab = (size_t)N * K * EB;
+    const size_t slab = FP4 ? (size_t)N * K / 2 : (size_t)N * K * EB;
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(wa + (size_t)e * slab, (uint32_t)slab);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc((GLU ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
     uint32_t wo[NR];
@@ -98,10 +105,24 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
       if (PK) {
         const uint32_t rblk = (uint32_t)(fb * BN) / 16 + rb_;
         const uint32_t kb0 = IL ? wave : wave * nks;  // this wave's first 32-column block
-        wo[b] = ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 8u * EB;
+        wo[b] = FP4 ? ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 4u
+                    : ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 8u * EB;
       } else {
         const int f = fb * BN + rb_ * 16 + (lane & 15);
         wo[b] = ((uint32_t)f * (uint32_t)K + kcol) * EB;
+      }
+    }
+    // MXFP4 scales: row f's E8M0 bytes, one per 32-column block (k-step), of expert e.
+    const size_t sslab = (size_t)N * (K / 32);
+    __amdgpu_buffer_rsrc_t rsa, rsb;
+    uint32_t so[NR];
+    if constexpr (FP4) {
+      rsa = make_rsrc(reinterpret_cast<const uint8_t*>(a.sa) + (size_t)e * sslab, (uint32_t)sslab);
+      rsb = make_rsrc(reinterpret_cast<const uint8_t*>(GLU ? a.sb : a.sa) + (size_t)e * sslab, (uint32_t)sslab);
+#pragma unroll
+      for (int b = 0; b < NR; ++b) {
+        const int f = fb * BN + (GLU ? (b % (NR / 2)) : b) * 16 + (lane & 15);
+        so[b] = (uint32_t)f * (uint32_t)(K / 32) + (IL ? wave : wave * nks);
       }
     }
     const float* sa = a.sa;
@@ -118,17 +139,31 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
 
     WT wf[D][NR];
     uint4 xf[D][NX];
+    uint32_t sf[FP4 ? D : 1][NR];
     auto load = [&](int ks, int st) __attribute__((always_inline)) {
-      const uint32_t sw = PK ? (uint32_t)ks * (KSTEP / 32) * 512u * EB : (uint32_t)ks * KSTEP * EB;
+      const uint32_t sw = FP4 ? (uint32_t)ks * (KSTEP / 32) * 256u
+                              : PK ? (uint32_t)ks * (KSTEP / 32) * 512u * EB : (uint32_t)ks * KSTEP * EB;
 #pragma unroll
       for (int b = 0; b < NR; ++b)
         wf[st][b] = buf_load<WT, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b], sw);
+      if constexpr (FP4) {
+#pragma unroll
+        for (int b = 0; b < NR; ++b)
+          sf[st][b] = buf_load<uint8_t, 0>((GLU && b >= NR / 2) ? rsb : rsa, so[b], (uint32_t)ks * (KSTEP / 32));
+      }
       const uint32_t sx = (uint32_t)ks * KSTEP * 2;
 #pragma unroll
       for (int s = 0; s < NX; ++s) xf[st][s] = buf_load<uint4, 0>(rx, xo[s], sx);
     };
     auto compute = [&](int ks, int st) __attribute__((always_inline)) {
-      if constexpr (FP8) {
+      if constexpr (FP4) {
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+          const uint4 wv = fp4x8_to_bf16x8(wf[st][b], e8m0_to_f32(sf[st][b]));
+#pragma unroll
+          for (int s = 0; s < NX; ++s) acc[b][s] = mfma16x16x32(wv, xf[st][s], acc[b][s]);
+        }
+      } else if constexpr (FP8) {
         const int kb = (IL ? ks * 128 + wave * 32 : wave * kw + ks * 32) >> 7;
         const float s_g = sa[sbase + kb] * 0x1p120f;
         const float s_u = GLU ? sb[sbase + kb] * 0x1p120f : 0.f;
@@ -441,6 +476,33 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   }
 }
 
+// MXFP4 weights: the stream variants only (fragment-packed); any other dispatched id is
+// flagged like an id outside the launch's candidates.
+template <bool GLU>
+__global__ void __launch_bounds__(kGemmThreads, 2) k_gemm_fp4(GemmArgs a) {
+  extern __shared__ float smem[];
+  pin_gemm_args(a);
+  int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
+  if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
+  if (!variant_admitted(v, a.force_variant, a.candidates)) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
+    return;
+  }
+  switch (v) {
+#define DAMOE_CASE(ID, NAME, BM, BN1, BN2, IL, NT, D)                                          \
+  case ID: {                                                                                   \
+    constexpr int BN = GLU ? BN1 : BN2;                                                        \
+    stream_body<BM, BN, GLU, false, IL, NT, D, true, true>(a, a.tiles.list[tile_class(BM)], smem); \
+    break;                                                                                     \
+  }
+    DAMOE_STREAM_VARIANTS(DAMOE_CASE)
+#undef DAMOE_CASE
+    default:
+      if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
+      break;
+  }
+}
+
 // a8: y[t] = sum_j w[t][j] out[inv_perm[t*k+j]], summed in slot order in fp32.
 // Grid (T, H / 1024): each thread owns 4 consecutive features of one token.  The k slot
 // indices and gates arrive with one lane-parallel load (lane j holds slot j) and are
@@ -518,7 +580,9 @@ size_t gemm_lds_bytes() { return max_lds(); }
 template <bool GLU>
 static hipError_t launch_stage(const GemmArgs& a, int grid, hipStream_t stream) {
   const size_t lds = gemm_lds_bytes();
-  if (a.fp8) {
+  if (a.fp4) {
+    hipLaunchKernelGGL((k_gemm_fp4<GLU>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
+  } else if (a.fp8) {
     if (a.packed) hipLaunchKernelGGL((k_gemm<GLU, true, true>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
     else hipLaunchKernelGGL((k_gemm<GLU, true, false>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
   } else {
@@ -533,7 +597,8 @@ hipError_t gemm_set_lds_limits() {
       reinterpret_cast<const void*>(&k_gemm<true, false, false>), reinterpret_cast<const void*>(&k_gemm<false, false, false>),
       reinterpret_cast<const void*>(&k_gemm<true, true, false>), reinterpret_cast<const void*>(&k_gemm<false, true, false>),
       reinterpret_cast<const void*>(&k_gemm<true, false, true>), reinterpret_cast<const void*>(&k_gemm<false, false, true>),
-      reinterpret_cast<const void*>(&k_gemm<true, true, true>), reinterpret_cast<const void*>(&k_gemm<false, true, true>)};
+      reinterpret_cast<const void*>(&k_gemm<true, true, true>), reinterpret_cast<const void*>(&k_gemm<false, true, true>),
+      reinterpret_cast<const void*>(&k_gemm_fp4<true>), reinterpret_cast<const void*>(&k_gemm_fp4<false>)};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)gemm_lds_bytes());
     if (e != hipSuccess) return e;

@@ -3,7 +3,8 @@
 // For a [rows][cols] matrix: 16-row x 32-column block (rb, kb) becomes 64 lanes x 8 elements
 // stored contiguously at block index rb * (cols / 32) + kb, lane l holding row rb * 16 + l % 16,
 // columns kb * 32 + 8 * (l / 16) .. + 7 -- exactly the A-operand of v_mfma_f32_16x16x32_bf16
-// that one lane loads, so a wavefront reads a whole block in one contiguous access.
+// that one lane loads, so a wavefront reads a whole block in one contiguous access.  MXFP4
+// codes (two per byte) pack the same way, 4 bytes per lane.
 #include "common.h"
 
 namespace damoe {
@@ -23,6 +24,11 @@ __global__ void __launch_bounds__(256) k_pack(const uint8_t* __restrict__ src, u
     const uint32_t rb = (uint32_t)(blk / kbn), kb = (uint32_t)(blk % kbn);
     const uint64_t row = (uint64_t)rb * 16 + (lane & 15);
     const uint64_t col = (uint64_t)kb * 32 + (lane >> 4) * 8;
+    if constexpr (EB == 0) {  // MXFP4 codes: 8 columns are 4 bytes
+      *reinterpret_cast<uint32_t*>(dst + g * 4) =
+          *reinterpret_cast<const uint32_t*>(src + (slab * rows * cols + row * cols + col) / 2);
+      continue;
+    }
     const uint8_t* s = src + (slab * rows * cols + row * cols + col) * EB;
     uint8_t* d = dst + g * 8 * EB;
     if constexpr (EB == 2) {
@@ -40,7 +46,10 @@ hipError_t launch_pack(const void* src, void* dst, int32_t slabs, int32_t rows, 
   const uint64_t n_lanes = (uint64_t)slabs * (rows / 16) * (cols / 32) * 64;
   if (n_lanes == 0) return hipSuccess;
   const uint64_t blocks = std::min<uint64_t>((n_lanes + 255) / 256, 1u << 20);
-  if (elem_bytes == 2)
+  if (elem_bytes == 0)
+    hipLaunchKernelGGL(k_pack<0>, dim3((unsigned)blocks), dim3(256), 0, stream, (const uint8_t*)src,
+                       (uint8_t*)dst, n_lanes, (uint32_t)rows, (uint32_t)cols);
+  else if (elem_bytes == 2)
     hipLaunchKernelGGL(k_pack<2>, dim3((unsigned)blocks), dim3(256), 0, stream, (const uint8_t*)src,
                        (uint8_t*)dst, n_lanes, (uint32_t)rows, (uint32_t)cols);
   else

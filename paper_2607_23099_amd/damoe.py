@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdamoe.so")
 
 N_TILE_SIZES = 5
-W_BF16, W_FP8_B128 = 0, 1
+W_BF16, W_FP8_B128, W_MXFP4 = 0, 1, 2
 DEVERR_EXPERT_ID, DEVERR_TILES, DEVERR_VARIANT = 1, 2, 4
 LAYOUT_ROWMAJOR, LAYOUT_FRAG16 = 0, 1
 

@@ -20,7 +20,7 @@ class DeviceLayer:
     def __init__(self, shape: synth.Shape, device: str = "cuda", packed: bool = True):
         self.shape = shape
         E, H, I = shape.E, shape.H, shape.I
-        self.wdtype = damoe.W_FP8_B128 if shape.wdtype == "fp8" else damoe.W_BF16
+        self.wdtype = {"fp8": damoe.W_FP8_B128, "mxfp4": damoe.W_MXFP4}.get(shape.wdtype, damoe.W_BF16)
         stream = torch.cuda.current_stream(device).cuda_stream
         self.w, self.s = {}, {}
         for name in ("w1", "w3", "w2"):
@@ -30,6 +30,12 @@ class DeviceLayer:
                 synth.fill_bf16_device(t.data_ptr(), t.numel(), seed=shape.weight_seed, tensor=tid,
                                        slab_elems=r * c, sigma=shape.w_sigma, stream=stream)
                 self.w[name] = t
+            elif self.wdtype == damoe.W_MXFP4:
+                q = torch.empty((E, r, c // 2), dtype=torch.uint8, device=device)
+                s = torch.empty((E, r, c // 32), dtype=torch.uint8, device=device)
+                synth.fill_mxfp4_device(q.data_ptr(), s.data_ptr(), r, c, E, seed=shape.weight_seed, tensor=tid,
+                                        sigma=shape.w_sigma, stream=stream)
+                self.w[name], self.s[name] = q, s
             else:
                 q = torch.empty((E, r, c), dtype=torch.uint8, device=device)
                 s = torch.empty((E, r // 128, c // 128), dtype=torch.float32, device=device)
@@ -53,6 +59,8 @@ class DeviceLayer:
         sh = self.shape
         if self.wdtype == damoe.W_BF16:
             return 3 * sh.H * sh.I * 2
+        if self.wdtype == damoe.W_MXFP4:
+            return 3 * sh.H * sh.I // 2 + 3 * sh.H * sh.I // 32
         return 3 * sh.H * sh.I + 3 * (sh.H // 128) * (sh.I // 128) * 4
 
 

@@ -72,6 +72,12 @@ def lib() -> ctypes.CDLL:
         L.synth_fill_fp8_b128_host.restype = ctypes.c_int
         L.synth_fill_fp8_b128_device.argtypes = [vp, vp, u32, u32, u32, u32, u64, u32, f32, vp]
         L.synth_fill_fp8_b128_device.restype = ctypes.c_int
+        L.synth_fill_mxfp4_host.argtypes = [vp, vp, u32, u32, u32, u32, u64, u32, f32]
+        L.synth_fill_mxfp4_host.restype = ctypes.c_int
+        L.synth_fill_mxfp4_device.argtypes = [vp, vp, u32, u32, u32, u32, u64, u32, f32, vp]
+        L.synth_fill_mxfp4_device.restype = ctypes.c_int
+        L.synth_mxfp4_quantize_host.argtypes = [vp, u64, vp, vp]
+        L.synth_mxfp4_quantize_host.restype = None
         _lib = L
     return _lib
 
@@ -125,6 +131,38 @@ def fill_fp8_device(q_ptr: int, s_ptr: int, rows: int, cols: int, n_slabs: int, 
                                           ctypes.c_void_p(stream))
     if rc != 0:
         raise RuntimeError(f"synth_fill_fp8_b128_device failed with code {rc}")
+
+
+def fill_mxfp4_host(rows: int, cols: int, n_slabs: int, *, seed: int, tensor: int, slab0: int = 0,
+                    sigma: float = 0.02):
+    """MXFP4 quantisation of the generator's bf16 values: packed e2m1 codes
+    [n_slabs][rows][cols / 2] and E8M0 scales [n_slabs][rows][cols / 32] (uint8)."""
+    q = np.empty((n_slabs, rows, cols // 2), dtype=np.uint8)
+    s = np.empty((n_slabs, rows, cols // 32), dtype=np.uint8)
+    rc = lib().synth_fill_mxfp4_host(q.ctypes.data, s.ctypes.data, rows, cols, slab0, n_slabs, int(seed),
+                                     int(tensor), ih_scale(sigma))
+    if rc != 0:
+        raise ValueError("MXFP4 fill needs cols divisible by 32")
+    return q, s
+
+
+def mxfp4_quantize(w) -> tuple:
+    """MXFP4 quantisation of float32 values in blocks of 32: (packed codes [n/2], E8M0 [n/32])."""
+    w = np.ascontiguousarray(np.asarray(w, np.float32).ravel())
+    if w.size % 32:
+        raise ValueError("blocks of 32")
+    q = np.empty(w.size // 2, np.uint8)
+    s = np.empty(w.size // 32, np.uint8)
+    lib().synth_mxfp4_quantize_host(w.ctypes.data, w.size // 32, q.ctypes.data, s.ctypes.data)
+    return q, s
+
+
+def fill_mxfp4_device(q_ptr: int, s_ptr: int, rows: int, cols: int, n_slabs: int, *, seed: int, tensor: int,
+                      slab0: int = 0, sigma: float = 0.02, stream: int = 0) -> None:
+    rc = lib().synth_fill_mxfp4_device(ctypes.c_void_p(q_ptr), ctypes.c_void_p(s_ptr), rows, cols, slab0, n_slabs,
+                                       int(seed), int(tensor), ih_scale(sigma), ctypes.c_void_p(stream))
+    if rc != 0:
+        raise RuntimeError(f"synth_fill_mxfp4_device failed with code {rc}")
 
 
 # ----------------------------------------------------------------------------------------------
@@ -233,7 +271,7 @@ class Shape:
     H: int
     I: int
     shape_id: int          # seeds the weights
-    wdtype: str = "bf16"   # "bf16" or "fp8"
+    wdtype: str = "bf16"   # "bf16", "fp8" or "mxfp4"
     w_sigma: float = 0.02
 
     @property
@@ -244,6 +282,7 @@ class Shape:
 TINY = Shape("tiny", E=8, k=2, H=256, I=512, shape_id=0)
 DS = Shape("dsv3", E=256, k=8, H=7168, I=2048, shape_id=1)
 DS_FP8 = Shape("dsv3-fp8", E=256, k=8, H=7168, I=2048, shape_id=1, wdtype="fp8")
+DS_MXFP4 = Shape("dsv3-mxfp4", E=256, k=8, H=7168, I=2048, shape_id=1, wdtype="mxfp4")
 KIMI = Shape("kimi-k2", E=384, k=8, H=7168, I=2048, shape_id=3)
 # One expert-parallel rank's layer of DeepSeek-V3 at EP = 2, 4, 8 (weights of its own experts).
 DS_EP = {ep: Shape(f"dsv3-ep{ep}", E=256 // ep, k=8, H=7168, I=2048, shape_id=1) for ep in (2, 4, 8)}
@@ -270,6 +309,16 @@ def expert_weights_host(shape: Shape, e: int, out=None):
     return tuple(res)
 
 
+def expert_weights_mxfp4_host(shape: Shape, e: int):
+    """MXFP4 weights of expert e: ((q1, s1), (q3, s3), (q2, s2)), codes and E8M0 scales."""
+    out = []
+    for name in ("w1", "w3", "w2"):
+        tid, r, c = weight_dims(shape, name)
+        q, s = fill_mxfp4_host(r, c, 1, seed=shape.weight_seed, tensor=tid, slab0=e, sigma=shape.w_sigma)
+        out.append((q[0], s[0]))
+    return tuple(out)
+
+
 class ExpertWeightSource:
     """Callable e -> expert e's host weights, refilling one set of buffers."""
 
@@ -280,6 +329,8 @@ class ExpertWeightSource:
     def __call__(self, e: int):
         if self.shape.wdtype == "fp8":
             return expert_weights_fp8_host(self.shape, e)
+        if self.shape.wdtype == "mxfp4":
+            return expert_weights_mxfp4_host(self.shape, e)
         self.buf = expert_weights_host(self.shape, e, self.buf)
         return self.buf
 

@@ -107,6 +107,77 @@ __host__ __device__ inline uint8_t f32_to_e4m3_rne_sat(float f) {
   return (uint8_t)(sign | q);
 }
 
+// OCP MX FP4 (e2m1) code of a = |v| / X with round-to-nearest-even onto the magnitudes
+// {0, 0.5, 1, 1.5, 2, 3, 4, 6} (ties to the code with an even mantissa bit) and saturation at
+// 6; the sign goes to bit 3.  Exact comparisons, so the host and device agree.
+__host__ __device__ inline uint8_t e2m1_rne_sat(float v) {
+  uint32_t u;
+  memcpy(&u, &v, 4);
+  const uint32_t ua = u & 0x7FFFFFFFu;
+  float a;
+  memcpy(&a, &ua, 4);
+  uint8_t c;
+  if (a <= 0.25f) c = 0;
+  else if (a < 0.75f) c = 1;
+  else if (a <= 1.25f) c = 2;
+  else if (a < 1.75f) c = 3;
+  else if (a <= 2.5f) c = 4;
+  else if (a < 3.5f) c = 5;
+  else if (a <= 5.0f) c = 6;
+  else c = 7;
+  return (uint8_t)(c | ((u >> 31) ? 8u : 0u));
+}
+
+// One MXFP4 block: 32 consecutive values of a weight row -> 16 packed bytes (even element in
+// the low nibble) and its E8M0 scale, X = 2^(floor(log2 amax) - 2) (the largest e2m1
+// magnitude is 6 = 1.5 * 2^2); an all-zero block takes X = 1.
+__host__ __device__ inline uint8_t mxfp4_block(const float* w, uint8_t* q16) {
+  float amax = 0.f;
+  for (int i = 0; i < 32; ++i) {
+    const float a = w[i] < 0.f ? -w[i] : w[i];
+    amax = a > amax ? a : amax;
+  }
+  int e = 0;
+  if (amax > 0.f) {
+    uint32_t u;
+    memcpy(&u, &amax, 4);
+    const int be = (int)((u >> 23) & 255u);
+    e = be == 0 ? -127 : be - 127;  // bf16 inputs of this generator are normal
+    e -= 2;
+    if (e < -127) e = -127;
+    if (e > 127) e = 127;
+  }
+  // 1 / X = 2^-e exactly, from its bits (e in [-127, 127]: 2^127 down to 2^-127).
+  const uint32_t ib = (127 - e) >= 1 ? (uint32_t)(127 - e) << 23 : 0x00400000u;
+  float inv;
+  memcpy(&inv, &ib, 4);
+  for (int i = 0; i < 16; ++i)
+    q16[i] = (uint8_t)(e2m1_rne_sat(w[2 * i] * inv) | (e2m1_rne_sat(w[2 * i + 1] * inv) << 4));
+  return (uint8_t)(e + 127);
+}
+
+// One thread per MXFP4 block of n_slabs [rows][cols] slabs: q [slab][rows][cols / 2],
+// s [slab][rows][cols / 32].
+__global__ void __launch_bounds__(256) k_fill_mxfp4(uint8_t* __restrict__ q, uint8_t* __restrict__ s, uint32_t rows,
+                                                    uint32_t cols, uint32_t slab0, uint32_t n_slabs, uint64_t seed,
+                                                    uint32_t tensor, float scale) {
+  const uint64_t nb = (uint64_t)n_slabs * rows * (cols / 32);
+  for (uint64_t b = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (uint64_t)gridDim.x * blockDim.x) {
+    const uint64_t per_slab = (uint64_t)rows * (cols / 32);
+    const uint32_t sl = (uint32_t)(b / per_slab);
+    const uint64_t rem = b % per_slab;
+    const uint32_t r = (uint32_t)(rem / (cols / 32)), cb = (uint32_t)(rem % (cols / 32));
+    float w[32];
+    for (int i = 0; i < 32; ++i)
+      w[i] = bf16_to_f32(synth_bf16(seed, tensor, slab0 + sl, (uint64_t)r * cols + cb * 32 + i, scale));
+    uint8_t q16[16];
+    const uint8_t sc = mxfp4_block(w, q16);
+    uint8_t* dst = q + (uint64_t)sl * rows * (cols / 2) + (uint64_t)r * (cols / 2) + cb * 16;
+    for (int i = 0; i < 16; ++i) dst[i] = q16[i];
+    s[b] = sc;
+  }
+}
+
 __global__ void __launch_bounds__(256) k_fill_bf16(uint16_t* __restrict__ out, uint64_t n,
                                                    uint64_t start, uint64_t slab_elems,
                                                    uint32_t slab0, uint64_t seed, uint32_t tensor,
@@ -227,6 +298,43 @@ int synth_fill_bf16_device(uint16_t* out, uint64_t n, uint64_t start, uint64_t s
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(k_fill_bf16, dim3((unsigned)blocks), dim3(256), 0, stream, out, n, start,
                      slab_elems, slab0, seed, tensor, scale);
+  return (int)hipGetLastError();
+}
+
+// MXFP4 fill of n_slabs consecutive [rows][cols] slabs from the bf16 values of the same
+// generator: q [n_slabs][rows][cols / 2] packed e2m1 codes, s [n_slabs][rows][cols / 32] E8M0.
+int synth_fill_mxfp4_host(uint8_t* q, uint8_t* s, uint32_t rows, uint32_t cols, uint32_t slab0,
+                          uint32_t n_slabs, uint64_t seed, uint32_t tensor, float scale) {
+  if (cols % 32) return -1;
+  const uint64_t per_slab = (uint64_t)rows * (cols / 32);
+  parallel_for((uint64_t)n_slabs * per_slab, [&](uint64_t b0, uint64_t b1) {
+    float w[32];
+    for (uint64_t b = b0; b < b1; ++b) {
+      const uint32_t sl = (uint32_t)(b / per_slab);
+      const uint64_t rem = b % per_slab;
+      const uint32_t r = (uint32_t)(rem / (cols / 32)), cb = (uint32_t)(rem % (cols / 32));
+      for (int i = 0; i < 32; ++i)
+        w[i] = bf16_to_f32(synth_bf16(seed, tensor, slab0 + sl, (uint64_t)r * cols + cb * 32 + i, scale));
+      s[b] = mxfp4_block(w, q + (uint64_t)sl * rows * (cols / 2) + (uint64_t)r * (cols / 2) + cb * 16);
+    }
+  });
+  return 0;
+}
+
+// MXFP4 quantisation of n_blocks blocks of 32 given values (exported for tests).
+void synth_mxfp4_quantize_host(const float* w, uint64_t n_blocks, uint8_t* q, uint8_t* s) {
+  for (uint64_t b = 0; b < n_blocks; ++b) s[b] = mxfp4_block(w + 32 * b, q + 16 * b);
+}
+
+int synth_fill_mxfp4_device(uint8_t* q, uint8_t* s, uint32_t rows, uint32_t cols, uint32_t slab0,
+                            uint32_t n_slabs, uint64_t seed, uint32_t tensor, float scale, hipStream_t stream) {
+  if (cols % 32) return -1;
+  const uint64_t nb = (uint64_t)n_slabs * rows * (cols / 32);
+  if (nb == 0) return 0;
+  uint64_t blocks = (nb + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(k_fill_mxfp4, dim3((unsigned)blocks), dim3(256), 0, stream, q, s, rows, cols, slab0, n_slabs,
+                     seed, tensor, scale);
   return (int)hipGetLastError();
 }
 

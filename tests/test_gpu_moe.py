@@ -235,3 +235,103 @@ def test_ds_prefill_fp8(ds_fp8, T, alpha):
         log(f"ds fp8 prefill T={T} alpha={alpha} variant={damoe.variant_name(v)}")
         _run(path, r, 200 + T, v)
         assert row_err(bf16_rows(path.y, rows), ref) <= TOL["fp8"]
+
+
+SMALL_MXFP4 = synth.Shape("small-mxfp4", E=8, k=2, H=512, I=1024, shape_id=6, wdtype="mxfp4")
+
+
+def _stream_variants(wdtype):
+    return [v for v in range(damoe.num_variants()) if damoe.variant_supports(v, wdtype)]
+
+
+@pytest.fixture(scope="module")
+def small_mxfp4():
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    dl = DeviceLayer(SMALL_MXFP4, packed=True)
+    yield dl, Path(dl, 512), synth.ExpertWeightSource(SMALL_MXFP4)
+    torch.cuda.empty_cache()
+
+
+def test_mxfp4_device_fill_equals_host_fill(small_mxfp4):
+    # The row-major fill before packing: regenerate one expert on the device and on the host.
+    torch = torch_cuda()
+    sh = SMALL_MXFP4
+    for name in ("w1", "w2"):
+        tid, r, c = synth.weight_dims(sh, name)
+        q = torch.empty((2, r, c // 2), dtype=torch.uint8, device="cuda")
+        s = torch.empty((2, r, c // 32), dtype=torch.uint8, device="cuda")
+        synth.fill_mxfp4_device(q.data_ptr(), s.data_ptr(), r, c, 2, seed=sh.weight_seed, tensor=tid, slab0=3,
+                                sigma=sh.w_sigma, stream=torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        qh, sh_ = synth.fill_mxfp4_host(r, c, 2, seed=sh.weight_seed, tensor=tid, slab0=3, sigma=sh.w_sigma)
+        np.testing.assert_array_equal(q.cpu().numpy(), qh)
+        np.testing.assert_array_equal(s.cpu().numpy(), sh_)
+
+
+@pytest.mark.parametrize("T,alpha,seed", [(64, 1.0, 7), (300, 0.05, 8), (3, 10.0, 9), (1, 1.0, 10)])
+def test_small_mxfp4_every_stream_variant(small_mxfp4, T, alpha, seed):
+    dl, path, src = small_mxfp4
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, alpha, [seed])
+    rows = np.arange(T) if T <= 64 else np.sort(np.random.default_rng(T).choice(T, 48, replace=False))
+    ref = oracle_rows(sh, r, seed, rows, src)
+    variants = _stream_variants(damoe.W_MXFP4)
+    assert len(variants) >= 5 and not damoe.variant_supports(damoe.num_variants() - 1, damoe.W_MXFP4)
+    for v in variants:
+        log(f"small mxfp4 T={T} alpha={alpha} variant={damoe.variant_name(v)}")
+        _run(path, r, seed, v)
+        err = row_err(bf16_rows(path.y, rows), ref)
+        assert err <= TOL["bf16"], (v, err)
+
+
+def test_mxfp4_rejects_other_kernel_classes(small_mxfp4):
+    # Host: a forced tiled or big variant is unsupported.  Device: a dispatched id of another
+    # class runs nothing and sets the sticky error.
+    torch = torch_cuda()
+    dl, path, _ = small_mxfp4
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, 64, 1.0, [11])
+    path.set_routing(r)
+    path.fill_x(64, 11)
+    path.route(64)
+    for v in range(damoe.num_variants()):
+        if not damoe.variant_supports(v, damoe.W_MXFP4):
+            with pytest.raises(damoe.DamoeError) as ei:
+                path.fused(64, v)
+            assert ei.value.code == -2
+    q = np.full((1, sh.E), 1000, np.int32)
+    td = damoe.TableData(E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=damoe.W_MXFP4, bucket_T=np.array([1 << 20]),
+                         n_ex=np.array([1]), Q=q, kid=np.array([6]), noda=np.array([0]))
+    table = damoe.Table.create(td)
+    path.route_dispatch(table, 64)
+    path.candidates = 0b1100001  # the tiled id plus two stream variants
+    path.fused(64, -1)
+    torch.cuda.synchronize()
+    assert int(path.variant.item()) == 6
+    assert damoe.read_device_error(path.ws) == damoe.DEVERR_VARIANT
+
+
+@pytest.fixture(scope="module")
+def ds_mxfp4():
+    torch = torch_cuda()
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+    log("filling DeepSeek-V3-shaped MXFP4 layer (5.9 GB)")
+    dl = DeviceLayer(synth.DS_MXFP4)
+    torch.cuda.synchronize()
+    yield dl, Path(dl, 128), synth.ExpertWeightSource(synth.DS_MXFP4)
+    del dl
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("T,alpha", [(1, 0.3), (32, 1.0), (128, 0.05)])
+def test_ds_mxfp4_decode(ds_mxfp4, T, alpha):
+    dl, path, src = ds_mxfp4
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, T, alpha, synth.seed_decode(T, alpha, 0))
+    rows = np.arange(T) if T <= 2 else np.sort(np.random.default_rng(T).choice(T, 3, replace=False))
+    ref = oracle_rows(sh, r, 400 + T, rows, src)
+    for v in _stream_variants(damoe.W_MXFP4):
+        log(f"ds mxfp4 T={T} alpha={alpha} variant={damoe.variant_name(v)}")
+        _run(path, r, 400 + T, v)
+        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["bf16"]

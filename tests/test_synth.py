@@ -125,3 +125,38 @@ def test_routing_repeated_groups():
     eff = [oracle.effexp(oracle.histogram(synth.routing_repeated(256, 8, 256, f, 1.0, [5, 256, f, 0]).ids,
                                           256))[2] for f in (0, 10, 50, 100)]
     assert eff[0] > eff[1] > eff[2] > eff[3] == 8.0
+
+
+def test_mxfp4_quantizer():
+    # Scale: X = 2^(floor(log2 amax) - 2); codes: round-to-nearest-even onto the e2m1 grid
+    # (ties to an even mantissa bit), saturating at 6; the even element in the low nibble.
+    import oracle
+    oracle.build()
+    grid = np.array([0, 0.5, 1, 1.5, 2, 3, 4, 6])
+    w = np.zeros(32, np.float32)
+    w[0] = 7.9         # amax: floor(log2 7.9) = 2 -> X = 1, 7.9 saturates to 6
+    w[1:8] = [0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0]   # ties -> 0, 1, 1, 2, 2, 4, 4
+    w[8:12] = [-0.26, -0.74, 1.26, -5.01]              # just past ties -> -0.5, -0.5, 1.5, -6
+    q, s = synth.mxfp4_quantize(w)
+    assert s[0] == 127
+    codes = np.stack([q & 15, q >> 4], axis=1).ravel()
+    dec = np.array([oracle.mxfp4_value(int(c), int(s[0])) for c in codes])
+    np.testing.assert_array_equal(dec[:12], [6, 0, 1, 1, 2, 2, 4, 4, -0.5, -0.5, 1.5, -6])
+    # A block scaled by 2^-9 gets X 2^-9 smaller and the same codes; an all-zero block X = 1.
+    q2, s2 = synth.mxfp4_quantize(w * np.float32(2.0 ** -9))
+    assert s2[0] == 127 - 9 and np.array_equal(q2, q)
+    q3, s3 = synth.mxfp4_quantize(np.zeros(32, np.float32))
+    assert s3[0] == 127 and not q3.any()
+    # Round trip on generator values: within half a grid step (at most X) unless the value
+    # saturates (amax < 8 X, so at most 2 X), and so within half the block's amax.
+    rng = np.random.default_rng(9)
+    v = rng.normal(0, 0.02, 32 * 50).astype(np.float32)
+    q, s = synth.mxfp4_quantize(v)
+    codes = np.stack([q & 15, q >> 4], axis=1).ravel()
+    dec = np.array([oracle.mxfp4_value(int(c), int(s[i // 32])) for i, c in enumerate(codes)])
+    X = 2.0 ** (s.astype(np.float64) - 127)
+    err = np.abs(dec - v)
+    sat = np.abs(v) > 6 * np.repeat(X, 32)
+    assert np.all(err[~sat] <= np.repeat(X, 32)[~sat] + 1e-12)
+    assert np.all(err <= 2 * np.repeat(X, 32) + 1e-12)
+    assert np.all(err <= np.repeat(np.abs(v.reshape(-1, 32)).max(axis=1), 32) * 0.5 + 1e-12)
