@@ -925,6 +925,8 @@ def main():
     ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router", "imbalance", "ep"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
+    ap.add_argument("--wdtype", choices=["bf16", "mxfp4"], default="bf16",
+                    help="decode sweep: expert weight format (activations and MFMA stay bf16)")
     ap.add_argument("--dispatch-reps", type=int, default=200)
     ap.add_argument("--trace-steps", type=int, default=1000)
     ap.add_argument("--trace-reps", type=int, default=3)
@@ -964,11 +966,13 @@ def main():
     if args.workload == "ep":
         return run_ep(args)
 
-    shape = synth.DS
-    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    shape = synth.DS_MXFP4 if args.wdtype == "mxfp4" else synth.DS
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, {args.wdtype})")
     dl = DeviceLayer(shape)
     path = Path(dl, max(DECODE_T))
     points = [(T, a) for T in DECODE_T for a in DECODE_ALPHA]
+    # HBM bytes of one weight element: bf16 2; MXFP4 half a byte of code + 1/32 of a scale byte.
+    wbytes = 17.0 / 32.0 if args.wdtype == "mxfp4" else 2.0
     dev = "cuda"
     ids_d, w_d, U = {}, {}, {}
     for (T, a) in points:
@@ -1031,7 +1035,7 @@ def main():
         g1 = e[1].elapsed_time(e[2])
         g2 = e[2].elapsed_time(e[3])
         rec[T, a].append((path_ms, g1, g2, e[0].elapsed_time(e[1]), e[3].elapsed_time(e[4])))
-        g1_bytes += U[T, a, rep] * 2 * shape.I * shape.H * 2 + T * shape.H * 2
+        g1_bytes += U[T, a, rep] * 2 * shape.I * shape.H * wbytes + T * shape.H * 2
         g1_ms += g1
 
     per_point = {}
@@ -1062,13 +1066,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "dsv3-decode-sweep: E=256 top-8 H=7168 I=2048 bf16, T in {1,8,32,128} x "
-                               "Dirichlet alpha in {0.05,0.3,1,10}, adaptive dispatch"
+        "config": {"workload": f"dsv3-decode-sweep: E=256 top-8 H=7168 I=2048 {args.wdtype} weights, T in "
+                               "{1,8,32,128} x Dirichlet alpha in {0.05,0.3,1,10}, adaptive dispatch"
                                + ("" if force < 0 else f" (forced variant {damoe.variant_name(force)})"),
                    "points": len(points), "table": table_note},
         "roofline": {"bound": "hbm", "kernel": "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(),
+                     "traffic": measured_traffic() if args.wdtype == "bf16" else None,
                      "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1))},
         "per_point": per_point,
     }

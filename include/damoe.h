@@ -77,10 +77,18 @@ typedef enum damoe_wdtype {
   DAMOE_W_FP8_B128 = 1, /* OCP e4m3fn weights, one fp32 scale per 128x128 block         */
   DAMOE_W_MXFP4 = 2     /* OCP MXFP4: e2m1 codes, two per byte (even column in the low
                            nibble), one E8M0 scale byte 2^(s - 127) per 32 columns of a
-                           row; the s1, s3, s2 pointers carry the uint8 scale arrays
-                           [E][rows][cols / 32], row-major in both layouts.  The fused
-                           layer needs the fragment-packed layout and runs the stream
-                           variants only (damoe_variant_supports)                     */
+                           row.  Row-major: w* hold the codes [E][rows][cols / 2] and
+                           s1, s3, s2 the uint8 scales [E][rows][cols / 32].  Packed:
+                           each 16-row x 128-column quad fragment (rb, kq) is 1088
+                           bytes at (e (rows / 16) + rb) (cols / 128) + kq: 1024 code
+                           bytes, lane l's 16 at 16 l (its 4 bytes, columns
+                           8 (l / 16) .. + 7, of 32-column blocks 4 kq .. + 3), then
+                           the 16 rows' scales, row rb 16 + i's four bytes at
+                           1024 + 4 i; a slab is rows cols 17 / 32 bytes and s1, s3,
+                           s2 are ignored (may be NULL).  The fused layer needs the
+                           packed layout, H and I multiples of 512, and runs the
+                           stream variants with token tiles of at most 32 rows
+                           (damoe_variant_supports)                                    */
 } damoe_wdtype;
 
 /* Weight layouts.  Row-major is the interchange layout; the fragment-packed
@@ -289,9 +297,11 @@ damoe_status damoe_fused_moe_stage(const damoe_layer* layer /* host */, int32_t 
                                    hipStream_t stream);
 
 /* Converts the row-major weights of `src` (layout must be DAMOE_LAYOUT_ROWMAJOR)
- * into the fragment-packed layout, written to w1, w3, w2 (device buffers of the
- * same sizes, not overlapping the sources).  Scales are not touched.  A layer
- * descriptor with layout = DAMOE_LAYOUT_FRAG16 and these pointers then runs the
+ * into the fragment-packed layout, written to w1, w3, w2 (disjoint device
+ * buffers, overlapping no source).  bf16 and fp8: buffers of the sources' sizes;
+ * fp8 scales are not touched.  MXFP4: buffers of E rows cols 17 / 32 bytes that
+ * receive codes and scales together.  A layer descriptor with layout =
+ * DAMOE_LAYOUT_FRAG16 and these pointers (plus the fp8 scales) then runs the
  * same computation.  Stream-ordered. */
 damoe_status damoe_pack_weights(const damoe_layer* src /* host */, void* w1, void* w3, void* w2,
                                 hipStream_t stream);

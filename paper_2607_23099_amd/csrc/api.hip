@@ -62,7 +62,9 @@ damoe_status check_layer(const damoe_layer* L) {
     return DAMOE_OK;
   }
   if (L->wdtype == DAMOE_W_MXFP4) {
-    if (!L->s1 || !L->s3 || !L->s2) return DAMOE_ERR_INVALID_ARG;
+    // Packed MXFP4 carries its scales inside the quad fragments.
+    if (L->layout == DAMOE_LAYOUT_ROWMAJOR && (!L->s1 || !L->s3 || !L->s2)) return DAMOE_ERR_INVALID_ARG;
+    if (L->H % 512 || L->I % 512) return DAMOE_ERR_UNSUPPORTED;  // whole 128-column quads per wave
     return DAMOE_OK;
   }
   return DAMOE_ERR_UNSUPPORTED;
@@ -162,7 +164,7 @@ int32_t damoe_variant_tile_m(int32_t v) {
 
 int32_t damoe_variant_supports(int32_t v, int32_t wdtype) {
   if (v < 0 || v >= num_variants()) return 0;
-  if (wdtype == DAMOE_W_MXFP4) return variant(v).kind == kStream;  // the weight-streaming family
+  if (wdtype == DAMOE_W_MXFP4) return variant(v).kind == kStream && variant(v).bm <= kFp4MaxBM;
   return wdtype == DAMOE_W_BF16 || wdtype == DAMOE_W_FP8_B128;
 }
 
@@ -422,21 +424,31 @@ damoe_status damoe_pack_weights(const damoe_layer* L, void* w1, void* w3, void* 
   const damoe_status st = check_layer(L);
   if (st != DAMOE_OK) return st;
   if (L->layout != DAMOE_LAYOUT_ROWMAJOR || !w1 || !w3 || !w2) return DAMOE_ERR_INVALID_ARG;
-  // Element bytes for the packer; 0 = MXFP4 codes (half a byte each; the scales keep their
-  // row-major layout).
-  const int eb = L->wdtype == DAMOE_W_FP8_B128 ? 1 : L->wdtype == DAMOE_W_MXFP4 ? 0 : 2;
-  const size_t bytes = eb ? (size_t)L->E * L->H * L->I * eb : (size_t)L->E * L->H * L->I / 2;
-  const void* src[3] = {L->w1, L->w3, L->w2};
+  // Element bytes for the packer; 0 = MXFP4 (codes, half a byte each, packed together with
+  // their scale bytes: 17/32 byte per weight on both sides).  fp8 scales are not touched.
+  const bool fp4 = L->wdtype == DAMOE_W_MXFP4;
+  const int eb = L->wdtype == DAMOE_W_FP8_B128 ? 1 : fp4 ? 0 : 2;
+  const size_t n = (size_t)L->E * L->H * L->I;
+  const size_t bytes = eb ? n * eb : n / 2;
+  const size_t dst_bytes = eb ? bytes : n / 32 * 17;
+  const void* src[6] = {L->w1, L->w3, L->w2, L->s1, L->s3, L->s2};
+  const size_t src_bytes[6] = {bytes, bytes, bytes, n / 32, n / 32, n / 32};
   void* dst[3] = {w1, w3, w2};
-  for (int m = 0; m < 3; ++m)
-    for (int n = 0; n < 3; ++n) {  // no destination may overlap any source
-      const char* s0 = static_cast<const char*>(src[n]);
-      const char* d0 = static_cast<const char*>(dst[m]);
-      if (d0 < s0 + bytes && s0 < d0 + bytes) return DAMOE_ERR_INVALID_ARG;
+  for (int m = 0; m < 3; ++m) {
+    for (int j = m + 1; j < 3; ++j) {  // destinations are disjoint
+      const char* a0 = static_cast<const char*>(dst[m]);
+      const char* b0 = static_cast<const char*>(dst[j]);
+      if (a0 < b0 + dst_bytes && b0 < a0 + dst_bytes) return DAMOE_ERR_INVALID_ARG;
     }
-  if (launch_pack(L->w1, w1, L->E, L->I, L->H, eb, stream) != hipSuccess ||
-      launch_pack(L->w3, w3, L->E, L->I, L->H, eb, stream) != hipSuccess ||
-      launch_pack(L->w2, w2, L->E, L->H, L->I, eb, stream) != hipSuccess)
+    for (int j = 0; j < (fp4 ? 6 : 3); ++j) {  // and overlap no source
+      const char* s0 = static_cast<const char*>(src[j]);
+      const char* d0 = static_cast<const char*>(dst[m]);
+      if (d0 < s0 + src_bytes[j] && s0 < d0 + dst_bytes) return DAMOE_ERR_INVALID_ARG;
+    }
+  }
+  if (launch_pack(L->w1, w1, L->E, L->I, L->H, eb, stream, fp4 ? L->s1 : nullptr) != hipSuccess ||
+      launch_pack(L->w3, w3, L->E, L->I, L->H, eb, stream, fp4 ? L->s3 : nullptr) != hipSuccess ||
+      launch_pack(L->w2, w2, L->E, L->H, L->I, eb, stream, fp4 ? L->s2 : nullptr) != hipSuccess)
     return DAMOE_ERR_HIP;
   return DAMOE_OK;
 }

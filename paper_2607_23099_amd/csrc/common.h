@@ -33,6 +33,11 @@ enum VariantKind : int32_t {
 // Id of the big-tile variant (its kernel is launched separately from the others).
 constexpr int32_t kBigVariant = 7;
 
+// Largest token tile of the MXFP4 stream kernel.
+constexpr int32_t kFp4MaxBM = 32;
+// Bytes of one packed MXFP4 quad fragment: 16 rows x 128 columns of codes, then their scales.
+constexpr uint32_t kFp4QuadBytes = 1024 + 64;
+
 struct VariantDesc {
   const char* name;
   int32_t kind;
@@ -71,7 +76,7 @@ struct GemmArgs {
   int32_t K;           // reduction length: H for GEMM1, I for GEMM2
   int32_t N;           // output features: I for GEMM1, H for GEMM2
   int32_t fp8;
-  int32_t fp4;         // MXFP4 weights: wa / wb packed e2m1 codes, sa / sb E8M0 scales [E][N][K / 32]
+  int32_t fp4;         // MXFP4 weights: wa / wb quad fragments of e2m1 codes and E8M0 scales
   int32_t packed;      // weights in the fragment-packed layout
 };
 
@@ -108,8 +113,9 @@ hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t big_set_lds_limits();
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream);
 hipError_t gemm_set_lds_limits();
+// elem_bytes 0: MXFP4 codes, packed with their row-major E8M0 `scales` into quad fragments.
 hipError_t launch_pack(const void* src, void* dst, int32_t slabs, int32_t rows, int32_t cols, int32_t elem_bytes,
-                       hipStream_t stream);
+                       hipStream_t stream, const void* scales = nullptr);
 
 // Dynamic LDS bytes the GEMM kernels are launched with.
 size_t gemm_lds_bytes();

@@ -32,6 +32,48 @@ namespace {
 constexpr int LDS_PAD = 1;
 
 
+// The 4 waves' partial tiles of a stream item -> LDS (rows = output features, columns =
+// tokens), summed in wave order, then the SwiGLU epilogue (GEMM1, bf16 h) or the fp32 output
+// (GEMM2) of the tile's valid rows.
+template <int BM, int BN, bool GLU, int NR, int NX>
+__device__ __forceinline__ void stream_finish(const GemmArgs& a, float* __restrict__ red, const floatx4 (&acc)[NR][NX],
+                                              int p0, int rows, int fb) {
+  constexpr int LDR = BM + LDS_PAD;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int N = a.N;
+  // Partial tiles of the 4 waves -> LDS, rows = output features, columns = tokens.
+#pragma unroll
+  for (int b = 0; b < NR; ++b)
+#pragma unroll
+    for (int s = 0; s < NX; ++s)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        red[(wave * NR * 16 + b * 16 + 4 * (lane >> 4) + r) * LDR + s * 16 + (lane & 15)] = acc[b][s][r];
+  __syncthreads();
+
+  for (int idx = threadIdx.x; idx < BN * BM; idx += kGemmThreads) {
+    const int f = idx % BN, i = idx / BN;
+    if (i < rows) {
+      if (GLU) {
+        float g = 0.f, u = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          g += red[(w * NR * 16 + f) * LDR + i];
+          u += red[(w * NR * 16 + BN + f) * LDR + i];
+        }
+        const float hval = g / (1.0f + __expf(-g)) * u;
+        reinterpret_cast<uint16_t*>(a.out)[(size_t)(p0 + i) * N + fb * BN + f] = f32_to_bf16(hval);
+      } else {
+        float o = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) o += red[(w * NR * 16 + f) * LDR + i];
+        reinterpret_cast<float*>(a.out)[(size_t)(p0 + i) * N + fb * BN + f] = o;
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // IL: the waves take interleaved 32-wide k-steps (wave w reads k-steps w, w+4, ...), so the
 //     4 waves of a workgroup read 256 contiguous bytes of every weight row at a time;
 //     otherwise each wave reads one contiguous quarter of the row.
@@ -39,18 +81,12 @@ constexpr int LDS_PAD = 1;
 // D:  register-ring depth, k-steps in flight per wave.
 // PK: weights in the fragment-packed layout (block (rb, kb) of 16 rows x 32 columns is one
 //     contiguous 64-lane fragment); otherwise row-major.
-// FP4: MXFP4 weights (fragment-packed only): a lane's 8 e2m1 codes are 4 bytes of its
-//     fragment, its row's E8M0 scale of the k-step one byte of the row-major scale array; a
-//     k-step moves a quarter of the bf16 bytes, so the ring is twice as deep.
-template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D0, bool PK, bool FP4 = false>
+template <int BM, int BN, bool GLU, bool FP8, bool IL, bool NT, int D, bool PK>
 __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __restrict__ list,
                                             float* __restrict__ red) {
-  static_assert(!FP4 || (PK && !FP8), "MXFP4 weights are fragment-packed");
-  constexpr int D = FP4 ? 2 * D0 : D0;
   constexpr int NX = BM / 16;
   constexpr int NR = (GLU ? 2 : 1) * BN / 16;
-  constexpr int LDR = BM + LDS_PAD;
-  using WT = typename std::conditional<FP4, uint32_t, typename WFrag<FP8>::T>::type;
+  using WT = typename WFrag<FP8>::T;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n_tiles = list[0];
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
@@ -95,7 +131,7 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
       }
     }
     // Weight operand: rows f of W1 (gate) and W3 (up) for GEMM1, of W2 for GEMM2.
-    const size_t slab = FP4 ? (size_t)N * K / 2 : (size_t)N * K * EB;
+    const size_t slab = (size_t)N * K * EB;
     const __amdgpu_buffer_rsrc_t ra = make_rsrc(wa + (size_t)e * slab, (uint32_t)slab);
     const __amdgpu_buffer_rsrc_t rb = make_rsrc((GLU ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
     uint32_t wo[NR];
@@ -105,24 +141,10 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
       if (PK) {
         const uint32_t rblk = (uint32_t)(fb * BN) / 16 + rb_;
         const uint32_t kb0 = IL ? wave : wave * nks;  // this wave's first 32-column block
-        wo[b] = FP4 ? ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 4u
-                    : ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 8u * EB;
+        wo[b] = ((rblk * (uint32_t)(K / 32) + kb0) * 64u + lane) * 8u * EB;
       } else {
         const int f = fb * BN + rb_ * 16 + (lane & 15);
         wo[b] = ((uint32_t)f * (uint32_t)K + kcol) * EB;
-      }
-    }
-    // MXFP4 scales: row f's E8M0 bytes, one per 32-column block (k-step), of expert e.
-    const size_t sslab = (size_t)N * (K / 32);
-    __amdgpu_buffer_rsrc_t rsa, rsb;
-    uint32_t so[NR];
-    if constexpr (FP4) {
-      rsa = make_rsrc(reinterpret_cast<const uint8_t*>(a.sa) + (size_t)e * sslab, (uint32_t)sslab);
-      rsb = make_rsrc(reinterpret_cast<const uint8_t*>(GLU ? a.sb : a.sa) + (size_t)e * sslab, (uint32_t)sslab);
-#pragma unroll
-      for (int b = 0; b < NR; ++b) {
-        const int f = fb * BN + (GLU ? (b % (NR / 2)) : b) * 16 + (lane & 15);
-        so[b] = (uint32_t)f * (uint32_t)(K / 32) + (IL ? wave : wave * nks);
       }
     }
     const float* sa = a.sa;
@@ -139,31 +161,18 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
 
     WT wf[D][NR];
     uint4 xf[D][NX];
-    uint32_t sf[FP4 ? D : 1][NR];
     auto load = [&](int ks, int st) __attribute__((always_inline)) {
-      const uint32_t sw = FP4 ? (uint32_t)ks * (KSTEP / 32) * 256u
-                              : PK ? (uint32_t)ks * (KSTEP / 32) * 512u * EB : (uint32_t)ks * KSTEP * EB;
+      const uint32_t sw = PK ? (uint32_t)ks * (KSTEP / 32) * 512u * EB : (uint32_t)ks * KSTEP * EB;
 #pragma unroll
       for (int b = 0; b < NR; ++b)
         wf[st][b] = buf_load<WT, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b], sw);
-      if constexpr (FP4) {
-#pragma unroll
-        for (int b = 0; b < NR; ++b)
-          sf[st][b] = buf_load<uint8_t, 0>((GLU && b >= NR / 2) ? rsb : rsa, so[b], (uint32_t)ks * (KSTEP / 32));
-      }
+
       const uint32_t sx = (uint32_t)ks * KSTEP * 2;
 #pragma unroll
       for (int s = 0; s < NX; ++s) xf[st][s] = buf_load<uint4, 0>(rx, xo[s], sx);
     };
     auto compute = [&](int ks, int st) __attribute__((always_inline)) {
-      if constexpr (FP4) {
-#pragma unroll
-        for (int b = 0; b < NR; ++b) {
-          const uint4 wv = fp4x8_to_bf16x8(wf[st][b], e8m0_to_f32(sf[st][b]));
-#pragma unroll
-          for (int s = 0; s < NX; ++s) acc[b][s] = mfma16x16x32(wv, xf[st][s], acc[b][s]);
-        }
-      } else if constexpr (FP8) {
+      if constexpr (FP8) {
         const int kb = (IL ? ks * 128 + wave * 32 : wave * kw + ks * 32) >> 7;
         const float s_g = sa[sbase + kb] * 0x1p120f;
         const float s_u = GLU ? sb[sbase + kb] * 0x1p120f : 0.f;
@@ -198,37 +207,125 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
     for (int d = 0; d < D - 1; ++d)
       if (ks + d < nks) compute(ks + d, d);
 
-    // Partial tiles of the 4 waves -> LDS, rows = output features, columns = tokens.
+    stream_finish<BM, BN, GLU, NR, NX>(a, red, acc, p0, rows, fb);
+  }
+}
+
+
+// MXFP4 weights, stream variants.  Quad-fragment packed layout: for row block rb and k-block
+// quad kq (4 consecutive 32-column blocks), lane l holds 16 contiguous bytes, the e2m1 codes
+// of row rb * 16 + l % 16 at columns 8 (l / 16) .. + 7 of k-blocks 4 kq .. 4 kq + 3 (4 bytes
+// each), so one 16-byte load feeds 4 MFMA k-steps and a ring slot moves as many weight bytes
+// as a bf16 one.  The 16 rows' E8M0 scales of the quad (4 bytes a row) follow its 1024 code
+// bytes, so a wave's scale load is one 64-byte segment beside the codes it scales (row-major
+// scales cost a cache line per row).  Each wave takes one contiguous quarter of K.
+template <int BM, int BN, bool GLU, bool NT, int D>
+__device__ __forceinline__ void stream_body_fp4(const GemmArgs& a, const int32_t* __restrict__ list,
+                                                float* __restrict__ red) {
+  constexpr int NX = BM / 16;
+  constexpr int NR = (GLU ? 2 : 1) * BN / 16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n_tiles = list[0];
+  const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
+  const int K = a.K, N = a.N;
+  const int n_fb = N / BN;
+  const long long n_items = (long long)n_tiles * n_fb;
+  const int kw = K >> 2;     // columns per wave
+  const int nq = kw >> 7;    // quads (4 k-steps of 32 columns) per wave
+  const int kcol = wave * kw + (lane >> 4) * 8;
+  const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
+  const uint8_t* __restrict__ wb = reinterpret_cast<const uint8_t*>(a.wb);
+
+  for (long long it = blockIdx.x; it < n_items; it += gridDim.x) {
+    const int tile = (int)(it / n_fb);
+    const int fb = (int)(it - (long long)tile * n_fb);
+    const int2 en = ent[tile];
+    const int p0 = en.x, e = en.y & 0xFFFF, rows = en.y >> 16;
+    if (p0 < 0 || rows <= 0 || rows > BM || p0 + rows > a.A || e >= a.E) {
+      if (threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
+      continue;
+    }
+    __amdgpu_buffer_rsrc_t rx;
+    uint32_t xo[NX];
+    if (GLU) rx = make_rsrc(a.x, (uint32_t)((size_t)(a.A / a.k) * K * 2));
+    else rx = make_rsrc(a.x + (size_t)p0 * K, (uint32_t)((size_t)rows * K * 2));
+#pragma unroll
+    for (int s = 0; s < NX; ++s) {
+      const int r = s * 16 + (lane & 15);
+      if (r < rows) {
+        const uint32_t row = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) : (uint32_t)r;
+        xo[s] = (row * (uint32_t)K + kcol) * 2u;
+      } else {
+        xo[s] = kOobOffset;
+      }
+    }
+    // Quad fragment f = row block * (K / 128) + quad: 1024 code bytes (lane l's 16 at 16 l), then
+    // the 16 rows' scale words (row i's four E8M0 bytes at 1024 + 4 i).
+    const size_t slab = (size_t)(N / 16) * (K / 128) * kFp4QuadBytes;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc(wa + (size_t)e * slab, (uint32_t)slab);
+    const __amdgpu_buffer_rsrc_t rb = make_rsrc((GLU ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
+    uint32_t wo[NR], so[NR];
+#pragma unroll
+    for (int b = 0; b < NR; ++b) {
+      const int rb_ = GLU ? (b % (NR / 2)) : b;
+      const uint32_t f0 = ((uint32_t)(fb * BN) / 16 + rb_) * (uint32_t)(K / 128) + (uint32_t)(wave * nq);
+      wo[b] = f0 * kFp4QuadBytes + lane * 16u;
+      so[b] = f0 * kFp4QuadBytes + 1024u + (lane & 15) * 4u;
+    }
+
+    floatx4 acc[NR][NX];
 #pragma unroll
     for (int b = 0; b < NR; ++b)
 #pragma unroll
-      for (int s = 0; s < NX; ++s)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          red[(wave * NR * 16 + b * 16 + 4 * (lane >> 4) + r) * LDR + s * 16 + (lane & 15)] = acc[b][s][r];
-    __syncthreads();
+      for (int s = 0; s < NX; ++s) acc[b][s] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    for (int idx = threadIdx.x; idx < BN * BM; idx += kGemmThreads) {
-      const int f = idx % BN, i = idx / BN;
-      if (i < rows) {
-        if (GLU) {
-          float g = 0.f, u = 0.f;
+    uint4 wf[D][NR];
+    uint32_t sf[D][NR];
+    uint4 xf[D][4][NX];
+    auto load = [&](int q, int st) __attribute__((always_inline)) {
 #pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            g += red[(w * NR * 16 + f) * LDR + i];
-            u += red[(w * NR * 16 + BN + f) * LDR + i];
-          }
-          const float hval = g / (1.0f + __expf(-g)) * u;
-          reinterpret_cast<uint16_t*>(a.out)[(size_t)(p0 + i) * N + fb * BN + f] = f32_to_bf16(hval);
-        } else {
-          float o = 0.f;
+      for (int b = 0; b < NR; ++b)
+        wf[st][b] = buf_load<uint4, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b],
+                                                              (uint32_t)q * kFp4QuadBytes);
 #pragma unroll
-          for (int w = 0; w < 4; ++w) o += red[(w * NR * 16 + f) * LDR + i];
-          reinterpret_cast<float*>(a.out)[(size_t)(p0 + i) * N + fb * BN + f] = o;
+      for (int b = 0; b < NR; ++b)
+        sf[st][b] = buf_load<uint32_t, 0>((GLU && b >= NR / 2) ? rb : ra, so[b], (uint32_t)q * kFp4QuadBytes);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int s = 0; s < NX; ++s) xf[st][j][s] = buf_load<uint4, 0>(rx, xo[s], (uint32_t)(q * 4 + j) * 64u);
+    };
+    auto compute = [&](int st) __attribute__((always_inline)) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int b = 0; b < NR; ++b) {
+          const uint32_t code = j == 0 ? wf[st][b].x : j == 1 ? wf[st][b].y : j == 2 ? wf[st][b].z : wf[st][b].w;
+          const uint4 wv = fp4x8_to_bf16x8(code, e8m0_to_f32((sf[st][b] >> (8 * j)) & 255u));
+#pragma unroll
+          for (int s = 0; s < NX; ++s) acc[b][s] = mfma16x16x32(wv, xf[st][j][s], acc[b][s]);
         }
+    };
+    // Register ring over quads, as in the bf16 body: slot q % D, loaded D - 1 quads ahead.  The
+    // scheduler would interleave a quad's loads with the previous quad's MFMAs and wait on them
+    // early; scheduling barriers keep each quad's loads ahead of the multiplies.
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d) load(min(d, nq - 1), d);
+    int q = 0;
+    for (; q + D <= nq; q += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        load(min(q + d + D - 1, nq - 1), (d + D - 1) % D);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(d);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __syncthreads();
+#pragma unroll
+    for (int d = 0; d < D - 1; ++d)
+      if (q + d < nq) compute(d);
+
+    stream_finish<BM, BN, GLU, NR, NX>(a, red, acc, p0, rows, fb);
   }
 }
 
@@ -440,9 +537,27 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
   X(4, "stream_bm32_n32", 32, 32, 32, false, false, 3)   \
   X(5, "stream_bm32_il", 32, 32, 64, true, false, 4)
 
+// MXFP4 shapes of the stream variants with BM <= 32: (id, BN1, BN2, ring depth in quads).  A
+// quad moves a quarter of the bf16 weight bytes per k-step, so the rings hold more steps than
+// the bf16 ones, as deep as the register file allows without spilling (twice the features
+// per item would amortise the token loads better but spills the GLU accumulators).
+#define DAMOE_FP4_SHAPES(X) \
+  X(0, 32, 32, 4)           \
+  X(1, 32, 64, 2)           \
+  X(3, 32, 32, 4)           \
+  X(4, 32, 32, 2)           \
+  X(5, 32, 64, 3)
+
 // Tiled variants: (id, name, ring depth D); token tile BM = 128.
 #define DAMOE_TILED_VARIANTS(X) \
   X(6, "tiled_bm128", 2)
+
+// Token tile rows of each stream variant id (for the MXFP4 shapes).
+constexpr int kVariantBM[] = {
+#define DAMOE_BM(ID, NAME, BM, BN1, BN2, IL, NT, D) BM,
+    DAMOE_STREAM_VARIANTS(DAMOE_BM)
+#undef DAMOE_BM
+};
 
 constexpr int tile_class(int bm) { return bm == 16 ? 0 : bm == 32 ? 1 : bm == 64 ? 2 : bm == 128 ? 3 : 4; }
 
@@ -476,8 +591,9 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   }
 }
 
-// MXFP4 weights: the stream variants only (fragment-packed); any other dispatched id is
-// flagged like an id outside the launch's candidates.
+// MXFP4 weights: the stream variants with token tiles of at most kFp4MaxBM rows (a ring slot
+// holds 4 k-steps of token fragments; larger tiles would spill), in their MXFP4 shapes; any
+// other dispatched id is flagged like an id outside the launch's candidates.
 template <bool GLU>
 __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm_fp4(GemmArgs a) {
   extern __shared__ float smem[];
@@ -489,13 +605,14 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm_fp4(GemmArgs a) {
     return;
   }
   switch (v) {
-#define DAMOE_CASE(ID, NAME, BM, BN1, BN2, IL, NT, D)                                          \
+#define DAMOE_CASE(ID, BN1, BN2, DQ)                                                           \
   case ID: {                                                                                   \
-    constexpr int BN = GLU ? BN1 : BN2;                                                        \
-    stream_body<BM, BN, GLU, false, IL, NT, D, true, true>(a, a.tiles.list[tile_class(BM)], smem); \
+    constexpr int BM = kVariantBM[ID];                                                         \
+    static_assert(BM <= kFp4MaxBM, "MXFP4 token tile");                                         \
+    stream_body_fp4<BM, GLU ? BN1 : BN2, GLU, false, DQ>(a, a.tiles.list[tile_class(BM)], smem); \
     break;                                                                                     \
   }
-    DAMOE_STREAM_VARIANTS(DAMOE_CASE)
+    DAMOE_FP4_SHAPES(DAMOE_CASE)
 #undef DAMOE_CASE
     default:
       if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
@@ -571,6 +688,16 @@ constexpr size_t max_lds() {
   return m;
 }
 
+constexpr size_t fp4_lds() {
+  size_t m = 0;
+#define DAMOE_LDS4(ID, BN1, BN2, DQ)                                                             \
+  m = m > (size_t)4 * 2 * BN1 * (kVariantBM[ID] + LDS_PAD) * 4 ? m : (size_t)4 * 2 * BN1 * (kVariantBM[ID] + LDS_PAD) * 4; \
+  m = m > (size_t)4 * BN2 * (kVariantBM[ID] + LDS_PAD) * 4 ? m : (size_t)4 * BN2 * (kVariantBM[ID] + LDS_PAD) * 4;
+  DAMOE_FP4_SHAPES(DAMOE_LDS4)
+#undef DAMOE_LDS4
+  return m;
+}
+
 }  // namespace
 
 int32_t num_variants() { return (int32_t)(sizeof(kVariants) / sizeof(kVariants[0])); }
@@ -581,7 +708,7 @@ template <bool GLU>
 static hipError_t launch_stage(const GemmArgs& a, int grid, hipStream_t stream) {
   const size_t lds = gemm_lds_bytes();
   if (a.fp4) {
-    hipLaunchKernelGGL((k_gemm_fp4<GLU>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
+    hipLaunchKernelGGL((k_gemm_fp4<GLU>), dim3(grid), dim3(kGemmThreads), fp4_lds(), stream, a);
   } else if (a.fp8) {
     if (a.packed) hipLaunchKernelGGL((k_gemm<GLU, true, true>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
     else hipLaunchKernelGGL((k_gemm<GLU, true, false>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
@@ -597,10 +724,15 @@ hipError_t gemm_set_lds_limits() {
       reinterpret_cast<const void*>(&k_gemm<true, false, false>), reinterpret_cast<const void*>(&k_gemm<false, false, false>),
       reinterpret_cast<const void*>(&k_gemm<true, true, false>), reinterpret_cast<const void*>(&k_gemm<false, true, false>),
       reinterpret_cast<const void*>(&k_gemm<true, false, true>), reinterpret_cast<const void*>(&k_gemm<false, false, true>),
-      reinterpret_cast<const void*>(&k_gemm<true, true, true>), reinterpret_cast<const void*>(&k_gemm<false, true, true>),
-      reinterpret_cast<const void*>(&k_gemm_fp4<true>), reinterpret_cast<const void*>(&k_gemm_fp4<false>)};
+      reinterpret_cast<const void*>(&k_gemm<true, true, true>), reinterpret_cast<const void*>(&k_gemm<false, true, true>)};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)gemm_lds_bytes());
+    if (e != hipSuccess) return e;
+  }
+  const void* fns4[] = {reinterpret_cast<const void*>(&k_gemm_fp4<true>),
+                        reinterpret_cast<const void*>(&k_gemm_fp4<false>)};
+  for (const void* f : fns4) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)fp4_lds());
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

@@ -46,10 +46,16 @@ class DeviceLayer:
                                       self.w["w2"], self.s.get("w1"), self.s.get("w3"), self.s.get("w2"))
         self.packed = packed
         if packed:
-            dst = {n: torch.empty_like(t) for n, t in self.w.items()}
+            if self.wdtype == damoe.W_MXFP4:  # codes and scales into one array of quad fragments
+                dst = {n: torch.empty((E, t.shape[1] * t.shape[2] * 17 // 16), dtype=torch.uint8, device=device)
+                       for n, t in self.w.items()}
+            else:
+                dst = {n: torch.empty_like(t) for n, t in self.w.items()}
             damoe.pack_weights(self.layer, dst["w1"], dst["w3"], dst["w2"])
             torch.cuda.synchronize()
             self.w = dst
+            if self.wdtype == damoe.W_MXFP4:
+                self.s = {}
             self.layer = damoe.make_layer(E, shape.k, H, I, self.wdtype, dst["w1"], dst["w3"], dst["w2"],
                                           self.s.get("w1"), self.s.get("w3"), self.s.get("w2"),
                                           layout=damoe.LAYOUT_FRAG16)

@@ -28,7 +28,8 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
     import torch
     from . import damoe, synth
     from .moe import DeviceLayer
-    shapes = {"dsv3": synth.DS, "dsv3-fp8": synth.DS_FP8, "kimi-k2": synth.KIMI, "tiny": synth.TINY,
+    shapes = {"dsv3": synth.DS, "dsv3-fp8": synth.DS_FP8, "dsv3-mxfp4": synth.DS_MXFP4, "kimi-k2": synth.KIMI,
+              "tiny": synth.TINY,
               **{f"dsv3-ep{ep}": sh for ep, sh in synth.DS_EP.items()}}
     shape = shapes[shape_name]
     if dl is None:
@@ -50,7 +51,8 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("shape", choices=["dsv3", "dsv3-fp8", "kimi-k2", "tiny", "dsv3-ep2", "dsv3-ep4", "dsv3-ep8"])
+    ap.add_argument("shape", choices=["dsv3", "dsv3-fp8", "dsv3-mxfp4", "kimi-k2", "tiny", "dsv3-ep2", "dsv3-ep4",
+                                      "dsv3-ep8"])
     ap.add_argument("--max-T", type=int, default=128)
     ap.add_argument("--samples", type=int, default=10)
     ap.add_argument("--reps", type=int, default=5)

@@ -104,6 +104,19 @@ def test_validation_before_launch():
     assert pk(ctypes.byref(_fake_layer(layout=1)), P, P, P, None) == -1
     assert pk(ctypes.byref(_fake_layer()), 0x1000, 0x900000, 0xA00000, None) == -1  # w1 dst == w1 src
     assert pk(ctypes.byref(_fake_layer()), None, P, P, None) == -1
+    far = 1 << 40
+    assert pk(ctypes.byref(_fake_layer()), far, far + (1 << 20), far + (1 << 30), None) == -1  # w1, w3 dsts overlap
+    # MXFP4: row-major needs scales; packed carries them (so the 512-multiple check is reached
+    # first); destinations (E rows cols 17 / 32 bytes) must not overlap the scale sources either
+    fp4 = dict(wdtype=2, H=512, I=512)
+    assert fm(ctypes.byref(_fake_layer(**dict(fp4, H=256))), P, P, 4, P, P, P, -1, 0, P, P, ws_ok, None) == -1
+    assert fm(ctypes.byref(_fake_layer(**dict(fp4, H=256), layout=1)), P, P, 4, P, P, P, -1, 0, P, P, ws_ok,
+              None) == -2
+    s1 = far + (1 << 34)
+    lay4 = _fake_layer(**fp4, s1=s1, s3=s1 + (1 << 30), s2=s1 + (2 << 30))
+    n = 8 * 512 * 512
+    assert pk(ctypes.byref(lay4), s1 - n // 32 * 17 + 1, far, far + (1 << 30), None) == -1
+    assert pk(ctypes.byref(lay4), far, far + (1 << 31), s1 + (1 << 30) - 100, None) == -1  # w2 dst over s3
     assert fm(ctypes.byref(lay), P, P, 4, P, P, P, damoe.num_variants(), 0, P, P, ws_ok, None) == -1
     assert fm(ctypes.byref(lay), P, P, 4, P, P, None, -1, 0, P, P, ws_ok, None) == -1  # no variant id
     assert fm(ctypes.byref(lay), P, P, 4, P, P, P, -1, 0, P, P, 1024, None) == -3

@@ -277,7 +277,7 @@ def test_small_mxfp4_every_stream_variant(small_mxfp4, T, alpha, seed):
     rows = np.arange(T) if T <= 64 else np.sort(np.random.default_rng(T).choice(T, 48, replace=False))
     ref = oracle_rows(sh, r, seed, rows, src)
     variants = _stream_variants(damoe.W_MXFP4)
-    assert len(variants) >= 5 and not damoe.variant_supports(damoe.num_variants() - 1, damoe.W_MXFP4)
+    assert len(variants) >= 4 and not damoe.variant_supports(damoe.num_variants() - 1, damoe.W_MXFP4)
     for v in variants:
         log(f"small mxfp4 T={T} alpha={alpha} variant={damoe.variant_name(v)}")
         _run(path, r, seed, v)
