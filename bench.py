@@ -11,7 +11,9 @@ device -- over each of the 16 sweep points, every point on its own routing
 cannot serve repeated weights).  All inputs are resident in HBM before the
 timed region.
 
-value = geomean over the 16 points of the mean path latency (us per layer).
+value = geomean over the 16 points of the median path latency over the timed
+steps (us per layer; each point's mean is reported beside it).  Each step is
+queued behind a ~1 ms GPU spin, so the events time the GPU, not the host.
 roofline = the dominant kernel (grouped GEMM1 + SwiGLU): algorithmic bytes
 (W1 and W3 of every touched expert + the token rows) / its mean duration,
 timed with HIP events on its own stream inside the timed region.
@@ -1011,7 +1013,11 @@ def main():
         if events:
             events[4].record(stream)
 
+    # Each step starts behind a ~1 ms spin, so the host has queued the step's first points
+    # before the GPU reaches them and events time the GPU, not the host's launch pace.
+    spin = gpu_spin(torch, stream, 1000.0)
     for s in range(args.warmup):
+        torch.cuda._sleep(spin)
         for (T, a) in points:
             run_point(T, a, s % REPS)
     torch.cuda.synchronize()
@@ -1022,6 +1028,7 @@ def main():
     t0 = time.perf_counter()
     for s in range(args.steps):
         rep = (s + args.warmup) % REPS
+        torch.cuda._sleep(spin)
         for (T, a) in points:
             e = [ev() for _ in range(5)]
             run_point(T, a, rep, e)
@@ -1038,15 +1045,19 @@ def main():
         g1_bytes += U[T, a, rep] * 2 * shape.I * shape.H * wbytes + T * shape.H * 2
         g1_ms += g1
 
+    # Per point: medians over the timed steps (a stall of the host between two launches lands
+    # inside one step's events), and the path's mean beside its median.
     per_point = {}
     for (T, a), v in rec.items():
         arr = np.array(v)
+        med = np.median(arr, axis=0) * 1e3
         per_point[f"T{T}_a{a}"] = {
-            "path_us": round(float(arr[:, 0].mean()) * 1e3, 1),
-            "gemm1_us": round(float(arr[:, 1].mean()) * 1e3, 1),
-            "gemm2_us": round(float(arr[:, 2].mean()) * 1e3, 1),
-            "route_dispatch_us": round(float(arr[:, 3].mean()) * 1e3, 1),
-            "reduce_us": round(float(arr[:, 4].mean()) * 1e3, 1),
+            "path_us": round(float(med[0]), 1),
+            "path_us_mean": round(float(arr[:, 0].mean()) * 1e3, 1),
+            "gemm1_us": round(float(med[1]), 1),
+            "gemm2_us": round(float(med[2]), 1),
+            "route_dispatch_us": round(float(med[3]), 1),
+            "reduce_us": round(float(med[4]), 1),
         }
     value = geomean([per_point[f"T{T}_a{a}"]["path_us"] for (T, a) in points])
     achieved = g1_bytes / (g1_ms * 1e-3) / 1e9
@@ -1070,7 +1081,8 @@ def main():
                                "{1,8,32,128} x Dirichlet alpha in {0.05,0.3,1,10}, adaptive dispatch"
                                + ("" if force < 0 else f" (forced variant {damoe.variant_name(force)})"),
                    "points": len(points), "table": table_note},
-        "roofline": {"bound": "hbm", "kernel": "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": "k_gemm_fp4<GEMM1+SwiGLU>" if args.wdtype == "mxfp4"
+                     else "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic() if args.wdtype == "bf16" else None,
                      "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1))},

@@ -388,13 +388,12 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   const bool mega = force_variant >= 0 ? force_variant != kBigVariant : (candidates & ~big_bit) != 0;
   // The big-tile kernel holds an item's fp8 scale rows in LDS: at most 128 scale columns.
   if (big && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128) return DAMOE_ERR_UNSUPPORTED;
-  const int grid = dev->cus * 2;
   if (stage_mask & 1) {
-    if (mega && launch_gemm1(g1, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if (mega && launch_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if (big && launch_big_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
   if (stage_mask & 2) {
-    if (mega && launch_gemm2(g2, grid, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if (mega && launch_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if (big && launch_big_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
   ReduceArgs r{reinterpret_cast<const float*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};

@@ -106,8 +106,9 @@ hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int
                         const DispatchArgs* dispatch, hipStream_t stream);
 hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
                            hipStream_t stream);
-hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
-hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
+// Grouped GEMM stages on a persistent grid sized from the device's CU count.
+hipError_t launch_gemm1(const GemmArgs& a, int cus, hipStream_t stream);
+hipError_t launch_gemm2(const GemmArgs& a, int cus, hipStream_t stream);
 hipError_t launch_big_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t big_set_lds_limits();

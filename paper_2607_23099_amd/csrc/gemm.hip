@@ -537,16 +537,19 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
   X(4, "stream_bm32_n32", 32, 32, 32, false, false, 3)   \
   X(5, "stream_bm32_il", 32, 32, 64, true, false, 4)
 
-// MXFP4 shapes of the stream variants with BM <= 32: (id, BN1, BN2, ring depth in quads).  A
-// quad moves a quarter of the bf16 weight bytes per k-step, so the rings hold more steps than
-// the bf16 ones, as deep as the register file allows without spilling (twice the features
-// per item would amortise the token loads better but spills the GLU accumulators).
+// MXFP4 shapes of the stream variants with BM <= 32: (id, BN1, BN2).  Ring depths in quads:
+// 2 for GEMM1 (waves of 14 quads at H = 7168; deeper rings and a third wave per SIMD measured
+// no faster), 1 for GEMM2 (4 quads per wave at I = 2048) in a kernel of 3 waves per SIMD:
+// there the extra workgroup per CU hides more latency than a ring does (about 10% faster than
+// depth 2 or 3 at 2 waves).  Twice the features per item would amortise the token loads
+// better but spills the GLU accumulators.
 #define DAMOE_FP4_SHAPES(X) \
-  X(0, 32, 32, 4)           \
-  X(1, 32, 64, 2)           \
-  X(3, 32, 32, 4)           \
-  X(4, 32, 32, 2)           \
-  X(5, 32, 64, 3)
+  X(0, 32, 32)              \
+  X(1, 32, 64)              \
+  X(3, 32, 32)              \
+  X(4, 32, 32)              \
+  X(5, 32, 64)
+constexpr int kFp4Ring[2] = {1, 2};       // ring depth of k_gemm_fp4<false>, <true>
 
 // Tiled variants: (id, name, ring depth D); token tile BM = 128.
 #define DAMOE_TILED_VARIANTS(X) \
@@ -594,8 +597,10 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
 // MXFP4 weights: the stream variants with token tiles of at most kFp4MaxBM rows (a ring slot
 // holds 4 k-steps of token fragments; larger tiles would spill), in their MXFP4 shapes; any
 // other dispatched id is flagged like an id outside the launch's candidates.
+constexpr int kFp4Occupancy[2] = {3, 2};  // waves per SIMD of k_gemm_fp4<false>, <true>
+
 template <bool GLU>
-__global__ void __launch_bounds__(kGemmThreads, 2) k_gemm_fp4(GemmArgs a) {
+__global__ void __launch_bounds__(kGemmThreads, kFp4Occupancy[GLU]) k_gemm_fp4(GemmArgs a) {
   extern __shared__ float smem[];
   pin_gemm_args(a);
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
@@ -605,11 +610,11 @@ __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm_fp4(GemmArgs a) {
     return;
   }
   switch (v) {
-#define DAMOE_CASE(ID, BN1, BN2, DQ)                                                           \
+#define DAMOE_CASE(ID, BN1, BN2)                                                               \
   case ID: {                                                                                   \
     constexpr int BM = kVariantBM[ID];                                                         \
     static_assert(BM <= kFp4MaxBM, "MXFP4 token tile");                                         \
-    stream_body_fp4<BM, GLU ? BN1 : BN2, GLU, false, DQ>(a, a.tiles.list[tile_class(BM)], smem); \
+    stream_body_fp4<BM, GLU ? BN1 : BN2, GLU, false, kFp4Ring[GLU]>(a, a.tiles.list[tile_class(BM)], smem); \
     break;                                                                                     \
   }
     DAMOE_FP4_SHAPES(DAMOE_CASE)
@@ -690,7 +695,7 @@ constexpr size_t max_lds() {
 
 constexpr size_t fp4_lds() {
   size_t m = 0;
-#define DAMOE_LDS4(ID, BN1, BN2, DQ)                                                             \
+#define DAMOE_LDS4(ID, BN1, BN2)                                                             \
   m = m > (size_t)4 * 2 * BN1 * (kVariantBM[ID] + LDS_PAD) * 4 ? m : (size_t)4 * 2 * BN1 * (kVariantBM[ID] + LDS_PAD) * 4; \
   m = m > (size_t)4 * BN2 * (kVariantBM[ID] + LDS_PAD) * 4 ? m : (size_t)4 * BN2 * (kVariantBM[ID] + LDS_PAD) * 4;
   DAMOE_FP4_SHAPES(DAMOE_LDS4)
@@ -704,11 +709,13 @@ int32_t num_variants() { return (int32_t)(sizeof(kVariants) / sizeof(kVariants[0
 const VariantDesc& variant(int32_t v) { return kVariants[v]; }
 size_t gemm_lds_bytes() { return max_lds(); }
 
+// Persistent grids: as many workgroups as the CUs hold at the kernel's occupancy.
 template <bool GLU>
-static hipError_t launch_stage(const GemmArgs& a, int grid, hipStream_t stream) {
+static hipError_t launch_stage(const GemmArgs& a, int cus, hipStream_t stream) {
   const size_t lds = gemm_lds_bytes();
+  const int grid = cus * 2;
   if (a.fp4) {
-    hipLaunchKernelGGL((k_gemm_fp4<GLU>), dim3(grid), dim3(kGemmThreads), fp4_lds(), stream, a);
+    hipLaunchKernelGGL((k_gemm_fp4<GLU>), dim3(cus * kFp4Occupancy[GLU]), dim3(kGemmThreads), fp4_lds(), stream, a);
   } else if (a.fp8) {
     if (a.packed) hipLaunchKernelGGL((k_gemm<GLU, true, true>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
     else hipLaunchKernelGGL((k_gemm<GLU, true, false>), dim3(grid), dim3(kGemmThreads), lds, stream, a);
@@ -738,9 +745,9 @@ hipError_t gemm_set_lds_limits() {
   return hipSuccess;
 }
 
-hipError_t launch_gemm1(const GemmArgs& a, int grid, hipStream_t stream) { return launch_stage<true>(a, grid, stream); }
+hipError_t launch_gemm1(const GemmArgs& a, int cus, hipStream_t stream) { return launch_stage<true>(a, cus, stream); }
 
-hipError_t launch_gemm2(const GemmArgs& a, int grid, hipStream_t stream) { return launch_stage<false>(a, grid, stream); }
+hipError_t launch_gemm2(const GemmArgs& a, int cus, hipStream_t stream) { return launch_stage<false>(a, cus, stream); }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream) {
   if (a.T == 0) return hipSuccess;
