@@ -125,7 +125,9 @@ typedef struct damoe_layer {
  * depends only on (E, k, H, I, T); every call of one step uses the same T.
  *   ctrl       : int32[64] control words: [0] sticky device error,
  *                [1] chosen exemplar index, [2..3] its int64 score (lo, hi),
- *                [4] variant id used by the last fused_moe
+ *                [4] variant id used by the last fused_moe,
+ *                [8..16] work-queue words of the big-tile kernel (zero between calls:
+ *                the routing call clears them and each launch leaves them cleared)
  *   tiles[s]   : token tiles for tile size BM_s = 16 << s: int32 n_tiles, int32 pad,
  *                then n_tiles entries of int32x2 {start position, expert | rows << 16}
  *   h          : bf16 [T*k][I]   SwiGLU activations in permuted order

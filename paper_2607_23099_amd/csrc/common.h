@@ -18,6 +18,11 @@ constexpr int kWave = 64;
 constexpr int kGemmThreads = 256;  // every GEMM variant runs 4 waves per workgroup
 constexpr int kRouteThreads = 1024;
 constexpr int kCtrlWords = 64;
+// Control words kQueueCtrl .. + 8: the big-tile kernel's work-queue tickets (one per XCD) and
+// its count of finished workgroups.  Zero between launches: the routing kernel clears them,
+// and each big-tile launch returns them to zero when its last workgroup finishes.
+constexpr int kQueueCtrl = 8;
+constexpr int kQueueWords = 9;
 
 // ---------------------------------------------------------------------------------------------
 // Variant registry.  A variant is one template instance of the grouped GEMM pair; all variants

@@ -358,6 +358,7 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     }
     if (sm.bad) atomicOr(&o.ctrl[0], DAMOE_DEVERR_EXPERT_ID);
   }
+  if (tid < kQueueWords) o.ctrl[kQueueCtrl + tid] = 0;
 #pragma unroll
   for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
     const int bm = 16 << cls;
