@@ -35,6 +35,14 @@ constexpr int LDS_PAD = 1;
 // The 4 waves' partial tiles of a stream item -> LDS (rows = output features, columns =
 // tokens), summed in wave order, then the SwiGLU epilogue (GEMM1, bf16 h) or the fp32 output
 // (GEMM2) of the tile's valid rows.
+// True if the expert of tile `tile` has no other tile in the list (an expert's tiles are
+// adjacent entries): its weights are read by this tile's items only.
+__device__ __forceinline__ bool solo_expert(const int2* __restrict__ ent, int n_tiles, int tile, int e) {
+  const bool prev = tile > 0 && (ent[tile - 1].y & 0xFFFF) == e;
+  const bool next = tile + 1 < n_tiles && (ent[tile + 1].y & 0xFFFF) == e;
+  return !prev && !next;
+}
+
 template <int BM, int BN, bool GLU, int NR, int NX>
 __device__ __forceinline__ void stream_finish(const GemmArgs& a, float* __restrict__ red, const floatx4 (&acc)[NR][NX],
                                               int p0, int rows, int fb) {
@@ -77,7 +85,9 @@ __device__ __forceinline__ void stream_finish(const GemmArgs& a, float* __restri
 // IL: the waves take interleaved 32-wide k-steps (wave w reads k-steps w, w+4, ...), so the
 //     4 waves of a workgroup read 256 contiguous bytes of every weight row at a time;
 //     otherwise each wave reads one contiguous quarter of the row.
-// NT: weight loads carry the nontemporal hint (streamed once, not worth caching).
+// NT: per item, bf16 weights of an expert whose rows all fit this one tile are loaded with the
+//     nontemporal hint (read once in the launch: streamed past the caches, about 10% more
+//     read bandwidth); an expert with further tiles keeps its weights cached for them.
 // D:  register-ring depth, k-steps in flight per wave.
 // PK: weights in the fragment-packed layout (block (rb, kb) of 16 rows x 32 columns is one
 //     contiguous 64-lane fragment); otherwise row-major.
@@ -161,11 +171,13 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
 
     WT wf[D][NR];
     uint4 xf[D][NX];
+    auto ring = [&](auto nt_c) __attribute__((always_inline)) {
+    constexpr int kAuxW = decltype(nt_c)::value ? kAuxNontemporal : 0;
     auto load = [&](int ks, int st) __attribute__((always_inline)) {
       const uint32_t sw = PK ? (uint32_t)ks * (KSTEP / 32) * 512u * EB : (uint32_t)ks * KSTEP * EB;
 #pragma unroll
       for (int b = 0; b < NR; ++b)
-        wf[st][b] = buf_load<WT, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b], sw);
+        wf[st][b] = buf_load<WT, kAuxW>((GLU && b >= NR / 2) ? rb : ra, wo[b], sw);
 
       const uint32_t sx = (uint32_t)ks * KSTEP * 2;
 #pragma unroll
@@ -206,6 +218,14 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
 #pragma unroll
     for (int d = 0; d < D - 1; ++d)
       if (ks + d < nks) compute(ks + d, d);
+    };
+    // fp8 weights keep one instance: a second one costs the GEMM2 kernel spills.
+    if constexpr (NT && !FP8) {
+      if (solo_expert(ent, n_tiles, tile, e)) ring(std::true_type{});
+      else ring(std::false_type{});
+    } else {
+      ring(std::false_type{});
+    }
 
     stream_finish<BM, BN, GLU, NR, NX>(a, red, acc, p0, rows, fb);
   }
@@ -282,11 +302,12 @@ __device__ __forceinline__ void stream_body_fp4(const GemmArgs& a, const int32_t
     uint4 wf[D][NR];
     uint32_t sf[D][NR];
     uint4 xf[D][4][NX];
+    auto ring = [&](auto nt_c) __attribute__((always_inline)) {
+    constexpr int kAuxW = decltype(nt_c)::value ? kAuxNontemporal : 0;
     auto load = [&](int q, int st) __attribute__((always_inline)) {
 #pragma unroll
       for (int b = 0; b < NR; ++b)
-        wf[st][b] = buf_load<uint4, NT ? kAuxNontemporal : 0>((GLU && b >= NR / 2) ? rb : ra, wo[b],
-                                                              (uint32_t)q * kFp4QuadBytes);
+        wf[st][b] = buf_load<uint4, kAuxW>((GLU && b >= NR / 2) ? rb : ra, wo[b], (uint32_t)q * kFp4QuadBytes);
 #pragma unroll
       for (int b = 0; b < NR; ++b)
         sf[st][b] = buf_load<uint32_t, 0>((GLU && b >= NR / 2) ? rb : ra, so[b], (uint32_t)q * kFp4QuadBytes);
@@ -324,6 +345,9 @@ __device__ __forceinline__ void stream_body_fp4(const GemmArgs& a, const int32_t
 #pragma unroll
     for (int d = 0; d < D - 1; ++d)
       if (q + d < nq) compute(d);
+    };
+    if (NT && solo_expert(ent, n_tiles, tile, e)) ring(std::true_type{});
+    else ring(std::false_type{});
 
     stream_finish<BM, BN, GLU, NR, NX>(a, red, acc, p0, rows, fb);
   }
@@ -530,19 +554,21 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
 
 // The registry.  Indices are the public variant ids: (id, name, BM, BN1, BN2, IL, NT, D).
 #define DAMOE_STREAM_VARIANTS(X)                         \
-  X(0, "stream_bm16", 16, 32, 32, true, false, 6)        \
-  X(1, "stream_bm32", 32, 32, 64, false, false, 3)       \
-  X(2, "stream_bm64", 64, 32, 64, false, false, 2)       \
-  X(3, "stream_bm16_n16", 16, 32, 16, true, false, 6)    \
-  X(4, "stream_bm32_n32", 32, 32, 32, false, false, 3)   \
-  X(5, "stream_bm32_il", 32, 32, 64, true, false, 4)
+  X(0, "stream_bm16", 16, 32, 32, true, true, 6)        \
+  X(1, "stream_bm32", 32, 32, 64, false, true, 3)       \
+  X(2, "stream_bm64", 64, 32, 64, false, true, 2)       \
+  X(3, "stream_bm16_n16", 16, 32, 16, true, true, 6)    \
+  X(4, "stream_bm32_n32", 32, 32, 32, false, true, 3)   \
+  X(5, "stream_bm32_il", 32, 32, 64, true, true, 4)
 
 // MXFP4 shapes of the stream variants with BM <= 32: (id, BN1, BN2).  Ring depths in quads:
 // 2 for GEMM1 (waves of 14 quads at H = 7168; deeper rings and a third wave per SIMD measured
 // no faster), 1 for GEMM2 (4 quads per wave at I = 2048) in a kernel of 3 waves per SIMD:
 // there the extra workgroup per CU hides more latency than a ring does (about 10% faster than
 // depth 2 or 3 at 2 waves).  Twice the features per item would amortise the token loads
-// better but spills the GLU accumulators.
+// better but spills the GLU accumulators.  GEMM1's code loads take the per-item nontemporal
+// choice of the bf16 kernels; GEMM2 (latency-bound) and the scale words, which share cache
+// lines with the next fragment's codes, load plainly (nontemporal measured slower there).
 #define DAMOE_FP4_SHAPES(X) \
   X(0, 32, 32)              \
   X(1, 32, 64)              \
@@ -614,7 +640,7 @@ __global__ void __launch_bounds__(kGemmThreads, kFp4Occupancy[GLU]) k_gemm_fp4(G
   case ID: {                                                                                   \
     constexpr int BM = kVariantBM[ID];                                                         \
     static_assert(BM <= kFp4MaxBM, "MXFP4 token tile");                                         \
-    stream_body_fp4<BM, GLU ? BN1 : BN2, GLU, false, kFp4Ring[GLU]>(a, a.tiles.list[tile_class(BM)], smem); \
+    stream_body_fp4<BM, GLU ? BN1 : BN2, GLU, GLU, kFp4Ring[GLU]>(a, a.tiles.list[tile_class(BM)], smem); \
     break;                                                                                     \
   }
     DAMOE_FP4_SHAPES(DAMOE_CASE)
