@@ -25,6 +25,7 @@
 
 #include "common.h"
 #include "device.h"
+#include "queue.h"
 
 namespace damoe {
 namespace {
@@ -382,7 +383,6 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = N / FEAT;
-  const long long n_items = (long long)n_tiles * n_fb;
   const int nst = K / kTiledBK;  // K stages
   const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
   const uint8_t* __restrict__ wb = reinterpret_cast<const uint8_t*>(a.wb);
@@ -391,15 +391,29 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
   // MFMA operand read: lane l reads row s*16 + (l & 15), logical chunk kk*4 + (l >> 4).
   const int rl = lane & 15, gl = lane >> 4;
 
-  for (long long it = blockIdx.x; it < n_items; it += gridDim.x) {
-    const int tile = (int)(it / n_fb);
-    const int fb = (int)(it - (long long)tile * n_fb);
-    const int2 en = ent[tile];
+  // Items come from the per-XCD work queues; thread 0 takes the tickets, one item ahead, and
+  // hands each to the workgroup through the LDS word after the two token stages.
+  const ItemMap map(n_tiles, n_fb);
+  QueueTaker taker(a.ctrl);
+  volatile int32_t* const slot = reinterpret_cast<volatile int32_t*>(lds + kTiledLds);
+  int next = 0;
+  if (tid == 0) slot[0] = taker.take(map);
+  __syncthreads();
+
+  for (;;) {
+    const int cur = slot[0];
+    __syncthreads();  // every wave has read the ticket before thread 0 may replace it
+    if (cur < 0) break;
+    if (tid == 0) next = taker.take(map);  // the next ticket, while this item runs
+    int tile = 0, fb = 0;
+    bool ok = map.item(cur >> 28, cur & 0x0FFFFFFF, n_tiles, tile, fb);
+    const int2 en = ok ? ent[tile] : make_int2(0, 0);
     const int p0 = en.x, e = en.y & 0xFFFF, rows = en.y >> 16;
-    if (p0 < 0 || rows <= 0 || rows > BM || p0 + rows > a.A || e >= a.E) {
+    if (ok && (p0 < 0 || rows <= 0 || rows > BM || p0 + rows > a.A || e >= a.E)) {
       if (tid == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
-      continue;
+      ok = false;
     }
+    if (ok) {
     // Token rows this thread stages (byte offsets in x / h; padding rows read as zero).
     __amdgpu_buffer_rsrc_t rx;
     if (GLU) rx = make_rsrc(a.x, (uint32_t)((size_t)(a.A / a.k) * K * 2));
@@ -549,7 +563,12 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
         }
       }
     }
+    }  // ok
+    // The K loop ended with a barrier after its last LDS reads (or there was none).
+    if (tid == 0) slot[0] = next;
+    __syncthreads();
   }
+  if (tid == 0) taker.finish();
 }
 
 // The registry.  Indices are the public variant ids: (id, name, BM, BN1, BN2, IL, NT, D).
@@ -715,7 +734,7 @@ constexpr size_t max_lds() {
   m = m > (size_t)4 * BN2 * (BM + LDS_PAD) * 4 ? m : (size_t)4 * BN2 * (BM + LDS_PAD) * 4;
   DAMOE_STREAM_VARIANTS(DAMOE_LDS)
 #undef DAMOE_LDS
-  m = m > kTiledLds ? m : kTiledLds;
+  m = m > kTiledLds + 4 ? m : kTiledLds + 4;  // + the tiled kernel's ticket word
   return m;
 }
 

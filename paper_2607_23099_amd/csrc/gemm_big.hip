@@ -20,6 +20,7 @@
 
 #include "common.h"
 #include "device.h"
+#include "queue.h"
 
 namespace damoe {
 namespace {
@@ -42,7 +43,6 @@ struct BigCfg {
   static constexpr size_t kLds = kScaleOff + (FP8 ? 4 * 2 * kBigMaxSk * 4 : 0);
   static_assert(kLds <= 160 * 1024, "LDS of one CU");
 };
-constexpr int kXcds = 8;
 
 typedef __attribute__((address_space(3))) uint8_t lds_t;
 typedef __attribute__((address_space(3))) float lds_f32;
@@ -69,42 +69,6 @@ __device__ __forceinline__ void wait_cnt() {
   __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (LGKM << 8) | ((VM >> 4) << 14));
 }
 
-// Item order.  Workgroup b runs on XCD b % 8 (round-robin placement).  Items are grouped in
-// chunks of tg token tiles x fg feature blocks (tg * fg = the workgroups of one XCD), so one
-// XCD's L2 is shared by tg token tiles and fg weight blocks instead of every token tile being
-// spread over all XCDs.  The chunks form one work queue per XCD (chunk c in queue c % 8, in
-// order), taken item by item through an atomic ticket: the items an XCD runs at one time are
-// then always neighbours in chunk order, however far its workgroups drift apart (a fixed
-// round-robin assignment let them drift whole chunks apart over the rounds, and the sharing
-// with them).  A workgroup whose queue is empty takes items from the next XCDs' queues.
-struct ItemMap {
-  bool xcd;
-  int fg, tg, n_fg, nq, n_chunks;
-
-  __device__ ItemMap(int n_tiles, int n_fb) {
-    const int per_xcd = gridDim.x / kXcds;
-    xcd = gridDim.x % kXcds == 0 && per_xcd > 0;
-    fg = n_fb % 4 == 0 ? 4 : n_fb % 2 == 0 ? 2 : 1;
-    if (!xcd || fg > per_xcd) fg = 1;
-    tg = xcd ? per_xcd / fg : 1;
-    n_fg = n_fb / fg;
-    nq = xcd ? kXcds : 1;
-    n_chunks = (n_tiles + tg - 1) / tg * n_fg;
-  }
-
-  // Tickets of queue q: its chunks q, q + nq, ... times tg * fg items each.
-  __device__ int queue_len(int q) const { return q < n_chunks ? ((n_chunks - 1 - q) / nq + 1) * (tg * fg) : 0; }
-
-  __device__ bool item(int q, int t, int n_tiles, int& tile, int& fb) const {
-    const int chunk = q + t / (tg * fg) * nq;
-    const int local = t % (tg * fg);
-    const int tgroup = chunk / n_fg;
-    tile = tgroup * tg + local / fg;
-    fb = (chunk - tgroup * n_fg) * fg + local % fg;
-    return tile < n_tiles;
-  }
-};
-
 template <bool GLU, bool FP8, bool PK>
 __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
   constexpr int FEAT = GLU ? kBigRows / 2 : kBigRows;  // output features per item
@@ -129,32 +93,21 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
   const int lr = lane & 15, lg = lane >> 4, l32 = lane & 31, lh = lane >> 5;
   const ItemMap map(n_tiles, n_fb);
 
-  // Work queues: ticket counters in ctrl[kQueueCtrl + q], the count of finished workgroups
-  // in ctrl[kQueueCtrl + kXcds].  Thread 0 takes the tickets, one item ahead, and hands
-  // each (queue << 28 | ticket, -1 when every queue is empty) to the workgroup through an
-  // LDS word of ring buffer NB - 1, which is idle from the end of an item's K loop until the
-  // first iteration of the next item's loop.
-  uint32_t* const qctrl = reinterpret_cast<uint32_t*>(a.ctrl + kQueueCtrl);
-  int qj = 0;  // thread 0: queues emptied so far, own queue first
-  auto take = [&]() -> int {
-    while (qj < map.nq) {
-      const int q = ((int)blockIdx.x + qj) % map.nq;
-      const int t = (int)atomicAdd(qctrl + q, 1u);
-      if (t < map.queue_len(q)) return q << 28 | t;
-      ++qj;
-    }
-    return -1;
-  };
+  // Items come from the per-XCD work queues.  Thread 0 takes the tickets, one item ahead, and
+  // hands each to the workgroup through an LDS word of ring buffer NB - 1, which is idle from
+  // the end of an item's K loop until the first iteration of the next item's loop.
+  QueueTaker taker(a.ctrl);
   typedef volatile __attribute__((address_space(3))) int32_t lds_i32;
   lds_i32* const slot = reinterpret_cast<lds_i32*>(lds + (NB - 1) * SB);
   int next = 0;
-  if (tid == 0) slot[0] = take();
+  if (tid == 0) slot[0] = taker.take(map);
   __syncthreads();
 
   for (;;) {
     const int cur = slot[0];
+    __syncthreads();  // every wave has read the ticket before thread 0 may replace it
     if (cur < 0) break;
-    if (tid == 0) next = take();  // the next ticket, while this item runs
+    if (tid == 0) next = taker.take(map);  // the next ticket, while this item runs
     int tile = 0, fb = 0;
     bool ok = map.item(cur >> 28, cur & 0x0FFFFFFF, n_tiles, tile, fb);
     const int2 en = ok ? ent[tile] : make_int2(0, 0);
@@ -383,14 +336,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
     if (tid == 0) slot[0] = next;
     __syncthreads();
   }
-  // The last workgroup out returns the queue words to zero for the next launch: every other
-  // workgroup has finished taking tickets (its last ticket returned before its count).
-  if (tid == 0) {
-    const uint32_t done = atomicAdd(qctrl + kXcds, 1u);
-    if (done == gridDim.x - 1) {
-      for (int x = 0; x <= kXcds; ++x) __hip_atomic_store(qctrl + x, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
+  if (tid == 0) taker.finish();
 }
 
 template <bool GLU, bool FP8, bool PK>
