@@ -333,12 +333,19 @@ typedef struct damoe_tune_config {
                                one rank's E experts of a pool of E * ep, and each sample
                                keeps the tokens with a slot on the rank, the other slots
                                masked (-1), up to the bucket's token count              */
+  int32_t n_repeat;         /* repeated-row exemplars per bucket (0 = none; needs ep <= 1) */
+  const int32_t* repeat_f;  /* host [n_repeat], percentages in 1..100: S routings whose
+                               groups of max(1, round(f T / 100)) consecutive tokens share
+                               one Gumbel-top-k row (ids and gates) under a Dirichlet(1) p,
+                               the token analog of repeated prompts (Sec. V-E); each f adds
+                               one exemplar after the skews' in every bucket             */
 } damoe_tune_config;
 
 /* Builds a table: for each bucket T_b and skew X_j, alpha_j = Alg1(E / X_j);
  * S Dirichlet routings (Gumbel-top-k at T_b tokens) are timed on every
  * variant; kid = the variant with the lowest mean latency; the exemplar is the
- * renormalised centroid of the S sorted unit count vectors.  The noda row holds
+ * renormalised centroid of the S sorted unit count vectors.  The repeated-row
+ * samples (repeat_f) add exemplars the same way.  The noda row holds
  * each bucket's fastest variant under uniform routing.  Host-synchronous; the
  * only call that allocates device memory on its own. */
 damoe_status damoe_tune(const damoe_layer* layer /* host */, const damoe_tune_config* cfg,

@@ -51,17 +51,28 @@ struct ItemMap {
 };
 
 // Thread 0's side of the queues.  take() returns queue << 28 | ticket, or -1 once every queue
-// is empty; the workgroup learns it through an LDS word (the kernels' item loops).
+// is empty; the workgroup learns it through an LDS word (the kernels' item loops).  A
+// workgroup's first ticket is fixed: ticket blockIdx.x / nq of its own queue, so that the
+// first items spread over the workgroups in launch order, one per CU while there are fewer
+// items than CUs (taken first-come, two could land on one CU and leave another idle); the
+// counters hand out the tickets after those.
 struct QueueTaker {
   uint32_t* qctrl;
-  int qj = 0;  // queues found empty so far, own queue first
+  int qj = 0;          // queues found empty so far, own queue first
+  bool first = true;
 
   __device__ explicit QueueTaker(int32_t* ctrl) : qctrl(reinterpret_cast<uint32_t*>(ctrl + kQueueCtrl)) {}
 
   __device__ int take(const ItemMap& m) {
+    const int fixed = (int)gridDim.x / m.nq;  // tickets per queue taken as first tickets
+    if (first) {
+      first = false;
+      const int q = (int)blockIdx.x % m.nq, t = (int)blockIdx.x / m.nq;
+      if (t < m.queue_len(q)) return q << 28 | t;
+    }
     while (qj < m.nq) {
       const int q = ((int)blockIdx.x + qj) % m.nq;
-      const int t = (int)atomicAdd(qctrl + q, 1u);
+      const int t = fixed + (int)atomicAdd(qctrl + q, 1u);
       if (t < m.queue_len(q)) return q << 28 | t;
       ++qj;
     }

@@ -166,6 +166,27 @@ void sample_routing(const Philox& g, const std::vector<double>& lp, int32_t T, i
   }
 }
 
+// Routing of T tokens whose groups of `group` consecutive tokens share one row: group r draws
+// one Gumbel-top-k row under lp (as token r of sample_routing) and every token of the group
+// takes its ids and gates.
+void repeated_routing(const Philox& g, const std::vector<double>& lp, int32_t T, int32_t k, int32_t group,
+                      uint32_t s, std::vector<int32_t>& ids, std::vector<float>& w) {
+  const int32_t E = (int32_t)lp.size();
+  ids.assign((size_t)T * k, -1);
+  w.assign((size_t)T * k, 0.f);
+  std::vector<double> key(E);
+  std::vector<int32_t> idx(E);
+  for (int32_t t = 0; t < T; ++t) {
+    if (t % group == 0) {
+      gumbel_token(g, lp, (uint32_t)(t / group), k, s, key, idx, ids.data() + (size_t)t * k,
+                   w.data() + (size_t)t * k);
+    } else {
+      std::copy_n(ids.data() + (size_t)(t - 1) * k, k, ids.data() + (size_t)t * k);
+      std::copy_n(w.data() + (size_t)(t - 1) * k, k, w.data() + (size_t)t * k);
+    }
+  }
+}
+
 void exemplar(const std::vector<std::vector<int32_t>>& counts, int32_t E, int32_t* Q) {
   std::vector<double> c(E, 0.0);
   for (const auto& v : counts) {
@@ -227,6 +248,11 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   if (ws_bytes == 0) return DAMOE_ERR_INVALID_ARG;
   // Expert parallelism: the layer is one rank's share of a global pool of E * ep experts.
   if (cfg->ep < 0 || cfg->ep > 64) return DAMOE_ERR_INVALID_ARG;
+  // Repeated-row exemplars (not combined with expert parallelism).
+  if (cfg->n_repeat < 0 || cfg->n_repeat > 64 || (cfg->n_repeat > 0 && (!cfg->repeat_f || cfg->ep > 1)))
+    return DAMOE_ERR_INVALID_ARG;
+  for (int32_t r = 0; r < cfg->n_repeat; ++r)
+    if (cfg->repeat_f[r] < 1 || cfg->repeat_f[r] > 100) return DAMOE_ERR_INVALID_ARG;
   const int32_t ep = cfg->ep > 1 ? cfg->ep : 1;
   const int32_t Eg = E * ep;
   const int32_t a_samples = cfg->alpha_samples > 0 ? cfg->alpha_samples : 64;
@@ -333,6 +359,35 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
       ++n_added;
       if (cfg->verbose)
         std::fprintf(stderr, "damoe_tune: T=%d ddist:%.2f -> %s (%.1f us)\n", T, cfg->skew_X[j],
+                     damoe_variant_name(best), mean[best] * 1e3);
+    }
+    // Repeated-row exemplars: groups of max(1, round(f T / 100)) consecutive tokens share one
+    // row under a Dirichlet(1) p (round half to even).  Their sorted histograms are step-shaped,
+    // unlike every Dirichlet exemplar, so without them the match takes an exemplar of another
+    // shape for such batches.
+    for (int32_t r = 0; r < cfg->n_repeat; ++r) {
+      const int32_t group = std::max(1, (int32_t)std::nearbyint(cfg->repeat_f[r] * (double)T / 100.0));
+      std::vector<std::vector<int32_t>> cs;
+      std::vector<double> mean(nv, 0.0), lat;
+      for (int32_t s = 0; s < cfg->samples; ++s) {
+        const uint32_t sid = 0x4000000u + ((uint32_t)b << 16) + ((uint32_t)r << 8) + (uint32_t)s;
+        dirichlet_logp(g, 1.0, Eg, sid, lp);
+        repeated_routing(g, lp, T, k, group, sid, ids, w);
+        std::vector<int32_t> c;
+        TRY(time_routing(lat, &c));
+        cs.push_back(c);
+        for (int32_t v = 0; v < nv; ++v) mean[v] += lat[v] / cfg->samples;
+      }
+      int32_t best = 0;
+      for (int32_t v = 1; v < nv; ++v)
+        if (mean[v] < mean[best]) best = v;
+      t_kid.push_back(best);
+      t_Q.resize(t_Q.size() + E);
+      exemplar(cs, E, t_Q.data() + t_Q.size() - E);
+      skew_mean.push_back(mean);
+      ++n_added;
+      if (cfg->verbose)
+        std::fprintf(stderr, "damoe_tune: T=%d repeat:%d%% -> %s (%.1f us)\n", T, cfg->repeat_f[r],
                      damoe_variant_name(best), mean[best] * 1e3);
     }
     t_nex.push_back(n_added);

@@ -20,11 +20,17 @@ import time
 
 PAPER_SKEWS = [1.1, 1.3, 1.5, 1.7, 2.0, 2.5, 4.0]
 EXTENDED_SKEWS = PAPER_SKEWS + [6.0, 8.0, 12.0, 16.0, 24.0, 32.0]
+# Repeated-row exemplars (percent of a batch sharing one routing row).  Tuned with them by
+# default: the DeepSeek-V3 decode layers, whose tables serve the repeated-row sweep, and the
+# tiny test layer; the others (the Kimi-K2 trace is Dirichlet; expert-parallel ranks cannot
+# take them) use the ddist:X skews only unless --repeat is given.
+REPEAT_F = [10, 20, 50, 100]
+REPEAT_BY_DEFAULT = ("dsv3", "dsv3-fp8", "tiny")
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, verbose: bool = True,
-               dl=None):
+               dl=None, repeat_f=None):
     import torch
     from . import damoe, synth
     from .moe import DeviceLayer
@@ -44,8 +50,10 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
                            slab_elems=x.numel(), sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
     t0 = time.perf_counter()
     ep = int(shape_name.split("-ep")[1]) if "-ep" in shape_name else 1
+    if repeat_f is None:
+        repeat_f = REPEAT_F if shape_name in REPEAT_BY_DEFAULT else []
     table = damoe.tune(dl.layer, buckets, EXTENDED_SKEWS, x, samples=samples, reps=reps, seed=seed,
-                       verbose=verbose, ep=ep)
+                       verbose=verbose, ep=ep, repeat_f=repeat_f)
     return table, time.perf_counter() - t0, buckets, dl
 
 
@@ -58,8 +66,12 @@ def main():
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0x7AB1E)
     ap.add_argument("--out", required=True)
+    rep = ap.add_mutually_exclusive_group()
+    rep.add_argument("--no-repeat", action="store_true", help="ddist:X skews only")
+    rep.add_argument("--repeat", action="store_true", help="add the repeated-row exemplars")
     args = ap.parse_args()
-    table, secs, buckets, _ = tune_shape(args.shape, args.max_T, args.samples, args.reps, args.seed)
+    table, secs, buckets, _ = tune_shape(args.shape, args.max_T, args.samples, args.reps, args.seed,
+                                         repeat_f=[] if args.no_repeat else REPEAT_F if args.repeat else None)
     table.save(args.out)
     print(f"tuned {args.shape}: buckets {buckets}, {len(EXTENDED_SKEWS)} skews, S={args.samples}, "
           f"reps={args.reps} in {secs:.1f} s -> {args.out}", file=sys.stderr, flush=True)

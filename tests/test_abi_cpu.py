@@ -278,3 +278,24 @@ def test_effexp_dispatch_validation():
     assert rd(t.handle, P, 4, 3, E, P, P, P, P, P, P, P, P, 1 << 30, None) == -4
     assert L.damoe_table_effexp_map(None, 4, P) == -1
     assert L.damoe_table_effexp_candidates(None, 4) == 0
+
+
+def test_tune_rejects_bad_repeat_config():
+    # Validated before any device work: repeat fractions outside 1..100, a missing array, too
+    # many, or combined with expert parallelism.
+    L = damoe.lib()
+    lay = _fake_layer()
+    bT = np.array([1, 4], np.int32)
+    sx = np.array([1.1, 2.0], np.float64)
+
+    def cfg(n_repeat, rf, ep=1):
+        arr = np.asarray(rf, np.int32)
+        c = damoe.TuneConfig(2, bT.ctypes.data, 2, sx.ctypes.data, 1, 1, 4, 4, 0, 0x10000, 0, ep, n_repeat,
+                             arr.ctypes.data if len(arr) else None)
+        return c, arr
+
+    for n, rf, ep in [(1, [0], 1), (1, [101], 1), (2, [50, -3], 1), (1, [], 1), (65, [50] * 65, 1),
+                      (-1, [], 1), (1, [50], 2)]:
+        c, keep = cfg(n, rf, ep)
+        h = ctypes.c_void_p()
+        assert L.damoe_tune(ctypes.byref(lay), ctypes.byref(c), ctypes.byref(h), None) == -1, (n, rf, ep)

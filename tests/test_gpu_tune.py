@@ -17,13 +17,22 @@ pytestmark = pytest.mark.gpu
 def test_tune_tiny_table(tmp_path):
     torch = torch_cuda()
     from paper_2607_23099_amd.moe import DeviceLayer, Path
-    from paper_2607_23099_amd.tune_tables import EXTENDED_SKEWS, tune_shape
+    from paper_2607_23099_amd.tune_tables import EXTENDED_SKEWS, REPEAT_F, tune_shape
     log("tuning the tiny layer")
     table, secs, buckets, dl = tune_shape("tiny", 64, samples=2, reps=2, seed=5, verbose=False)
     sh = dl.shape
     td = table.data(sh.E)
+    nsk = len(EXTENDED_SKEWS)
     assert list(td.bucket_T) == buckets == [1, 2, 4, 8, 16, 32, 64]
-    assert list(td.n_ex) == [len(EXTENDED_SKEWS)] * len(buckets)
+    assert list(td.n_ex) == [nsk + len(REPEAT_F)] * len(buckets)
+    # Repeated-row exemplars follow the skews'.  At f = 100 every token of a sample takes one
+    # row, so each sample's sorted histogram is k equal counts: the exemplar is k entries of
+    # 2^15 / sqrt(k), then zeros, in every bucket.
+    assert REPEAT_F[-1] == 100
+    step = np.zeros(sh.E, np.int64)
+    step[:sh.k] = int(np.rint(2 ** 15 / np.sqrt(sh.k)))
+    for b in range(len(buckets)):
+        np.testing.assert_array_equal(td.Q[td.bucket_rows(b)][nsk + len(REPEAT_F) - 1], step)
     nv = damoe.num_variants()
     assert td.kid.min() >= 0 and td.kid.max() < nv and td.noda.min() >= 0 and td.noda.max() < nv
     for q in td.Q:
@@ -32,7 +41,7 @@ def test_tune_tiny_table(tmp_path):
     # With enough tokens (T = 64 over 8 experts), a larger skew multiplier X concentrates the
     # exemplar: the most skewed grid point's top entry exceeds the least skewed one's.
     rows = td.bucket_rows(len(buckets) - 1)
-    assert td.Q[rows][-1][0] > td.Q[rows][0][0]
+    assert td.Q[rows][nsk - 1][0] > td.Q[rows][0][0]
     # Save / load round trip, then adaptive dispatch with the tuned table.
     p = str(tmp_path / "tiny.damoe")
     table.save(p)
@@ -50,6 +59,17 @@ def test_tune_tiny_table(tmp_path):
     assert int(path.variant.item()) == int(td.kid[td.bucket_rows(6)][i])
     ref = oracle_rows(sh, r, 31, np.arange(50))
     assert row_err(bf16_rows(path.y, np.arange(50)), ref) <= TOL["bf16"]
+    # A batch of one repeated row scores the f = 100 exemplar at its maximum (cosine 1); the
+    # device picks what the oracle's match picks.  (With E = 8 and k = 2 the most skewed
+    # Dirichlet exemplars are step-shaped as well, so the winner may be one of them.)
+    rr = synth.routing_repeated(sh.E, sh.k, 50, 100, 1.0, [32])
+    path.set_routing(rr)
+    path.route_dispatch(t2, 50)
+    torch.cuda.synchronize()
+    ch = oracle.histogram(rr.ids, sh.E)
+    i, scores = oracle.match(ch, td.Q[td.bucket_rows(6)])
+    assert scores[i] == scores.max() >= int(np.dot(np.sort(ch)[::-1].astype(np.int64), step))
+    assert int(path.variant.item()) == int(td.kid[td.bucket_rows(6)][i])
 
 
 def test_tune_expert_parallel_rank():
@@ -71,5 +91,7 @@ def test_tune_expert_parallel_rank():
         assert np.all(np.diff(q) <= 0) and q[0] > 0
     with pytest.raises(damoe.DamoeError):
         damoe.tune(dl.layer, [1], [1.1], x, samples=1, reps=1, ep=-1)
+    with pytest.raises(damoe.DamoeError):  # repeated rows are not combined with expert parallelism
+        damoe.tune(dl.layer, [1], [1.1], x, samples=1, reps=1, ep=4, repeat_f=[50])
     del dl
     torch.cuda.empty_cache()
