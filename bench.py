@@ -47,7 +47,7 @@ def log(msg):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemm_glu_decode_sweep_traffic.txt")
-GEMM_SOURCES = ("csrc/gemm.hip", "csrc/device.h", "csrc/common.h")
+GEMM_SOURCES = ("csrc/gemm.hip", "csrc/device.h", "csrc/common.h", "csrc/queue.h")
 
 
 def gemm_source_digest() -> str:

@@ -38,7 +38,9 @@ damoe_status device_info(DeviceInfo** out) {
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus <= 0)
       return DAMOE_ERR_HIP;
-    if (gemm_set_lds_limits() != hipSuccess || big_set_lds_limits() != hipSuccess) return DAMOE_ERR_HIP;
+    if (gemm_set_lds_limits() != hipSuccess || big_set_lds_limits() != hipSuccess ||
+        router_set_lds_limits() != hipSuccess)
+      return DAMOE_ERR_HIP;
     d.cus = cus;
     d.ready = true;
   }
@@ -92,6 +94,13 @@ damoe_status layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T, damoe
 }
 
 }  // namespace
+
+// Per-device set-up for the entry points that need no device properties themselves.
+damoe_status damoe::device_setup() {
+  DeviceInfo* d = nullptr;
+  return device_info(&d);
+}
+
 
 struct damoe_table {
   int32_t E, k, H, I, wdtype;

@@ -119,6 +119,9 @@ hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t big_set_lds_limits();
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream);
 hipError_t gemm_set_lds_limits();
+hipError_t router_set_lds_limits();
+// Once per device (thread-safe): the CU count and the LDS limits of every kernel above 64 KB.
+damoe_status device_setup();
 // elem_bytes 0: MXFP4 codes, packed with their row-major E8M0 `scales` into quad fragments.
 hipError_t launch_pack(const void* src, void* dst, int32_t slabs, int32_t rows, int32_t cols, int32_t elem_bytes,
                        hipStream_t stream, const void* scales = nullptr);

@@ -14,6 +14,8 @@
 //                    a wave per token otherwise), adds the bias, selects the top k with an
 //                    order-preserving integer key (ties to the lower expert id) and writes ids
 //                    and softmax gates.
+#include <type_traits>
+
 #include "common.h"
 #include "device.h"
 
@@ -24,6 +26,7 @@ constexpr int kTok = 32;           // tokens per wave tile (MFMA rows)
 constexpr int kExpTile = 64;       // experts per block tile (two 32-wide MFMA blocks)
 constexpr int kStepK = 64;         // k per step: 128 contiguous bytes of each row
 constexpr int kTargetBlocks = 256; // blocks the few-token plan aims for (one per compute unit)
+constexpr int kLdsMinTiles = 8;    // 128-token tiles from which the LDS kernel takes over
 
 struct LogitsArgs {
   const uint16_t* x;   // [T][H]
@@ -159,6 +162,145 @@ __global__ __launch_bounds__(kWave * WT * WK) void k_router_logits(LogitsArgs a)
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const int e = e0 + 32 * c + r;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int t = t0 + 8 * (q >> 2) + 4 * h + (q & 3);
+      if (t < a.T && e < a.E) out[(size_t)t * a.E + e] = acc[c][q];
+    }
+  }
+}
+
+// Many tokens: a block takes 128 tokens (4 waves of 32 rows) and all experts (NE blocks of 32)
+// for one K range of the split, so every token row is read once per split.  The gate rows of
+// each 64-wide K step move into LDS once per block with direct buffer -> LDS loads (two
+// buffers: step st + 1 moves while step st is multiplied) and are shared by the 4 waves; the
+// token rows stream into a ring of NB register sets as in k_router_logits, with the same k
+// assignment (lane (r, h): row r, bytes [64 h, 64 h + 64) of the step; MFMA i takes the i-th
+// 16 bytes), so both operands agree without an LDS transpose.  In LDS a gate row's 16-byte
+// chunk j sits in slot j ^ (row & 7): the 8 lanes an LDS read serves together hit distinct
+// banks.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+typedef uint32_t u32x4_r __attribute__((ext_vector_type(4)));
+
+// 16 bytes per lane from a buffer straight into LDS at dst + 16 lane.
+__device__ __forceinline__ void lds_move16(__amdgpu_buffer_rsrc_t r, lds_u8* dst, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, soff, 0, 0);
+}
+
+// s_waitcnt vmcnt(VM), other counters left alone (gfx9 encoding).
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(VM >= 0 && VM < 64, "counter range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (15 << 8) | ((VM >> 4) << 14));
+}
+
+__device__ __forceinline__ uint4 lds_read16_r(const lds_u8* p) {
+  return __builtin_bit_cast(uint4, *reinterpret_cast<const __attribute__((address_space(3))) u32x4_r*>(p));
+}
+
+template <int NE, int NB>
+__global__ __launch_bounds__(256) void k_router_logits_lds(LogitsArgs a) {
+  extern __shared__ __attribute__((aligned(1024))) uint8_t router_smem[];
+  lds_u8* const lds = (lds_u8*)router_smem;
+  constexpr uint32_t kStage = NE * 32 * 128;  // gate bytes of one K step
+  pin(a.x);
+  pin(a.wg);
+  pin(a.part);
+  pin(a.T);
+  pin(a.H);
+  pin(a.E);
+  pin(a.S);
+  const int b = blockIdx.x;
+  const int item = (b & 7) * a.per_xcd + (b >> 3);
+  if (item >= a.n_items) return;
+  const int tt = item % a.tiles_t;
+  const int s = item / a.tiles_t;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 31, h = lane >> 5;
+  const int t0 = tt * 4 * kTok + wave * kTok;
+  const uint32_t row_bytes = (uint32_t)a.H * 2u;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, (uint32_t)a.T * row_bytes);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.wg, (uint32_t)a.E * row_bytes);
+  const uint32_t vx = (t0 + r < a.T) ? (uint32_t)(t0 + r) * row_bytes + 64u * h : kOobOffset;
+  // Gate rows this thread moves: row 32 p + tid / 8 of each pass p, into slot tid % 8 (a wave's
+  // move covers 8 whole rows, 1 KB of LDS in lane order), holding chunk slot ^ (row & 7).
+  uint32_t vw[NE];
+#pragma unroll
+  for (int p = 0; p < NE; ++p) {
+    const int row = 32 * p + (tid >> 3);
+    const uint32_t chunk = (uint32_t)((tid & 7) ^ (row & 7));
+    vw[p] = row < a.E ? (uint32_t)row * row_bytes + chunk * 16u : kOobOffset;
+  }
+
+  const int steps = a.H / kStepK;
+  const int st0 = (int)((int64_t)s * steps / a.S), st1 = (int)((int64_t)(s + 1) * steps / a.S);
+
+  floatx16 acc[NE];
+#pragma unroll
+  for (int c = 0; c < NE; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[c][i] = 0.0f;
+
+  uint4 xa[NB][4];
+  auto load_x = [&](int st, int slot) __attribute__((always_inline)) {
+    const uint32_t soff = (uint32_t)min(st, st1 - 1) * (kStepK * 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xa[slot][i] = buf_load<uint4, 0>(rx, vx + 16u * i, soff);
+  };
+  auto move_w = [&](int st, int buf) __attribute__((always_inline)) {
+    const uint32_t soff = (uint32_t)min(st, st1 - 1) * (kStepK * 2);
+#pragma unroll
+    for (int p = 0; p < NE; ++p) lds_move16(rw, lds + buf * kStage + (32 * p + 8 * wave) * 128, vw[p], soff);
+  };
+
+  // Each iteration issues NE gate moves and 4 token loads (steps past the last re-issue it, so
+  // the counts stay exact); waiting for all but the newest NE + 8 completes the gate moves of
+  // step st (issued one iteration earlier) and its token loads (NB - 1 iterations earlier).
+  static_assert(NB >= 3 && NE + 8 < 64, "wait count");
+  // One step: free the other buffer, start step st + 1's gate moves into it and the token
+  // loads of step st + NB - 1, wait for step st's, then multiply.  `u` = (st - st0) % NB, the
+  // ring slot of step st (compile-time: the steps run in unrolled groups of NB).
+  auto step = [&](int st, auto u_c) __attribute__((always_inline)) {
+    constexpr int u = decltype(u_c)::value;
+    const int buf = (st - st0) & 1;
+    __syncthreads();  // every wave is done with the buffer step st + 1 moves into
+    move_w(st + 1, buf ^ 1);
+    load_x(st + NB - 1, (u + NB - 1) % NB);
+    wait_vmcnt<NE + 8>();
+    __syncthreads();  // ... and every wave's moves of step st have landed
+    const lds_u8* cur = lds + buf * kStage;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t off = (uint32_t)r * 128u + (uint32_t)(((4 * h + i) ^ (r & 7)) * 16);
+#pragma unroll
+      for (int c = 0; c < NE; ++c) {
+        acc[c] = mfma32x32x16(xa[u][i], lds_read16_r(cur + c * 32 * 128 + off), acc[c]);
+      }
+    }
+  };
+  static_assert(NB == 3, "the step groups below are written for a ring of 3");
+  if (st0 < st1) {  // the plan gives every split a step; st0 and st1 are uniform over the block
+    move_w(st0, 0);
+#pragma unroll
+    for (int u = 0; u < NB - 1; ++u) load_x(st0 + u, u);
+    int st = st0;
+    for (; st + NB <= st1; st += NB) {
+      step(st, std::integral_constant<int, 0>{});
+      step(st + 1, std::integral_constant<int, 1>{});
+      step(st + 2, std::integral_constant<int, 2>{});
+    }
+    if (st < st1) step(st, std::integral_constant<int, 0>{});
+    if (st + 1 < st1) step(st + 1, std::integral_constant<int, 1>{});
+    // The last steps' moves and loads re-read the last step: drain them (moves into LDS must
+    // land before the workgroup ends).
+    wait_vmcnt<0>();
+  }
+
+  float* out = a.part + (size_t)s * a.T * a.E;
+#pragma unroll
+  for (int c = 0; c < NE; ++c) {
+    const int e = 32 * c + r;
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int t = t0 + 8 * (q >> 2) + 4 * h + (q & 3);
@@ -336,14 +478,28 @@ hipError_t launch_topk(const TopkArgs& ta, bool per_block, hipStream_t stream) {
 
 struct Plan {
   int wt, S, tiles_t, tiles_e, n_items, per_xcd;
+  int ne;  // > 0: the LDS kernel with ne 32-expert blocks
 };
+
+// 32-expert blocks the LDS kernel holds for E experts (its instances), 0 if E is too large.
+int lds_blocks(int32_t E) {
+  const int nb = (E + 31) / 32;
+  return nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : nb <= 12 ? 12 : nb <= 16 ? 16 : 0;
+}
 
 Plan plan(int32_t T, int32_t H, int32_t E) {
   Plan p{};
   p.tiles_e = (E + kExpTile - 1) / kExpTile;
   const int steps = H / kStepK;
   const int big_tiles = (T + 4 * kTok - 1) / (4 * kTok);
-  if (big_tiles * p.tiles_e >= kTargetBlocks / 2) {
+  if (big_tiles >= kLdsMinTiles && lds_blocks(E) > 0) {
+    // Many tokens: 128-token tiles over all experts, K split to fill the target grid.
+    p.ne = lds_blocks(E);
+    p.wt = 4;
+    p.tiles_e = 1;
+    p.tiles_t = big_tiles;
+    p.S = std::max(1, std::min((kTargetBlocks + big_tiles - 1) / big_tiles, std::max(1, steps / 4)));
+  } else if (big_tiles * p.tiles_e >= kTargetBlocks / 2) {
     p.wt = 4;
     p.S = 1;
     p.tiles_t = big_tiles;
@@ -369,6 +525,7 @@ size_t partial_bytes(int32_t T, int32_t H, int32_t E) {
 }
 
 }  // namespace
+
 }  // namespace damoe
 
 using namespace damoe;
@@ -380,8 +537,9 @@ size_t damoe_router_workspace_size(int32_t E, int32_t H, int32_t T_max) {
   // The split count falls as T grows, so S * T is not monotone: take the largest over T <= T_max.
   // Above the point where a single split fills the target grid S is 1 and S * T = T.
   size_t best = partial_bytes(T_max, H, E);
-  const int32_t tiles_e = (E + kExpTile - 1) / kExpTile;
-  const int32_t t_split = std::min<int32_t>(T_max, (kTargetBlocks / tiles_e + 1) * kTok);
+  // Both split plans have S = 1 once T fills the target grid with 32-token (few-token plan)
+  // or 128-token (LDS plan) tiles alone.
+  const int32_t t_split = std::min<int32_t>(T_max, (kTargetBlocks + 1) * 4 * kTok);
   for (int32_t T = 1; T <= t_split; ++T) best = std::max(best, partial_bytes(T, H, E));
   return std::max<size_t>(256, (best + 255) / 256 * 256);
 }
@@ -398,15 +556,31 @@ damoe_status damoe_router(const uint16_t* x, const uint16_t* wg, const float* bi
   if (ws_bytes < partial_bytes(T, H, E)) return DAMOE_ERR_WORKSPACE;
   if (!x || !wg || !topk_ids || !topk_w || !ws) return DAMOE_ERR_INVALID_ARG;
   const Plan p = plan(T, H, E);
+  if (p.ne > 0) {
+    const damoe_status st = device_setup();  // the LDS kernels' limits
+    if (st != DAMOE_OK) return st;
+  }
   LogitsArgs la{x, wg, static_cast<float*>(ws), T, H, E, p.S, p.tiles_t, p.tiles_e, p.n_items, p.per_xcd};
   const dim3 grid(8 * p.per_xcd);
-  if (p.wt == 4)
+  if (p.ne > 0) {
+    const size_t lds = 2 * (size_t)p.ne * 32 * 128;
+    switch (p.ne) {
+      case 2: hipLaunchKernelGGL((k_router_logits_lds<2, 3>), grid, dim3(256), lds, stream, la); break;
+      case 4: hipLaunchKernelGGL((k_router_logits_lds<4, 3>), grid, dim3(256), lds, stream, la); break;
+      case 8: hipLaunchKernelGGL((k_router_logits_lds<8, 3>), grid, dim3(256), lds, stream, la); break;
+      case 12: hipLaunchKernelGGL((k_router_logits_lds<12, 3>), grid, dim3(256), lds, stream, la); break;
+      default: hipLaunchKernelGGL((k_router_logits_lds<16, 3>), grid, dim3(256), lds, stream, la); break;
+    }
+  } else if (p.wt == 4) {
     hipLaunchKernelGGL((k_router_logits<4, 2, 3>), grid, dim3(512), 0, stream, la);
-  else
+  } else {
     hipLaunchKernelGGL((k_router_logits<1, 4, 2>), grid, dim3(256), 0, stream, la);
+  }
   if (hipGetLastError() != hipSuccess) return DAMOE_ERR_HIP;
   TopkArgs ta{static_cast<const float*>(ws), bias, logits, topk_ids, topk_w, T, E, k, p.S};
-  const bool per_block = p.S > 2;
+  // A block per token for many splits at few tokens; a wave per token otherwise (at thousands
+  // of tokens a block each costs more in scheduling than a few partials per lane do).
+  const bool per_block = p.S > 8 || (p.S > 2 && T <= 1024);
   const int groups = (E + kWave - 1) / kWave;
   const hipError_t e = groups <= 1   ? launch_topk<1>(ta, per_block, stream)
                        : groups <= 2 ? launch_topk<2>(ta, per_block, stream)
@@ -417,3 +591,23 @@ damoe_status damoe_router(const uint16_t* x, const uint16_t* wg, const float* bi
 }
 
 }  // extern "C"
+
+namespace damoe {
+
+// Dynamic LDS above 64 KB needs the per-kernel limit (set once per device).
+hipError_t router_set_lds_limits() {
+  const void* fns[] = {reinterpret_cast<const void*>(&k_router_logits_lds<2, 3>),
+                       reinterpret_cast<const void*>(&k_router_logits_lds<4, 3>),
+                       reinterpret_cast<const void*>(&k_router_logits_lds<8, 3>),
+                       reinterpret_cast<const void*>(&k_router_logits_lds<12, 3>),
+                       reinterpret_cast<const void*>(&k_router_logits_lds<16, 3>)};
+  const int ne[] = {2, 4, 8, 12, 16};
+  for (int i = 0; i < 5; ++i) {
+    const hipError_t e =
+        hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, 2 * ne[i] * 32 * 128);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace damoe
