@@ -170,15 +170,6 @@ __global__ __launch_bounds__(kWave * WT * WK) void k_router_logits(LogitsArgs a)
   }
 }
 
-// Many tokens: a block takes 128 tokens (4 waves of 32 rows) and all experts (NE blocks of 32)
-// for one K range of the split, so every token row is read once per split.  The gate rows of
-// each 64-wide K step move into LDS once per block with direct buffer -> LDS loads (two
-// buffers: step st + 1 moves while step st is multiplied) and are shared by the 4 waves; the
-// token rows stream into a ring of NB register sets as in k_router_logits, with the same k
-// assignment (lane (r, h): row r, bytes [64 h, 64 h + 64) of the step; MFMA i takes the i-th
-// 16 bytes), so both operands agree without an LDS transpose.  In LDS a gate row's 16-byte
-// chunk j sits in slot j ^ (row & 7): the 8 lanes an LDS read serves together hit distinct
-// banks.
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 typedef uint32_t u32x4_r __attribute__((ext_vector_type(4)));
 
@@ -198,11 +189,30 @@ __device__ __forceinline__ uint4 lds_read16_r(const lds_u8* p) {
   return __builtin_bit_cast(uint4, *reinterpret_cast<const __attribute__((address_space(3))) u32x4_r*>(p));
 }
 
+// Many tokens: a block takes 128 tokens and all experts (NE blocks of 32, a quarter of them per
+// wave) for one K range of the split, so every token row is read once per split and every gate
+// row once per block.  The token rows of each 64-wide K step move into LDS once per block with
+// direct buffer -> LDS loads (two buffers: step st + 1 moves while step st is multiplied) and
+// are shared by the 4 waves; each wave streams its own gate rows into a ring of NB register
+// sets.  The k assignment is k_router_logits' (lane (r, h): row r, bytes [64 h, 64 h + 64) of
+// the step; MFMA i takes the i-th 16 bytes) for both operands, so no LDS transpose is needed.
+// The token stages are a ring of ND in LDS, moved ND - 1 steps ahead: the rows come from HBM
+// once, and one step of lead did not cover the miss latency.
+// In LDS a token row's 16-byte chunk j sits in slot j ^ (row & 7): the 8 lanes an LDS read
+// serves together hit distinct banks.  Per MFMA a wave reads 1 KB of LDS (one token
+// fragment) where holding the gate in LDS would cost one gate fragment per wave and token
+// block (twice the LDS traffic at E = 256).
+constexpr int kRouterStages = 4;  // token stages in LDS (16 KB each)
+
 template <int NE, int NB>
 __global__ __launch_bounds__(256) void k_router_logits_lds(LogitsArgs a) {
+  static_assert(NE % 4 == 0, "a quarter of the expert blocks per wave");
+  constexpr int NW = NE / 4;                 // 32-expert blocks per wave
+  constexpr int TB = 4;                      // 32-token blocks per block tile (128 tokens)
+  constexpr int ND = kRouterStages;
+  constexpr uint32_t kStage = TB * 32 * 128; // token bytes of one K step (16 KB)
   extern __shared__ __attribute__((aligned(1024))) uint8_t router_smem[];
   lds_u8* const lds = (lds_u8*)router_smem;
-  constexpr uint32_t kStage = NE * 32 * 128;  // gate bytes of one K step
   pin(a.x);
   pin(a.wg);
   pin(a.part);
@@ -218,72 +228,85 @@ __global__ __launch_bounds__(256) void k_router_logits_lds(LogitsArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r = lane & 31, h = lane >> 5;
-  const int t0 = tt * 4 * kTok + wave * kTok;
+  const int t0 = tt * TB * 32;
+  const int e0 = wave * NW * 32;
   const uint32_t row_bytes = (uint32_t)a.H * 2u;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, (uint32_t)a.T * row_bytes);
   const __amdgpu_buffer_rsrc_t rw = make_rsrc(a.wg, (uint32_t)a.E * row_bytes);
-  const uint32_t vx = (t0 + r < a.T) ? (uint32_t)(t0 + r) * row_bytes + 64u * h : kOobOffset;
-  // Gate rows this thread moves: row 32 p + tid / 8 of each pass p, into slot tid % 8 (a wave's
+  // Token rows this thread moves: row 32 p + tid / 8 of each pass p, into slot tid % 8 (a wave's
   // move covers 8 whole rows, 1 KB of LDS in lane order), holding chunk slot ^ (row & 7).
-  uint32_t vw[NE];
+  uint32_t vx[TB];
 #pragma unroll
-  for (int p = 0; p < NE; ++p) {
+  for (int p = 0; p < TB; ++p) {
     const int row = 32 * p + (tid >> 3);
     const uint32_t chunk = (uint32_t)((tid & 7) ^ (row & 7));
-    vw[p] = row < a.E ? (uint32_t)row * row_bytes + chunk * 16u : kOobOffset;
+    vx[p] = t0 + row < a.T ? (uint32_t)(t0 + row) * row_bytes + chunk * 16u : kOobOffset;
+  }
+  uint32_t vw[NW];
+#pragma unroll
+  for (int c = 0; c < NW; ++c) {
+    const int e = e0 + 32 * c + r;
+    vw[c] = e < a.E ? (uint32_t)e * row_bytes + 64u * h : kOobOffset;
   }
 
   const int steps = a.H / kStepK;
   const int st0 = (int)((int64_t)s * steps / a.S), st1 = (int)((int64_t)(s + 1) * steps / a.S);
 
-  floatx16 acc[NE];
+  floatx16 acc[TB][NW];
 #pragma unroll
-  for (int c = 0; c < NE; ++c)
+  for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[c][i] = 0.0f;
+    for (int c = 0; c < NW; ++c)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[tb][c][i] = 0.0f;
 
-  uint4 xa[NB][4];
-  auto load_x = [&](int st, int slot) __attribute__((always_inline)) {
+  uint4 wr[NB][NW][4];
+  auto load_w = [&](int st, int slot) __attribute__((always_inline)) {
     const uint32_t soff = (uint32_t)min(st, st1 - 1) * (kStepK * 2);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xa[slot][i] = buf_load<uint4, 0>(rx, vx + 16u * i, soff);
+    for (int c = 0; c < NW; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wr[slot][c][i] = buf_load<uint4, 0>(rw, vw[c] + 16u * i, soff);
   };
-  auto move_w = [&](int st, int buf) __attribute__((always_inline)) {
+  auto move_x = [&](int st, int buf) __attribute__((always_inline)) {
     const uint32_t soff = (uint32_t)min(st, st1 - 1) * (kStepK * 2);
 #pragma unroll
-    for (int p = 0; p < NE; ++p) lds_move16(rw, lds + buf * kStage + (32 * p + 8 * wave) * 128, vw[p], soff);
+    for (int p = 0; p < TB; ++p) lds_move16(rx, lds + buf * kStage + (32 * p + 8 * wave) * 128, vx[p], soff);
   };
 
-  // Each iteration issues NE gate moves and 4 token loads (steps past the last re-issue it, so
-  // the counts stay exact); waiting for all but the newest NE + 8 completes the gate moves of
-  // step st (issued one iteration earlier) and its token loads (NB - 1 iterations earlier).
-  static_assert(NB >= 3 && NE + 8 < 64, "wait count");
-  // One step: free the other buffer, start step st + 1's gate moves into it and the token
-  // loads of step st + NB - 1, wait for step st's, then multiply.  `u` = (st - st0) % NB, the
-  // ring slot of step st (compile-time: the steps run in unrolled groups of NB).
+  // Step j issues the TB token moves of step j + ND - 1, then the 4 NW gate loads of step
+  // j + NB - 1 (steps past the last re-issue it, so the counts stay exact).  Waiting for all
+  // but the newest two steps' operations completes everything issued up to step j - 2, which
+  // holds step j's moves (issued at j - ND + 1) and gate loads (issued at j - NB + 1).
+  constexpr int kWait = 2 * (TB + 4 * NW);
+  static_assert(NB == 3 && ND >= NB && kWait < 64, "wait count");
   auto step = [&](int st, auto u_c) __attribute__((always_inline)) {
     constexpr int u = decltype(u_c)::value;
-    const int buf = (st - st0) & 1;
-    __syncthreads();  // every wave is done with the buffer step st + 1 moves into
-    move_w(st + 1, buf ^ 1);
-    load_x(st + NB - 1, (u + NB - 1) % NB);
-    wait_vmcnt<NE + 8>();
+    const int rel = st - st0;
+    __syncthreads();  // every wave is done with the stage step st + ND - 1 moves into
+    move_x(st + ND - 1, (rel + ND - 1) % ND);
+    load_w(st + NB - 1, (u + NB - 1) % NB);
+    wait_vmcnt<kWait>();
     __syncthreads();  // ... and every wave's moves of step st have landed
-    const lds_u8* cur = lds + buf * kStage;
+    const lds_u8* cur = lds + (rel % ND) * kStage;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint32_t off = (uint32_t)r * 128u + (uint32_t)(((4 * h + i) ^ (r & 7)) * 16);
 #pragma unroll
-      for (int c = 0; c < NE; ++c) {
-        acc[c] = mfma32x32x16(xa[u][i], lds_read16_r(cur + c * 32 * 128 + off), acc[c]);
+      for (int tb = 0; tb < TB; ++tb) {
+        const uint4 xf = lds_read16_r(cur + tb * 32 * 128 + off);
+#pragma unroll
+        for (int c = 0; c < NW; ++c) acc[tb][c] = mfma32x32x16(xf, wr[u][c][i], acc[tb][c]);
       }
     }
   };
-  static_assert(NB == 3, "the step groups below are written for a ring of 3");
   if (st0 < st1) {  // the plan gives every split a step; st0 and st1 are uniform over the block
-    move_w(st0, 0);
+    // The same issue order as the steps: moves of step d, then the gate loads of step d.
 #pragma unroll
-    for (int u = 0; u < NB - 1; ++u) load_x(st0 + u, u);
+    for (int d = 0; d < ND - 1; ++d) {
+      move_x(st0 + d, d);
+      if (d < NB - 1) load_w(st0 + d, d);
+    }
     int st = st0;
     for (; st + NB <= st1; st += NB) {
       step(st, std::integral_constant<int, 0>{});
@@ -297,16 +320,20 @@ __global__ __launch_bounds__(256) void k_router_logits_lds(LogitsArgs a) {
     wait_vmcnt<0>();
   }
 
+  // Accumulator register q of block (tb, c): token 32 tb + 8 (q / 4) + 4 h + q % 4, expert
+  // e0 + 32 c + r.
   float* out = a.part + (size_t)s * a.T * a.E;
 #pragma unroll
-  for (int c = 0; c < NE; ++c) {
-    const int e = 32 * c + r;
+  for (int tb = 0; tb < TB; ++tb)
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int t = t0 + 8 * (q >> 2) + 4 * h + (q & 3);
-      if (t < a.T && e < a.E) out[(size_t)t * a.E + e] = acc[c][q];
+    for (int c = 0; c < NW; ++c) {
+      const int e = e0 + 32 * c + r;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int t = t0 + 32 * tb + 8 * (q >> 2) + 4 * h + (q & 3);
+        if (t < a.T && e < a.E) out[(size_t)t * a.E + e] = acc[tb][c][q];
+      }
     }
-  }
 }
 
 // Order-preserving key of a float: larger float -> larger unsigned key; -0 is taken as +0.
@@ -484,7 +511,7 @@ struct Plan {
 // 32-expert blocks the LDS kernel holds for E experts (its instances), 0 if E is too large.
 int lds_blocks(int32_t E) {
   const int nb = (E + 31) / 32;
-  return nb <= 2 ? 2 : nb <= 4 ? 4 : nb <= 8 ? 8 : nb <= 12 ? 12 : nb <= 16 ? 16 : 0;
+  return nb <= 4 ? 4 : nb <= 8 ? 8 : nb <= 12 ? 12 : nb <= 16 ? 16 : 0;
 }
 
 Plan plan(int32_t T, int32_t H, int32_t E) {
@@ -563,9 +590,8 @@ damoe_status damoe_router(const uint16_t* x, const uint16_t* wg, const float* bi
   LogitsArgs la{x, wg, static_cast<float*>(ws), T, H, E, p.S, p.tiles_t, p.tiles_e, p.n_items, p.per_xcd};
   const dim3 grid(8 * p.per_xcd);
   if (p.ne > 0) {
-    const size_t lds = 2 * (size_t)p.ne * 32 * 128;
+    const size_t lds = (size_t)kRouterStages * 4 * 32 * 128;  // 128-token x 64-k stages
     switch (p.ne) {
-      case 2: hipLaunchKernelGGL((k_router_logits_lds<2, 3>), grid, dim3(256), lds, stream, la); break;
       case 4: hipLaunchKernelGGL((k_router_logits_lds<4, 3>), grid, dim3(256), lds, stream, la); break;
       case 8: hipLaunchKernelGGL((k_router_logits_lds<8, 3>), grid, dim3(256), lds, stream, la); break;
       case 12: hipLaunchKernelGGL((k_router_logits_lds<12, 3>), grid, dim3(256), lds, stream, la); break;
@@ -596,15 +622,12 @@ namespace damoe {
 
 // Dynamic LDS above 64 KB needs the per-kernel limit (set once per device).
 hipError_t router_set_lds_limits() {
-  const void* fns[] = {reinterpret_cast<const void*>(&k_router_logits_lds<2, 3>),
-                       reinterpret_cast<const void*>(&k_router_logits_lds<4, 3>),
+  const void* fns[] = {reinterpret_cast<const void*>(&k_router_logits_lds<4, 3>),
                        reinterpret_cast<const void*>(&k_router_logits_lds<8, 3>),
                        reinterpret_cast<const void*>(&k_router_logits_lds<12, 3>),
                        reinterpret_cast<const void*>(&k_router_logits_lds<16, 3>)};
-  const int ne[] = {2, 4, 8, 12, 16};
-  for (int i = 0; i < 5; ++i) {
-    const hipError_t e =
-        hipFuncSetAttribute(fns[i], hipFuncAttributeMaxDynamicSharedMemorySize, 2 * ne[i] * 32 * 128);
+  for (const void* f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kRouterStages * 4 * 32 * 128);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
