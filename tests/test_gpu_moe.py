@@ -102,6 +102,33 @@ def test_tiny_dispatch_outside_candidates_is_flagged(tiny):
 SMALL_FP8 = synth.Shape("small-fp8", E=8, k=2, H=512, I=1024, shape_id=5, wdtype="fp8")
 
 
+def test_tiny_large_tile_calls_repeat_after_one_route(tiny):
+    # The tiled and big-tile kernels take their items from work queues whose counters live in
+    # the workspace: each launch returns them to zero, so fused calls repeated after one routing
+    # call (as a tuner or a graph replay makes them) compute the same layer, bit for bit.
+    torch = torch_cuda()
+    dl, path = tiny
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, 250, 0.3, [77])
+    rows = np.arange(0, 250, 37)
+    ref = oracle_rows(sh, r, 77, rows)
+    big = [v for v in _variants() if damoe.variant_tile_m(v) >= 128]
+    assert big
+    _run(path, r, 77, big[0])
+    for v in big:
+        outs = []
+        for rep in range(3):
+            path.y.fill_(float("nan"))
+            path.fused(r.T, v)
+            torch.cuda.synchronize()
+            outs.append(path.y[:r.T].clone())
+        log(f"tiny repeated calls variant={damoe.variant_name(v)}")
+        assert row_err(bf16_rows(outs[0], rows), ref) <= TOL["bf16"]
+        for o in outs[1:]:
+            assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    assert damoe.read_device_error(path.ws) == 0
+
+
 @pytest.fixture(scope="module", params=[False, True], ids=["rowmajor", "packed"])
 def small_fp8(request):
     torch = torch_cuda()

@@ -72,6 +72,8 @@ def _host_case(T, H, E, seed, bias_alpha):
     (5, 64, 3, 3, None),         # k = E, one K step
     (300, 512, 1024, 16, 0.05),  # largest E and k
     (1000, 192, 40, 4, None),    # many token tiles, three K steps
+    (1100, 256, 512, 8, 0.5),    # the LDS kernel's largest expert count (16 blocks of 32)
+    (1500, 384, 300, 6, None),   # the LDS kernel with a ragged last expert block, six K steps
 ])
 def test_router_small_shapes(T, H, E, k, bias_alpha):
     torch = torch_cuda()
