@@ -130,6 +130,10 @@ typedef struct damoe_layer {
  *                the routing call clears them and each launch leaves them cleared)
  *   tiles[s]   : token tiles for tile size BM_s = 16 << s: int32 n_tiles, int32 pad,
  *                then n_tiles entries of int32x2 {start position, expert | rows << 16}
+ *   route      : scratch of the routing call at T k >= 8192 (per-block counts and
+ *                segment offsets of its 2048-assignment blocks, int32 [E][nb4] each,
+ *                nb4 the block count rounded up to a multiple of 4, then each expert's
+ *                first tile of each tile size, int32 [DAMOE_N_TILE_SIZES][E]); empty below
  *   h          : bf16 [T*k][I]   SwiGLU activations in permuted order
  *   out        : fp32 [T*k][H]   GEMM2 output in permuted order                     */
 typedef struct damoe_ws_layout {
@@ -139,6 +143,7 @@ typedef struct damoe_ws_layout {
   size_t tiles_cap; /* entries each tile list can hold */
   size_t h;
   size_t out;
+  size_t route;     /* routing scratch (before h; the routing calls need ws up to h) */
 } damoe_ws_layout;
 
 damoe_status damoe_workspace_layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T,

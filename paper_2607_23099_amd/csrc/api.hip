@@ -85,6 +85,8 @@ damoe_status layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T, damoe
     o->tiles[c] = off;
     off += align_up(8 + 8 * o->tiles_cap);
   }
+  o->route = off;
+  off += align_up(route_scratch_bytes(A, E));
   o->h = off;
   off += align_up((size_t)A * I * 2);
   o->out = off;
@@ -233,7 +235,8 @@ static damoe_status route_impl(const int32_t* topk_ids, int32_t T, int32_t k, in
   int32_t* lists[DAMOE_N_TILE_SIZES];
   for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) lists[c] = reinterpret_cast<int32_t*>(base + lo.tiles[c]);
   const hipError_t e = launch_route(topk_ids, T, k, E, counts, offsets, perm, inv_perm, numden, bucket,
-                                    reinterpret_cast<int32_t*>(base + lo.ctrl), lists, d, stream);
+                                    reinterpret_cast<int32_t*>(base + lo.ctrl), lists, d,
+                                    reinterpret_cast<int32_t*>(base + lo.route), stream);
   return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
 }
 
@@ -286,7 +289,7 @@ damoe_status damoe_route_dispatch_effexp(const damoe_table* t, const int32_t* to
   const hipError_t e = launch_route_effexp(topk_ids, T, k, E, counts, offsets, perm, inv_perm, effexp_numden,
                                            effexp_bucket, reinterpret_cast<int32_t*>(base + lo.ctrl), lists,
                                            t->d_effmap + (size_t)table_bucket(t, T) * kEffMapLen, variant_id,
-                                           stream);
+                                           reinterpret_cast<int32_t*>(base + lo.route), stream);
   return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
 }
 

@@ -23,6 +23,20 @@ constexpr int kCtrlWords = 64;
 // and each big-tile launch returns them to zero when its last workgroup finishes.
 constexpr int kQueueCtrl = 8;
 constexpr int kQueueWords = 9;
+// Routing of many assignments runs over blocks of kRouteChunk (a histogram per block, the
+// one-workgroup pass over their counts, a scatter per block); from kRouteMultiMinA on.  Its
+// scratch in the workspace: per-block counts and per-block segment offsets, [E][route_row]
+// each (one row per expert, the blocks padded to a multiple of 4 for 16-byte access), then
+// each expert's first tile in the list of each tile size, [DAMOE_N_TILE_SIZES][E].
+constexpr int32_t kRouteChunk = 2048;
+constexpr int64_t kRouteMultiMinA = 8192;
+inline int32_t route_blocks(int64_t A) { return (int32_t)((A + kRouteChunk - 1) / kRouteChunk); }
+__host__ __device__ inline int32_t route_row(int32_t nb) { return (nb + 3) & ~3; }
+inline size_t route_scratch_bytes(int64_t A, int32_t E) {
+  return A >= kRouteMultiMinA
+             ? (2 * (size_t)route_row(route_blocks(A)) + DAMOE_N_TILE_SIZES) * E * sizeof(int32_t)
+             : 0;
+}
 
 // ---------------------------------------------------------------------------------------------
 // Variant registry.  A variant is one template instance of the grouped GEMM pair; all variants
@@ -108,7 +122,7 @@ struct DispatchArgs {
 hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
                         int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                         int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
-                        const DispatchArgs* dispatch, hipStream_t stream);
+                        const DispatchArgs* dispatch, int32_t* scratch, hipStream_t stream);
 hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
                            hipStream_t stream);
 // Grouped GEMM stages on a persistent grid sized from the device's CU count.

@@ -27,6 +27,6 @@ constexpr int kEffMapLen = 15;
 hipError_t launch_route_effexp(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
                                int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                                int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
-                               const int32_t* eff_map, int32_t* variant_id, hipStream_t stream);
+                               const int32_t* eff_map, int32_t* variant_id, int32_t* scratch, hipStream_t stream);
 
 }  // namespace damoe

@@ -128,6 +128,10 @@ struct RouteOut {
   int32_t* bucket;
   int32_t* ctrl;
   TileOut tiles;
+  int32_t* bcnt;   // multi-block path: per-block counts [E][route_row(nb)] (read),
+  int32_t* boff;   // each block's start inside the segment of each expert, same shape,
+  int32_t* tst;    // and each expert's first tile in the list of each tile size [sizes][E]
+  int32_t nb;
 };
 
 struct Smem {
@@ -236,7 +240,7 @@ __device__ void dispatch_core(Smem& sm, int E, int total, int ci, const Dispatch
 // the wave's counter of that expert.  Per expert, an exclusive scan of the 16 wave counts
 // gives each wave's starting offset in the expert's segment, so the order inside a segment
 // is the flat order a = t k + j.
-template <bool DISPATCH>
+template <bool DISPATCH, bool MULTI>
 __global__ void __launch_bounds__(kRouteThreads)
 k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, DispatchIn d) {
   __shared__ Smem sm;
@@ -269,7 +273,8 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     const int r = lane + 64 * m;
     qpre[m] = (DISPATCH && w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
   }
-  for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wcnt[x / E][x % E] = 0;
+  if (!MULTI)
+    for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wcnt[x / E][x % E] = 0;
   if (DISPATCH)
     for (int v = tid; v < kValueBins; v += kRouteThreads) sm.vh[v] = 0;
   if (tid == 0) {
@@ -287,6 +292,7 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   const bool one_batch = R <= 64 * kIdBatch;
   int bad = 0;
   int eb[kIdBatch];
+  if (!MULTI)
   for (int a0 = a_lo; a0 < a_hi; a0 += 64 * kIdBatch) {
     // Unconditional loads (index clamped into the range) so the batch issues back to back.
 #pragma unroll
@@ -311,14 +317,43 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     for (int m = 0; m < kMaxExemplarRegs; ++m) sm.qpre[w][lane + 64 * m] = qpre[m];
   __syncthreads();
 
-  // Per expert: the wave counts become each wave's starting offset inside the segment.
+  // Per expert: the wave counts become each wave's starting offset inside the segment (the
+  // multi-block path sums the blocks' counts instead).
   int c = 0;
   if (tid < E) {
+    if (MULTI) {
+      // Running sum over the blocks, 16 at a time from this expert's row of counts; each
+      // block's start relative to the expert's segment goes to its row of boff (the scatter
+      // adds the segment start).  Entries from nb to the padded row length are left alone.
+      const int nbp = route_row(o.nb);
+      const int4* cr = reinterpret_cast<const int4*>(o.bcnt + (size_t)tid * nbp);
+      int4* orow = reinterpret_cast<int4*>(o.boff + (size_t)tid * nbp);
+      for (int b0 = 0; b0 < o.nb; b0 += 16) {
+        int4 t[4];
 #pragma unroll
-    for (int u = 0; u < kNW; ++u) {
-      const uint32_t t = sm.wcnt[u][tid];
-      sm.wcnt[u][tid] = (uint32_t)c;
-      c += (int)t;
+        for (int u = 0; u < 4; ++u) t[u] = b0 + 4 * u < nbp ? cr[b0 / 4 + u] : make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int b = b0 + 4 * u;
+          int4 r;
+          r.x = c;
+          c += b + 0 < o.nb ? t[u].x : 0;
+          r.y = c;
+          c += b + 1 < o.nb ? t[u].y : 0;
+          r.z = c;
+          c += b + 2 < o.nb ? t[u].z : 0;
+          r.w = c;
+          c += b + 3 < o.nb ? t[u].w : 0;
+          if (b < nbp) orow[b0 / 4 + u] = r;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kNW; ++u) {
+        const uint32_t t = sm.wcnt[u][tid];
+        sm.wcnt[u][tid] = (uint32_t)c;
+        c += (int)t;
+      }
     }
     sm.cnt[tid] = c;
     if (c >= kValueBins) sm.big = 1;
@@ -359,18 +394,27 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     if (sm.bad) atomicOr(&o.ctrl[0], DAMOE_DEVERR_EXPERT_ID);
   }
   if (tid < kQueueWords) o.ctrl[kQueueCtrl + tid] = 0;
+  if (tid == 0)
 #pragma unroll
-  for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
-    const int bm = 16 << cls;
-    int32_t* list = o.tiles.list[cls];
-    if (tid == 0) {
-      list[0] = tot[1 + cls];
-      list[1] = 0;
+    for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
+      o.tiles.list[cls][0] = tot[1 + cls];
+      o.tiles.list[cls][1] = 0;
     }
-    int2* ent = reinterpret_cast<int2*>(list + 2);
-    for (int jt = 0; jt < v[1 + cls]; ++jt) {
-      const int rows = min(bm, c - jt * bm);
-      ent[ex[1 + cls] + jt] = make_int2(off + jt * bm, tid | (rows << 16));
+  if (MULTI) {
+    // Many tiles: k_route_scatter writes the lists; here each class's tile start per expert.
+    if (tid < E)
+#pragma unroll
+      for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) o.tst[cls * E + tid] = ex[1 + cls];
+  } else {
+    // Few tiles: each expert's thread writes its own.
+#pragma unroll
+    for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
+      const int bm = 16 << cls;
+      int2* ent = reinterpret_cast<int2*>(o.tiles.list[cls] + 2);
+      for (int jt = 0; jt < v[1 + cls]; ++jt) {
+        const int rows = min(bm, c - jt * bm);
+        ent[ex[1 + cls] + jt] = make_int2(off + jt * bm, tid | (rows << 16));
+      }
     }
   }
 
@@ -383,6 +427,7 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     o.ctrl[2] = 0;
     o.ctrl[3] = 0;
   }
+  if (MULTI) return;  // the blocks scatter in k_route_scatter
   __syncthreads();  // segment bases
 
   // a4: stable scatter, per wave over its own range.
@@ -410,6 +455,106 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
       }
       if (valid && rank == 0) sm.wcnt[w][e] += (uint32_t)__popcll(peers);
     }
+  }
+}
+
+// Many assignments, part 1: block b's histogram of assignments [b C, b C + C) (C =
+// kRouteChunk) into bcnt[e][b] (rows of route_row(nb) entries): per 64 ids a ballot multisplit finds the lanes of each expert
+// and the first of them adds their number in LDS.  Out-of-range ids set the device error here.
+__global__ void __launch_bounds__(kRouteThreads)
+k_route_hist(const int32_t* __restrict__ ids, int32_t A, int32_t E, int32_t* __restrict__ bcnt,
+             int32_t* __restrict__ ctrl) {
+  __shared__ int lc[DAMOE_MAX_E];
+  __shared__ int lbad;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, b = blockIdx.x;
+  for (int e = tid; e < E; e += kRouteThreads) lc[e] = 0;
+  if (tid == 0) lbad = 0;
+  __syncthreads();
+  int nbits = 1;
+  while ((1 << nbits) < E) ++nbits;
+  const int a_lo = b * kRouteChunk, a_hi = min(A, a_lo + kRouteChunk);
+  int bad = 0;
+  for (int a0 = a_lo + 64 * w; a0 < a_hi; a0 += 64 * kNW) {  // wave-uniform bounds
+    const int a = a0 + lane;
+    const int e = a < a_hi ? ids[a] : -1;
+    bad += (a < a_hi && e >= E) ? 1 : 0;  // negative ids are masked slots, not errors
+    const bool valid = e >= 0 && e < E;
+    const uint64_t peers = same_expert(e, valid, nbits);
+    if (valid && (peers & lanemask_lt()) == 0) atomicAdd(&lc[e], (int)__popcll(peers));
+  }
+  if (bad) atomicAdd(&lbad, bad);
+  __syncthreads();
+  const int nbp = route_row((int)gridDim.x);
+  for (int e = tid; e < E; e += kRouteThreads) bcnt[(size_t)e * nbp + b] = lc[e];
+  if (tid == 0 && lbad) atomicOr(&ctrl[0], DAMOE_DEVERR_EXPERT_ID);
+}
+
+// Many assignments, part 3: block b scatters its assignments from offsets[e] + boff[e][b] on
+// (boff: the start of block b inside the segment of expert e), wave w taking
+// the contiguous range [b C + w C / 16, + C / 16) in order, so perm is the stable (expert, a)
+// order across blocks and waves alike.
+__global__ void __launch_bounds__(kRouteThreads)
+k_route_scatter(const int32_t* __restrict__ ids, int32_t A, int32_t E, const int32_t* __restrict__ counts,
+                const int32_t* __restrict__ offsets, const int32_t* __restrict__ boff,
+                const int32_t* __restrict__ tst, TileOut tiles, int32_t* __restrict__ perm,
+                int32_t* __restrict__ inv_perm) {
+  constexpr int RW = kRouteChunk / kNW;  // assignments per wave
+  constexpr int NQ = RW / 64;
+  static_assert(RW % 64 == 0, "whole 64-id chunks per wave");
+  __shared__ uint32_t wc[kNW][DAMOE_MAX_E];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, b = blockIdx.x;
+  for (int x = tid; x < kNW * E; x += kRouteThreads) wc[x / E][x % E] = 0;
+  __syncthreads();
+  int nbits = 1;
+  while ((1 << nbits) < E) ++nbits;
+  const int w_lo = b * kRouteChunk + w * RW, w_hi = min(A, w_lo + RW);
+  int eb[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int a = w_lo + 64 * q + lane;
+    eb[q] = a < w_hi ? ids[a] : -1;
+  }
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const bool valid = eb[q] >= 0 && eb[q] < E;
+    const uint64_t peers = same_expert(eb[q], valid, nbits);
+    if (valid && (peers & lanemask_lt()) == 0) wc[w][eb[q]] += (uint32_t)__popcll(peers);
+  }
+  __syncthreads();
+  if (tid < E) {  // wave counts -> each wave's start: the block's offset plus earlier waves'
+    uint32_t run = (uint32_t)(offsets[tid] + boff[(size_t)tid * route_row((int)gridDim.x) + b]);
+#pragma unroll
+    for (int u = 0; u < kNW; ++u) {
+      const uint32_t t = wc[u][tid];
+      wc[u][tid] = run;
+      run += t;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int a = w_lo + 64 * q + lane, e = eb[q];
+    const bool valid = e >= 0 && e < E;
+    const uint64_t peers = same_expert(e, valid, nbits);
+    const int rank = __popcll(peers & lanemask_lt());
+    if (valid) {
+      const int p = (int)wc[w][e] + rank;
+      perm[p] = a;
+      inv_perm[a] = p;
+    } else if (a < w_hi) {
+      inv_perm[a] = -1;
+    }
+    if (valid && rank == 0) wc[w][e] += (uint32_t)__popcll(peers);
+  }
+
+  // The token tiles: item (size s, expert e) = s E + e writes that expert's tiles of size
+  // 16 << s; the items are dealt round robin over the blocks (item i to block i mod nb).
+  const int nb = (int)gridDim.x;
+  for (int i = b + nb * tid; i < DAMOE_N_TILE_SIZES * E; i += nb * kRouteThreads) {
+    const int cls = i / E, e = i - cls * E, bm = 16 << cls;
+    const int ce = counts[e], be = offsets[e];
+    int2* ent = reinterpret_cast<int2*>(tiles.list[cls] + 2) + tst[i];
+    for (int jt = 0; jt * bm < ce; ++jt) ent[jt] = make_int2(be + jt * bm, e | (min(bm, ce - jt * bm) << 16));
   }
 }
 
@@ -446,33 +591,56 @@ k_dispatch(const int32_t* __restrict__ counts, int32_t E, DispatchIn d, int32_t*
 
 }  // namespace
 
+namespace {
+
+// The one-workgroup pass, with the multi-block histogram and scatter around it for many
+// assignments (the same outputs: the stable permutation is unique).
+template <bool DISPATCH>
+hipError_t run_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, RouteOut o, const DispatchIn& d,
+                     int32_t* scratch, hipStream_t stream) {
+  const int64_t A = (int64_t)T * k;
+  if (A < kRouteMultiMinA) {
+    hipLaunchKernelGGL((k_route<DISPATCH, false>), dim3(1), dim3(kRouteThreads), 0, stream, ids, (int32_t)A, E, o, d);
+    return hipGetLastError();
+  }
+  o.nb = route_blocks(A);
+  o.bcnt = scratch;
+  o.boff = scratch + (size_t)route_row(o.nb) * E;
+  o.tst = scratch + 2 * (size_t)route_row(o.nb) * E;
+  hipLaunchKernelGGL(k_route_hist, dim3(o.nb), dim3(kRouteThreads), 0, stream, ids, (int32_t)A, E, o.bcnt, o.ctrl);
+  hipLaunchKernelGGL((k_route<DISPATCH, true>), dim3(1), dim3(kRouteThreads), 0, stream, ids, (int32_t)A, E, o, d);
+  hipLaunchKernelGGL(k_route_scatter, dim3(o.nb), dim3(kRouteThreads), 0, stream, ids, (int32_t)A, E,
+                     (const int32_t*)o.counts, (const int32_t*)o.offsets, (const int32_t*)o.boff,
+                     (const int32_t*)o.tst, o.tiles, o.perm, o.inv_perm);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
                         int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                         int32_t* bucket, int32_t* ctrl,
                         int32_t* const tile_lists[DAMOE_N_TILE_SIZES], const DispatchArgs* dispatch,
-                        hipStream_t stream) {
-  RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}};
+                        int32_t* scratch, hipStream_t stream) {
+  RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}, nullptr, nullptr, nullptr, 0};
   for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) o.tiles.list[i] = tile_lists[i];
   if (dispatch && dispatch->fixed < 0) {
     DispatchIn d{dispatch->Q, dispatch->kid, dispatch->n_ex, dispatch->noda, dispatch->variant_id, -1, nullptr};
-    hipLaunchKernelGGL(k_route<true>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
-  } else {
-    DispatchIn d{nullptr, nullptr, 0, dispatch ? dispatch->noda : 0, dispatch ? dispatch->variant_id : nullptr,
-                 dispatch ? dispatch->fixed : -1, nullptr};
-    hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
+    return run_route<true>(ids, T, k, E, o, d, scratch, stream);
   }
-  return hipGetLastError();
+  DispatchIn d{nullptr, nullptr, 0, dispatch ? dispatch->noda : 0, dispatch ? dispatch->variant_id : nullptr,
+               dispatch ? dispatch->fixed : -1, nullptr};
+  return run_route<false>(ids, T, k, E, o, d, scratch, stream);
 }
 
 hipError_t launch_route_effexp(const int32_t* ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
                                int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                                int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
-                               const int32_t* eff_map, int32_t* variant_id, hipStream_t stream) {
-  RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}};
+                               const int32_t* eff_map, int32_t* variant_id, int32_t* scratch, hipStream_t stream) {
+  RouteOut o{counts, offsets, perm, inv_perm, numden, bucket, ctrl, {}, nullptr, nullptr, nullptr, 0};
   for (int i = 0; i < DAMOE_N_TILE_SIZES; ++i) o.tiles.list[i] = tile_lists[i];
   DispatchIn d{nullptr, nullptr, 0, 0, variant_id, -1, eff_map};
-  hipLaunchKernelGGL(k_route<false>, dim3(1), dim3(kRouteThreads), 0, stream, ids, T * k, E, o, d);
-  return hipGetLastError();
+  return run_route<false>(ids, T, k, E, o, d, scratch, stream);
 }
 
 hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,

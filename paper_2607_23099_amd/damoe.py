@@ -52,7 +52,7 @@ class Layer(ctypes.Structure):
 class WsLayout(ctypes.Structure):
     _fields_ = [("total", ctypes.c_size_t), ("ctrl", ctypes.c_size_t),
                 ("tiles", ctypes.c_size_t * N_TILE_SIZES), ("tiles_cap", ctypes.c_size_t),
-                ("h", ctypes.c_size_t), ("out", ctypes.c_size_t)]
+                ("h", ctypes.c_size_t), ("out", ctypes.c_size_t), ("route", ctypes.c_size_t)]
 
 
 class TableDesc(ctypes.Structure):
@@ -166,7 +166,7 @@ def workspace_layout(E: int, k: int, H: int, I: int, T: int) -> dict:
     lo = WsLayout()
     _check("damoe_workspace_layout", lib().damoe_workspace_layout(E, k, H, I, T, ctypes.byref(lo)))
     return {"total": lo.total, "ctrl": lo.ctrl, "tiles": list(lo.tiles), "tiles_cap": lo.tiles_cap,
-            "h": lo.h, "out": lo.out}
+            "h": lo.h, "out": lo.out, "route": lo.route}
 
 
 def make_layer(E, k, H, I, wdtype, w1, w3, w2, s1=None, s3=None, s2=None, layout=LAYOUT_ROWMAJOR) -> Layer:

@@ -51,11 +51,15 @@ def test_status_strings_and_registry():
 
 def test_workspace_layout():
     for (E, k, H, I, T) in [(8, 2, 256, 512, 64), (256, 8, 7168, 2048, 128), (384, 8, 7168, 2048, 8192),
-                            (256, 8, 7168, 2048, 0)]:
+                            (256, 8, 7168, 2048, 0), (1024, 16, 256, 128, 3000), (37, 5, 64, 64, 1639)]:
         lo = damoe.workspace_layout(E, k, H, I, T)
         A = T * k
+        nbp = (-(-A // 2048) + 3) // 4 * 4  # 2048-assignment blocks, rows padded to a multiple of 4
+        # Per-block counts and offsets, and the tile starts of each size, at many tokens.
+        route = (2 * nbp + damoe.N_TILE_SIZES) * E * 4 if A >= 8192 else 0
         regions = [(lo["ctrl"], 256)] + [(o, 8 + 8 * lo["tiles_cap"]) for o in lo["tiles"]] + \
-                  [(lo["h"], A * I * 2), (lo["out"], A * H * 4)]
+                  [(lo["route"], route), (lo["h"], A * I * 2), (lo["out"], A * H * 4)]
+        assert lo["route"] + route <= lo["h"]  # the routing calls need the workspace up to h
         for off, size in regions:
             assert off % 256 == 0 and off + size <= lo["total"]
         ends = sorted(regions)

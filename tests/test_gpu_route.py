@@ -19,7 +19,9 @@ ROUTE_CASES = (
      for a in (0.05, 10.0)] +
     [("kimi", 384, 8, T, 0.05, 4, synth.seed_kimi(T, 0)) for T in (16, 256, 2048, 8192)] +
     [("e1k1", 1, 1, 100, 1.0, 0, [7]), ("emax", 1024, 16, 3000, 0.3, 0, [8]),
-     ("odd", 37, 5, 777, 0.2, 0, [9])]
+     ("odd", 37, 5, 777, 0.2, 0, [9])] +
+    # Many assignments (blocks of 2048): 5 blocks, the last one 3 ids long; a single expert.
+    [("odd-blocks", 37, 5, 1639, 0.2, 0, [10]), ("e1k1-blocks", 1, 1, 9001, 1.0, 0, [11])]
 )
 
 
@@ -105,26 +107,30 @@ def test_route_edge_cases():
         assert nd[0] == k * nd[1]  # num / den == k
 
 
-def test_route_drops_invalid_ids_and_flags_them():
+# (E, k, T): one workgroup, and T * k = 20000 assignments over ten blocks with a ragged last one.
+@pytest.mark.parametrize("E,k,T", [(16, 2, 40), (64, 8, 2500)])
+def test_route_drops_invalid_ids_and_flags_them(E, k, T):
     torch = torch_cuda()
-    E, k, T = 16, 2, 40
     r = synth.routing(E, k, T, 1.0, [11])
     ids = r.ids.copy()
-    ids[3, 0], ids[7, 1], ids[20, 0] = -1, E, 1000
+    bad = [(3, 0, -1), (7, 1, E), (20, 0, 1000), (T - 1, k - 1, -7)]
+    for t, j, v in bad:
+        ids[t, j] = v
     b = RouteBufs(torch, E, k, T)
     b.run(ids)
     _check_route(b, ids)
     inv = b.inv.cpu().numpy()
-    assert inv[3 * k] == -1 and inv[7 * k + 1] == -1 and inv[20 * k] == -1
+    assert all(inv[t * k + j] == -1 for t, j, _ in bad)
     assert damoe.read_device_error(b.ws) == 1
     assert damoe.read_device_error(b.ws) == 0  # read clears it
 
 
-def test_route_masked_slots_are_not_errors():
+@pytest.mark.parametrize("T", [300, 3000])
+def test_route_masked_slots_are_not_errors(T):
     # Expert parallelism: negative ids are slots whose expert lives on another rank; they are
     # dropped like invalid ids but raise no device error, also when whole tokens are masked.
     torch = torch_cuda()
-    E, k, T = 64, 8, 300
+    E, k = 64, 8
     r = synth.routing(256, k, T, 1.0, [12])
     ids = np.where(r.ids < E, r.ids, -1).astype(np.int32)  # rank 0 of four
     ids[5] = -1
