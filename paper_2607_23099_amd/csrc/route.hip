@@ -547,14 +547,36 @@ k_route_scatter(const int32_t* __restrict__ ids, int32_t A, int32_t E, const int
     if (valid && rank == 0) wc[w][e] += (uint32_t)__popcll(peers);
   }
 
-  // The token tiles: item (size s, expert e) = s E + e writes that expert's tiles of size
-  // 16 << s; the items are dealt round robin over the blocks (item i to block i mod nb).
-  const int nb = (int)gridDim.x;
-  for (int i = b + nb * tid; i < DAMOE_N_TILE_SIZES * E; i += nb * kRouteThreads) {
-    const int cls = i / E, e = i - cls * E, bm = 16 << cls;
-    const int ce = counts[e], be = offsets[e];
-    int2* ent = reinterpret_cast<int2*>(tiles.list[cls] + 2) + tst[i];
-    for (int jt = 0; jt * bm < ce; ++jt) ent[jt] = make_int2(be + jt * bm, e | (min(bm, ce - jt * bm) << 16));
+  // The token tiles.  Expert e's tiles of every size are written by one wave, its lanes
+  // taking consecutive tiles (a hot expert has hundreds); the experts go round robin over the
+  // waves of all blocks, and a wave fetches the count, offset and tile starts of its experts
+  // at once (one expert per lane), then steps through them.
+  const int nb = (int)gridDim.x, GW = nb * kNW, gw = b + nb * w;
+  for (int e0 = gw; e0 < E; e0 += 64 * GW) {
+    const int me = e0 + GW * lane;
+    int mc = 0, mo = 0, mt[DAMOE_N_TILE_SIZES];
+#pragma unroll
+    for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) mt[cls] = 0;
+    if (me < E) {
+      mc = counts[me];
+      mo = offsets[me];
+#pragma unroll
+      for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) mt[cls] = tst[cls * E + me];
+    }
+    const int n = min(64, (E - e0 + GW - 1) / GW);
+#pragma unroll
+    for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
+      const int bm = 16 << cls;
+      int2* list = reinterpret_cast<int2*>(tiles.list[cls] + 2);
+      for (int L = 0; L < n; ++L) {
+        const int ce = __builtin_amdgcn_readlane(mc, L);
+        if (ce == 0) continue;
+        const int be = __builtin_amdgcn_readlane(mo, L), e = e0 + GW * L;
+        int2* ent = list + __builtin_amdgcn_readlane(mt[cls], L);
+        const int nt = (ce + bm - 1) / bm;
+        for (int jt = lane; jt < nt; jt += 64) ent[jt] = make_int2(be + jt * bm, e | (min(bm, ce - jt * bm) << 16));
+      }
+    }
   }
 }
 
