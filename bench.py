@@ -824,7 +824,7 @@ def run_prefill(args):
 
     V = [int(v) for v in args.variants.split(",")] if args.variants else \
         [v for v in range(damoe.num_variants()) if damoe.variant_tile_m(v) >= 128]
-    rows = {}
+    rows, library = {}, {}
     best = None
     for shape, Ts, alphas, hot in ((synth.KIMI, (2048, 8192), (0.05,), 4),
                                    (synth.DS_FP8, (4096, 16384), (0.05, 1.0), 0)):
@@ -868,6 +868,15 @@ def run_prefill(args):
                     log(f"{key}: {rows[key]}")
                     if shape is synth.KIMI and T == 8192 and (best is None or m1 < best[1]):
                         best = (key, m1, f1)
+                lkey = f"{shape.name}_T{T}_a{a}"
+                fastest = min((rows[k_]["gemm1_us"] for k_ in rows if k_.startswith(lkey + "_")), default=None)
+                if dl.wdtype == damoe.W_BF16 and fastest is not None:
+                    lm = library_gemm1_ms(counts, shape.H, shape.I, args.steps)
+                    dm = library_gemm1_ms(np.array([A]), shape.H, shape.I, args.steps)
+                    library[lkey] = {"gemm1_us": round(lm * 1e3, 1), "gemm1_tflops": round(f1 / lm / 1e9, 1),
+                                     "fused_best_speedup": round(lm * 1e3 / fastest, 3),
+                                     "dense_gemm_us": round(dm * 1e3, 1), "dense_tflops": round(f1 / dm / 1e9, 1)}
+                    log(f"{lkey} per-expert hipBLASLt GEMM1: {library[lkey]}")
         del dl, path
         torch.cuda.empty_cache()
     peak = 2500.0
@@ -890,8 +899,39 @@ def run_prefill(args):
         "roofline": {"bound": "mfma", "achieved": round(best[2] / best[1] / 1e9, 1), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(best[2] / best[1] / 1e9 / peak, 4), "traffic": None},
         "per_point": rows,
+        # bf16 points: one hipBLASLt GEMM per touched expert on pre-gathered tokens, against the
+        # fastest fused GEMM1 + SwiGLU variant of the same point; and one dense hipBLASLt GEMM of
+        # the same FLOPs (T k x H times H x 2I), the practical MFMA ceiling of a plain GEMM.
+        "library_gemm1_per_expert": library,
     }
     print(json.dumps(out), flush=True)
+
+
+def library_gemm1_ms(counts, H: int, I: int, steps: int) -> float:
+    """Library baseline for GEMM1 at one routing: one hipBLASLt GEMM (torch's F.linear) per
+    touched expert, x_e [t_e, H] times [W1_e; W3_e]^T.  The tokens are already gathered per
+    expert and there is no SwiGLU epilogue, both in the library's favour.  Median over `steps`
+    timed passes after one untimed pass, in ms."""
+    import torch
+    import torch.nn.functional as F
+    rows = [int(c) for c in counts if c > 0]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    xs = [torch.randn(c, H, device="cuda", dtype=torch.bfloat16, generator=g) for c in rows]
+    ws = [torch.randn(2 * I, H, device="cuda", dtype=torch.bfloat16, generator=g) for _ in rows]
+    t = []
+    for rep in range(steps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for x, w in zip(xs, ws):
+            F.linear(x, w)
+        e1.record()
+        torch.cuda.synchronize()
+        if rep:
+            t.append(e0.elapsed_time(e1))
+    del xs, ws
+    torch.cuda.empty_cache()
+    return float(np.median(t))
 
 
 def run_copy(args):
