@@ -69,6 +69,9 @@ def test_workspace_layout():
     L = damoe.lib()
     bad = damoe.WsLayout()
     assert L.damoe_workspace_layout(0, 1, 128, 128, 4, ctypes.byref(bad)) == -1
+    # At most 2^20 tokens per call (the largest layout still fits the 32-bit positions).
+    assert L.damoe_workspace_layout(1024, 16, 128, 128, 1 << 20, ctypes.byref(bad)) == 0
+    assert L.damoe_workspace_layout(1024, 16, 128, 128, (1 << 20) + 1, ctypes.byref(bad)) == -1
     assert L.damoe_workspace_layout(8, 9, 128, 128, 4, ctypes.byref(bad)) == -1
     assert L.damoe_workspace_layout(2048, 8, 128, 128, 4, ctypes.byref(bad)) == -1
     assert L.damoe_workspace_layout(8, 2, 128, 128, -1, ctypes.byref(bad)) == -1

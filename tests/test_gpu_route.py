@@ -141,6 +141,22 @@ def test_route_masked_slots_are_not_errors(T):
     assert damoe.read_device_error(b.ws) == 0
 
 
+def test_route_at_the_largest_sizes():
+    # The largest call the header admits: T = 2^20 tokens, k = 16, E = 1024, i.e. 2^24
+    # assignments over 8192 blocks of 2048.  Each token takes 16 distinct experts 64 apart
+    # from a base skewed towards low ids, so the first experts hold tens of thousands of tiles.
+    torch = torch_cuda()
+    E, k, T = 1024, 16, 1 << 20
+    rng = np.random.default_rng(21)
+    base = (E * rng.random(T) ** 3).astype(np.int64)
+    ids = ((base[:, None] + 64 * np.arange(k)[None, :]) % E).astype(np.int32)
+    log(f"route at the largest sizes: E={E} k={k} T={T}")
+    b = RouteBufs(torch, E, k, T)
+    b.run(ids)
+    _check_route(b, ids)
+    assert damoe.read_device_error(b.ws) == 0
+
+
 def _random_table(rng, E, buckets, nv):
     n_ex = rng.integers(1, 14, len(buckets))
     Q = []
