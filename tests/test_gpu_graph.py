@@ -12,16 +12,19 @@ from tests.gpu_common import TOL, bf16_rows, log, one_bucket_table, oracle_rows,
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("kids,noda", [([0, 1, 3], 0), ([6, 7, 6], 7), ([2], 2)],
-                         ids=["stream-variants", "tiled-and-big", "single-variant"])
-def test_graph_replays_match_eager(kids, noda):
+# T = 4100 routes its 8200 assignments in blocks of 2048 (three launches in the graph, the last
+# block ragged).
+@pytest.mark.parametrize("kids,noda,T", [([0, 1, 3], 0, 96), ([6, 7, 6], 7, 96), ([2], 2, 96),
+                                         ([0, 1, 3], 0, 4100), ([6, 7, 6], 7, 4100)],
+                         ids=["stream-variants", "tiled-and-big", "single-variant",
+                              "stream-variants-blocks", "tiled-and-big-blocks"])
+def test_graph_replays_match_eager(kids, noda, T):
     torch = torch_cuda()
     from paper_2607_23099_amd.moe import DeviceLayer, Path
     sh = synth.TINY
     dl = DeviceLayer(sh, packed=True)
-    path = Path(dl, 256)
+    path = Path(dl, max(T, 256))
     table = one_bucket_table(sh, kids, noda)
-    T = 96
     routings = [synth.routing(sh.E, sh.k, T, a, [40 + i]) for i, a in enumerate((1.0, 0.05, 10.0, 0.3))]
 
     # Eager reference of every routing.
@@ -34,7 +37,7 @@ def test_graph_replays_match_eager(kids, noda):
         torch.cuda.synchronize()
         eager.append(path.y[:T].clone())
         chosen.append(int(path.variant.item()))
-    log(f"graph test kids={kids}: eager variants {chosen}")
+    log(f"graph test kids={kids} T={T}: eager variants {chosen}")
 
     # Capture once on a side stream (the calls run on torch's current stream).
     path.set_routing(routings[0])
