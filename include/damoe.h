@@ -168,7 +168,11 @@ size_t damoe_workspace_size(const damoe_layer* layer /* host */, int32_t T_max);
  *                             num/den <= E/X} (ddist:X grid of Sec. III-A / V-A,
  *                             extended); -1 when T = 0
  * Also writes the token-tile lists of every tile size into the workspace.
- * T = 0 is valid (empty histogram).  Stream-ordered; no host sync. */
+ * T = 0 is valid (empty histogram).  Below T*k = 8192 one workgroup does all of it in
+ * one launch; from there on three launches split the assignments into blocks of 2048
+ * (histogram per block, one workgroup over the block counts, stable scatter per block),
+ * using the workspace's route region.  Stream-ordered; no host sync, no memset, so the
+ * call can be captured in a graph. */
 damoe_status damoe_route_histogram(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
                                    int32_t* counts, int32_t* offsets, int32_t* perm,
                                    int32_t* inv_perm, uint64_t* effexp_numden,
@@ -225,9 +229,11 @@ uint32_t damoe_table_candidates(const damoe_table* table, int32_t T);
 damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int32_t T,
                             int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* a2-a5 in one launch: exactly damoe_route_histogram followed by damoe_dispatch on
- * its counts (same outputs, same workspace contents), with the histogram, the
- * exemplar match and the permutation sharing one workgroup's LDS.  This is the
+/* a2-a5 in one launch below T*k = 8192 (three from there on, as for
+ * damoe_route_histogram, the match inside the one-workgroup pass): exactly
+ * damoe_route_histogram followed by damoe_dispatch on its counts (same outputs, same
+ * workspace contents), with the histogram, the exemplar match and the permutation
+ * sharing one workgroup's LDS.  This is the
  * paper's online step 5 (Sec. IV-B): histogram, sort, match, kernel id, all on
  * the device.  The table must be built for this E and k.  When every exemplar
  * of the bucket maps to the same variant, that variant is written without
