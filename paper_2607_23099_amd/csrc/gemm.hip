@@ -585,15 +585,16 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
 // no faster), 1 for GEMM2 (4 quads per wave at I = 2048) in a kernel of 3 waves per SIMD:
 // there the extra workgroup per CU hides more latency than a ring does (about 10% faster than
 // depth 2 or 3 at 2 waves).  Twice the features per item would amortise the token loads
-// better but spills the GLU accumulators.  GEMM2 of id 3 takes 128 rows per item: a GEMM2
-// item moves more bf16 token bytes than MXFP4 weight bytes, and at BM = 16 the 8 row blocks
-// still fit 3 waves per SIMD.  GEMM1's code loads take the per-item nontemporal
+// better but spills the GLU accumulators at BM = 32.  Id 3 (BM = 16) takes 64 features per
+// GEMM1 item and 128 rows per GEMM2 item: an item's bf16 token bytes are about its MXFP4
+// weight bytes (GEMM1) or more (GEMM2), so wider items amortise them; the 8 row blocks still
+// fit 2 (GEMM1) and 3 (GEMM2) waves per SIMD.  GEMM1's code loads take the per-item nontemporal
 // choice of the bf16 kernels; GEMM2 (latency-bound) and the scale words, which share cache
 // lines with the next fragment's codes, load plainly (nontemporal measured slower there).
 #define DAMOE_FP4_SHAPES(X) \
   X(0, 32, 32)              \
   X(1, 32, 64)              \
-  X(3, 32, 128)             \
+  X(3, 64, 128)             \
   X(4, 32, 32)              \
   X(5, 32, 64)
 constexpr int kFp4Ring[2] = {1, 2};       // ring depth of k_gemm_fp4<false>, <true>
