@@ -221,12 +221,12 @@ def kimi():
     log("filling Kimi-K2-shaped bf16 layer (33.8 GB)")
     dl = DeviceLayer(synth.KIMI)
     torch.cuda.synchronize()
-    yield dl, Path(dl, 2048), synth.ExpertWeightSource(synth.KIMI)
+    yield dl, Path(dl, 8192), synth.ExpertWeightSource(synth.KIMI)
     del dl
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T", [16, 256, 2048])
+@pytest.mark.parametrize("T", [16, 256, 2048, 8192])
 def test_kimi_hot_experts(kimi, T):
     dl, path, src = kimi
     sh = dl.shape
@@ -246,12 +246,12 @@ def ds_fp8():
     log("filling DeepSeek-V3-shaped fp8 block-128 layer")
     dl = DeviceLayer(synth.DS_FP8)
     torch.cuda.synchronize()
-    yield dl, Path(dl, 4096), synth.ExpertWeightSource(synth.DS_FP8)
+    yield dl, Path(dl, 16384), synth.ExpertWeightSource(synth.DS_FP8)
     del dl
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T,alpha", [(1024, 0.05), (1024, 10.0), (4096, 0.3)])
+@pytest.mark.parametrize("T,alpha", [(1024, 0.05), (1024, 10.0), (4096, 0.3), (16384, 0.05), (16384, 1.0)])
 def test_ds_prefill_fp8(ds_fp8, T, alpha):
     dl, path, src = ds_fp8
     sh = dl.shape
