@@ -187,8 +187,8 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
     auto compute = [&](int ks, int st) __attribute__((always_inline)) {
       if constexpr (FP8) {
         const int kb = (IL ? ks * 128 + wave * 32 : wave * kw + ks * 32) >> 7;
-        const float s_g = sa[sbase + kb] * 0x1p120f;
-        const float s_u = GLU ? sb[sbase + kb] * 0x1p120f : 0.f;
+        const float s_g = sa[sbase + kb];
+        const float s_u = GLU ? sb[sbase + kb] : 0.f;
 #pragma unroll
         for (int b = 0; b < NR; ++b) {
           const uint4 wv = fp8x8_to_bf16x8(wf[st][b], (GLU && b >= NR / 2) ? s_u : s_g);
@@ -504,8 +504,8 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
         uint4 wv[NRW];
         if constexpr (FP8) {
           const int kb = ks >> 2;
-          const float s_g = a.sa[sbase + kb] * 0x1p120f;
-          const float s_u = GLU ? a.sb[sbase + kb] * 0x1p120f : 0.f;
+          const float s_g = a.sa[sbase + kb];
+          const float s_u = GLU ? a.sb[sbase + kb] : 0.f;
           float s_r[NRW];
           if (!GLU) {
             // GEMM2: a wave's 64 rows lie in one 128-row scale block.

@@ -177,8 +177,8 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
       for (int h = 0; h < kBigMaxSk / 64; ++h) {
         const int i = h * 64 + lane;
         if (i < sk) {
-          wsc[i] = srow_ok ? a.sa[sbase + i] * 0x1p120f : 0.f;
-          if (GLU) wsc[kBigMaxSk + i] = srow_ok ? a.sb[sbase + i] * 0x1p120f : 0.f;
+          wsc[i] = srow_ok ? a.sa[sbase + i] : 0.f;
+          if (GLU) wsc[kBigMaxSk + i] = srow_ok ? a.sb[sbase + i] : 0.f;
         }
       }
       sc_lds = wsc;
@@ -205,7 +205,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
     struct Ops {
       WRaw w[4];
       uint4 t[4];
-      float sg, su;  // fp8: block scales of the stage (times 2^120)
+      float sg, su;  // fp8: block scales of the stage
     };
     auto read_ops = [&](int ks, int st, const lds_t* cur, Ops& o, auto nn_c) __attribute__((always_inline)) {
       constexpr int NN = decltype(nn_c)::value;
