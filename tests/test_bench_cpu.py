@@ -1,0 +1,30 @@
+"""Host arithmetic of bench.py's roofline figures (no GPU): the algorithmic work per call."""
+import importlib.util
+import os
+
+import numpy as np
+
+from paper_2607_23099_amd import synth
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def _bench():
+    spec = importlib.util.spec_from_file_location("bench", os.path.join(_HERE, "..", "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_prefill_algorithmic_work_per_expert():
+    # Per touched expert: 3 H I weights, 88,080,384 B in bf16 and 44,050,944 B in fp8 with its
+    # 2688 fp32 block scales (H = 7168, I = 2048); 6 H I FLOPs per assignment.
+    b = _bench()
+    for shape, w_e in ((synth.KIMI, 88_080_384), (synth.DS_FP8, 44_050_944)):
+        T = 64
+        counts = np.zeros(shape.E, np.int64)
+        counts[:3] = [T * shape.k - 10, 7, 3]  # three touched experts
+        f, by, U = b.prefill_alg(shape, T, counts)
+        assert U == 3
+        assert f == 6.0 * shape.H * shape.I * T * shape.k
+        assert by == 3 * w_e + 2 * T * shape.H * 2 + 8 * T * shape.k
