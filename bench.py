@@ -820,6 +820,13 @@ PREFILL_GRID = (("kimi-k2", (16, 256, 2048, 8192), (0.05,), 4),
                 ("dsv3-fp8", (1024, 4096, 16384), (0.05, 0.3, 1.0, 10.0), 0))
 
 
+def gemm1_alg_bytes(shape, U: int, T: int, wbytes: float) -> float:
+    """Algorithmic HBM bytes of one GEMM1 + SwiGLU launch (the decode roofline unit): W1 and W3
+    of the U touched experts at `wbytes` per weight (bf16 2, MXFP4 17/32 with its E8M0 scales),
+    plus the T token rows of x."""
+    return U * 2 * shape.I * shape.H * wbytes + T * shape.H * 2
+
+
 def prefill_alg(shape, T: int, counts) -> tuple:
     """Algorithmic FLOPs and HBM bytes of one a6-a8 call: 6 H I per assignment; the weights of
     the touched experts (fp8: codes and block scales), x and y, ids and gates."""
@@ -1127,7 +1134,7 @@ def main():
         g1 = e[1].elapsed_time(e[2])
         g2 = e[2].elapsed_time(e[3])
         rec[T, a].append((path_ms, g1, g2, e[0].elapsed_time(e[1]), e[3].elapsed_time(e[4])))
-        g1_bytes += U[T, a, rep] * 2 * shape.I * shape.H * wbytes + T * shape.H * 2
+        g1_bytes += gemm1_alg_bytes(shape, U[T, a, rep], T, wbytes)
         g1_ms += g1
 
     # Per point: medians over the timed steps (a stall of the host between two launches lands

@@ -28,3 +28,13 @@ def test_prefill_algorithmic_work_per_expert():
         assert U == 3
         assert f == 6.0 * shape.H * shape.I * T * shape.k
         assert by == 3 * w_e + 2 * T * shape.H * 2 + 8 * T * shape.k
+
+
+def test_decode_gemm1_algorithmic_bytes():
+    # W1 + W3 of one DeepSeek-V3 expert: 58,720,256 B in bf16; MXFP4 codes and scales 17/32 of
+    # a byte per weight: 15,597,568 B.  Plus the token rows, T H 2 B.
+    b = _bench()
+    sh = synth.DS
+    assert b.gemm1_alg_bytes(sh, 1, 0, 2.0) == 58_720_256
+    assert b.gemm1_alg_bytes(sh, 1, 0, 17.0 / 32.0) == 15_597_568
+    assert b.gemm1_alg_bytes(sh, 54, 8, 2.0) == 54 * 58_720_256 + 8 * 7168 * 2
