@@ -71,6 +71,8 @@ typedef enum damoe_status {
 #define DAMOE_DEVERR_EXPERT_ID 1 /* an id >= E was dropped (negative ids are masked slots) */
 #define DAMOE_DEVERR_TILES 2     /* fused_moe found tile lists of another T; items skipped */
 #define DAMOE_DEVERR_VARIANT 4   /* the dispatched id was outside fused_moe's candidates  */
+#define DAMOE_DEVERR_COUNTS 8    /* damoe_dispatch got a negative count, or counts summing
+                                    past T k; it wrote the bucket's noda variant          */
 
 typedef enum damoe_wdtype {
   DAMOE_W_BF16 = 0,     /* bf16 weights                                                */
@@ -126,10 +128,14 @@ typedef struct damoe_layer {
  *   ctrl       : int32[64] control words: [0] sticky device error,
  *                [1] chosen exemplar index, [2..3] its int64 score (lo, hi),
  *                [4] variant id used by the last fused_moe,
+ *                [5] assignment count T k of the last routing call,
  *                [8..16] work-queue words of the big-tile kernel (zero between calls:
  *                the routing call clears them and each launch leaves them cleared)
- *   tiles[s]   : token tiles for tile size BM_s = 16 << s: int32 n_tiles, int32 pad,
- *                then n_tiles entries of int32x2 {start position, expert | rows << 16}
+ *   tiles[s]   : token tiles for tile size BM_s = 16 << s: int32 n_tiles, int32 stamp
+ *                (T k of the routing call that wrote the list), then n_tiles entries of
+ *                int32x2 {start position, expert | rows << 16}.  fused_moe reads the lists
+ *                only when control word [5] and their stamps hold its own T k and their
+ *                counts fit tiles_cap; otherwise it skips them and sets DAMOE_DEVERR_TILES
  *   route      : scratch of the routing call at T k >= 8192 (per-block counts and
  *                segment offsets of its 2048-assignment blocks, int32 [E][nb4] each,
  *                nb4 the block count rounded up to a multiple of 4, then each expert's
@@ -226,6 +232,8 @@ damoe_status damoe_table_load(const char* path, damoe_table** out);
  * to damoe_fused_moe.  0 for a null table or T < 0. */
 uint32_t damoe_table_candidates(const damoe_table* table, int32_t T);
 
+/* counts must be a histogram of at most T k assignments (k of the table): a negative count
+ * or a sum above T k writes the bucket's noda variant and sets DAMOE_DEVERR_COUNTS. */
 damoe_status damoe_dispatch(const damoe_table* table, const int32_t* counts, int32_t T,
                             int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream);
 

@@ -522,6 +522,7 @@ void oracle_topk_softmax(const double* logits, int32_t T, int32_t E, int32_t k, 
  * selection and gates above. */
 void oracle_router(const uint16_t* x, const uint16_t* wg, const float* bias, int32_t T, int32_t H,
                    int32_t E, int32_t k, double* logits, int32_t* ids, double* w) {
+#pragma omp parallel for schedule(static)
   for (int32_t t = 0; t < T; ++t)
     for (int32_t e = 0; e < E; ++e) {
       double s = 0.0;

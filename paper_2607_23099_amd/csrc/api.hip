@@ -310,11 +310,11 @@ uint32_t damoe_table_effexp_candidates(const damoe_table* t, int32_t T) {
 
 damoe_status damoe_dispatch(const damoe_table* t, const int32_t* counts, int32_t T,
                             int32_t* variant_id, void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!t || !counts || !variant_id || !ws || T < 0) return DAMOE_ERR_INVALID_ARG;
+  if (!t || !counts || !variant_id || !ws || T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
   if (ws_bytes < kCtrlWords * sizeof(int32_t)) return DAMOE_ERR_WORKSPACE;
   if (!t->d_Q) return DAMOE_ERR_HIP;  // table built without a device
-  const hipError_t e =
-      launch_dispatch(counts, t->E, table_args(t, T, variant_id), reinterpret_cast<int32_t*>(ws), stream);
+  const hipError_t e = launch_dispatch(counts, t->E, T * t->k, table_args(t, T, variant_id),
+                                       reinterpret_cast<int32_t*>(ws), stream);
   return e == hipSuccess ? DAMOE_OK : DAMOE_ERR_HIP;
 }
 
@@ -375,6 +375,7 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g1.ctrl = reinterpret_cast<int32_t*>(base + lo.ctrl);
   g1.k = L->k;
   g1.A = T * L->k;
+  g1.tiles_cap = (int32_t)lo.tiles_cap;
   g1.E = L->E;
   g1.K = L->H;
   g1.N = L->I;

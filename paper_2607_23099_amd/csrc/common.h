@@ -18,6 +18,8 @@ constexpr int kWave = 64;
 constexpr int kGemmThreads = 256;  // every GEMM variant runs 4 waves per workgroup
 constexpr int kRouteThreads = 1024;
 constexpr int kCtrlWords = 64;
+// Control word holding the assignment count T k of the last routing call on the workspace.
+constexpr int kRoutedA = 5;
 // Control words kQueueCtrl .. + 8: the big-tile kernel's work-queue tickets (one per XCD) and
 // its count of finished workgroups.  Zero between launches: the routing kernel clears them,
 // and each big-tile launch returns them to zero when its last workgroup finishes.
@@ -91,6 +93,7 @@ struct GemmArgs {
   int32_t* ctrl;
   int32_t k;
   int32_t A;           // assignments T * k
+  int32_t tiles_cap;   // entries each tile list of this call's workspace layout can hold
   int32_t E;
   int32_t K;           // reduction length: H for GEMM1, I for GEMM2
   int32_t N;           // output features: I for GEMM1, H for GEMM2
@@ -123,8 +126,9 @@ hipError_t launch_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, int
                         int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* numden,
                         int32_t* bucket, int32_t* ctrl, int32_t* const tile_lists[DAMOE_N_TILE_SIZES],
                         const DispatchArgs* dispatch, int32_t* scratch, hipStream_t stream);
-hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
-                           hipStream_t stream);
+// max_total: the call's assignment count T k; counts outside it are rejected on the device.
+hipError_t launch_dispatch(const int32_t* counts, int32_t E, int32_t max_total, const DispatchArgs& dispatch,
+                           int32_t* ctrl, hipStream_t stream);
 // Grouped GEMM stages on a persistent grid sized from the device's CU count.
 hipError_t launch_gemm1(const GemmArgs& a, int cus, hipStream_t stream);
 hipError_t launch_gemm2(const GemmArgs& a, int cus, hipStream_t stream);
@@ -182,9 +186,24 @@ __device__ __forceinline__ void pin_gemm_args(const GemmArgs& a) {
   pin(a.ctrl);
   pin(a.k);
   pin(a.A);
+  pin(a.tiles_cap);
   pin(a.E);
   pin(a.K);
   pin(a.N);
+}
+
+// Tile count of a list for this call.  Every routing call writes its assignment count T k to
+// control word kRoutedA (at the same offset for every T) and stamps word 1 of each of its lists
+// with it.  The lists sit at offsets that depend on T, so after a routing call with another T
+// than the fused call's, the lists at the fused call's offsets hold another call's entries,
+// stale ones of an older call with this T, or nothing: such lists (control word or stamp not
+// this call's T k, or a count beyond the list's capacity) are never read; their tiles are
+// skipped and DAMOE_DEVERR_TILES is set.
+__device__ __forceinline__ int tile_count(const int32_t* list, const GemmArgs& a) {
+  const int n = list[0];
+  if (a.ctrl[kRoutedA] == a.A && list[1] == a.A && n >= 0 && n <= a.tiles_cap) return n;
+  if (threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
+  return 0;
 }
 
 // Device-side variant check of a fused launch: a forced variant is trusted (validated on the

@@ -99,7 +99,7 @@ __device__ __forceinline__ void stream_body(const GemmArgs& a, const int32_t* __
   constexpr int NR = (GLU ? 2 : 1) * BN / 16;
   using WT = typename WFrag<FP8>::T;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n_tiles = list[0];
+  const int n_tiles = tile_count(list, a);
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = N / BN;
@@ -246,7 +246,7 @@ __device__ __forceinline__ void stream_body_fp4(const GemmArgs& a, const int32_t
   constexpr int NX = BM / 16;
   constexpr int NR = (GLU ? 2 : 1) * BN / 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int n_tiles = list[0];
+  const int n_tiles = tile_count(list, a);
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = N / BN;
@@ -379,7 +379,7 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
   using WT = typename WFrag<FP8>::T;
   constexpr int EB = WFrag<FP8>::kBytesPerElem;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int n_tiles = list[0];
+  const int n_tiles = tile_count(list, a);
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = N / FEAT;
@@ -691,6 +691,9 @@ __global__ void __launch_bounds__(256) k_reduce(ReduceArgs a) {
   if (lane < a.k) {
     p_l = a.inv_perm[(size_t)t * a.k + lane];
     g_l = a.w[(size_t)t * a.k + lane];
+    // A position outside this call's T k rows (an inverse permutation of another call) reads
+    // nothing: the slot counts as dropped.
+    if ((uint32_t)p_l >= (uint32_t)(a.T * a.k)) p_l = -1;
   }
   if (n >= a.H) return;
   float4 o[DAMOE_MAX_K];

@@ -83,7 +83,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wt = wave >> 1, wr = wave & 1;  // token half, weight-row half of the output
   const int32_t* __restrict__ list = a.tiles.list[4];
-  const int n_tiles = list[0];
+  const int n_tiles = tile_count(list, a);
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = (N + FEAT - 1) / FEAT;

@@ -394,12 +394,15 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
     if (sm.bad) atomicOr(&o.ctrl[0], DAMOE_DEVERR_EXPERT_ID);
   }
   if (tid < kQueueWords) o.ctrl[kQueueCtrl + tid] = 0;
-  if (tid == 0)
+  if (tid == 0) {
+    // The assignment count the GEMM kernels check before reading a list (tile_count).
+    o.ctrl[kRoutedA] = A;
 #pragma unroll
     for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) {
       o.tiles.list[cls][0] = tot[1 + cls];
-      o.tiles.list[cls][1] = 0;
+      o.tiles.list[cls][1] = A;
     }
+  }
   if (MULTI) {
     // Many tiles: k_route_scatter writes the lists; here each class's tile start per expert.
     if (tid < E)
@@ -580,9 +583,13 @@ k_route_scatter(const int32_t* __restrict__ ids, int32_t A, int32_t E, const int
   }
 }
 
-// a5 on its own: counts from device memory.
+// a5 on its own: counts from device memory.  They come from the caller, so they are checked
+// before any of them indexes LDS: a negative count, or counts summing past the call's
+// assignment count T k, are not a histogram of this call; the bucket's noda variant is written
+// and DAMOE_DEVERR_COUNTS set.
 __global__ void __launch_bounds__(kRouteThreads)
-k_dispatch(const int32_t* __restrict__ counts, int32_t E, DispatchIn d, int32_t* __restrict__ ctrl) {
+k_dispatch(const int32_t* __restrict__ counts, int32_t E, int32_t max_total, DispatchIn d,
+           int32_t* __restrict__ ctrl) {
   __shared__ Smem sm;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   pin(counts);
@@ -599,9 +606,30 @@ k_dispatch(const int32_t* __restrict__ counts, int32_t E, DispatchIn d, int32_t*
     sm.qpre[w][r] = (w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
   }
   for (int v = tid; v < kValueBins; v += kRouteThreads) sm.vh[v] = 0;
-  if (tid == 0) sm.big = 0;
+  if (tid == 0) {
+    sm.big = 0;
+    sm.bad = 0;
+  }
   __syncthreads();
   const int c = tid < E ? counts[tid] : 0;
+  const bool in_range = c >= 0 && c <= max_total;
+  const uint64_t wsum = wave_sum_u64(in_range ? (uint64_t)c : 0);  // no int overflow: 64-bit sum
+  if (lane == 0) sm.tmp64[w] = wsum;
+  if (!in_range) sm.bad = 1;
+  __syncthreads();
+  uint64_t sum = 0;
+#pragma unroll
+  for (int u = 0; u < kNW; ++u) sum += sm.tmp64[u];
+  if (sm.bad || sum > (uint64_t)max_total) {  // uniform over the workgroup
+    if (tid == 0) {
+      *d.variant_id = d.noda;
+      ctrl[1] = -1;
+      ctrl[2] = 0;
+      ctrl[3] = 0;
+      atomicOr(&ctrl[0], DAMOE_DEVERR_COUNTS);
+    }
+    return;
+  }
   if (tid < E) {
     sm.cnt[tid] = c;
     if (c >= kValueBins) sm.big = 1;
@@ -665,10 +693,10 @@ hipError_t launch_route_effexp(const int32_t* ids, int32_t T, int32_t k, int32_t
   return run_route<false>(ids, T, k, E, o, d, scratch, stream);
 }
 
-hipError_t launch_dispatch(const int32_t* counts, int32_t E, const DispatchArgs& dispatch, int32_t* ctrl,
-                           hipStream_t stream) {
+hipError_t launch_dispatch(const int32_t* counts, int32_t E, int32_t max_total, const DispatchArgs& dispatch,
+                           int32_t* ctrl, hipStream_t stream) {
   DispatchIn d{dispatch.Q, dispatch.kid, dispatch.n_ex, dispatch.noda, dispatch.variant_id, -1, nullptr};
-  hipLaunchKernelGGL(k_dispatch, dim3(1), dim3(kRouteThreads), 0, stream, counts, E, d, ctrl);
+  hipLaunchKernelGGL(k_dispatch, dim3(1), dim3(kRouteThreads), 0, stream, counts, E, max_total, d, ctrl);
   return hipGetLastError();
 }
 

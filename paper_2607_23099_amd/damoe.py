@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdamoe.so")
 
 N_TILE_SIZES = 5
 W_BF16, W_FP8_B128, W_MXFP4 = 0, 1, 2
-DEVERR_EXPERT_ID, DEVERR_TILES, DEVERR_VARIANT = 1, 2, 4
+DEVERR_EXPERT_ID, DEVERR_TILES, DEVERR_VARIANT, DEVERR_COUNTS = 1, 2, 4, 8
 LAYOUT_ROWMAJOR, LAYOUT_FRAG16 = 0, 1
 
 STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported", -3: "workspace too small",

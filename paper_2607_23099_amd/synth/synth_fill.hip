@@ -245,10 +245,12 @@ int host_threads() {
   return (int)std::min(n, 16u);
 }
 
+// Splits [0, n) over the host threads when there are at least min_n items (elements, or
+// whole blocks of work for the block fills).
 template <class F>
-void parallel_for(uint64_t n, F&& f) {
+void parallel_for(uint64_t n, F&& f, uint64_t min_n = 65536) {
   const int nt = host_threads();
-  if (n < 65536 || nt == 1) {
+  if (n < min_n || nt == 1) {
     f(0, n);
     return;
   }
@@ -366,7 +368,7 @@ int synth_fill_fp8_b128_host(uint8_t* q, float* s, uint32_t rows, uint32_t cols,
       }
       s[(uint64_t)sl * rb_n * cb_n + rem] = sc;
     }
-  });
+  }, 16);  // a 128 x 128 block is 16K values: worth a thread from a few blocks on
   return 0;
 }
 

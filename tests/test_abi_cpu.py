@@ -77,6 +77,20 @@ def test_workspace_layout():
     assert L.damoe_workspace_layout(8, 2, 128, 128, -1, ctypes.byref(bad)) == -1
 
 
+def test_tile_lists_of_two_token_counts_do_not_line_up():
+    # The tile lists sit at offsets that depend on T (their capacity grows with T k), so a fused
+    # call with another T than its routing call would read another list's entries or memory no
+    # routing call wrote: the reason the routing call stamps each list with T k and the GEMM
+    # kernels read only lists stamped with their own.
+    for (E, k, T1, T2) in [(256, 8, 128, 64), (8, 2, 200, 150), (384, 8, 8192, 2048)]:
+        a = damoe.workspace_layout(E, k, 7168, 2048, T1)
+        b = damoe.workspace_layout(E, k, 7168, 2048, T2)
+        assert a["tiles_cap"] != b["tiles_cap"]
+        assert a["tiles"][0] == b["tiles"][0]  # the first list starts at the same offset
+        assert all(x != y for x, y in zip(a["tiles"][1:], b["tiles"][1:]))
+        assert a["h"] != b["h"] and a["out"] != b["out"]
+
+
 def _fake_layer(**kw):
     d = dict(E=8, k=2, H=256, I=512, wdtype=0, layout=0, w1=0x1000, w3=0x2000, w2=0x3000, s1=0, s3=0, s2=0)
     d.update(kw)

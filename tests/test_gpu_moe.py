@@ -3,7 +3,8 @@ import numpy as np
 import pytest
 
 from paper_2607_23099_amd import damoe, synth
-from tests.gpu_common import TOL, bf16_rows, log, oracle_rows, row_err, torch_cuda
+from tests.gpu_common import (TOL, Reference, bf16_rows, log, oracle_rows, row_err, tile_rows, torch_cuda,
+                               variants_agree)
 
 pytestmark = pytest.mark.gpu
 
@@ -153,6 +154,58 @@ def test_small_fp8_every_variant(small_fp8, T, alpha, seed):
         assert err <= TOL["fp8"], (v, err)
 
 
+def test_fused_reads_no_tile_list_of_another_T(tiny):
+    # The routing call stamps its tile lists with T k.  A fused call with another T (whose
+    # layout puts the lists elsewhere) reads none of them: every kernel class skips its items
+    # and sets DAMOE_DEVERR_TILES.  The same T afterwards runs cleanly.
+    torch = torch_cuda()
+    dl, path = tiny
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, 200, 1.0, [31])
+    path.set_routing(r)
+    path.fill_x(200, 31)
+    path.route(200)
+    assert damoe.read_device_error(path.ws) == 0
+    for v in _variants():
+        for T2 in (64, 150):
+            log(f"stale tile lists: routed T=200, fused T={T2}, variant={damoe.variant_name(v)}")
+            path.fused(T2, v)
+            torch.cuda.synchronize()
+            assert damoe.read_device_error(path.ws) == damoe.DEVERR_TILES, (v, T2)
+    rows = np.arange(0, 200, 9)
+    ref = oracle_rows(sh, r, 31, rows)
+    for v in _variants():
+        _run(path, r, 31, v)
+        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["bf16"]
+    assert damoe.read_device_error(path.ws) == 0
+
+
+def test_dispatch_rejects_counts_that_are_no_histogram(tiny):
+    # damoe_dispatch takes its counts from the caller: a negative count, or counts summing past
+    # T k, write the bucket's noda variant and set DAMOE_DEVERR_COUNTS.
+    torch = torch_cuda()
+    dl, path = tiny
+    sh = dl.shape
+    table = damoe.Table.create(damoe.TableData(
+        E=sh.E, k=sh.k, H=sh.H, I=sh.I, wdtype=0, bucket_T=np.array([1 << 20]), n_ex=np.array([2]),
+        Q=np.array([[30000] + [0] * (sh.E - 1), [11585] * sh.E], np.int32), kid=np.array([1, 2]),
+        noda=np.array([5])))
+    T = 64
+    good = np.full(sh.E, T * sh.k // sh.E, np.int32)
+    for counts, want_v, want_err in [
+            (good, 2, 0),                                                     # uniform: exemplar 1
+            (np.r_[T * sh.k, np.zeros(sh.E - 1, np.int32)], 1, 0),           # one expert: exemplar 0
+            (np.r_[-1, good[1:]], 5, damoe.DEVERR_COUNTS),                    # a negative count
+            (good + 1, 5, damoe.DEVERR_COUNTS),                               # sum above T k
+            (np.r_[2 ** 31 - 1, 2 ** 31 - 1, good[2:]], 5, damoe.DEVERR_COUNTS)]:  # no int overflow
+        path.counts.copy_(torch.from_numpy(np.asarray(counts, np.int32)))
+        path.variant.fill_(-9)
+        damoe.dispatch(table, path.counts, T, path.variant, path.ws)
+        torch.cuda.synchronize()
+        assert int(path.variant.item()) == want_v, counts
+        assert damoe.read_device_error(path.ws) == want_err, counts
+
+
 def test_tiny_zero_tokens_is_noop(tiny):
     torch = torch_cuda()
     dl, path = tiny
@@ -184,6 +237,46 @@ def test_cold_experts_are_never_read():
         assert row_err(y, ref) <= TOL["bf16"]
 
 
+# Full-size cases: every point the benchmarks time, on their routing seeds and tokens.  Each
+# case compares at least 64 token rows chosen from the oracle's tile lists (tile_rows: the
+# ends of the first, last and first full tile of every tile size, the hottest expert's ragged
+# last tile, token blocks 4..7 of a 256-row tile, a one-token expert) with the oracle, and
+# every row of every variant with the first variant's output.
+DS_POINTS = [(T, a) for T in (1, 8, 32, 128) for a in (0.05, 0.3, 1.0, 10.0)]
+PREFILL_POINTS = [(T, a) for T in (1024, 4096, 16384) for a in (0.05, 0.3, 1.0, 10.0)]
+KIMI_POINTS = [16, 256, 2048, 8192]
+DECODE_X, PREFILL_X = 1, 5  # activation tags of the decode sweep and of the prefill grid
+
+
+def _check_variants(path, r, x_tag, rows, ref, tol, variants, what):
+    """Every variant on one routing: the chosen rows against the oracle, all rows against the
+    first variant's output."""
+    torch = torch_cuda()
+    first = None
+    for v in variants:
+        log(f"{what} variant={damoe.variant_name(v)} ({len(rows)} oracle rows)")
+        _run(path, r, x_tag, v)
+        err = row_err(bf16_rows(path.y, rows), ref)
+        assert err <= tol, (v, err)
+        if first is None:
+            first = path.y[:r.T].clone()
+        else:
+            agree = variants_agree(path.y, first, r.T)
+            assert agree <= tol, (v, agree)
+    assert damoe.read_device_error(path.ws) == 0
+    del first
+    torch.cuda.empty_cache()
+
+
+def _cases(sh, points, routing_of, x_tag):
+    cases = {}
+    for p in points:
+        r = routing_of(p)
+        rows = tile_rows(r, sh.E, seed=r.T)
+        cases[p] = (r, synth.activations_host(r.T, sh.H, x_tag, rows), rows)
+    return cases
+
+
 @pytest.fixture(scope="module")
 def ds():
     torch = torch_cuda()
@@ -191,27 +284,21 @@ def ds():
     log("filling DeepSeek-V3-shaped bf16 layer (22.5 GB)")
     dl = DeviceLayer(synth.DS)
     torch.cuda.synchronize()
-    yield dl, Path(dl, 128), synth.ExpertWeightSource(synth.DS)
+    sh = dl.shape
+    cases = _cases(sh, DS_POINTS, lambda p: synth.routing(sh.E, sh.k, p[0], p[1], synth.seed_decode(p[0], p[1], 0)),
+                   DECODE_X)
+    ref = Reference(sh, cases)
+    yield dl, Path(dl, 128), cases, ref
     del dl
     torch.cuda.empty_cache()
 
 
-DS_CASES = [(1, 0.3), (8, 0.05), (8, 10.0), (32, 1.0), (128, 0.05), (128, 10.0)]
-
-
-@pytest.mark.parametrize("T,alpha", DS_CASES)
+@pytest.mark.parametrize("T,alpha", DS_POINTS)
 def test_ds_decode_every_variant(ds, T, alpha):
-    dl, path, src = ds
-    sh = dl.shape
-    r = synth.routing(sh.E, sh.k, T, alpha, synth.seed_decode(T, alpha, 0))
-    rows = np.arange(T) if T <= 4 else np.sort(np.random.default_rng(T).choice(T, 4, replace=False))
-    log(f"ds decode T={T} alpha={alpha}: oracle on rows {rows.tolist()}")
-    ref = oracle_rows(sh, r, 100 + T, rows, src)
-    for v in _variants():
-        log(f"ds decode T={T} alpha={alpha} variant={damoe.variant_name(v)}")
-        _run(path, r, 100 + T, v)
-        err = row_err(bf16_rows(path.y, rows), ref)
-        assert err <= TOL["bf16"], (v, err)
+    dl, path, cases, ref = ds
+    r, _, rows = cases[T, alpha]
+    _check_variants(path, r, DECODE_X, rows, ref.y[T, alpha], TOL["bf16"], _variants(),
+                    f"ds decode T={T} alpha={alpha}")
 
 
 @pytest.fixture(scope="module")
@@ -221,22 +308,20 @@ def kimi():
     log("filling Kimi-K2-shaped bf16 layer (33.8 GB)")
     dl = DeviceLayer(synth.KIMI)
     torch.cuda.synchronize()
-    yield dl, Path(dl, 8192), synth.ExpertWeightSource(synth.KIMI)
+    sh = dl.shape
+    cases = _cases(sh, KIMI_POINTS, lambda T: synth.routing(sh.E, sh.k, T, 0.05, synth.seed_kimi(T, 0), n_hot=4),
+                   PREFILL_X)
+    ref = Reference(sh, cases)
+    yield dl, Path(dl, 8192), cases, ref
     del dl
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T", [16, 256, 2048, 8192])
+@pytest.mark.parametrize("T", KIMI_POINTS)
 def test_kimi_hot_experts(kimi, T):
-    dl, path, src = kimi
-    sh = dl.shape
-    r = synth.routing(sh.E, sh.k, T, 0.05, synth.seed_kimi(T, 0), n_hot=4)
-    rows = np.sort(np.random.default_rng(T).choice(T, 3, replace=False))
-    ref = oracle_rows(sh, r, 300 + T, rows, src)
-    for v in _variants():
-        log(f"kimi T={T} variant={damoe.variant_name(v)}")
-        _run(path, r, 300 + T, v)
-        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["bf16"]
+    dl, path, cases, ref = kimi
+    r, _, rows = cases[T]
+    _check_variants(path, r, PREFILL_X, rows, ref.y[T], TOL["bf16"], _variants(), f"kimi T={T}")
 
 
 @pytest.fixture(scope="module")
@@ -246,22 +331,21 @@ def ds_fp8():
     log("filling DeepSeek-V3-shaped fp8 block-128 layer")
     dl = DeviceLayer(synth.DS_FP8)
     torch.cuda.synchronize()
-    yield dl, Path(dl, 16384), synth.ExpertWeightSource(synth.DS_FP8)
+    sh = dl.shape
+    cases = _cases(sh, PREFILL_POINTS,
+                   lambda p: synth.routing(sh.E, sh.k, p[0], p[1], synth.seed_prefill(p[0], p[1], 0)), PREFILL_X)
+    ref = Reference(sh, cases)
+    yield dl, Path(dl, 16384), cases, ref
     del dl
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T,alpha", [(1024, 0.05), (1024, 10.0), (4096, 0.3), (16384, 0.05), (16384, 1.0)])
+@pytest.mark.parametrize("T,alpha", PREFILL_POINTS)
 def test_ds_prefill_fp8(ds_fp8, T, alpha):
-    dl, path, src = ds_fp8
-    sh = dl.shape
-    r = synth.routing(sh.E, sh.k, T, alpha, synth.seed_prefill(T, alpha, 0))
-    rows = np.sort(np.random.default_rng(T).choice(T, 2, replace=False))
-    ref = oracle_rows(sh, r, 200 + T, rows, src)
-    for v in _variants():
-        log(f"ds fp8 prefill T={T} alpha={alpha} variant={damoe.variant_name(v)}")
-        _run(path, r, 200 + T, v)
-        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["fp8"]
+    dl, path, cases, ref = ds_fp8
+    r, _, rows = cases[T, alpha]
+    _check_variants(path, r, PREFILL_X, rows, ref.y[T, alpha], TOL["fp8"], _variants(),
+                    f"ds fp8 prefill T={T} alpha={alpha}")
 
 
 SMALL_MXFP4 = synth.Shape("small-mxfp4", E=8, k=2, H=512, I=1024, shape_id=6, wdtype="mxfp4")
@@ -312,6 +396,21 @@ def test_small_mxfp4_every_stream_variant(small_mxfp4, T, alpha, seed):
         assert err <= TOL["bf16"], (v, err)
 
 
+def test_mxfp4_reads_no_tile_list_of_another_T(small_mxfp4):
+    torch = torch_cuda()
+    dl, path, _ = small_mxfp4
+    sh = dl.shape
+    r = synth.routing(sh.E, sh.k, 100, 1.0, [12])
+    path.set_routing(r)
+    path.fill_x(100, 12)
+    path.route(100)
+    assert damoe.read_device_error(path.ws) == 0
+    for v in _stream_variants(damoe.W_MXFP4):
+        path.fused(40, v)
+        torch.cuda.synchronize()
+        assert damoe.read_device_error(path.ws) == damoe.DEVERR_TILES, v
+
+
 def test_mxfp4_rejects_other_kernel_classes(small_mxfp4):
     # Host: a forced tiled or big variant is unsupported.  Device: a dispatched id of another
     # class runs nothing and sets the sticky error.
@@ -346,19 +445,18 @@ def ds_mxfp4():
     log("filling DeepSeek-V3-shaped MXFP4 layer (5.9 GB)")
     dl = DeviceLayer(synth.DS_MXFP4)
     torch.cuda.synchronize()
-    yield dl, Path(dl, 128), synth.ExpertWeightSource(synth.DS_MXFP4)
+    sh = dl.shape
+    cases = _cases(sh, DS_POINTS, lambda p: synth.routing(sh.E, sh.k, p[0], p[1], synth.seed_decode(p[0], p[1], 0)),
+                   DECODE_X)
+    ref = Reference(sh, cases)
+    yield dl, Path(dl, 128), cases, ref
     del dl
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("T,alpha", [(1, 0.3), (32, 1.0), (128, 0.05)])
+@pytest.mark.parametrize("T,alpha", DS_POINTS)
 def test_ds_mxfp4_decode(ds_mxfp4, T, alpha):
-    dl, path, src = ds_mxfp4
-    sh = dl.shape
-    r = synth.routing(sh.E, sh.k, T, alpha, synth.seed_decode(T, alpha, 0))
-    rows = np.arange(T) if T <= 2 else np.sort(np.random.default_rng(T).choice(T, 3, replace=False))
-    ref = oracle_rows(sh, r, 400 + T, rows, src)
-    for v in _stream_variants(damoe.W_MXFP4):
-        log(f"ds mxfp4 T={T} alpha={alpha} variant={damoe.variant_name(v)}")
-        _run(path, r, 400 + T, v)
-        assert row_err(bf16_rows(path.y, rows), ref) <= TOL["bf16"]
+    dl, path, cases, ref = ds_mxfp4
+    r, _, rows = cases[T, alpha]
+    _check_variants(path, r, DECODE_X, rows, ref.y[T, alpha], TOL["bf16"], _stream_variants(damoe.W_MXFP4),
+                    f"ds mxfp4 T={T} alpha={alpha}")

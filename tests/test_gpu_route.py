@@ -236,11 +236,14 @@ def test_dispatch_ties_pick_lowest_index():
                          kid=np.array([0, 2, 1, 0], np.int32) % damoe.num_variants(),
                          noda=np.array([0], np.int32))
     table = damoe.Table.create(td)
-    counts = torch.from_numpy(np.rint(np.geomspace(90, 10, E)).astype(np.int32)).cuda()
+    c = np.rint(np.geomspace(90, 10, E)).astype(np.int32)
+    counts = torch.from_numpy(c).cuda()
     vid = torch.zeros(1, dtype=torch.int32, device="cuda")
     ws = torch.zeros(4096, dtype=torch.uint8, device="cuda")
-    damoe.dispatch(table, counts, 100, vid, ws)
+    T = -(-int(c.sum()) // 8)  # the fewest tokens whose k = 8 slots hold these counts
+    damoe.dispatch(table, counts, T, vid, ws)
     torch.cuda.synchronize()
+    assert ws[:16].view(torch.int32).cpu().numpy()[0] == 0
     assert ws[:16].view(torch.int32).cpu().numpy()[1] == 1
     assert int(vid.item()) == td.kid[1]
 
