@@ -317,6 +317,28 @@ damoe_status damoe_fused_moe_stage(const damoe_layer* layer /* host */, int32_t 
                                    uint32_t candidates, uint16_t* y, void* ws, size_t ws_bytes,
                                    hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): damoe_route_dispatch followed by
+ * damoe_fused_moe on the same arguments (candidates = damoe_table_candidates(table, T)),
+ * with the workspace taken from a fixed array of damoe_noalloc_scratch_bytes() (64 MiB) that
+ * the library holds in device memory, one per GPU it runs on, until the process ends.  The
+ * caller passes the inputs (x [T][H], topk_ids [T][k], topk_w [T][k]) and every output of
+ * the two calls (counts [E], offsets [E+1], perm and inv_perm [T k], effexp_numden [2],
+ * effexp_bucket [1], variant_id [1], y [T][H]), all device pointers, with the meanings given
+ * there.  Nothing is allocated, freed or memset.  A call whose workspace
+ * (damoe_workspace_size(layer, T)) exceeds the array returns DAMOE_ERR_WORKSPACE before any
+ * launch (DeepSeek-V3 shape: up to T = 255 tokens); every argument error of the two calls is
+ * reported before the first launch too.  All calls on one GPU share its array, which keeps
+ * the last call's contents: calls that overlap on one GPU (other streams, other threads)
+ * race and give undefined results.  Ids >= E are dropped as in damoe_route_dispatch; the
+ * array's sticky error word is not reported.  Stream-ordered, never synchronises. */
+size_t damoe_noalloc_scratch_bytes(void);
+damoe_status damoe_moe_layer_noalloc(const damoe_table* table, const damoe_layer* layer /* host */,
+                                     const uint16_t* x, const int32_t* topk_ids, const float* topk_w,
+                                     int32_t T, int32_t* counts, int32_t* offsets, int32_t* perm,
+                                     int32_t* inv_perm, uint64_t* effexp_numden, int32_t* effexp_bucket,
+                                     int32_t* variant_id, uint16_t* y, hipStream_t stream);
+
 /* Converts the row-major weights of `src` (layout must be DAMOE_LAYOUT_ROWMAJOR)
  * into the fragment-packed layout, written to w1, w3, w2 (disjoint device
  * buffers, overlapping no source).  bf16 and fp8: buffers of the sources' sizes;

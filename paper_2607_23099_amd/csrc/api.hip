@@ -13,6 +13,12 @@
 
 using namespace damoe;
 
+// Workspace of damoe_moe_layer_noalloc: a fixed array in device memory, one per GPU the library
+// runs on, held until the process ends.  In host code its name is not a device address: the
+// per-device set-up below looks the address up once per device, and only that address is used.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -20,6 +26,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct DeviceInfo {
   int cus = 0;
+  void* scratch = nullptr;  // this device's copy of `scratch` (null if the lookup failed)
   bool ready = false;
 };
 
@@ -41,6 +48,14 @@ damoe_status device_info(DeviceInfo** out) {
     if (gemm_set_lds_limits() != hipSuccess || big_set_lds_limits() != hipSuccess ||
         router_set_lds_limits() != hipSuccess)
       return DAMOE_ERR_HIP;
+    // With this device current: the address of its copy of the allocation-free workspace.  A
+    // failed lookup only disables damoe_moe_layer_noalloc.
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      p = nullptr;
+    }
+    d.scratch = p;
     d.cus = cus;
     d.ready = true;
   }
@@ -430,6 +445,42 @@ damoe_status damoe_fused_moe_stage(const damoe_layer* L, int32_t stage, const ui
   if (stage < 0 || stage > 2) return DAMOE_ERR_INVALID_ARG;
   return fused_impl(L, 1 << stage, x, topk_w, T, perm, inv_perm, variant_id, force_variant, candidates,
                     y, ws, ws_bytes, stream);
+}
+
+size_t damoe_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+damoe_status damoe_moe_layer_noalloc(const damoe_table* t, const damoe_layer* L, const uint16_t* x,
+                                     const int32_t* topk_ids, const float* topk_w, int32_t T, int32_t* counts,
+                                     int32_t* offsets, int32_t* perm, int32_t* inv_perm, uint64_t* effexp_numden,
+                                     int32_t* effexp_bucket, int32_t* variant_id, uint16_t* y,
+                                     hipStream_t stream) {
+  // Everything the two calls below would reject is rejected here, before the first launch.
+  damoe_status st = check_layer(L);
+  if (st != DAMOE_OK) return st;
+  if (!t || !variant_id) return DAMOE_ERR_INVALID_ARG;
+  if (t->E != L->E || t->k != L->k) return DAMOE_ERR_TABLE_MISMATCH;
+  if (!t->d_Q) return DAMOE_ERR_HIP;  // table built without a device
+  if (T < 0 || T > DAMOE_MAX_T) return DAMOE_ERR_INVALID_ARG;
+  if (!counts || !offsets || !effexp_numden || !effexp_bucket) return DAMOE_ERR_INVALID_ARG;
+  if (T > 0 && (!topk_ids || !perm || !inv_perm || !x || !topk_w || !y)) return DAMOE_ERR_INVALID_ARG;
+  if (L->wdtype == DAMOE_W_MXFP4 && L->layout != DAMOE_LAYOUT_FRAG16) return DAMOE_ERR_UNSUPPORTED;
+  if ((size_t)T * L->H * 2 >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
+  const uint32_t cand = damoe_table_candidates(t, T);
+  if (L->wdtype == DAMOE_W_FP8_B128 && (cand & (1u << kBigVariant)) && std::max(L->H, L->I) > 128 * 128)
+    return DAMOE_ERR_UNSUPPORTED;
+  damoe_ws_layout lo;
+  if (layout(L->E, L->k, L->H, L->I, T, &lo) != DAMOE_OK) return DAMOE_ERR_INVALID_ARG;
+  if (lo.total > kNoAllocScratchBytes) return DAMOE_ERR_WORKSPACE;
+  DeviceInfo* dev = nullptr;
+  if ((st = device_info(&dev)) != DAMOE_OK) return st;
+  if (!dev->scratch) return DAMOE_ERR_HIP;
+  // The routing call clears the work-queue words and stamps the tile lists; every other region
+  // of the array is written before it is read, so the previous call's contents never matter.
+  st = damoe_route_dispatch(t, topk_ids, T, L->k, L->E, counts, offsets, perm, inv_perm, effexp_numden,
+                            effexp_bucket, variant_id, dev->scratch, kNoAllocScratchBytes, stream);
+  if (st != DAMOE_OK) return st;
+  return damoe_fused_moe(L, x, topk_w, T, perm, inv_perm, variant_id, -1, cand, y, dev->scratch,
+                         kNoAllocScratchBytes, stream);
 }
 
 damoe_status damoe_pack_weights(const damoe_layer* L, void* w1, void* w3, void* w2, hipStream_t stream) {

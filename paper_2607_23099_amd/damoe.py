@@ -31,7 +31,8 @@ EXPORTED = [
     "damoe_variant_tile_m", "damoe_variant_supports", "damoe_tune", "damoe_alpha_search",
     "damoe_read_device_error", "damoe_fused_moe_stage", "damoe_route_dispatch", "damoe_pack_weights",
     "damoe_table_candidates", "damoe_router", "damoe_router_workspace_size", "damoe_route_dispatch_effexp",
-    "damoe_table_effexp_map", "damoe_table_effexp_candidates",
+    "damoe_table_effexp_map", "damoe_table_effexp_candidates", "damoe_noalloc_scratch_bytes",
+    "damoe_moe_layer_noalloc",
 ]
 
 
@@ -111,6 +112,8 @@ def lib() -> ctypes.CDLL:
             "damoe_route_dispatch_effexp": ([vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
             "damoe_table_effexp_map": ([vp, i32, vp], i32),
             "damoe_table_effexp_candidates": ([vp, i32], u32),
+            "damoe_noalloc_scratch_bytes": ([], sz),
+            "damoe_moe_layer_noalloc": ([vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         }
         for name, (args, res) in sigs.items():
             fn = getattr(L, name)
@@ -227,6 +230,18 @@ def fused_moe_stage(layer: Layer, stage, x, w, T, perm, inv_perm, variant_id, fo
         ctypes.byref(layer), int(stage), _p(x), _p(w), T, _p(perm), _p(inv_perm), _p(variant_id),
         int(force_variant), int(candidates), _p(y), _p(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(lib().damoe_noalloc_scratch_bytes())
+
+
+def moe_layer_noalloc(table: "Table", layer: Layer, x, ids, w, T, counts, offsets, perm, inv_perm, numden, bucket,
+                      variant_id, y, stream=None):
+    """route_dispatch + fused_moe with the library's own fixed workspace (no workspace argument)."""
+    _check("damoe_moe_layer_noalloc", lib().damoe_moe_layer_noalloc(
+        table.handle, ctypes.byref(layer), _p(x), _p(ids), _p(w), T, _p(counts), _p(offsets), _p(perm),
+        _p(inv_perm), _p(numden), _p(bucket), _p(variant_id), _p(y), _stream(stream)))
 
 
 def router_workspace_size(E: int, H: int, T_max: int) -> int:
