@@ -17,7 +17,12 @@ queued behind a ~1 ms GPU spin, so the events time the GPU, not the host.
 roofline = the dominant kernel (grouped GEMM1 + SwiGLU): algorithmic bytes
 (W1 and W3 of every touched expert + the token rows) / its mean duration,
 timed with HIP events on its own stream inside the timed region.
-cpu_baseline = the fp64 CPU oracle on one sweep point (T=8, alpha=1).
+cpu_baseline = the fp64 CPU oracle on every sweep point in full, geomean of its
+per-point layer times (us, like value).
+dispatch_trace = the other half of the metric, after the timed region: a
+paired 100-step Kimi-K2 trace (adaptive dispatch against the best static token
+bucket, NoDA and the per-step best variant, with bootstrap 95% intervals and the
+protocol's A/A noise floor), with its own oracle leg.
 """
 from __future__ import annotations
 
@@ -46,7 +51,13 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemm_glu_decode_sweep_traffic.txt")
+# HBM traffic summaries of the decode roofline kernel, per weight format: file, rocprof kernel
+# name prefix, and the bench flag that selects the format.
+TRAFFIC = {
+    "bf16": (os.path.join(ROOT, "profiles", "k_gemm_glu_decode_sweep_traffic.txt"), "k_gemm<true", ""),
+    "mxfp4": (os.path.join(ROOT, "profiles", "k_gemm_fp4_glu_decode_sweep_traffic.txt"), "k_gemm_fp4<true",
+              " --wdtype mxfp4"),
+}
 GEMM_SOURCES = ("csrc/gemm.hip", "csrc/device.h", "csrc/common.h", "csrc/queue.h")
 
 
@@ -59,11 +70,11 @@ def gemm_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(wdtype: str = "bf16"):
     """HBM bytes per GEMM1 launch from the committed counter summary, or None when it is missing
     or was taken on other kernel sources."""
     try:
-        kv = dict(l.split(":", 1) for l in open(TRAFFIC_FILE).read().splitlines() if ":" in l)
+        kv = dict(l.split(":", 1) for l in open(TRAFFIC[wdtype][0]).read().splitlines() if ":" in l)
     except OSError:
         return None
     kv = {k.strip(): v.strip() for k, v in kv.items()}
@@ -72,10 +83,11 @@ def measured_traffic():
     return int(float(kv["hbm_bytes_per_launch"]))
 
 
-def summarize_traffic(pmc_dir: str):
-    """Write TRAFFIC_FILE from four rocprofv3 --pmc runs under pmc_dir (subfolders fetch/,
-    write/: the decode sweep; copy_fetch/, copy_write/: `--workload copy`).  Counters are in KiB
-    per dispatch; each is scaled by what it reads for the plain copy of known size."""
+def summarize_traffic(pmc_dir: str, wdtype: str = "bf16"):
+    """Write the traffic summary of the GEMM1 kernel of `wdtype` from four rocprofv3 --pmc runs
+    under pmc_dir (subfolders fetch/, write/: the decode sweep; copy_fetch/, copy_write/:
+    `--workload copy`).  Counters are in KiB per dispatch; each is scaled by what it reads for
+    the plain copy of known size."""
     import csv
     import glob
 
@@ -84,7 +96,8 @@ def summarize_traffic(pmc_dir: str):
         return [float(r["Counter_Value"]) * 1024 for r in csv.DictReader(open(f))
                 if r["Counter_Name"] == counter and match(r["Kernel_Name"])]
 
-    is_glu = lambda n: "k_gemm<true" in n
+    path, prefix, flag = TRAFFIC[wdtype]
+    is_glu = lambda n: prefix in n
     is_copy = lambda n: "copy" in n.lower() or "elementwise" in n.lower()
     n_copy = 4 << 30
     fcal = max(values("copy_fetch", "FETCH_SIZE", is_copy)) / n_copy
@@ -92,10 +105,10 @@ def summarize_traffic(pmc_dir: str):
     fetch = values("fetch", "FETCH_SIZE", is_glu)
     write = values("write", "WRITE_SIZE", is_glu)
     per_launch = float(np.mean(fetch)) / fcal + float(np.mean(write)) / wcal
-    with open(TRAFFIC_FILE, "w") as f:
-        f.write("# HBM traffic of k_gemm<GEMM1+SwiGLU> over the DeepSeek-V3 decode sweep\n")
+    with open(path, "w") as f:
+        f.write(f"# HBM traffic of {prefix}...> (GEMM1 + SwiGLU) over the DeepSeek-V3 decode sweep{flag}\n")
         f.write("# rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv -d <dir>/fetch -- "
-                "python3 -u bench.py --steps 2 --warmup 1 --no-cpu-baseline\n")
+                f"python3 -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --bench-trace-steps 0{flag}\n")
         f.write("# calibration: the same counters on python3 -u bench.py --workload copy --steps 3 "
                 "(4 GiB read + 4 GiB written per call)\n")
         f.write(f"source_digest: {gemm_source_digest()}\n")
@@ -105,7 +118,7 @@ def summarize_traffic(pmc_dir: str):
         f.write(f"fetch_bytes_per_launch: {np.mean(fetch) / fcal:.0f}\n")
         f.write(f"write_bytes_per_launch: {np.mean(write) / wcal:.0f}\n")
         f.write(f"hbm_bytes_per_launch: {per_launch:.0f}\n")
-    print(open(TRAFFIC_FILE).read())
+    print(open(path).read())
 
 
 def geomean(v):
@@ -117,23 +130,50 @@ def touched_experts(ids) -> int:
     return int(len(np.unique(ids)))
 
 
-def cpu_baseline(shape, T, alpha):
-    """Time the CPU oracle on the full layer at one sweep point (weights pre-generated)."""
+def oracle_cores() -> int:
+    """Host threads the oracle's OpenMP loops use."""
+    return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+
+def oracle_leg(shape, cases: dict) -> dict:
+    """The fp64 CPU oracle timed on the host cores, beside a GPU figure.
+
+    cases: name -> (routing, x tag, token rows or None for every row).  The oracle runs expert
+    by expert over the union of the cases, as it does on one call: each expert's weights are
+    generated once (not timed), then its share of every case is timed.  Per case: `us` (the
+    measured oracle time of the rows taken), `assignments` (their slots), `A` (the call's), and
+    `us_call` = us A / assignments: the layer call's oracle time, measured when every row is
+    taken and extrapolated per assignment otherwise (`extrapolated`)."""
     import oracle
     from paper_2607_23099_amd import synth
     oracle.build()
-    r = synth.routing(shape.E, shape.k, T, alpha, synth.seed_decode(T, alpha, 0))
-    x = synth.activations_host(T, shape.H, 7)
-    experts = np.unique(r.ids)
-    wts = {int(e): synth.expert_weights_host(shape, int(e)) for e in experts}
-    t0 = time.perf_counter()
-    oracle.moe_rows(r.ids, r.w, shape.k, np.arange(T), x, shape.H, shape.I, experts, lambda e: wts[e])
-    dt = time.perf_counter() - t0
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(dt * 1e6, 1), "unit": "us", "cores": cores, "kind": "oracle",
-            "sample": f"one full DeepSeek-V3-shaped layer call, T={T} alpha={alpha} "
-                      f"({T * shape.k} assignments over {len(experts)} experts), fp64, "
-                      "weight generation excluded"}
+    src = synth.ExpertWeightSource(shape)
+    prep = {}
+    for n, (r, x_tag, rows) in cases.items():
+        rows = np.arange(r.T) if rows is None else np.asarray(rows, np.int64)
+        ids = r.ids[rows]
+        prep[n] = (ids, r.w[rows], synth.activations_host(r.T, shape.H, x_tag, rows),
+                   int(np.sum((r.ids >= 0) & (r.ids < shape.E))), int(np.sum((ids >= 0) & (ids < shape.E))),
+                   len(rows) < r.T)
+    experts = sorted({int(e) for p in prep.values() for e in np.unique(p[0]) if 0 <= e < shape.E})
+    spent = {n: 0.0 for n in prep}
+    t_start = time.perf_counter()
+    for i, e in enumerate(experts):
+        wts = src(e)
+        for n, (ids, w, x, _, _, _) in prep.items():
+            if not np.any(ids == e):
+                continue
+            t0 = time.perf_counter()
+            oracle.moe_rows(ids, w, shape.k, np.arange(len(ids)), x, shape.H, shape.I, [e], lambda _e: wts)
+            spent[n] += time.perf_counter() - t0
+        if (i + 1) % 64 == 0:
+            log(f"oracle {shape.name}: expert {i + 1}/{len(experts)} ({time.perf_counter() - t_start:.0f} s)")
+    out = {}
+    for n, (_, _, _, A, a, sampled) in prep.items():
+        us = spent[n] * 1e6
+        out[n] = {"us": round(us, 1), "assignments": a, "A": A, "us_call": round(us * A / max(a, 1), 1),
+                  "extrapolated": sampled}
+    return out
 
 
 def load_or_tune_table(dl, x, quick, buckets=DECODE_T):
@@ -150,60 +190,74 @@ def load_or_tune_table(dl, x, quick, buckets=DECODE_T):
     return table, f"quick-tuned at start-up in {time.perf_counter() - t0:.1f} s (S=3, reps=3)"
 
 
-def run_trace(args):
-    """Dispatch trace on the Kimi-K2 shape: adaptive vs per-step best vs static buckets."""
-    import torch
-    from paper_2607_23099_amd import damoe, synth
-    from paper_2607_23099_amd.moe import DeviceLayer, Path
+def bootstrap_ci(ratios: np.ndarray, n: int = 2000, seed: int = 0) -> list:
+    """95% interval of the geomean of per-step ratios, resampling the steps."""
+    rng = np.random.default_rng(seed)
+    lr = np.log(ratios)
+    g = np.exp(lr[rng.integers(0, len(lr), (n, len(lr)))].mean(axis=1))
+    return [round(float(np.quantile(g, 0.025)), 4), round(float(np.quantile(g, 0.975)), 4)]
 
-    shape = synth.KIMI
-    T_MAX = 8192
-    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
-    dl = DeviceLayer(shape)
-    path = Path(dl, T_MAX)
-    path.fill_x(T_MAX, 4)
-    torch.cuda.synchronize()
-    table, note = load_or_tune_table(dl, path.x, args.quick_tune, [2 ** i for i in range(14)])
-    log(f"dispatch table: {note}")
+
+def trace_measure(torch, dl, path, table, n_steps: int, reps: int, t_max: int = 8192, log_every: int = 50) -> dict:
+    """Paired dispatch trace on one layer (Kimi-K2 shape): steps with T log-uniform in
+    [1, t_max] and Dirichlet alpha log-uniform in [0.03, 10], a fresh routing per step.
+
+    Per step, every configuration runs reps + 1 times (the first untimed), in an order shuffled
+    anew for every pass, each behind a 1 GiB write that evicts the weights from the L2 caches
+    and the 256 MB Infinity Cache:
+      * variant v: routing without the match, then the fused call with the one-bit candidate
+        mask of v -- the same launch path adaptive dispatch takes for a one-kernel bucket;
+      * adaptive, twice (A and A'): routing with the exemplar match, then the fused call with
+        the bucket's candidates, the kernels reading the device-side choice.
+    Latencies are path times (a2-a8), medians over the timed passes.  A' against A is the
+    noise floor of the protocol; the per-step best is the minimum over the variants."""
+    from paper_2607_23099_amd import damoe, synth
+    shape = dl.shape
     td = table.data(shape.E)
-    nv = damoe.num_variants()
-    V = [v for v in range(nv) if damoe.variant_supports(v, dl.wdtype)]
+    V = [v for v in range(damoe.num_variants()) if damoe.variant_supports(v, dl.wdtype)]
+    configs = [("v", v) for v in V] + [("adaptive", 0), ("adaptive", 1)]
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
     ev = lambda: torch.cuda.Event(enable_timing=True)
     steps = []
     t_start = time.perf_counter()
-    for s in range(args.trace_steps):
-        T, alpha = synth.trace_step_params(s, T_MAX)
+    for s in range(n_steps):
+        T, alpha = synth.trace_step_params(s, t_max)
         r = synth.routing(shape.E, shape.k, T, alpha, synth.seed_trace_step(s))
         path.set_routing(r)
-        # one untimed pass of every configuration, then reps timed passes
-        runs = {}
-        for rep in range(args.trace_reps + 1):
-            for v in V + [-1]:
+        rng = np.random.default_rng([9, s])
+        runs = {c: [] for c in configs}
+        for rep in range(reps + 1):
+            for ci in rng.permutation(len(configs)):
+                kind, v = configs[ci]
+                flush.fill_(rep & 0xFF)
                 e0, e1 = ev(), ev()
                 e0.record(stream)
-                if v < 0:
+                if kind == "adaptive":
                     path.route_dispatch(table, T)
                 else:
                     path.route(T)
-                path.fused(T, v)
+                    path.candidates = 1 << v
+                path.fused(T, -1)
                 e1.record(stream)
                 if rep:
-                    runs.setdefault(v, []).append((e0, e1))
+                    runs[configs[ci]].append((e0, e1))
         torch.cuda.synchronize()
-        lat = {v: float(np.median([a.elapsed_time(b) for a, b in runs[v]])) * 1e3 for v in runs}
-        chosen = int(path.variant.item())
+        lat = {c: float(np.median([a.elapsed_time(b) for a, b in runs[c]])) * 1e3 for c in configs}
         b = next((i for i, bt in enumerate(td.bucket_T) if T <= bt), len(td.bucket_T) - 1)
-        steps.append({"T": T, "alpha": alpha, "bucket": b, "chosen": chosen,
-                      "adaptive": lat[-1], "lat": [lat[v] for v in V]})
-        if (s + 1) % 50 == 0:
-            log(f"trace step {s + 1}/{args.trace_steps} ({time.perf_counter() - t_start:.0f} s)")
-    # Derived baselines from the one latency matrix.
-    L = np.array([st["lat"] for st in steps])            # [steps][variants]
+        steps.append({"step": s, "T": T, "alpha": alpha, "bucket": b, "chosen": int(path.variant.item()),
+                      "adaptive": lat[("adaptive", 0)], "adaptive_b": lat[("adaptive", 1)],
+                      "lat": [lat[("v", v)] for v in V]})
+        if (s + 1) % log_every == 0:
+            log(f"trace step {s + 1}/{n_steps} ({time.perf_counter() - t_start:.0f} s)")
+    del flush
+    L = np.array([st["lat"] for st in steps])
     A = np.array([st["adaptive"] for st in steps])
+    A2 = np.array([st["adaptive_b"] for st in steps])
     B = np.array([st["bucket"] for st in steps])
     step_best = L.min(axis=1)
     noda = np.array([L[i, V.index(int(td.noda[B[i]]))] for i in range(len(steps))])
+    chosen = np.array([L[i, V.index(st["chosen"])] if st["chosen"] in V else np.nan for i, st in enumerate(steps)])
     static = np.zeros(len(steps))
     static_choice = {}
     for b in sorted(set(B.tolist())):
@@ -222,10 +276,72 @@ def run_trace(args):
             "best_static_pct_of_step_best": round(100 * g(static[idx] / step_best[idx]), 1),
             "noda_pct_of_step_best": round(100 * g(noda[idx] / step_best[idx]), 1),
         }
-    picked_best = float(np.mean([V[int(np.argmin(st["lat"]))] == st["chosen"] for st in steps]))
+    ok = ~np.isnan(chosen)
+    res = {
+        "steps": len(steps),
+        "reps": reps,
+        "speedup_vs_best_static": round(g(static / A), 4),
+        "speedup_vs_best_static_ci95": bootstrap_ci(static / A),
+        "speedup_vs_noda": round(g(noda / A), 4),
+        "speedup_vs_noda_ci95": bootstrap_ci(noda / A, seed=1),
+        "adaptive_over_step_best": round(g(A / step_best), 4),
+        "adaptive_over_step_best_ci95": bootstrap_ci(A / step_best, seed=2),
+        "best_static_over_step_best": round(g(static / step_best), 4),
+        # A' over A: the same configuration timed twice, the protocol's noise floor.
+        "aa_noise": round(g(A2 / A), 4),
+        "aa_noise_ci95": bootstrap_ci(A2 / A, seed=3),
+        # Adaptive over its own choice forced: the cost of the match and the device-side read.
+        "adaptive_over_chosen_forced": round(g(A[ok] / chosen[ok]), 4),
+        "chose_step_best_fraction": round(float(np.mean([V[int(np.argmin(st["lat"]))] == st["chosen"]
+                                                         for st in steps])), 3),
+        "best_static_choice": static_choice,
+        "per_bucket": per_bucket,
+    }
+    lo = res["speedup_vs_best_static_ci95"][0]
+    res["faster_than_best_static"] = bool(lo > 1.0 and lo > res["aa_noise_ci95"][1])
+    res["within_5pct_of_step_best"] = bool(res["adaptive_over_step_best_ci95"][1] <= 1.05)
+    res["_steps"] = steps
+    res["_adaptive_us"] = A
+    return res
+
+
+def trace_oracle(shape, steps, rows_per_step: int = 4) -> dict:
+    """The oracle beside the trace: per step, its time on min(T, rows_per_step) token rows of the
+    step's routing, extrapolated per assignment to the step's T k; geomean over the steps."""
+    from paper_2607_23099_amd import synth
+    cases = {}
+    for st in steps:
+        r = synth.routing(shape.E, shape.k, st["T"], st["alpha"], synth.seed_trace_step(st["step"]))
+        rng = np.random.default_rng([10, st["step"]])
+        rows = np.sort(rng.choice(r.T, min(r.T, rows_per_step), replace=False))
+        cases[st["step"]] = (r, 4, rows)
+    leg = oracle_leg(shape, cases)
+    us = [leg[n]["us_call"] for n in cases]
+    return {"value": round(geomean(us), 1), "unit": "us", "cores": oracle_cores(), "kind": "oracle",
+            "sample": f"every trace step on min(T, {rows_per_step}) token rows, fp64, expert-major, weight "
+                      "generation excluded; extrapolated per assignment to each step's T k; geomean over steps"}
+
+
+def run_trace(args):
+    """Dispatch trace on the Kimi-K2 shape: adaptive vs per-step best vs static buckets."""
+    import torch
+    from paper_2607_23099_amd import synth
+    from paper_2607_23099_amd.moe import DeviceLayer, Path
+
+    shape = synth.KIMI
+    T_MAX = 8192
+    log(f"filling {shape.name} weights on the device ({shape.E} experts, bf16)")
+    dl = DeviceLayer(shape)
+    path = Path(dl, T_MAX)
+    path.fill_x(T_MAX, 4)
+    torch.cuda.synchronize()
+    table, note = load_or_tune_table(dl, path.x, args.quick_tune, [2 ** i for i in range(14)])
+    log(f"dispatch table: {note}")
+    res = trace_measure(torch, dl, path, table, args.trace_steps, args.trace_reps, T_MAX)
+    steps, A = res.pop("_steps"), res.pop("_adaptive_us")
     out = {
         "metric": "geomean dispatch speedup over the best static token-count bucket (Kimi-K2 trace)",
-        "value": round(g(static / A), 4),
+        "value": res["speedup_vs_best_static"],
         "unit": "x",
         "n_gpus": 1,
         "steps": len(steps),
@@ -238,17 +354,15 @@ def run_trace(args):
         "data": "synthetic",
         "config": {"workload": f"kimi-k2 dispatch trace: E=384 top-8 H=7168 I=2048 bf16, {len(steps)} steps, "
                                "T log-uniform in [1,8192], Dirichlet alpha log-uniform in [0.03,10]",
-                   "table": note, "variants": [damoe.variant_name(v) for v in V]},
-        "speedup_vs_noda": round(g(noda / A), 4),
-        "adaptive_over_step_best": round(g(A / step_best), 4),
-        "best_static_over_step_best": round(g(static / step_best), 4),
-        "chose_step_best_fraction": round(picked_best, 3),
-        "best_static_choice": static_choice,
-        "per_bucket": per_bucket,
+                   "table": note},
+        **res,
     }
-    with open(os.path.join(ROOT, "gpurun_out", "trace_steps.json") if os.path.isdir(os.path.join(ROOT, "gpurun_out"))
-              else os.devnull, "w") as f:
-        json.dump(steps, f)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = trace_oracle(shape, steps)
+    gdir = os.path.join(ROOT, "gpurun_out")
+    if os.path.isdir(gdir):
+        with open(os.path.join(gdir, "trace_steps.json"), "w") as f:
+            json.dump(steps, f)
     print(json.dumps(out), flush=True)
 
 
@@ -863,11 +977,14 @@ def run_prefill(args):
         path.fill_x(max(Ts), 5)
         V = [int(v) for v in args.variants.split(",")] if args.variants else list(range(damoe.num_variants()))
         V = [v for v in V if damoe.variant_supports(v, dl.wdtype)]
+        oracle_cases = {}
         for T in Ts:
             for a in alphas:
                 r = synth.routing(shape.E, shape.k, T, a, synth.seed_prefill(T, a, 0) if not hot else
                                   synth.seed_kimi(T, 0), n_hot=hot)
                 path.set_routing(r)
+                oracle_cases[f"{shape.name}_T{T}_a{a}"] = (
+                    r, 5, np.sort(np.random.default_rng([11, T]).choice(T, min(T, 16), replace=False)))
                 A = T * shape.k
                 counts = np.bincount(r.ids.ravel(), minlength=shape.E)
                 f_alg, b_alg, U = prefill_alg(shape, T, counts)
@@ -928,6 +1045,14 @@ def run_prefill(args):
                                      "fused_best_speedup": round(lm * 1e3 / g1best, 3),
                                      "dense_gemm_us": round(dm * 1e3, 1), "dense_tflops": round(f1 / dm / 1e9, 1)}
                     log(f"{pkey} per-expert hipBLASLt GEMM1: {library[pkey]}")
+        if not args.no_cpu_baseline:
+            # The oracle beside every point: 16 token rows of its routing, timed, extrapolated
+            # per assignment to the call.
+            log(f"oracle on 16 rows of every {shape.name} point (host cores)")
+            for pk, o in oracle_leg(shape, oracle_cases).items():
+                points[pk]["oracle_us"] = o["us_call"]
+                points[pk]["oracle_extrapolated"] = o["extrapolated"]
+                points[pk]["speedup_over_oracle"] = round(o["us_call"] / points[pk]["fused_us"], 1)
         del dl, path
         torch.cuda.empty_cache()
     out = {
@@ -956,6 +1081,14 @@ def run_prefill(args):
         # GEMM of the same FLOPs (T k x H times H x 2I), the practical MFMA ceiling of a plain GEMM.
         "library_gemm1_per_expert": library,
     }
+    kp = "kimi-k2_T8192_a0.05"
+    if kp in points and "oracle_us" in points[kp]:
+        out["cpu_baseline"] = {
+            "value": round(points[kp]["alg_gflop"] * 1e3 / points[kp]["oracle_us"], 6), "unit": "TFLOP/s",
+            "cores": oracle_cores(), "kind": "oracle",
+            "sample": "the Kimi-K2 T=8192 layer's algorithmic FLOPs over the fp64 oracle's time on 16 of its token "
+                      "rows, extrapolated per assignment (weight generation excluded); every point carries its own "
+                      "oracle_us the same way"}
     print(json.dumps(out), flush=True)
 
 
@@ -1024,11 +1157,13 @@ def main():
     ap.add_argument("--dispatch-reps", type=int, default=200)
     ap.add_argument("--trace-steps", type=int, default=1000)
     ap.add_argument("--trace-reps", type=int, default=3)
+    ap.add_argument("--bench-trace-steps", type=int, default=100,
+                    help="decode sweep: steps of the paired Kimi-K2 dispatch trace reported beside it (0 = none)")
     ap.add_argument("--summarize-traffic", default="", metavar="PMC_DIR",
                     help="write the GEMM1 traffic summary from rocprofv3 --pmc runs (no GPU needed)")
     args = ap.parse_args()
     if args.summarize_traffic:
-        return summarize_traffic(args.summarize_traffic)
+        return summarize_traffic(args.summarize_traffic, args.wdtype)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -1176,12 +1311,41 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "k_gemm_fp4<GEMM1+SwiGLU>" if args.wdtype == "mxfp4"
                      else "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic() if args.wdtype == "bf16" else None,
+                     "traffic": measured_traffic(args.wdtype),
                      "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1))},
         "per_point": per_point,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(shape, 8, 1.0)
+        log("oracle on every sweep point (host cores)")
+        cases = {(T, a): (synth.routing(shape.E, shape.k, T, a, synth.seed_decode(T, a, 0)), 1, None)
+                 for (T, a) in points}
+        leg = oracle_leg(shape, cases)
+        out["cpu_baseline"] = {
+            "value": round(geomean([leg[p]["us_call"] for p in points]), 1), "unit": "us",
+            "cores": oracle_cores(), "kind": "oracle",
+            "sample": f"every one of the {len(points)} sweep points in full ({sum(leg[p]['A'] for p in points)} "
+                      "assignments; each point's first routing and the benchmark's tokens), fp64, expert-major, "
+                      "weight generation excluded; geomean over the points of the oracle's layer time, as value",
+            "per_point_us": {f"T{T}_a{a}": leg[T, a]["us"] for (T, a) in points}}
+    if args.bench_trace_steps > 0 and args.wdtype == "bf16" and force < 0:
+        # The dispatch half of the metric: a paired Kimi-K2 trace (adaptive against the best
+        # static bucket and the per-step best), on a layer of its own.
+        del dl, path
+        torch.cuda.empty_cache()
+        log(f"filling {synth.KIMI.name} weights for the dispatch trace")
+        kl = DeviceLayer(synth.KIMI)
+        kpath = Path(kl, 8192)
+        kpath.fill_x(8192, 4)
+        torch.cuda.synchronize()
+        ktable, knote = load_or_tune_table(kl, kpath.x, args.quick_tune, [2 ** i for i in range(14)])
+        res = trace_measure(torch, kl, kpath, ktable, args.bench_trace_steps, args.trace_reps, 8192, log_every=25)
+        steps_ = res.pop("_steps")
+        res.pop("_adaptive_us")
+        res["workload"] = (f"kimi-k2 dispatch trace: E=384 top-8 H=7168 I=2048 bf16, {len(steps_)} steps, T "
+                           "log-uniform in [1,8192], Dirichlet alpha log-uniform in [0.03,10]; table: " + knote)
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = trace_oracle(synth.KIMI, steps_)
+        out["dispatch_trace"] = res
     print(json.dumps(out), flush=True)
 
 

@@ -201,9 +201,22 @@ __device__ __forceinline__ void pin_gemm_args(const GemmArgs& a) {
 // skipped and DAMOE_DEVERR_TILES is set.
 __device__ __forceinline__ int tile_count(const int32_t* list, const GemmArgs& a) {
   const int n = list[0];
-  if (a.ctrl[kRoutedA] == a.A && list[1] == a.A && n >= 0 && n <= a.tiles_cap) return n;
-  if (threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
-  return 0;
+  const bool ok = a.ctrl[kRoutedA] == a.A && list[1] == a.A && n >= 0 && n <= a.tiles_cap;
+  return ok ? n : 0;
+}
+
+// The flag of the check above, raised once per launch (block 0) at kernel entry for any list
+// of the call that tile_count would refuse; kept out of the item loops, where a side effect
+// costs the compiler's scheduling of the weight stream.
+__device__ __forceinline__ void flag_stale_tiles(const GemmArgs& a) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  bool ok = a.ctrl[kRoutedA] == a.A;
+#pragma unroll
+  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) {
+    const int32_t* l = a.tiles.list[c];
+    ok = ok && l[1] == a.A && l[0] >= 0 && l[0] <= a.tiles_cap;
+  }
+  if (!ok) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
 }
 
 // Device-side variant check of a fused launch: a forced variant is trusted (validated on the

@@ -616,6 +616,7 @@ template <bool GLU, bool FP8, bool PK>
 __global__ void __launch_bounds__(kGemmThreads, 2) k_gemm(GemmArgs a) {
   extern __shared__ float smem[];
   pin_gemm_args(a);
+  flag_stale_tiles(a);
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
   if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
   if (!variant_admitted(v, a.force_variant, a.candidates)) {
@@ -651,6 +652,7 @@ template <bool GLU>
 __global__ void __launch_bounds__(kGemmThreads, kFp4Occupancy[GLU]) k_gemm_fp4(GemmArgs a) {
   extern __shared__ float smem[];
   pin_gemm_args(a);
+  flag_stale_tiles(a);
   int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
   if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
   if (!variant_admitted(v, a.force_variant, a.candidates)) {

@@ -343,6 +343,7 @@ template <bool GLU, bool FP8, bool PK>
 __global__ void __launch_bounds__(kGemmThreads, 1) k_gemm_big(GemmArgs a) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_smem[];
   pin_gemm_args(a);
+  flag_stale_tiles(a);
   const int v = a.force_variant >= 0 ? a.force_variant : *a.variant_id;
   if (GLU && blockIdx.x == 0 && threadIdx.x == 0) a.ctrl[4] = v;
   if (!variant_admitted(v, a.force_variant, a.candidates)) {

@@ -38,3 +38,27 @@ def test_decode_gemm1_algorithmic_bytes():
     assert b.gemm1_alg_bytes(sh, 1, 0, 2.0) == 58_720_256
     assert b.gemm1_alg_bytes(sh, 1, 0, 17.0 / 32.0) == 15_597_568
     assert b.gemm1_alg_bytes(sh, 54, 8, 2.0) == 54 * 58_720_256 + 8 * 7168 * 2
+
+
+def test_oracle_leg_measures_and_extrapolates():
+    # Every row taken: the call's time is the measured one.  A sample of rows: scaled by the
+    # call's assignments over the sample's, and marked as extrapolated.
+    b = _bench()
+    sh = synth.TINY
+    r = synth.routing(sh.E, sh.k, 40, 1.0, [3])
+    leg = b.oracle_leg(sh, {"full": (r, 0, None), "sample": (r, 0, np.array([1, 7, 30]))})
+    assert leg["full"]["A"] == leg["full"]["assignments"] == 80 and not leg["full"]["extrapolated"]
+    assert leg["full"]["us_call"] == leg["full"]["us"] > 0
+    s = leg["sample"]
+    assert s["assignments"] == 6 and s["A"] == 80 and s["extrapolated"]
+    assert abs(s["us_call"] - s["us"] * 80 / 6) <= 0.05 * 80 / 6 + 0.05  # both rounded to 0.1 us
+
+
+def test_bootstrap_interval_brackets_the_geomean():
+    b = _bench()
+    rng = np.random.default_rng(0)
+    r = np.exp(rng.normal(0.05, 0.02, 400))
+    lo, hi = b.bootstrap_ci(r)
+    g = float(np.exp(np.mean(np.log(r))))
+    assert lo < g < hi and hi - lo < 0.01
+    assert b.bootstrap_ci(np.full(50, 1.25)) == [1.25, 1.25]
