@@ -969,7 +969,12 @@ def run_prefill(args):
     rows, points, library = {}, {}, {}
     best = None
     bw, mfma = 8000.0, 2500.0  # GB/s, TFLOP/s
+    keep = {tuple(p.split(":")) for p in args.points.split(",") if p}
     for name, Ts, alphas, hot in PREFILL_GRID:
+        if keep:
+            Ts = tuple(T for T in Ts if (name, str(T)) in keep)
+            if not Ts:
+                continue
         shape = shapes[name]
         log(f"filling {shape.name} weights")
         dl = DeviceLayer(shape)
@@ -1055,6 +1060,9 @@ def run_prefill(args):
                 points[pk]["speedup_over_oracle"] = round(o["us_call"] / points[pk]["fused_us"], 1)
         del dl, path
         torch.cuda.empty_cache()
+    if best is None:  # a --points selection without Kimi-K2 T = 8192: the best GEMM1 among those run
+        k_ = max(rows, key=lambda k2: rows[k2]["gemm1_tflops"])
+        best = (k_, rows[k_]["gemm1_us"], rows[k_]["gemm1_tflops"] * rows[k_]["gemm1_us"] * 1e6)
     out = {
         "metric": "grouped GEMM1 + SwiGLU TFLOP/s, Kimi-K2 prefill T=8192 (best variant)",
         "value": round(best[2] / best[1] / 1e6, 1),
@@ -1152,6 +1160,7 @@ def main():
     ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router", "imbalance", "ep"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
+    ap.add_argument("--points", default="", help="prefill: comma-separated points to run, e.g. kimi-k2:8192,dsv3-fp8:16384")
     ap.add_argument("--wdtype", choices=["bf16", "mxfp4"], default="bf16",
                     help="decode sweep: expert weight format (activations and MFMA stay bf16)")
     ap.add_argument("--dispatch-reps", type=int, default=200)
