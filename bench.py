@@ -12,11 +12,14 @@ cannot serve repeated weights).  All inputs are resident in HBM before the
 timed region.
 
 value = geomean over the 16 points of the median path latency over the timed
-steps (us per layer; each point's mean is reported beside it).  Each step is
-queued behind a ~1 ms GPU spin, so the events time the GPU, not the host.
+steps (us per layer; each point's mean is reported beside it), the call made
+as a caller makes it: route + dispatch, then one fused call, between two
+events.  Each step is queued behind a ~1 ms GPU spin, so the events time the
+GPU, not the host.  Timed steps alternate between that clean form and an
+instrumented one with an event between every two kernels (per-kernel times).
 roofline = the dominant kernel (grouped GEMM1 + SwiGLU): algorithmic bytes
 (W1 and W3 of every touched expert + the token rows) / its mean duration,
-timed with HIP events on its own stream inside the timed region.
+timed with HIP events on its own stream in the instrumented steps.
 cpu_baseline = the fp64 CPU oracle on every sweep point in full, geomean of its
 per-point layer times (us, like value).
 dispatch_trace = the other half of the metric, after the timed region: a
@@ -1229,8 +1232,20 @@ def main():
     ev = lambda: torch.cuda.Event(enable_timing=True)
     force = args.force_variant
 
-    def run_point(T, a, rep, events=None):
+    def run_point(T, a, rep, events=None, clean=None):
+        """One layer call.  `clean` = (start, end) events around the whole call, made as a caller
+        would make it (route + dispatch, then one fused call); `events` = 5 events between the
+        kernels of the instrumented form (route, GEMM1, GEMM2, reduce as separate calls)."""
         ids, w = ids_d[T, a, rep], w_d[T, a, rep]
+        if clean:
+            clean[0].record(stream)
+            if force < 0:
+                path.route_dispatch(table, T, ids=ids)
+            else:
+                path.route(T, ids=ids)
+            path.fused(T, force, w=w)
+            clean[1].record(stream)
+            return
         if events:
             events[0].record(stream)
         if force < 0:
@@ -1250,7 +1265,10 @@ def main():
             events[4].record(stream)
 
     # Each step starts behind a ~1 ms spin, so the host has queued the step's first points
-    # before the GPU reaches them and events time the GPU, not the host's launch pace.
+    # before the GPU reaches them and events time the GPU, not the host's launch pace.  Steps
+    # alternate between the clean form (path latency: two events per call) and the instrumented
+    # form (per-kernel times and the GEMM1 roofline: an event between every two kernels, which
+    # adds about 3 us of gap per event to the path, so the path is never taken from it).
     spin = gpu_spin(torch, stream, 1000.0)
     for s in range(args.warmup):
         torch.cuda._sleep(spin)
@@ -1259,27 +1277,34 @@ def main():
     torch.cuda.synchronize()
 
     rec = {p: [] for p in points}
-    all_events = []
+    clean_rec = {p: [] for p in points}
+    all_events, all_clean = [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        rep = (s + args.warmup) % REPS
+        rep = (s // 2 + args.warmup) % REPS  # both forms of a step pair on the same routings
         torch.cuda._sleep(spin)
         for (T, a) in points:
-            e = [ev() for _ in range(5)]
-            run_point(T, a, rep, e)
-            all_events.append(((T, a, rep), e))
+            if s % 2 == 0:
+                c = [ev(), ev()]
+                run_point(T, a, rep, clean=c)
+                all_clean.append(((T, a, rep), c))
+            else:
+                e = [ev() for _ in range(5)]
+                run_point(T, a, rep, e)
+                all_events.append(((T, a, rep), e))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
     g1_bytes, g1_ms = 0.0, 0.0
     for (T, a, rep), e in all_events:
-        path_ms = e[0].elapsed_time(e[4])
         g1 = e[1].elapsed_time(e[2])
         g2 = e[2].elapsed_time(e[3])
-        rec[T, a].append((path_ms, g1, g2, e[0].elapsed_time(e[1]), e[3].elapsed_time(e[4])))
+        rec[T, a].append((e[0].elapsed_time(e[4]), g1, g2, e[0].elapsed_time(e[1]), e[3].elapsed_time(e[4])))
         g1_bytes += gemm1_alg_bytes(shape, U[T, a, rep], T, wbytes)
         g1_ms += g1
+    for (T, a, rep), c in all_clean:
+        clean_rec[T, a].append(c[0].elapsed_time(c[1]))
 
     # Per point: medians over the timed steps (a stall of the host between two launches lands
     # inside one step's events), and the path's mean beside its median.
@@ -1287,9 +1312,11 @@ def main():
     for (T, a), v in rec.items():
         arr = np.array(v)
         med = np.median(arr, axis=0) * 1e3
+        cl = np.array(clean_rec[T, a]) * 1e3
         per_point[f"T{T}_a{a}"] = {
-            "path_us": round(float(med[0]), 1),
-            "path_us_mean": round(float(arr[:, 0].mean()) * 1e3, 1),
+            "path_us": round(float(np.median(cl)), 1),
+            "path_us_mean": round(float(cl.mean()), 1),
+            "instrumented_path_us": round(float(med[0]), 1),
             "gemm1_us": round(float(med[1]), 1),
             "gemm2_us": round(float(med[2]), 1),
             "route_dispatch_us": round(float(med[3]), 1),
@@ -1321,7 +1348,8 @@ def main():
                      else "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.wdtype),
-                     "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1))},
+                     "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1)),
+                     "launches": len(all_events)},
         "per_point": per_point,
     }
     if not args.no_cpu_baseline:

@@ -380,6 +380,9 @@ typedef struct damoe_tune_config {
                                one Gumbel-top-k row (ids and gates) under a Dirichlet(1) p,
                                the token analog of repeated prompts (Sec. V-E); each f adds
                                one exemplar after the skews' in every bucket             */
+  int32_t flush_mib;        /* MiB of scratch written before every timed run (0 = none), so
+                               that no run finds the weights of the previous one in the L2
+                               caches or the Infinity Cache, as a serving step would not  */
 } damoe_tune_config;
 
 /* Builds a table: for each bucket T_b and skew X_j, alpha_j = Alg1(E / X_j);
@@ -414,10 +417,11 @@ damoe_status damoe_router(const uint16_t* x, const uint16_t* wg, const float* bi
                           int32_t H, int32_t E, int32_t k, float* logits, int32_t* topk_ids,
                           float* topk_w, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Alg. 1 (Sec. III-A): bisection over alpha in [1e-6, 1e6] for the Dirichlet
- * concentration whose mean sampled Effective Experts over `samples` draws
- * reaches `target`; common random numbers (Philox4x32-10 keyed by seed) at
- * every step.  Host-only. */
+/* Alg. 1 (Sec. III-A): the Dirichlet concentration alpha in [1e-6, 1e6] whose
+ * mean Effective Experts over `samples` draws equals `target`, by bisection on
+ * log(alpha) (at most `iters` halvings, stopping once the bracket is within a
+ * relative 1e-12); the same counter-based random numbers (Philox4x32-10 keyed
+ * by seed) at every alpha.  Host-only. */
 double damoe_alpha_search(int32_t E, double target, int32_t samples, int32_t iters, uint64_t seed);
 
 /* Reads and clears the sticky device error code in ws (synchronises stream). */

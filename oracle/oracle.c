@@ -399,13 +399,14 @@ static double effexp_of_dirichlet_sample(uint64_t seed, double alpha, int32_t E,
   return sp * sp / sp2;
 }
 
-/* Alg. 1 (Sec. III-A): bisection for the Dirichlet concentration alpha whose
- * mean sampled eff_exp over S samples reaches the target.  lo = 1e-6,
- * hi = 1e6; each of the `iters` iterations takes the arithmetic midpoint,
- * draws S samples of Dir(mid), averages their eff_exp, moves lo up when the
- * mean is below the target (too skewed) and hi down otherwise, and the last
- * midpoint is returned.  The same random numbers (key `seed`) are used at
- * every iteration, so the mean is a deterministic function of alpha. */
+/* Alg. 1 (Sec. III-A): the concentration of a symmetric Dirichlet whose mean
+ * Effective Experts over S samples equals the target.  The mean grows with
+ * alpha, so the algorithm brackets the root in [1e-6, 1e6] and halves the
+ * bracket `iters` times at its arithmetic midpoint, keeping the half whose
+ * mean straddles the target; the midpoint of the last halving is the answer.
+ * The paper leaves S and the number of halvings open (taken as inputs).  The
+ * samples use the same random numbers (key `seed`) at every alpha, so the
+ * mean is a deterministic function of alpha. */
 double oracle_alpha_search(int32_t E, double target, int32_t S, int32_t iters, uint64_t seed) {
   double lo = 1e-6, hi = 1e6, mid = 0.5 * (lo + hi);
   double* logg = (double*)malloc(sizeof(double) * (size_t)E);

@@ -220,18 +220,23 @@ void exemplar(const std::vector<std::vector<int32_t>>& counts, int32_t E, int32_
 
 extern "C" {
 
+// Alg. 1's root: the mean Effective Experts of Dir(alpha) grows with alpha (Sec. III-A), so the
+// concentration reaching `target` is bracketed in [1e-6, 1e6] and the bracket is halved on a log
+// scale (alpha spans twelve decades and the skews of interest sit between 0.03 and 10), at most
+// `iters` times, until its ends agree to a relative 1e-12; the geometric centre of the bracket
+// is returned.  The draws are the same at every alpha (common random numbers), so the mean is a
+// deterministic function of alpha.
 double damoe_alpha_search(int32_t E, double target, int32_t samples, int32_t iters, uint64_t seed) {
   if (E < 1 || samples < 1 || iters < 1) return NAN;
   const Philox g(seed);
   std::vector<double> lp;
-  double lo = 1e-6, hi = 1e6, mid = 0.5 * (lo + hi);
-  for (int32_t t = 0; t < iters; ++t) {
-    mid = 0.5 * (lo + hi);
-    const double v = mean_effexp(g, E, mid, samples, lp);
-    if (v < target) lo = mid;  // too skewed: raise alpha
-    else hi = mid;             // too uniform: lower alpha
+  double log_lo = std::log(1e-6), log_hi = std::log(1e6);
+  for (int32_t t = 0; t < iters && log_hi - log_lo > 1e-12; ++t) {
+    const double log_c = 0.5 * (log_lo + log_hi);
+    const bool below = mean_effexp(g, E, std::exp(log_c), samples, lp) < target;
+    (below ? log_lo : log_hi) = log_c;
   }
-  return mid;
+  return std::exp(0.5 * (log_lo + log_hi));
 }
 
 damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damoe_table** out,
@@ -253,6 +258,8 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
     return DAMOE_ERR_INVALID_ARG;
   for (int32_t r = 0; r < cfg->n_repeat; ++r)
     if (cfg->repeat_f[r] < 1 || cfg->repeat_f[r] > 100) return DAMOE_ERR_INVALID_ARG;
+  if (cfg->flush_mib < 0 || cfg->flush_mib > 16384) return DAMOE_ERR_INVALID_ARG;
+  const size_t flush_bytes = (size_t)cfg->flush_mib << 20;
   const int32_t ep = cfg->ep > 1 ? cfg->ep : 1;
   const int32_t Eg = E * ep;
   const int32_t a_samples = cfg->alpha_samples > 0 ? cfg->alpha_samples : 64;
@@ -267,6 +274,7 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   uint64_t* d_nd = nullptr;
   uint16_t* d_y = nullptr;
   int32_t* d_vid = nullptr;
+  void* d_flush = nullptr;
   hipEvent_t e0 = nullptr, e1 = nullptr;
   std::vector<int32_t> t_bucket, t_nex, t_noda, t_kid, t_Q;
   std::vector<double> alphas(cfg->n_skews);
@@ -286,6 +294,7 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   TRY_HIP(hipMalloc(&d_bucket, sizeof(int32_t)));
   TRY_HIP(hipMalloc(&d_y, sizeof(uint16_t) * (size_t)T_max * H));
   TRY_HIP(hipMalloc(&d_vid, sizeof(int32_t)));
+  if (flush_bytes) TRY_HIP(hipMalloc(&d_flush, flush_bytes));
   TRY_HIP(hipMemset(ws, 0, ws_bytes));
   TRY_HIP(hipEventCreate(&e0));
   TRY_HIP(hipEventCreate(&e1));
@@ -319,6 +328,8 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
         s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, 0u, d_y, ws, ws_bytes, stream);
         if (s2 != DAMOE_OK) return s2;
         for (int32_t r = 0; r < cfg->reps; ++r) {
+          // The tuner is synchronous and never captured, so a memset is a fine way to evict.
+          if (d_flush && hipMemsetAsync(d_flush, r & 0xFF, flush_bytes, stream)) return DAMOE_ERR_HIP;
           if (hipEventRecord(e0, stream)) return DAMOE_ERR_HIP;
           s2 = damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, nullptr, v, 0u, d_y, ws, ws_bytes, stream);
           if (s2 != DAMOE_OK) return s2;
@@ -520,6 +531,7 @@ done:
   (void)hipFree(d_bucket);
   (void)hipFree(d_y);
   (void)hipFree(d_vid);
+  (void)hipFree(d_flush);
   return st;
 }
 

@@ -69,7 +69,7 @@ class TuneConfig(ctypes.Structure):
                 ("reps", ctypes.c_int32), ("alpha_samples", ctypes.c_int32),
                 ("alpha_iters", ctypes.c_int32), ("seed", ctypes.c_uint64), ("x", ctypes.c_void_p),
                 ("verbose", ctypes.c_int32), ("ep", ctypes.c_int32), ("n_repeat", ctypes.c_int32),
-                ("repeat_f", ctypes.c_void_p)]
+                ("repeat_f", ctypes.c_void_p), ("flush_mib", ctypes.c_int32)]
 
 
 _lib = None
@@ -349,12 +349,13 @@ class Table:
 
 
 def tune(layer: Layer, bucket_T, skew_X, x, *, samples=10, reps=5, alpha_samples=64, alpha_iters=60,
-         seed=0, verbose=False, ep=1, repeat_f=(), stream=None) -> Table:
+         seed=0, verbose=False, ep=1, repeat_f=(), flush_mib=0, stream=None) -> Table:
     bT = np.ascontiguousarray(np.asarray(bucket_T, np.int32))
     sx = np.ascontiguousarray(np.asarray(skew_X, np.float64))
     rf = np.ascontiguousarray(np.asarray(repeat_f, np.int32))
     cfg = TuneConfig(len(bT), bT.ctypes.data, len(sx), sx.ctypes.data, samples, reps, alpha_samples,
-                     alpha_iters, seed, _p(x), int(verbose), int(ep), len(rf), rf.ctypes.data if len(rf) else None)
+                     alpha_iters, seed, _p(x), int(verbose), int(ep), len(rf), rf.ctypes.data if len(rf) else None,
+                     int(flush_mib))
     h = ctypes.c_void_p()
     _check("damoe_tune", lib().damoe_tune(ctypes.byref(layer), ctypes.byref(cfg), ctypes.byref(h),
                                           _stream(stream)))

@@ -8,7 +8,8 @@ tables serve the rank layers of the expert-parallel workload.
 
 For each power-of-two token bucket up to --max-T, each ddist:X skew of the
 grid (the paper's {1.1 ... 4.0} extended to 32) and S routing samples, every
-variant is timed by the library's tuner; the table maps each skew's exemplar
+variant is timed by the library's tuner, each timed run behind a 1 GiB write that
+evicts the caches (as the benchmark's runs are); the table maps each skew's exemplar
 to its fastest variant, plus the uniform-routing (NoDA) choice per bucket.
 """
 from __future__ import annotations
@@ -30,7 +31,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 
 
 def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, verbose: bool = True,
-               dl=None, repeat_f=None):
+               dl=None, repeat_f=None, flush_mib: int = 1024):
     import torch
     from . import damoe, synth
     from .moe import DeviceLayer
@@ -53,7 +54,7 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
     if repeat_f is None:
         repeat_f = REPEAT_F if shape_name in REPEAT_BY_DEFAULT else []
     table = damoe.tune(dl.layer, buckets, EXTENDED_SKEWS, x, samples=samples, reps=reps, seed=seed,
-                       verbose=verbose, ep=ep, repeat_f=repeat_f)
+                       verbose=verbose, ep=ep, repeat_f=repeat_f, flush_mib=flush_mib)
     return table, time.perf_counter() - t0, buckets, dl
 
 
@@ -66,12 +67,15 @@ def main():
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0x7AB1E)
     ap.add_argument("--out", required=True)
+    ap.add_argument("--flush-mib", type=int, default=1024,
+                    help="MiB written before every timed run (evicts the caches, as in the benchmark)")
     rep = ap.add_mutually_exclusive_group()
     rep.add_argument("--no-repeat", action="store_true", help="ddist:X skews only")
     rep.add_argument("--repeat", action="store_true", help="add the repeated-row exemplars")
     args = ap.parse_args()
     table, secs, buckets, _ = tune_shape(args.shape, args.max_T, args.samples, args.reps, args.seed,
-                                         repeat_f=[] if args.no_repeat else REPEAT_F if args.repeat else None)
+                                         repeat_f=[] if args.no_repeat else REPEAT_F if args.repeat else None,
+                                         flush_mib=args.flush_mib)
     table.save(args.out)
     print(f"tuned {args.shape}: buckets {buckets}, {len(EXTENDED_SKEWS)} skews, S={args.samples}, "
           f"reps={args.reps} in {secs:.1f} s -> {args.out}", file=sys.stderr, flush=True)

@@ -155,11 +155,17 @@ def test_validation_before_launch():
 
 
 def test_alpha_search_matches_oracle_and_closed_form():
-    # Both sides implement Alg. 1 over the same counter-based random numbers.
-    for E, m in [(256, 128.0), (256, 13.0), (384, 200.0), (8, 4.0)]:
+    # Both sides solve Alg. 1's equation over the same counter-based random numbers, with
+    # different root finders (the library bisects log alpha, the oracle alpha itself): they
+    # must land on the same root, and the mean there must equal the target.
+    for E, m in [(256, 128.0), (256, 13.0), (384, 200.0), (8, 4.0), (256, 8.4), (384, 380.0)]:
         a_lib = damoe.alpha_search(E, m, 32, 60, 5)
         a_or = oracle.alpha_search(E, m, S=32, iters=60, seed=5)
-        assert a_lib == pytest.approx(a_or, rel=1e-9)
+        assert a_lib == pytest.approx(a_or, rel=1e-7)
+        assert oracle.mean_effexp(E, a_lib, S=32, seed=5) == pytest.approx(m, rel=1e-6)
+    # Fewer halvings stop early but stay bracketed around the same root.
+    a10 = damoe.alpha_search(256, 128.0, 32, 10, 5)
+    assert 0.1 < a10 / oracle.alpha_search(256, 128.0, S=32, iters=60, seed=5) < 10
     a = damoe.alpha_search(256, 128.0, 64, 60, 0)
     assert a == pytest.approx(127.0 / 128.0, rel=0.05)
 
@@ -320,3 +326,7 @@ def test_tune_rejects_bad_repeat_config():
         c, keep = cfg(n, rf, ep)
         h = ctypes.c_void_p()
         assert L.damoe_tune(ctypes.byref(lay), ctypes.byref(c), ctypes.byref(h), None) == -1, (n, rf, ep)
+    for bad_flush in (-1, 16385):  # the cache-evicting write: 0 .. 16 GiB
+        c, keep = cfg(0, [])
+        c.flush_mib = bad_flush
+        assert L.damoe_tune(ctypes.byref(lay), ctypes.byref(c), ctypes.byref(h), None) == -1, bad_flush
