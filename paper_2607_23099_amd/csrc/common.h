@@ -207,16 +207,24 @@ __device__ __forceinline__ int tile_count(const int32_t* list, const GemmArgs& a
 
 // The flag of the check above, raised once per launch (block 0) at kernel entry for any list
 // of the call that tile_count would refuse; kept out of the item loops, where a side effect
-// costs the compiler's scheduling of the weight stream.
+// costs the compiler's scheduling of the weight stream.  Lane c of wave 0 reads list c's
+// header and lane DAMOE_N_TILE_SIZES the routed count, so the check costs one memory round
+// trip: a chain of dependent loads here would hold block 0, and with it the end of a launch
+// whose variant the device did not choose, for several round trips.
 __device__ __forceinline__ void flag_stale_tiles(const GemmArgs& a) {
-  if (blockIdx.x != 0 || threadIdx.x != 0) return;
-  bool ok = a.ctrl[kRoutedA] == a.A;
+  if (blockIdx.x != 0 || threadIdx.x >= 64) return;
+  const int lane = threadIdx.x;
+  bool ok = true;
+  if (lane < DAMOE_N_TILE_SIZES) {
+    const int32_t* l = a.tiles.list[0];
 #pragma unroll
-  for (int c = 0; c < DAMOE_N_TILE_SIZES; ++c) {
-    const int32_t* l = a.tiles.list[c];
-    ok = ok && l[1] == a.A && l[0] >= 0 && l[0] <= a.tiles_cap;
+    for (int c = 1; c < DAMOE_N_TILE_SIZES; ++c) l = lane == c ? a.tiles.list[c] : l;  // no indexed kernarg
+    const int n = l[0], stamp = l[1];
+    ok = stamp == a.A && n >= 0 && n <= a.tiles_cap;
+  } else if (lane == DAMOE_N_TILE_SIZES) {
+    ok = a.ctrl[kRoutedA] == a.A;
   }
-  if (!ok) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
+  if (__ballot(!ok) != 0ull && lane == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_TILES);
 }
 
 // Device-side variant check of a fused launch: a forced variant is trusted (validated on the

@@ -140,7 +140,7 @@ struct Smem {
   int sorted[DAMOE_MAX_E];
   uint32_t wcnt[kNW][DAMOE_MAX_E];  // per-wave counts, then per-wave running offsets
   int tmp[(1 + DAMOE_N_TILE_SIZES) * kNW];
-  int qpre[kNW][64 * kMaxExemplarRegs];  // first exemplar of each wave
+  int qpre[2][kNW][64 * kMaxExemplarRegs];  // first two exemplars of each wave (x = w, w + 16)
   uint64_t tmp64[kNW];
   long long score[256];
   int vh[kValueBins];  // value histogram of the counts, then start positions
@@ -196,11 +196,12 @@ __device__ void dispatch_core(Smem& sm, int E, int total, int ci, const Dispatch
   __syncthreads();
   for (int x = w; x < d.n_ex; x += kNW) {
     long long acc = 0;
-    if (x == w) {
+    if (x < 2 * kNW) {
+      const int* qp = sm.qpre[x / kNW][w];
 #pragma unroll
       for (int m = 0; m < kMaxExemplarRegs; ++m) {
         const int r = lane + 64 * m;
-        if (r < E) acc += (long long)sm.sorted[r] * sm.qpre[w][r];
+        if (r < E) acc += (long long)sm.sorted[r] * qp[r];
       }
       const int32_t* q = d.Q + (size_t)x * E;
       for (int r = lane + 64 * kMaxExemplarRegs; r < E; r += 64) acc += (long long)sm.sorted[r] * q[r];
@@ -265,14 +266,18 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   pin(d.fixed);
   pin(d.eff_map);
 
-  // The wave's first exemplar is fetched before anything else so its latency hides behind
-  // the histogram; it moves to LDS once the histogram is done.
-  int qpre[kMaxExemplarRegs];
+  // The wave's first two exemplars (x = w and w + 16) are fetched before anything else so
+  // their latency hides behind the histogram; they move to LDS once the histogram is done.
+  // Tables of up to 32 exemplars per bucket then score with no memory round trip after the
+  // sort.
+  int qpre[2][kMaxExemplarRegs];
 #pragma unroll
-  for (int m = 0; m < kMaxExemplarRegs; ++m) {
-    const int r = lane + 64 * m;
-    qpre[m] = (DISPATCH && w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
-  }
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int m = 0; m < kMaxExemplarRegs; ++m) {
+      const int r = lane + 64 * m, x = w + h * kNW;
+      qpre[h][m] = (DISPATCH && x < d.n_ex && r < E) ? d.Q[(size_t)x * E + r] : 0;
+    }
   if (!MULTI)
     for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wcnt[x / E][x % E] = 0;
   if (DISPATCH)
@@ -314,7 +319,9 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   if (bad) atomicAdd(&sm.bad, bad);
   if (DISPATCH)
 #pragma unroll
-    for (int m = 0; m < kMaxExemplarRegs; ++m) sm.qpre[w][lane + 64 * m] = qpre[m];
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int m = 0; m < kMaxExemplarRegs; ++m) sm.qpre[h][w][lane + 64 * m] = qpre[h][m];
   __syncthreads();
 
   // Per expert: the wave counts become each wave's starting offset inside the segment (the
@@ -601,10 +608,12 @@ k_dispatch(const int32_t* __restrict__ counts, int32_t E, int32_t max_total, Dis
   pin(d.noda);
   pin(d.variant_id);
 #pragma unroll
-  for (int m = 0; m < kMaxExemplarRegs; ++m) {
-    const int r = lane + 64 * m;
-    sm.qpre[w][r] = (w < d.n_ex && r < E) ? d.Q[(size_t)w * E + r] : 0;
-  }
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int m = 0; m < kMaxExemplarRegs; ++m) {
+      const int r = lane + 64 * m, x = w + h * kNW;
+      sm.qpre[h][w][r] = (x < d.n_ex && r < E) ? d.Q[(size_t)x * E + r] : 0;
+    }
   for (int v = tid; v < kValueBins; v += kRouteThreads) sm.vh[v] = 0;
   if (tid == 0) {
     sm.big = 0;
