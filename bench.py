@@ -962,8 +962,9 @@ def run_prefill(args):
     in {0.05, 0.3, 1, 10}.  Per (point, variant), medians of `--steps` timed calls after one
     untimed call: routing (no match), GEMM1, GEMM2, reduce, fused (a6-a8) and path (a2-a8);
     algorithmic and padded TFLOP/s; weight-stream GB/s; and roofline_frac = t_roof / t_fused with
-    t_roof = max(B_alg / 8 TB/s, F_alg / 2.5 PFLOP/s), the bf16 MFMA the kernels issue (fp8
-    weights are scaled to bf16 in registers), beside the fraction of the 5 PFLOP/s fp8 peak."""
+    t_roof = max(B_alg / 8 TB/s, F_alg / P) with P the peak of the MFMA the variant issues: 5.0
+    PFLOP/s for the fp8-MFMA big tile, 2.5 PFLOP/s bf16 for the others (their fp8 weights are
+    scaled to bf16 in registers); fp8 points also give the fraction of the 5 PFLOP/s fp8 peak."""
     import torch
     from paper_2607_23099_amd import damoe, synth
     from paper_2607_23099_amd.moe import DeviceLayer, Path
@@ -1002,6 +1003,10 @@ def run_prefill(args):
                 for v in V:
                     bm = damoe.variant_tile_m(v)
                     pad = float(np.sum(-(-counts // bm) * bm)) / A
+                    # The variant's own MFMA peak: fp8 x fp8 for the fp8-MFMA big tile, else the
+                    # bf16 MFMA the kernels issue.
+                    peak_v = 5000.0 if damoe.variant_name(v).startswith("big8") else mfma
+                    t_roof_v = max(b_alg / bw / 1e3, f_alg / peak_v / 1e6)
                     t = []
                     for rep in range(args.steps + 1):
                         e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
@@ -1032,7 +1037,8 @@ def run_prefill(args):
                                  "padded_gemm1_tflops": round(float(f1 * pad / med[1]) / 1e6, 1),
                                  "fused_tflops": round(float(f_alg / fused) / 1e6, 1),
                                  "weight_gbs": round(float(b_alg / fused) / 1e3, 1),
-                                 "roofline_frac": round(float(t_roof / fused), 4)}
+                                 "mfma_peak_tflops": peak_v,
+                                 "roofline_frac": round(float(t_roof_v / fused), 4)}
                     if shape.wdtype == "fp8":
                         rows[key]["fp8_peak_frac"] = round(float(f_alg / fused) / 1e6 / 5000.0, 4)
                     log(f"{key}: {rows[key]}")

@@ -46,7 +46,7 @@ damoe_status device_info(DeviceInfo** out) {
         cus <= 0)
       return DAMOE_ERR_HIP;
     if (gemm_set_lds_limits() != hipSuccess || big_set_lds_limits() != hipSuccess ||
-        router_set_lds_limits() != hipSuccess)
+        big8_set_lds_limits() != hipSuccess || router_set_lds_limits() != hipSuccess)
       return DAMOE_ERR_HIP;
     // With this device current: the address of its copy of the allocation-free workspace.  A
     // failed lookup only disables damoe_moe_layer_noalloc.
@@ -190,6 +190,7 @@ int32_t damoe_variant_tile_m(int32_t v) {
 
 int32_t damoe_variant_supports(int32_t v, int32_t wdtype) {
   if (v < 0 || v >= num_variants()) return 0;
+  if (variant(v).kind == kBig8) return wdtype == DAMOE_W_FP8_B128;
   if (wdtype == DAMOE_W_MXFP4) return variant(v).kind == kStream && variant(v).bm <= kFp4MaxBM;
   return wdtype == DAMOE_W_BF16 || wdtype == DAMOE_W_FP8_B128;
 }
@@ -346,10 +347,11 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   const uint32_t all = (uint32_t)((1ull << num_variants()) - 1);
   if (candidates & ~all) return DAMOE_ERR_INVALID_ARG;
   if (candidates == 0) candidates = all;
-  if (L->wdtype == DAMOE_W_MXFP4) {
-    // MXFP4 runs the stream variants only, fragment-packed: the launch covers just their kernel,
-    // and a dispatched id of another class is flagged by it.
-    if (L->layout != DAMOE_LAYOUT_FRAG16) return DAMOE_ERR_UNSUPPORTED;
+  // MXFP4 runs fragment-packed only.  Every dtype launches only the kernel classes of variants
+  // it supports (MXFP4: the stream variants; bf16: not the fp8-MFMA variant); a dispatched id
+  // of another class is flagged by the kernels that run.
+  if (L->wdtype == DAMOE_W_MXFP4 && L->layout != DAMOE_LAYOUT_FRAG16) return DAMOE_ERR_UNSUPPORTED;
+  {
     uint32_t supported = 0;
     for (int32_t v = 0; v < num_variants(); ++v)
       if (damoe_variant_supports(v, L->wdtype)) supported |= 1u << v;
@@ -397,6 +399,8 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g1.fp8 = L->wdtype == DAMOE_W_FP8_B128;
   g1.fp4 = L->wdtype == DAMOE_W_MXFP4;
   g1.packed = L->layout == DAMOE_LAYOUT_FRAG16;
+  // fp8-MFMA variant: h in e4m3 (bytes [A][I]) and its scales ([A][I / 32]) overlay `h`.
+  g1.o8s = reinterpret_cast<uint8_t*>(base + lo.h) + (size_t)T * L->k * L->I;
 
   GemmArgs g2 = g1;
   g2.x = reinterpret_cast<const uint16_t*>(base + lo.h);
@@ -408,21 +412,29 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g2.out = base + lo.out;
   g2.K = L->I;
   g2.N = L->H;
+  g2.q8 = reinterpret_cast<const uint8_t*>(base + lo.h);
+  g2.q8s = g1.o8s;
+  g2.o8s = nullptr;
 
   // Kernel classes to launch: the forced variant's, else every class holding a candidate.  The
   // launches of a class whose variant the device did not choose return at once.
-  const uint32_t big_bit = 1u << kBigVariant;
+  const uint32_t big_bit = 1u << kBigVariant, big8_bit = 1u << kBig8Variant;
+  // The big-tile kernel runs GEMM1 of both big-tile variants.
   const bool big = force_variant >= 0 ? force_variant == kBigVariant : (candidates & big_bit) != 0;
-  const bool mega = force_variant >= 0 ? force_variant != kBigVariant : (candidates & ~big_bit) != 0;
-  // The big-tile kernel holds an item's fp8 scale rows in LDS: at most 128 scale columns.
-  if (big && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128) return DAMOE_ERR_UNSUPPORTED;
+  const bool big8 = force_variant >= 0 ? force_variant == kBig8Variant : (candidates & big8_bit) != 0;
+  const bool mega = force_variant >= 0 ? (force_variant != kBigVariant && force_variant != kBig8Variant)
+                                       : (candidates & ~(big_bit | big8_bit)) != 0;
+  // The big-tile kernels hold an item's fp8 scale rows in LDS: at most 128 scale columns.
+  if ((big || big8) && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128)
+    return DAMOE_ERR_UNSUPPORTED;
   if (stage_mask & 1) {
     if (mega && launch_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
-    if (big && launch_big_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if ((big || big8) && launch_big_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
   if (stage_mask & 2) {
     if (mega && launch_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if (big && launch_big_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if (big8 && launch_big8_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
   ReduceArgs r{reinterpret_cast<const float*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};
   if ((stage_mask & 4) && launch_reduce(r, stream) != hipSuccess) return DAMOE_ERR_HIP;
@@ -466,7 +478,8 @@ damoe_status damoe_moe_layer_noalloc(const damoe_table* t, const damoe_layer* L,
   if (L->wdtype == DAMOE_W_MXFP4 && L->layout != DAMOE_LAYOUT_FRAG16) return DAMOE_ERR_UNSUPPORTED;
   if ((size_t)T * L->H * 2 >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
   const uint32_t cand = damoe_table_candidates(t, T);
-  if (L->wdtype == DAMOE_W_FP8_B128 && (cand & (1u << kBigVariant)) && std::max(L->H, L->I) > 128 * 128)
+  if (L->wdtype == DAMOE_W_FP8_B128 && (cand & ((1u << kBigVariant) | (1u << kBig8Variant))) &&
+      std::max(L->H, L->I) > 128 * 128)
     return DAMOE_ERR_UNSUPPORTED;
   damoe_ws_layout lo;
   if (layout(L->E, L->k, L->H, L->I, T, &lo) != DAMOE_OK) return DAMOE_ERR_INVALID_ARG;
@@ -630,6 +643,20 @@ static std::string variant_signature() {
   return s;
 }
 
+// A table written by a library whose variants are the first n of this one's (variants are only
+// ever appended, so its ids keep their meaning here): "n,name_0,...,name_{n-1}".
+static bool signature_prefix(const char* sig) {
+  char* end = nullptr;
+  const long n = std::strtol(sig, &end, 10);
+  if (end == sig || n < 1 || n > num_variants()) return false;
+  std::string want = std::to_string(n);
+  for (int32_t v = 0; v < n; ++v) {
+    want += ",";
+    want += variant(v).name;
+  }
+  return want == sig;
+}
+
 damoe_status damoe_table_save(const damoe_table* t, const char* path) {
   if (!t || !path) return DAMOE_ERR_INVALID_ARG;
   FILE* f = std::fopen(path, "w");
@@ -663,7 +690,7 @@ damoe_status damoe_table_load(const char* path, damoe_table** out) {
   do {
     if (std::fscanf(f, "%31s %d %4095s", magic, &ver, sig) != 3) break;
     if (std::strcmp(magic, "damoe-table") != 0 || ver != 1) break;
-    if (variant_signature() != sig) {
+    if (!signature_prefix(sig)) {
       st = DAMOE_ERR_TABLE_MISMATCH;
       break;
     }

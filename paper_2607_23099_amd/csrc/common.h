@@ -49,10 +49,14 @@ enum VariantKind : int32_t {
   kStream = 0,  // split-K over the 4 waves, weights streamed straight from HBM into registers
   kTiled = 1,   // LDS-staged token tile, weights streamed per wave, waves tile the output
   kBig = 2,     // own kernel, one workgroup per CU: both operands DMA'd into LDS, 256 x 256 items
+  kBig8 = 3,    // fp8 weights: big-tile GEMM1 writing MX-fp8 h, own fp8 x fp8 MFMA GEMM2 kernel
 };
 
 // Id of the big-tile variant (its kernel is launched separately from the others).
 constexpr int32_t kBigVariant = 7;
+// Id of the fp8-MFMA big-tile variant (fp8 weights only): GEMM1 on the big-tile kernel, GEMM2 on
+// its own kernel.
+constexpr int32_t kBig8Variant = 8;
 
 // Largest token tile of the MXFP4 stream kernel.
 constexpr int32_t kFp4MaxBM = 32;
@@ -100,6 +104,12 @@ struct GemmArgs {
   int32_t fp8;
   int32_t fp4;         // MXFP4 weights: wa / wb quad fragments of e2m1 codes and E8M0 scales
   int32_t packed;      // weights in the fragment-packed layout
+  // fp8-MFMA variant: h in e4m3 with one E8M0 scale per 32 features of a row.  GEMM1 (the
+  // big-tile kernel) writes h to out (bytes [A][I]) and its scales to o8s ([A][I / 32]);
+  // GEMM2 reads them as q8 and q8s.
+  const uint8_t* q8;
+  const uint8_t* q8s;
+  uint8_t* o8s;
 };
 
 struct ReduceArgs {
@@ -135,6 +145,9 @@ hipError_t launch_gemm2(const GemmArgs& a, int cus, hipStream_t stream);
 hipError_t launch_big_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t big_set_lds_limits();
+// GEMM2 of the fp8-MFMA variant (its GEMM1 is the big-tile kernel's, launch_big_gemm1).
+hipError_t launch_big8_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t big8_set_lds_limits();
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t stream);
 hipError_t gemm_set_lds_limits();
 hipError_t router_set_lds_limits();

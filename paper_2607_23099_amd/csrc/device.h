@@ -75,6 +75,27 @@ __device__ __forceinline__ uint4 fp4x8_to_bf16x8(uint32_t q, float scale) {
   return r;
 }
 
+// MX quantisation to e4m3 with one E8M0 scale per 32 elements: the scale of a block with
+// largest magnitude amax is the smallest 2^e with amax / 2^e <= 448 (the largest e4m3 value),
+// so no element saturates.  mx_scale_byte gives e + 127 (clamped to [0, 253]; 127 for an
+// all-zero block), mx_inv_scale the exact factor 2^(127 - s) that maps the block onto its codes.
+__device__ __forceinline__ uint32_t mx_scale_byte(float amax) {
+  const uint32_t b = __float_as_uint(amax);
+  if (b == 0) return 127u;
+  const int ea = (int)(b >> 23) - 127;
+  const int e = ea - 8 + ((b & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+  return (uint32_t)min(253, max(0, e + 127));
+}
+
+__device__ __forceinline__ float mx_inv_scale(uint32_t s) { return __uint_as_float((254u - s) << 23); }
+
+// Four floats (already divided by their block scale) -> four e4m3 bytes, round to nearest even.
+__device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
+  int r = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  r = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, r, true);
+  return (uint32_t)r;
+}
+
 template <bool FP8>
 struct WFrag;
 template <>

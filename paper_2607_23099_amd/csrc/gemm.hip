@@ -732,8 +732,9 @@ const VariantDesc kVariants[] = {
     DAMOE_TILED_VARIANTS(DAMOE_TDESC)
 #undef DAMOE_TDESC
     {"big_bm256", kBig, 256, 128, 256, tile_class(256)},  // k_gemm_big, id kBigVariant
+    {"big8_bm256", kBig8, 256, 128, 256, tile_class(256)},  // k_gemm_big8, id kBig8Variant (fp8 weights)
 };
-static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kBigVariant + 1, "big variant id");
+static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kBig8Variant + 1, "big-tile variant ids");
 
 constexpr size_t max_lds() {
   size_t m = 0;

@@ -69,8 +69,11 @@ __device__ __forceinline__ void wait_cnt() {
   __builtin_amdgcn_s_waitcnt((VM & 15) | (7 << 4) | (LGKM << 8) | ((VM >> 4) << 14));
 }
 
+// mx: GEMM1 of the fp8-MFMA variant (fp8 weights only): h is rounded to bf16 as for the other
+// variants, then quantised to e4m3 with one E8M0 scale per 32 features of a row, into out
+// (bytes [A][N]) and o8s ([A][N / 32]), the operand of its fp8-MFMA GEMM2.
 template <bool GLU, bool FP8, bool PK>
-__device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
+__device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx) {
   constexpr int FEAT = GLU ? kBigRows / 2 : kBigRows;  // output features per item
   constexpr int EB = FP8 ? 1 : 2;
   constexpr int NWDMA = FP8 ? 2 : 4;                   // weight DMAs per wave per stage
@@ -274,8 +277,38 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds) {
 #pragma unroll
       for (int n = 0; n < NN; ++n) {
         const int i = (2 * n + wt) * 32 + l32;
-        if (i >= rows) continue;
         const size_t orow = (size_t)(p0 + i) * N;
+        if constexpr (GLU && FP8) {
+          if (mx) {
+            // Block m (32 features fb * FEAT + wr * 64 + 32 m ..) of token i: lane l and lane
+            // l ^ 32 hold its 32 values, so the block maximum takes one exchange.
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+              float hb[16];
+              float amax = 0.f;
+#pragma unroll
+              for (int j = 0; j < 16; ++j) {
+                const float g = acc[m][n][j], u = acc[m + 2][n][j];
+                hb[j] = (float)(__bf16)(g / (1.0f + __expf(-g)) * u);
+                amax = fmaxf(amax, fabsf(hb[j]));
+              }
+              amax = fmaxf(amax, __shfl_xor(amax, 32));
+              const uint32_t sc = mx_scale_byte(amax);
+              const float inv = mx_inv_scale(sc);
+              if (i < rows) {
+                uint8_t* h8 = reinterpret_cast<uint8_t*>(a.out) + orow;
+                const int f0 = fb * FEAT + wr * 64 + m * 32;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                  *reinterpret_cast<uint32_t*>(h8 + f0 + 8 * q + 4 * lh) =
+                      e4m3x4(hb[4 * q] * inv, hb[4 * q + 1] * inv, hb[4 * q + 2] * inv, hb[4 * q + 3] * inv);
+                if (lh == 0) a.o8s[(size_t)(p0 + i) * (N / 32) + f0 / 32] = (uint8_t)sc;
+              }
+            }
+            continue;
+          }
+        }
+        if (i >= rows) continue;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (GLU) {
@@ -350,8 +383,10 @@ __global__ void __launch_bounds__(kGemmThreads, 1) k_gemm_big(GemmArgs a) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
     return;
   }
-  if (v != kBigVariant) return;  // the device chose a variant of the other kernel class
-  big_body<GLU, FP8, PK>(a, (lds_t*)big_smem);
+  // This kernel runs the big-tile variant, and GEMM1 of the fp8-MFMA variant (fp8 weights).
+  const bool mx = GLU && FP8 && v == kBig8Variant;
+  if (v != kBigVariant && !mx) return;  // the device chose a variant of another kernel class
+  big_body<GLU, FP8, PK>(a, (lds_t*)big_smem, mx);
 }
 
 template <bool GLU>

@@ -45,8 +45,30 @@ def test_status_strings_and_registry():
     assert len(set(names)) == nv and all(names)
     assert damoe.variant_name(nv) == "" and damoe.variant_tile_m(-1) == 0
     assert all(damoe.variant_tile_m(v) in (16, 32, 64, 128, 256) for v in range(nv))
-    assert all(damoe.variant_supports(v, damoe.W_BF16) for v in range(nv))
+    # Every variant runs fp8 weights; the fp8-MFMA big tile runs nothing else.
+    assert all(damoe.variant_supports(v, damoe.W_FP8_B128) for v in range(nv))
+    big8 = names.index("big8_bm256")
+    assert [v for v in range(nv) if not damoe.variant_supports(v, damoe.W_BF16)] == [big8]
+    assert not damoe.variant_supports(big8, damoe.W_MXFP4)
     assert not damoe.variant_supports(0, 7)
+
+
+def test_table_signature_prefix(tmp_path):
+    """A table saved by a library with fewer variants (the first n of this one's, same names)
+    loads; a header naming another variant, or more variants than the library has, does not."""
+    nv = damoe.num_variants()
+    names = [damoe.variant_name(v) for v in range(nv)]
+    src = os.path.join(ROOT, "paper_2607_23099_amd", "tables", "dsv3.damoe")
+    body = open(src).read().split("\n", 1)[1]
+    for n, sig_names, ok in [(nv - 1, names[:-1], True), (nv, names, True), (2, names[:2], True),
+                             (nv - 1, names[:-2] + ["bogus"], False), (nv + 1, names + ["next"], False)]:
+        f = tmp_path / f"t{n}_{ok}.damoe"
+        f.write_text(f"damoe-table 1 {n},{','.join(sig_names)}\n" + body)
+        if ok:
+            damoe.Table.load(str(f))
+        else:
+            with pytest.raises(RuntimeError):
+                damoe.Table.load(str(f))
 
 
 def test_workspace_layout():

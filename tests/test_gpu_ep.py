@@ -32,6 +32,8 @@ def _rank_case(full_shape, dl, ep, rank, T, alpha, seed, rows=None, extra_masked
     ref = oracle_rows(local_shape, rl_routing, 70 + rank, rows, lambda e: src(rl.global_expert(e)))
     worst = 0.0
     for v in range(damoe.num_variants()):
+        if not damoe.variant_supports(v, rl.wdtype):
+            continue
         path.set_routing(rl_routing)
         path.fill_x(tl, 70 + rank)
         path.y.fill_(float("nan"))
