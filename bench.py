@@ -124,6 +124,27 @@ def summarize_traffic(pmc_dir: str, wdtype: str = "bf16"):
     print(open(path).read())
 
 
+def summarize_trace(db_glob: str):
+    """Print the per-kernel table (calls, total / average / min / max duration, share of the
+    traced kernel time) of a rocprofv3 --kernel-trace run from its SQLite output
+    (`<dir>/**/*_results.db`)."""
+    import glob
+    import sqlite3
+
+    rows = {}
+    for db in sorted(glob.glob(db_glob, recursive=True)):
+        con = sqlite3.connect(db)
+        for name, dur in con.execute("select name, duration from kernels"):
+            rows.setdefault(name, []).append(dur / 1e3)
+        con.close()
+    total = sum(sum(v) for v in rows.values()) or 1.0
+    print("| kernel | calls | total us | avg us | min us | max us | % GPU time |")
+    print("|---|---|---|---|---|---|---|")
+    for name, v in sorted(rows.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{name[:90]}` | {len(v)} | {sum(v):.0f} | {sum(v) / len(v):.2f} | {min(v):.2f} | "
+              f"{max(v):.2f} | {100 * sum(v) / total:.2f} |")
+
+
 def geomean(v):
     v = [x for x in v if x > 0]
     return math.exp(sum(math.log(x) for x in v) / len(v)) if v else 0.0
@@ -1177,11 +1198,15 @@ def main():
     ap.add_argument("--trace-reps", type=int, default=3)
     ap.add_argument("--bench-trace-steps", type=int, default=100,
                     help="decode sweep: steps of the paired Kimi-K2 dispatch trace reported beside it (0 = none)")
+    ap.add_argument("--summarize-trace", default="", metavar="DB_GLOB",
+                    help="print the per-kernel table of rocprofv3 --kernel-trace SQLite output and exit")
     ap.add_argument("--summarize-traffic", default="", metavar="PMC_DIR",
                     help="write the GEMM1 traffic summary from rocprofv3 --pmc runs (no GPU needed)")
     args = ap.parse_args()
     if args.summarize_traffic:
         return summarize_traffic(args.summarize_traffic, args.wdtype)
+    if args.summarize_trace:
+        return summarize_trace(args.summarize_trace)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

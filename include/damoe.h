@@ -298,7 +298,14 @@ uint32_t damoe_table_effexp_candidates(const damoe_table* table, int32_t T);
  *   y          bf16 [T][H] output, y[t] = sum_j topk_w[t][j] FFN_{ids[t][j]}(x[t])
  * Only experts with at least one token are read.  Stream-ordered.  T * H * 2
  * must stay below 2^31 (32-bit row offsets), else DAMOE_ERR_UNSUPPORTED; so must
- * H and I of fp8 layers stay <= 16384 when the big-tile variant may run. */
+ * H and I of fp8 layers stay <= 16384 when a big-tile variant may run, and T k I below
+ * 2^31 when the fp8-MFMA variant may.
+ * The fp8-MFMA variant (big8_bm256, fp8 weights only) computes GEMM1 as the big-tile
+ * variant, then stores h (rounded to bf16) as OCP e4m3 with one E8M0 scale per 32
+ * features of a row (the smallest power of two that maps the block's largest magnitude
+ * to at most 448; round to nearest even), and GEMM2 as fp8 x fp8 MFMA on those codes and
+ * the fp8 W2 with its 128x128 block scales (Sec. II-C's low-precision kernels): y carries
+ * that quantisation of h besides fp32 accumulation, within the fp8 tolerance of y. */
 damoe_status damoe_fused_moe(const damoe_layer* layer /* host */, const uint16_t* x,
                              const float* topk_w, int32_t T, const int32_t* perm,
                              const int32_t* inv_perm, const int32_t* variant_id,
@@ -350,11 +357,14 @@ damoe_status damoe_pack_weights(const damoe_layer* src /* host */, void* w1, voi
                                 hipStream_t stream);
 
 /* Variant registry.  Variant v computes with token tiles of
- * damoe_variant_tile_m(v) rows. */
+ * damoe_variant_tile_m(v) rows.  Variants are only ever appended, so an id keeps its
+ * meaning across library versions (damoe_table_load accepts a table written by a
+ * library whose variants are a prefix of this one's). */
 int32_t damoe_num_variants(void);
 const char* damoe_variant_name(int32_t v);
 int32_t damoe_variant_tile_m(int32_t v);
-/* 1 if variant v supports the layer's weight dtype. */
+/* 1 if variant v supports the layer's weight dtype: every variant runs fp8 weights, all
+ * but big8_bm256 run bf16, the stream variants with tiles of at most 32 rows run MXFP4. */
 int32_t damoe_variant_supports(int32_t v, int32_t wdtype);
 
 /* Offline auto-tuning (Sec. IV-A, Fig. of the dispatch flow steps 1-4). */

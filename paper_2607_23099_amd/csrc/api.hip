@@ -399,7 +399,7 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   g1.fp8 = L->wdtype == DAMOE_W_FP8_B128;
   g1.fp4 = L->wdtype == DAMOE_W_MXFP4;
   g1.packed = L->layout == DAMOE_LAYOUT_FRAG16;
-  // fp8-MFMA variant: h in e4m3 (bytes [A][I]) and its scales ([A][I / 32]) overlay `h`.
+  // fp8-MFMA variant: h in e4m3 ([I / 64][A][64]) and its scale words ([I / 64][A][4]) overlay `h`.
   g1.o8s = reinterpret_cast<uint8_t*>(base + lo.h) + (size_t)T * L->k * L->I;
 
   GemmArgs g2 = g1;
@@ -427,6 +427,8 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   // The big-tile kernels hold an item's fp8 scale rows in LDS: at most 128 scale columns.
   if ((big || big8) && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128)
     return DAMOE_ERR_UNSUPPORTED;
+  // The fp8-MFMA GEMM2 addresses the stage-major h with 32-bit offsets.
+  if (big8 && (size_t)T * L->k * L->I >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
   if (stage_mask & 1) {
     if (mega && launch_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if ((big || big8) && launch_big_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
@@ -480,6 +482,8 @@ damoe_status damoe_moe_layer_noalloc(const damoe_table* t, const damoe_layer* L,
   const uint32_t cand = damoe_table_candidates(t, T);
   if (L->wdtype == DAMOE_W_FP8_B128 && (cand & ((1u << kBigVariant) | (1u << kBig8Variant))) &&
       std::max(L->H, L->I) > 128 * 128)
+    return DAMOE_ERR_UNSUPPORTED;
+  if (L->wdtype == DAMOE_W_FP8_B128 && (cand & (1u << kBig8Variant)) && (size_t)T * L->k * L->I >= ((size_t)1 << 31))
     return DAMOE_ERR_UNSUPPORTED;
   damoe_ws_layout lo;
   if (layout(L->E, L->k, L->H, L->I, T, &lo) != DAMOE_OK) return DAMOE_ERR_INVALID_ARG;

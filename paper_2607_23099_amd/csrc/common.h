@@ -104,8 +104,9 @@ struct GemmArgs {
   int32_t fp8;
   int32_t fp4;         // MXFP4 weights: wa / wb quad fragments of e2m1 codes and E8M0 scales
   int32_t packed;      // weights in the fragment-packed layout
-  // fp8-MFMA variant: h in e4m3 with one E8M0 scale per 32 features of a row.  GEMM1 (the
-  // big-tile kernel) writes h to out (bytes [A][I]) and its scales to o8s ([A][I / 32]);
+  // fp8-MFMA variant: h in e4m3 with one E8M0 scale per 32 features of a row, stage-major:
+  // GEMM1 (the big-tile kernel) writes the codes to out ([I / 64][A][64]) and the scales to
+  // o8s as 4-byte words ([I / 64][A][4]; bytes 0, 1: the two 32-feature blocks of the 64);
   // GEMM2 reads them as q8 and q8s.
   const uint8_t* q8;
   const uint8_t* q8s;

@@ -71,7 +71,8 @@ __device__ __forceinline__ void wait_cnt() {
 
 // mx: GEMM1 of the fp8-MFMA variant (fp8 weights only): h is rounded to bf16 as for the other
 // variants, then quantised to e4m3 with one E8M0 scale per 32 features of a row, into out
-// (bytes [A][N]) and o8s ([A][N / 32]), the operand of its fp8-MFMA GEMM2.
+// (codes [N / 64][A][64]) and o8s (scale words [N / 64][A][4]), the operand of its fp8-MFMA
+// GEMM2, stored stage-major so that each of GEMM2's moves reads contiguous bytes.
 template <bool GLU, bool FP8, bool PK>
 __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx) {
   constexpr int FEAT = GLU ? kBigRows / 2 : kBigRows;  // output features per item
@@ -296,13 +297,16 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
               const uint32_t sc = mx_scale_byte(amax);
               const float inv = mx_inv_scale(sc);
               if (i < rows) {
-                uint8_t* h8 = reinterpret_cast<uint8_t*>(a.out) + orow;
+                // Stage-major for GEMM2's 64-column stages: codes [N / 64][A][64], scale words
+                // [N / 64][A][4] (byte (f0 / 32) % 2; bytes 2 and 3 unused).
                 const int f0 = fb * FEAT + wr * 64 + m * 32;
+                const size_t srow = (size_t)(f0 / 64) * a.A + (p0 + i);
+                uint8_t* h8 = reinterpret_cast<uint8_t*>(a.out) + srow * 64 + f0 % 64;
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                  *reinterpret_cast<uint32_t*>(h8 + f0 + 8 * q + 4 * lh) =
+                  *reinterpret_cast<uint32_t*>(h8 + 8 * q + 4 * lh) =
                       e4m3x4(hb[4 * q] * inv, hb[4 * q + 1] * inv, hb[4 * q + 2] * inv, hb[4 * q + 3] * inv);
-                if (lh == 0) a.o8s[(size_t)(p0 + i) * (N / 32) + f0 / 32] = (uint8_t)sc;
+                if (lh == 0) a.o8s[srow * 4 + (f0 / 32) % 2] = (uint8_t)sc;
               }
             }
             continue;

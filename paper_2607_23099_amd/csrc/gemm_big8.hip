@@ -35,14 +35,18 @@ namespace damoe {
 namespace {
 
 constexpr int kQThreads = 512;
-constexpr int kQBK = 128;                    // K columns per stage
-constexpr uint32_t kQBlk = 16 * kQBK;        // one 16-row block of a stage: 2 KB
-constexpr uint32_t kQTok = 16 * kQBlk;       // 256 token rows
-constexpr uint32_t kQW = 16 * kQBlk;         // 256 weight rows
-constexpr uint32_t kQSc = 256 * 4;           // token scales: 4 E8M0 bytes per row
-constexpr uint32_t kQStage = kQTok + kQW + 2 * kQSc;  // + the scale moves of waves 4..7 (unread)
+constexpr int kQBK = 64;                     // K columns per stage: one 32x32x64 MFMA
+constexpr uint32_t kQGrp = 16 * kQBK;        // 16 token rows of a stage: 1 KB
+constexpr uint32_t kQTok = 16 * kQGrp;       // 256 token rows
+// 16 weight rows of a stage take 1 KB; consecutive row blocks sit 1152 bytes apart, so the two
+// row blocks one 8-byte read of a half-wave touches fall on distinct halves of the banks.
+constexpr uint32_t kQWBlk = kQGrp + 128;
+constexpr uint32_t kQW = 16 * kQWBlk;        // 256 weight rows
+constexpr uint32_t kQSc = 256 * 4;           // token scales: one 4-byte word per row
+constexpr uint32_t kQStage = kQTok + kQW + kQSc;
+constexpr int kQBufs = 4;                    // LDS ring: moves run up to 3 stages ahead
 constexpr int kQMaxSk = 128;                 // weight block-scale columns held per row (K <= 16384)
-constexpr size_t kQWsOff = 2 * (size_t)kQStage;
+constexpr size_t kQWsOff = kQBufs * (size_t)kQStage;
 constexpr size_t kQSlotOff = kQWsOff + 2 * kQMaxSk * 4;
 constexpr size_t kQLds = kQSlotOff + 16;
 static_assert(kQLds <= 160 * 1024, "LDS of one CU");
@@ -74,20 +78,24 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_u(const void* base, 
 __device__ __forceinline__ u32x4 ld16(const lds_t* p) { return *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(p); }
 __device__ __forceinline__ u32x2 ld8(const lds_t* p) { return *reinterpret_cast<const __attribute__((address_space(3))) u32x2*>(p); }
 
+// s_waitcnt operand: vmcnt(vm) with expcnt and lgkmcnt left at their maxima (gfx9 encoding).
+constexpr int wait_vm(int vm) { return (vm & 15) | (7 << 4) | (15 << 8) | ((vm >> 4) << 14); }
+
 template <bool PK>
 __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
   constexpr int FEAT = 256;  // W2 rows per item
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = w & 1, wt = w >> 1;  // weight-row half, token quarter of the output
-  const int r = lane & 15, g = lane >> 4;
+  const int r32 = lane & 31, g = lane >> 5, rr = lane & 15;
   const int32_t* __restrict__ list = a.tiles.list[4];
   const int n_tiles = tile_count(list, a);
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = N / FEAT;
   const int nst = K / kQBK;
-  const int ksc = K / 32;  // token scale bytes per row
+  const int ksw = K / 16;  // bytes of token scale words per row (4 per stage)
+  pin(a.A);
   const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
   const ItemMap map(n_tiles, n_fb);
 
@@ -113,57 +121,46 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
       ok = false;
     }
     if (ok) {
-      // Token moves of this wave: d = 4 w + j -> 16-row block tb = d / 2, column half d % 2.
-      // Lane L moves row 16 tb + L % 16 of the tile (h rows p0 ..), 16 bytes at column
-      // 16 (L / 16 + 4 half) of the stage, landing at slot (L / 16 + 4 half) * 16 + L % 16 of the
-      // block (padding rows read zero).
-      const __amdgpu_buffer_rsrc_t rx = make_rsrc_u(a.q8 + (size_t)p0 * K, (uint32_t)((size_t)rows * K));
-      const __amdgpu_buffer_rsrc_t rs = make_rsrc_u(a.q8s + (size_t)p0 * ksc, (uint32_t)((size_t)rows * ksc));
-      uint32_t xo[4];
+      // Token moves: h is stage-major ([K / 64][A][64]), so a stage's rows of the tile are
+      // contiguous.  Wave w moves 16-row groups 2 w, 2 w + 1: lane L moves row L % 16 of the
+      // group, its 16 bytes at column 16 (L / 16), to slot L of the group's 1 KB (slot c * 16 + r
+      // holds row r's column chunk c); the 64 lanes read 1 KB in one piece (padding rows read
+      // zero).
+      const __amdgpu_buffer_rsrc_t rx = make_rsrc_u(a.q8, (uint32_t)((size_t)a.A * K));
+      const __amdgpu_buffer_rsrc_t rs = make_rsrc_u(a.q8s, (uint32_t)((size_t)a.A * ksw));
+      uint32_t xo[2];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int d = 4 * w + j, tb = d >> 1, half = d & 1;
-        const int row = 16 * tb + (lane & 15);
-        xo[j] = row < rows ? (uint32_t)row * (uint32_t)K + 16u * (uint32_t)((lane >> 4) + 4 * half) : kOobOffset;
+      for (int j = 0; j < 2; ++j) {
+        const int row = 16 * (2 * w + j) + rr;
+        xo[j] = row < rows ? (uint32_t)(p0 + row) * 64u + 16u * (uint32_t)(lane >> 4) : kOobOffset;
       }
-      // Token scale move: 4 bytes (this stage's 4 blocks) of row 64 (w % 4) + lane; waves
-      // 4..7 repeat waves 0..3's into an unread region, so every wave issues the same moves.
+      // Token scale moves ([K / 64][A][4]): waves 0..3 move the stage's words of rows
+      // 64 w + lane, 256 contiguous bytes each.
       const int srow = 64 * (w & 3) + lane;
-      const uint32_t so = srow < rows ? (uint32_t)srow * (uint32_t)ksc : kOobOffset;
-      // Weight moves: d = 4 w + j -> item row block ib = d / 2 (W2 rows fb * 256 + 16 ib), block
-      // pair d % 2 of the stage's four 32-column blocks; one lane offset, the rest in the scalar
-      // offset.  Packed: a 1 KB move is two consecutive 512-byte fragments of one row block.
-      // Chunk c (16 bytes: rows 2 (c % 8), + 1 of the 8-column group c8 = c / 8) lands at slot c
-      // with the two bits of c8 swapped: a lane's two 8-byte reads of a 16-column half are then
-      // 256 bytes apart, and in each read the lanes of g = 0 and g = 1 (column groups 0 and 2, or
-      // 1 and 3) hit distinct halves of the banks.  Row-major: as the token rows.
+      const uint32_t so = srow < rows ? (uint32_t)(p0 + srow) * 4u : kOobOffset;
+      // Weight moves: wave w moves item row blocks 2 w, 2 w + 1 (W2 rows fb * 256 + 16 ib):
+      // packed, the row block's two 512-byte fragments of the stage, contiguous; row-major, as
+      // the token rows.  One lane offset, the rest in the scalar offset.
       const size_t slab = (size_t)N * K;
       const __amdgpu_buffer_rsrc_t rw = make_rsrc_u(wa + (size_t)e * slab, (uint32_t)slab);
-      const int gr0 = fb * 16 + 2 * w;  // global 16-row block of j = 0
-      uint32_t wo;
-      if (PK) {
-        const int sl = lane & 31;
-        const int c = (sl & 7) | ((sl & 8) << 1) | ((sl & 16) >> 1);
-        wo = ((uint32_t)gr0 * (uint32_t)(K / 32) + (uint32_t)(lane >> 5)) * 512u + (uint32_t)c * 16u;
-      } else {
-        wo = (uint32_t)(16 * gr0 + (lane & 15)) * (uint32_t)K + 16u * (uint32_t)(lane >> 4);
-      }
-      auto w_soff = [&](int j, int st) __attribute__((always_inline)) {
-        return PK ? (uint32_t)(j >> 1) * (uint32_t)(K / 32) * 512u + (uint32_t)(j & 1) * 1024u + (uint32_t)st * 2048u
-                  : (uint32_t)(j >> 1) * 16u * (uint32_t)K + (uint32_t)(j & 1) * 64u + (uint32_t)st * kQBK;
-      };
+      const int gr0 = fb * 16 + 2 * w;  // global 16-row block of the wave's first move
+      const uint32_t wo = PK ? (uint32_t)gr0 * (uint32_t)(K / 32) * 512u + (uint32_t)lane * 16u
+                             : (uint32_t)(16 * gr0 + rr) * (uint32_t)K + 16u * (uint32_t)(lane >> 4);
       auto dma_stage = [&](int st, lds_t* sb) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int d = 4 * w + j;
-          dma(rx, sb + (d >> 1) * kQBlk + (d & 1) * 1024, 16, xo[j], (uint32_t)st * kQBK);
-        }
+        for (int j = 0; j < 2; ++j) dma(rx, sb + (2 * w + j) * kQGrp, 16, xo[j], (uint32_t)st * (uint32_t)a.A * 64u);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int d = 4 * w + j;
-          dma(rw, sb + kQTok + (d >> 1) * kQBlk + (d & 1) * 1024, 16, wo, w_soff(j, st));
-        }
-        dma(rs, sb + kQTok + kQW + w * 256, 4, so, (uint32_t)st * 4u);
+        for (int j = 0; j < 2; ++j)
+          dma(rw, sb + kQTok + (2 * w + j) * kQWBlk, 16, wo,
+              (uint32_t)j * 16u * (uint32_t)K + (uint32_t)st * (PK ? 1024u : (uint32_t)kQBK));
+        if (w < 4) dma(rs, sb + kQTok + kQW + w * 256, 4, so, (uint32_t)st * (uint32_t)a.A * 4u);
+      };
+      // A wave's moves per stage: waves 0..3 also move the scale words.  Wait until this wave's
+      // moves of all but the newest `stages` stages have landed.
+      auto wait_stages = [&](auto stages) __attribute__((always_inline)) {
+        constexpr int S = decltype(stages)::value;
+        if (w < 4) __builtin_amdgcn_s_waitcnt(wait_vm(S * 5));
+        else __builtin_amdgcn_s_waitcnt(wait_vm(S * 4));
       };
 
       // Weight block scales of the item (the 128-row block 2 fb + wr of each wave half), staged
@@ -174,35 +171,66 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
         for (int i = lane; i < sk; i += 64) wsc[wr * kQMaxSk + i] = a.sa[sbase_w + i];
       }
 
-      // This wave's token blocks: tb = wt + 4 n, n < nn (those holding valid rows).
-      const int nblk = (rows + 15) / 16;
-      const int nn = nblk > wt ? min(4, (nblk - wt + 3) / 4) : 0;
+      // This wave's token blocks of 32: nb = wt + 4 n, n < nn (those holding valid rows).
+      const int nblk = (rows + 31) / 32;
+      const int nn = nblk > wt ? min(2, (nblk - wt + 3) / 4) : 0;
 
-      floatx4 acc[8][4];
+      floatx16 acc[4][2];
 #pragma unroll
-      for (int m = 0; m < 8; ++m)
+      for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int n = 0; n < 4; ++n) acc[m][n] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
 
-      // Weight operand of MFMA row block m (item row block 8 wr + m).
+      // The weight block scale s = 2^x * f (f in [1, 2)): 2^x is the MFMA's E8M0 scale of the
+      // weight operand, f is carried by the accumulators, which hold the sum in units of the
+      // current block's f: entering a block, they are multiplied by f_prev / f (in (1/2, 2)).
+      // A zero scale block adds nothing (its MFMAs are skipped); an fp32-subnormal scale takes
+      // x = -127 and f = s 2^127 < 1.
+      int wexp = 127;
+      bool wskip = false, have_f = false;
+      float f_cur = 1.f;
+      auto enter_block = [&](int kb) __attribute__((always_inline)) {
+        const float sc = wsc[wr * kQMaxSk + kb];
+        const uint32_t b = __float_as_uint(sc) & 0x7FFFFFFFu;
+        wskip = b == 0;
+        if (wskip) return;
+        const uint32_t ex = b >> 23;
+        const float f = ex ? __uint_as_float((b & 0x7FFFFFu) | 0x3F800000u) : sc * 0x1p127f;
+        wexp = ex ? (int)ex : 0;
+        if (have_f) {
+          const float rsc = f_cur / f;
+#pragma unroll
+          for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int n = 0; n < 2; ++n)
+#pragma unroll
+              for (int i = 0; i < 16; ++i) acc[m][n][i] *= rsc;
+        }
+        f_cur = f;
+        have_f = true;
+      };
+
+      // Operands of a 32x32x64 MFMA: lane (r32, g) holds row r32, bytes 0..15 = columns 16 g ..
+      // + 15 and bytes 16..31 = columns 32 + 16 g .. + 15 of the stage.
       auto read_w = [&](const lds_t* sb, int m) __attribute__((always_inline)) {
-        const lds_t* blk = sb + kQTok + (8 * wr + m) * kQBlk;
+        const lds_t* blk = sb + kQTok + (8 * wr + 2 * m + (r32 >> 4)) * kQWBlk;
         v8i o;
         if (PK) {
-          // Bytes 8 e8 .. + 7 of chunk h: fragment g / 2 + 2 h, column group c8 = 2 (g % 2) + e8,
-          // at slot (r / 2) + 8 (2 e8 + g % 2) (c8's bits swapped), byte 8 (r % 2) in it.
-          const lds_t* p = blk + (g >> 1) * 512 + ((r >> 1) + 8 * (g & 1)) * 16 + (r & 1) * 8;
+          // Fragment h (columns 32 h ..), 8-column group c8 = 2 g + e8: bytes (rr + 16 c8) * 8.
+          const lds_t* p = blk + rr * 8 + g * 256;
 #pragma unroll
           for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int e8 = 0; e8 < 2; ++e8) {
-              const u32x2 v = ld8(p + h * 1024 + e8 * 256);
+              const u32x2 v = ld8(p + h * 512 + e8 * 128);
               o[4 * h + 2 * e8] = (int)v[0];
               o[4 * h + 2 * e8 + 1] = (int)v[1];
             }
         } else {
-          const u32x4 lo = ld16(blk + (g * 16 + r) * 16);
-          const u32x4 hi = ld16(blk + ((g + 4) * 16 + r) * 16);
+          const u32x4 lo = ld16(blk + (g * 16 + rr) * 16);
+          const u32x4 hi = ld16(blk + ((2 + g) * 16 + rr) * 16);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             o[i] = (int)lo[i];
@@ -212,86 +240,86 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
         return o;
       };
 
-      auto compute = [&](const lds_t* sb, int st, auto nn_c) __attribute__((always_inline)) {
+      auto compute = [&](const lds_t* sb, auto nn_c) __attribute__((always_inline)) {
         constexpr int NN = decltype(nn_c)::value;
         if constexpr (NN > 0) {
+          if (wskip) return;
           v8i xt[NN];
           int xs[NN];
 #pragma unroll
           for (int n = 0; n < NN; ++n) {
-            const lds_t* blk = sb + (wt + 4 * n) * kQBlk;
-            const u32x4 lo = ld16(blk + (g * 16 + r) * 16);
-            const u32x4 hi = ld16(blk + ((g + 4) * 16 + r) * 16);
+            const int nb = wt + 4 * n;
+            const lds_t* grp = sb + (2 * nb + (r32 >> 4)) * kQGrp;
+            const u32x4 lo = ld16(grp + (g * 16 + rr) * 16);
+            const u32x4 hi = ld16(grp + ((2 + g) * 16 + rr) * 16);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               xt[n][i] = (int)lo[i];
               xt[n][4 + i] = (int)hi[i];
             }
-            xs[n] = (int)sb[kQTok + kQW + (16 * (wt + 4 * n) + r) * 4 + g];
+            xs[n] = (int)sb[kQTok + kQW + (32 * nb + r32) * 4 + g];
           }
-          const float sw = wsc[wr * kQMaxSk + st];
           v8i wcur = read_w(sb, 0);
 #pragma unroll
-          for (int m = 0; m < 8; ++m) {
+          for (int m = 0; m < 4; ++m) {
             v8i wnext;
-            if (m + 1 < 8) wnext = read_w(sb, m + 1);
-            floatx4 p[NN];
+            if (m + 1 < 4) wnext = read_w(sb, m + 1);
 #pragma unroll
             for (int n = 0; n < NN; ++n)
-              p[n] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(wcur, xt[n], floatx4{0.f, 0.f, 0.f, 0.f}, 0,
-                                                                     0, 0, 127, 0, xs[n]);
-#pragma unroll
-            for (int n = 0; n < NN; ++n)
-#pragma unroll
-              for (int i = 0; i < 4; ++i) acc[m][n][i] = __builtin_fmaf(sw, p[n][i], acc[m][n][i]);
-            if (m + 1 < 8) wcur = wnext;
+              acc[m][n] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wcur, xt[n], acc[m][n], 0, 0, 0, wexp, 0,
+                                                                         xs[n]);
+            if (m + 1 < 4) wcur = wnext;
           }
         }
       };
 
-      // out [A][N] fp32: token 16 (wt + 4 n) + r of the tile, W2 rows fb * 256 + 128 wr + 16 m + 4 g + i.
+      // out [A][N] fp32: lane l holds token 32 nb + l % 32 and, in registers 4 q .. 4 q + 3,
+      // W2 rows fb * 256 + 128 wr + 32 m + 8 q + 4 (l / 32) .. + 3.
       auto epilogue = [&](auto nn_c) __attribute__((always_inline)) {
         constexpr int NN = decltype(nn_c)::value;
+        const float fin = have_f ? f_cur : 0.f;
 #pragma unroll
         for (int n = 0; n < NN; ++n) {
-          const int tok = 16 * (wt + 4 * n) + r;
+          const int tok = 32 * (wt + 4 * n) + r32;
           if (tok >= rows) continue;
-          const size_t orow = (size_t)(p0 + tok) * N;
+          float* orow = reinterpret_cast<float*>(a.out) + (size_t)(p0 + tok) * N + fb * FEAT + 128 * wr + 4 * g;
 #pragma unroll
-          for (int m = 0; m < 8; ++m) {
-            const int f = fb * FEAT + 128 * wr + 16 * m + 4 * g;
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
-                make_float4(acc[m][n][0], acc[m][n][1], acc[m][n][2], acc[m][n][3]);
-          }
+          for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              *reinterpret_cast<float4*>(orow + 32 * m + 8 * q) =
+                  make_float4(acc[m][n][4 * q] * fin, acc[m][n][4 * q + 1] * fin, acc[m][n][4 * q + 2] * fin,
+                              acc[m][n][4 * q + 3] * fin);
         }
       };
 
-      // K loop: stage t + 1 moves into the other buffer while stage t is multiplied; a wave
-      // waits for its own moves of stage t + 1, then the barrier makes them visible to all and
-      // frees stage t's buffer for the moves of the next iteration.  `dst` and `cur` are distinct
-      // buffers, so the compiler need not hold the operand reads of `cur` behind the moves into
-      // `dst`.
+      // Ring of kQBufs stages.  Iteration t (between barriers t - 1 and t): the moves of stage
+      // t + 3 into the buffer stage t - 1 left, the MFMAs of stage t, then a wait for this wave's
+      // moves of stage t + 1 (at most the kQDma moves of each of stages t + 2 and t + 3 still in
+      // flight) and the barrier that makes stage t + 1 visible to all and frees stage t's buffer.
+      // Stages past the last are re-issued as the last into buffers nobody reads again.  `dst` and
+      // `cur` are distinct buffers, so the compiler need not hold the operand reads of `cur`
+      // behind the moves into `dst`.
       auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto nn_c)
           __attribute__((always_inline)) {
-        if (t + 1 < nst) dma_stage(t + 1, dst);
-        compute(cur, t, nn_c);
-        __builtin_amdgcn_s_waitcnt(0);  // vmcnt, expcnt and lgkmcnt all zero
+        dma_stage(min(t + kQBufs - 1, nst - 1), dst);
+        if ((t & 1) == 0) enter_block(t >> 1);
+        compute(cur, nn_c);
+        wait_stages(std::integral_constant<int, kQBufs - 2>{});
         __builtin_amdgcn_s_barrier();
       };
       auto k_loop = [&](auto nn_c) __attribute__((always_inline)) {
-        for (int t = 0; t < nst; ++t) {
-          const uint32_t cb = (uint32_t)(t & 1) * kQStage;
-          iter(lds + (kQStage - cb), lds + cb, t, nn_c);
-        }
+        for (int t = 0; t < nst; ++t)
+          iter(lds + ((t + kQBufs - 1) % kQBufs) * kQStage, lds + (t % kQBufs) * kQStage, t, nn_c);
+        __builtin_amdgcn_s_waitcnt(0);  // re-issued moves may still be in flight
         epilogue(nn_c);
       };
 
-      dma_stage(0, lds);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();  // stage 0 and the weight scales are in LDS
+#pragma unroll
+      for (int st = 0; st < kQBufs - 1; ++st) dma_stage(min(st, nst - 1), lds + st * kQStage);
+      wait_stages(std::integral_constant<int, kQBufs - 2>{});  // this wave's stage-0 moves
+      __syncthreads();  // every wave's, and the weight scales
       switch (nn) {
-        case 4: k_loop(std::integral_constant<int, 4>{}); break;
-        case 3: k_loop(std::integral_constant<int, 3>{}); break;
         case 2: k_loop(std::integral_constant<int, 2>{}); break;
         case 1: k_loop(std::integral_constant<int, 1>{}); break;
         default: k_loop(std::integral_constant<int, 0>{}); break;

@@ -1,5 +1,6 @@
 """GPU check of the fp8-MFMA variant's h quantisation: its GEMM1 (the big-tile kernel) writes h
-rounded to bf16, then as e4m3 codes with one E8M0 scale per 32 features of a row.  The same
+rounded to bf16, then as e4m3 codes with one E8M0 scale per 32 features of a row (stage-major,
+in 4-byte words per 64 features).  The same
 kernel with the big-tile variant stores the bf16 h itself, from the same accumulation, so the codes
 and scales must equal those of the test-side MX quantiser (tests/mx_ref.py, written from the OCP
 formats) applied to that bf16 h, bit for bit."""
@@ -46,8 +47,12 @@ def test_h_quantised_bit_exact(small_fp8, T, alpha, seed):
     h = h.astype(np.float64).reshape(A, sh.I)
     path.fused_stage(0, T, big8)
     torch.cuda.synchronize()
-    q = path.ws[lo["h"]: lo["h"] + A * sh.I].cpu().numpy().reshape(A, sh.I)
-    s = path.ws[lo["h"] + A * sh.I: lo["h"] + A * sh.I + A * sh.I // 32].cpu().numpy().reshape(A, sh.I // 32)
+    # Stage-major: codes [I / 64][A][64], scale words [I / 64][A][4] whose bytes 0 and 1 are the
+    # scales of the two 32-feature blocks of the 64.
+    q = path.ws[lo["h"]: lo["h"] + A * sh.I].cpu().numpy().reshape(sh.I // 64, A, 64)
+    q = q.transpose(1, 0, 2).reshape(A, sh.I)
+    s = path.ws[lo["h"] + A * sh.I: lo["h"] + A * sh.I + A * sh.I // 16].cpu().numpy().reshape(sh.I // 64, A, 4)
+    s = s[:, :, :2].transpose(1, 0, 2).reshape(A, sh.I // 32)
     assert np.all(np.isfinite(h))
     q_ref, s_ref = mx_quantise(h)
     np.testing.assert_array_equal(s, s_ref)
