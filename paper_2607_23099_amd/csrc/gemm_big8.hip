@@ -190,7 +190,10 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
       // x = -127 and f = s 2^127 < 1.
       int wexp = 127;
       bool wskip = false, have_f = false;
-      float f_cur = 1.f;
+      float f_cur = 1.f, rsc = 1.f;
+      // Entering 128-column block kb: its exponent for the MFMAs, and rsc = f_prev / f, by which
+      // the first stage of the block multiplies each accumulator block just before its MFMAs
+      // (1 for the first nonzero block).
       auto enter_block = [&](int kb) __attribute__((always_inline)) {
         const float sc = wsc[wr * kQMaxSk + kb];
         const uint32_t b = __float_as_uint(sc) & 0x7FFFFFFFu;
@@ -199,15 +202,7 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
         const uint32_t ex = b >> 23;
         const float f = ex ? __uint_as_float((b & 0x7FFFFFu) | 0x3F800000u) : sc * 0x1p127f;
         wexp = ex ? (int)ex : 0;
-        if (have_f) {
-          const float rsc = f_cur / f;
-#pragma unroll
-          for (int m = 0; m < 4; ++m)
-#pragma unroll
-            for (int n = 0; n < 2; ++n)
-#pragma unroll
-              for (int i = 0; i < 16; ++i) acc[m][n][i] *= rsc;
-        }
+        rsc = have_f ? f_cur / f : 1.f;
         f_cur = f;
         have_f = true;
       };
@@ -240,8 +235,9 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
         return o;
       };
 
-      auto compute = [&](const lds_t* sb, auto nn_c) __attribute__((always_inline)) {
+      auto compute = [&](const lds_t* sb, auto nn_c, auto first_c) __attribute__((always_inline)) {
         constexpr int NN = decltype(nn_c)::value;
+        constexpr bool FIRST = decltype(first_c)::value;  // first stage of a 128-column block
         if constexpr (NN > 0) {
           if (wskip) return;
           v8i xt[NN];
@@ -259,17 +255,20 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
             }
             xs[n] = (int)sb[kQTok + kQW + (32 * nb + r32) * 4 + g];
           }
-          v8i wcur = read_w(sb, 0);
+          // Every operand of the stage is read before the first MFMA, into registers of its own,
+          // so the LDS latency is paid once per stage (and hidden by the other wave of the SIMD).
+          v8i wv[4];
 #pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            v8i wnext;
-            if (m + 1 < 4) wnext = read_w(sb, m + 1);
+          for (int m = 0; m < 4; ++m) wv[m] = read_w(sb, m);
+          __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
 #pragma unroll
-            for (int n = 0; n < NN; ++n)
-              acc[m][n] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wcur, xt[n], acc[m][n], 0, 0, 0, wexp, 0,
+          for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int n = 0; n < NN; ++n) {
+              if constexpr (FIRST) acc[m][n] *= rsc;
+              acc[m][n] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wv[m], xt[n], acc[m][n], 0, 0, 0, wexp, 0,
                                                                          xs[n]);
-            if (m + 1 < 4) wcur = wnext;
-          }
+            }
         }
       };
 
@@ -300,17 +299,21 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
       // Stages past the last are re-issued as the last into buffers nobody reads again.  `dst` and
       // `cur` are distinct buffers, so the compiler need not hold the operand reads of `cur`
       // behind the moves into `dst`.
-      auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto nn_c)
+      auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto nn_c, auto first_c)
           __attribute__((always_inline)) {
         dma_stage(min(t + kQBufs - 1, nst - 1), dst);
-        if ((t & 1) == 0) enter_block(t >> 1);
-        compute(cur, nn_c);
+        if constexpr (decltype(first_c)::value) enter_block(t >> 1);
+        compute(cur, nn_c, first_c);
         wait_stages(std::integral_constant<int, kQBufs - 2>{});
         __builtin_amdgcn_s_barrier();
       };
+      // Two stages per trip (K is a multiple of 128): the first of each 128-column block enters it.
       auto k_loop = [&](auto nn_c) __attribute__((always_inline)) {
-        for (int t = 0; t < nst; ++t)
-          iter(lds + ((t + kQBufs - 1) % kQBufs) * kQStage, lds + (t % kQBufs) * kQStage, t, nn_c);
+        for (int t = 0; t < nst; t += 2) {
+          iter(lds + ((t + kQBufs - 1) % kQBufs) * kQStage, lds + (t % kQBufs) * kQStage, t, nn_c, std::true_type{});
+          iter(lds + ((t + kQBufs) % kQBufs) * kQStage, lds + ((t + 1) % kQBufs) * kQStage, t + 1, nn_c,
+               std::false_type{});
+        }
         __builtin_amdgcn_s_waitcnt(0);  // re-issued moves may still be in flight
         epilogue(nn_c);
       };
