@@ -983,9 +983,10 @@ def run_prefill(args):
     in {0.05, 0.3, 1, 10}.  Per (point, variant), medians of `--steps` timed calls after one
     untimed call: routing (no match), GEMM1, GEMM2, reduce, fused (a6-a8) and path (a2-a8);
     algorithmic and padded TFLOP/s; weight-stream GB/s; and roofline_frac = t_roof / t_fused with
-    t_roof = max(B_alg / 8 TB/s, F_alg / P) with P the peak of the MFMA the variant issues: 5.0
-    PFLOP/s for the fp8-MFMA big tile, 2.5 PFLOP/s bf16 for the others (their fp8 weights are
-    scaled to bf16 in registers); fp8 points also give the fraction of the 5 PFLOP/s fp8 peak."""
+    t_roof = max(B_alg / 8 TB/s, t_MFMA) with t_MFMA = F_GEMM1 / 2.5 PFLOP/s + F_GEMM2 / P2, the
+    peaks of the MFMAs the variant issues: bf16 for GEMM1 (fp8 weights are scaled to bf16 in
+    registers) and for GEMM2, except the fp8-MFMA big tile's GEMM2 (P2 = 5.0 PFLOP/s fp8); fp8
+    points also give the fraction of the 5 PFLOP/s fp8 peak."""
     import torch
     from paper_2607_23099_amd import damoe, synth
     from paper_2607_23099_amd.moe import DeviceLayer, Path
@@ -1024,10 +1025,12 @@ def run_prefill(args):
                 for v in V:
                     bm = damoe.variant_tile_m(v)
                     pad = float(np.sum(-(-counts // bm) * bm)) / A
-                    # The variant's own MFMA peak: fp8 x fp8 for the fp8-MFMA big tile, else the
-                    # bf16 MFMA the kernels issue.
-                    peak_v = 5000.0 if damoe.variant_name(v).startswith("big8") else mfma
-                    t_roof_v = max(b_alg / bw / 1e3, f_alg / peak_v / 1e6)
+                    # The peaks of the MFMAs the variant issues: bf16 for GEMM1 (every variant) and
+                    # for GEMM2, except the fp8-MFMA big tile's fp8 x fp8 GEMM2.
+                    peak2 = 5000.0 if damoe.variant_name(v).startswith("big8") else mfma
+                    t_mfma_v = (f_alg * 2 / 3 / mfma + f_alg / 3 / peak2) / 1e6  # us
+                    t_roof_v = max(b_alg / bw / 1e3, t_mfma_v)
+                    peak_v = f_alg / t_mfma_v / 1e6  # the effective MFMA peak of the call, TFLOP/s
                     t = []
                     for rep in range(args.steps + 1):
                         e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
@@ -1058,7 +1061,7 @@ def run_prefill(args):
                                  "padded_gemm1_tflops": round(float(f1 * pad / med[1]) / 1e6, 1),
                                  "fused_tflops": round(float(f_alg / fused) / 1e6, 1),
                                  "weight_gbs": round(float(b_alg / fused) / 1e3, 1),
-                                 "mfma_peak_tflops": peak_v,
+                                 "mfma_peak_tflops": round(peak_v, 1),
                                  "roofline_frac": round(float(t_roof_v / fused), 4)}
                     if shape.wdtype == "fp8":
                         rows[key]["fp8_peak_frac"] = round(float(f_alg / fused) / 1e6 / 5000.0, 4)
@@ -1190,7 +1193,8 @@ def main():
     ap.add_argument("--workload", choices=["decode-sweep", "trace", "dispatch", "prefill", "copy", "e2e", "router", "imbalance", "ep"],
                     default="decode-sweep")
     ap.add_argument("--variants", default="", help="prefill: comma-separated variant ids")
-    ap.add_argument("--points", default="", help="prefill: comma-separated points to run, e.g. kimi-k2:8192,dsv3-fp8:16384")
+    ap.add_argument("--points", default="", help="prefill: comma-separated points to run, e.g. kimi-k2:8192,dsv3-fp8:16384; "
+                    "decode sweep: e.g. T128_a0.05,T128_a1.0")
     ap.add_argument("--wdtype", choices=["bf16", "mxfp4"], default="bf16",
                     help="decode sweep: expert weight format (activations and MFMA stay bf16)")
     ap.add_argument("--dispatch-reps", type=int, default=200)
@@ -1243,6 +1247,11 @@ def main():
     dl = DeviceLayer(shape)
     path = Path(dl, max(DECODE_T))
     points = [(T, a) for T in DECODE_T for a in DECODE_ALPHA]
+    if args.points:  # e.g. --points T128_a0.05,T128_a1.0 (counter passes of chosen points)
+        keep = set(args.points.split(","))
+        points = [(T, a) for (T, a) in points if f"T{T}_a{a}" in keep]
+        if not points:
+            raise SystemExit(f"no decode point among {args.points}")
     # HBM bytes of one weight element: bf16 2; MXFP4 half a byte of code + 1/32 of a scale byte.
     wbytes = 17.0 / 32.0 if args.wdtype == "mxfp4" else 2.0
     dev = "cuda"

@@ -141,7 +141,7 @@ typedef struct damoe_layer {
  *                nb4 the block count rounded up to a multiple of 4, then each expert's
  *                first tile of each tile size, int32 [DAMOE_N_TILE_SIZES][E]); empty below
  *   h          : bf16 [T*k][I]   SwiGLU activations in permuted order
- *   out        : fp32 [T*k][H]   GEMM2 output in permuted order                     */
+ *   out        : bf16 [T*k][H]   GEMM2 output in permuted order                     */
 typedef struct damoe_ws_layout {
   size_t total;
   size_t ctrl;
@@ -334,7 +334,7 @@ damoe_status damoe_fused_moe_stage(const damoe_layer* layer /* host */, int32_t 
  * effexp_bucket [1], variant_id [1], y [T][H]), all device pointers, with the meanings given
  * there.  Nothing is allocated, freed or memset.  A call whose workspace
  * (damoe_workspace_size(layer, T)) exceeds the array returns DAMOE_ERR_WORKSPACE before any
- * launch (DeepSeek-V3 shape: up to T = 255 tokens); every argument error of the two calls is
+ * launch (DeepSeek-V3 shape: up to T = 454 tokens); every argument error of the two calls is
  * reported before the first launch too.  All calls on one GPU share its array, which keeps
  * the last call's contents: calls that overlap on one GPU (other streams, other threads)
  * race and give undefined results.  Ids >= E are dropped as in damoe_route_dispatch; the

@@ -105,7 +105,7 @@ damoe_status layout(int32_t E, int32_t k, int32_t H, int32_t I, int32_t T, damoe
   o->h = off;
   off += align_up((size_t)A * I * 2);
   o->out = off;
-  off += align_up((size_t)A * H * 4);
+  off += align_up((size_t)A * H * 2);
   o->total = off;
   return DAMOE_OK;
 }
@@ -438,7 +438,7 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
     if (big && launch_big_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if (big8 && launch_big8_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
-  ReduceArgs r{reinterpret_cast<const float*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};
+  ReduceArgs r{reinterpret_cast<const uint16_t*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};
   if ((stage_mask & 4) && launch_reduce(r, stream) != hipSuccess) return DAMOE_ERR_HIP;
   return DAMOE_OK;
 }

@@ -89,7 +89,7 @@ struct GemmArgs {
   const float* sa;     // fp8 block scales of wa
   const float* sb;     // fp8 block scales of wb
   const int32_t* perm; // GEMM1 gathers token rows perm[p] / k
-  void* out;           // GEMM1: h bf16 [A][I]; GEMM2: out fp32 [A][H]
+  void* out;           // GEMM1: h bf16 [A][I]; GEMM2: out bf16 [A][H]
   TileLists tiles;
   const int32_t* variant_id;
   int32_t force_variant;
@@ -114,7 +114,7 @@ struct GemmArgs {
 };
 
 struct ReduceArgs {
-  const float* out;    // [A][H]
+  const uint16_t* out; // bf16 [A][H]
   const float* w;      // [T][k]
   const int32_t* inv_perm;
   uint16_t* y;         // [T][H]

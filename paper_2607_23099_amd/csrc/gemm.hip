@@ -2,7 +2,7 @@
 // unpermute-reduce (a8).
 //
 // GEMM1 (+SwiGLU):  h[p][f]   = silu(sum_k x[tok(p)][k] W1_e[f][k]) * (sum_k x[tok(p)][k] W3_e[f][k])
-// GEMM2:            out[p][n] = sum_i h[p][i] W2_e[n][i]
+// GEMM2:            out[p][n] = sum_i h[p][i] W2_e[n][i]   (stored in bf16)
 // reduce:           y[t][n]   = sum_j w[t][j] out[inv_perm[t*k + j]][n]
 // where p runs over the positions of expert e's segment of the permuted order
 // and tok(p) = perm[p] / k.
@@ -34,7 +34,7 @@ constexpr int LDS_PAD = 1;
 
 
 // The 4 waves' partial tiles of a stream item -> LDS (rows = output features, columns =
-// tokens), summed in wave order, then the SwiGLU epilogue (GEMM1, bf16 h) or the fp32 output
+// tokens), summed in wave order, then the SwiGLU epilogue (GEMM1, bf16 h) or the bf16 output
 // (GEMM2) of the tile's valid rows.
 // True if the expert of tile `tile` has no other tile in the list (an expert's tiles are
 // adjacent entries): its weights are read by this tile's items only.
@@ -60,10 +60,10 @@ __device__ __forceinline__ void stream_finish(const GemmArgs& a, float* __restri
         red[(wave * NR * 16 + b * 16 + 4 * (lane >> 4) + r) * LDR + s * 16 + (lane & 15)] = acc[b][s][r];
   __syncthreads();
 
-  for (int idx = threadIdx.x; idx < BN * BM; idx += kGemmThreads) {
-    const int f = idx % BN, i = idx / BN;
-    if (i < rows) {
-      if (GLU) {
+  if (GLU) {
+    for (int idx = threadIdx.x; idx < BN * BM; idx += kGemmThreads) {
+      const int f = idx % BN, i = idx / BN;
+      if (i < rows) {
         float g = 0.f, u = 0.f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
@@ -72,11 +72,21 @@ __device__ __forceinline__ void stream_finish(const GemmArgs& a, float* __restri
         }
         const float hval = g / (1.0f + __expf(-g)) * u;
         reinterpret_cast<uint16_t*>(a.out)[(size_t)(p0 + i) * N + fb * BN + f] = f32_to_bf16(hval);
-      } else {
-        float o = 0.f;
+      }
+    }
+  } else {
+    // out in bf16, two features per thread.
+    for (int idx = threadIdx.x; idx < BN / 2 * BM; idx += kGemmThreads) {
+      const int f = 2 * (idx % (BN / 2)), i = idx / (BN / 2);
+      if (i < rows) {
+        float o0 = 0.f, o1 = 0.f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) o += red[(w * NR * 16 + f) * LDR + i];
-        reinterpret_cast<float*>(a.out)[(size_t)(p0 + i) * N + fb * BN + f] = o;
+        for (int w = 0; w < 4; ++w) {
+          o0 += red[(w * NR * 16 + f) * LDR + i];
+          o1 += red[(w * NR * 16 + f + 1) * LDR + i];
+        }
+        *reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(a.out) + (size_t)(p0 + i) * N + fb * BN + f) =
+            pack_bf16x2(o0, o1);
       }
     }
   }
@@ -558,8 +568,10 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, const int32_t* __r
 #pragma unroll
         for (int b = 0; b < NRW; ++b) {
           const int f = fb * FEAT + wave * NRW * 16 + b * 16 + 4 * gl;
-          *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
-              make_float4(acc[b][s][0], acc[b][s][1], acc[b][s][2], acc[b][s][3]);
+          uint2 pk;
+          pk.x = pack_bf16x2(acc[b][s][0], acc[b][s][1]);
+          pk.y = pack_bf16x2(acc[b][s][2], acc[b][s][3]);
+          *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
         }
       }
     }
@@ -675,7 +687,7 @@ __global__ void __launch_bounds__(kGemmThreads, kFp4Occupancy[GLU]) k_gemm_fp4(G
   }
 }
 
-// a8: y[t] = sum_j w[t][j] out[inv_perm[t*k+j]], summed in slot order in fp32.
+// a8: y[t] = sum_j w[t][j] out[inv_perm[t*k+j]], the bf16 rows of out summed in slot order in fp32.
 // Grid (T, H / 1024): each thread owns 4 consecutive features of one token.  The k slot
 // indices and gates arrive with one lane-parallel load (lane j holds slot j) and are
 // broadcast to the wave, then the loads of all k output rows are issued before the sum.
@@ -705,7 +717,13 @@ __global__ void __launch_bounds__(256) k_reduce(ReduceArgs a) {
     if (j < a.k) {
       const int p = __builtin_amdgcn_readlane(p_l, j);
       g[j] = p >= 0 ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, g_l), j)) : 0.f;
-      o[j] = p >= 0 ? *reinterpret_cast<const float4*>(a.out + (size_t)p * a.H + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (p >= 0) {
+        const uint2 v = *reinterpret_cast<const uint2*>(a.out + (size_t)p * a.H + n);
+        o[j] = make_float4(bf16_to_f32((uint16_t)v.x), bf16_to_f32((uint16_t)(v.x >> 16)), bf16_to_f32((uint16_t)v.y),
+                           bf16_to_f32((uint16_t)(v.y >> 16)));
+      } else {
+        o[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
   }
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);

@@ -336,8 +336,10 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
             for (int m = 0; m < 4; ++m) {
               const int f = fb * FEAT + wr * 128 + m * 32 + 8 * q + 4 * lh;
               if (f >= N) continue;
-              *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.out) + orow + f) =
-                  make_float4(acc[m][n][4 * q], acc[m][n][4 * q + 1], acc[m][n][4 * q + 2], acc[m][n][4 * q + 3]);
+              uint2 pk;
+              pk.x = pack_bf16x2(acc[m][n][4 * q], acc[m][n][4 * q + 1]);
+              pk.y = pack_bf16x2(acc[m][n][4 * q + 2], acc[m][n][4 * q + 3]);
+              *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
             }
           }
         }

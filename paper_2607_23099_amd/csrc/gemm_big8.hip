@@ -272,7 +272,7 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
         }
       };
 
-      // out [A][N] fp32: lane l holds token 32 nb + l % 32 and, in registers 4 q .. 4 q + 3,
+      // out [A][N] bf16: lane l holds token 32 nb + l % 32 and, in registers 4 q .. 4 q + 3,
       // W2 rows fb * 256 + 128 wr + 32 m + 8 q + 4 (l / 32) .. + 3.
       auto epilogue = [&](auto nn_c) __attribute__((always_inline)) {
         constexpr int NN = decltype(nn_c)::value;
@@ -281,14 +281,16 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
         for (int n = 0; n < NN; ++n) {
           const int tok = 32 * (wt + 4 * n) + r32;
           if (tok >= rows) continue;
-          float* orow = reinterpret_cast<float*>(a.out) + (size_t)(p0 + tok) * N + fb * FEAT + 128 * wr + 4 * g;
+          uint16_t* orow = reinterpret_cast<uint16_t*>(a.out) + (size_t)(p0 + tok) * N + fb * FEAT + 128 * wr + 4 * g;
 #pragma unroll
           for (int m = 0; m < 4; ++m)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-              *reinterpret_cast<float4*>(orow + 32 * m + 8 * q) =
-                  make_float4(acc[m][n][4 * q] * fin, acc[m][n][4 * q + 1] * fin, acc[m][n][4 * q + 2] * fin,
-                              acc[m][n][4 * q + 3] * fin);
+            for (int q = 0; q < 4; ++q) {
+              uint2 pk;
+              pk.x = pack_bf16x2(acc[m][n][4 * q] * fin, acc[m][n][4 * q + 1] * fin);
+              pk.y = pack_bf16x2(acc[m][n][4 * q + 2] * fin, acc[m][n][4 * q + 3] * fin);
+              *reinterpret_cast<uint2*>(orow + 32 * m + 8 * q) = pk;
+            }
         }
       };
 

@@ -80,7 +80,7 @@ def test_workspace_layout():
         # Per-block counts and offsets, and the tile starts of each size, at many tokens.
         route = (2 * nbp + damoe.N_TILE_SIZES) * E * 4 if A >= 8192 else 0
         regions = [(lo["ctrl"], 256)] + [(o, 8 + 8 * lo["tiles_cap"]) for o in lo["tiles"]] + \
-                  [(lo["route"], route), (lo["h"], A * I * 2), (lo["out"], A * H * 4)]
+                  [(lo["route"], route), (lo["h"], A * I * 2), (lo["out"], A * H * 2)]
         assert lo["route"] + route <= lo["h"]  # the routing calls need the workspace up to h
         for off, size in regions:
             assert off % 256 == 0 and off + size <= lo["total"]

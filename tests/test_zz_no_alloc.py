@@ -71,8 +71,8 @@ def test_noalloc_equals_route_dispatch_then_fused(shape, kids, calls):
 
 
 def test_noalloc_rejects_calls_beyond_its_array():
-    # DeepSeek-V3 shape: T = 128 needs about 34 MB of workspace and fits; T = 512 needs about
-    # 135 MB and is refused on the host before any launch, as is an invalid layer.
+    # DeepSeek-V3 shape: T = 128 needs about 19 MB of workspace and fits; T = 512 needs about
+    # 76 MB and is refused on the host before any launch, as is an invalid layer.
     torch = torch_cuda()
     sh = synth.DS
     lim = damoe.noalloc_scratch_bytes()
