@@ -3,7 +3,9 @@
 //
 // One workgroup of 4 waves per CU.  A work item is (tile of up to 256 tokens of one expert,
 // 256 weight rows): for GEMM1 the rows are 128 features of W1 (gate) and the same 128 of W3
-// (up), so the SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.
+// (up), so the SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.  h
+// passes between the two stage-major ([I / 32][A][32] bf16), so that each of GEMM2's token
+// moves reads 1 KB in one piece.
 //
 // Each K stage of 64 columns moves the item's token rows and weight rows into LDS with direct
 // buffer -> LDS loads (no registers on the way), double-buffered so that stage s + 1 is in
@@ -121,18 +123,19 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       ok = false;
     }
     if (ok) {
-    // Token fragments this wave moves: row blocks 4 * wave + j of the tile; lane l gathers
-    // row l % 16, columns 8 (l / 16) .. + 7 (padding rows read as zero).
-    __amdgpu_buffer_rsrc_t rx;
-    if (GLU) rx = make_rsrc(a.x, (uint32_t)((size_t)(a.A / a.k) * K * 2));
-    else rx = make_rsrc(a.x + (size_t)p0 * K, (uint32_t)((size_t)rows * K * 2));
+    // Token fragments this wave moves: row blocks 4 * wave + j of the tile; lane l moves row
+    // l % 16, columns 8 (l / 16) .. + 7 of the stage (padding rows read as zero).  GEMM1
+    // gathers rows perm[p] / k of x.  GEMM2 reads h stage-major ([K / 32][A][32], as this
+    // kernel's GEMM1 writes it): a stage's rows of the tile are contiguous, so a move reads 1 KB
+    // in one piece, through a resource per stage over those rows.
+    const int p0u = __builtin_amdgcn_readfirstlane(p0), rowsu = __builtin_amdgcn_readfirstlane(rows);
+    __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, GLU ? (uint32_t)((size_t)(a.A / a.k) * K * 2) : 0u);
     uint32_t xo[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = (4 * wave + j) * 16 + lr;
       if (r < rows) {
-        const uint32_t row = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) : (uint32_t)r;
-        xo[j] = row * (uint32_t)K * 2u + lg * 16u;
+        xo[j] = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) * (uint32_t)K * 2u + lg * 16u : (uint32_t)r * 64u + lg * 16u;
       } else {
         xo[j] = kOobOffset;
       }
@@ -158,8 +161,9 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       }
     }
     auto dma_stage = [&](int st, lds_t* sb) __attribute__((always_inline)) {
+      if (!GLU) rx = make_rsrc(a.x + ((size_t)st * a.A + p0u) * 32, (uint32_t)rowsu * 64u);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) dma16(rx, sb + (4 * wave + j) * kFrag, xo[j], (uint32_t)st * 64u);
+      for (int j = 0; j < 4; ++j) dma16(rx, sb + (4 * wave + j) * kFrag, xo[j], GLU ? (uint32_t)st * 64u : 0u);
 #pragma unroll
       for (int j = 0; j < NWDMA; ++j) {
         const uint32_t so = FP8 ? (PK ? (uint32_t)st * 512u : (uint32_t)st * 32u)
@@ -316,6 +320,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (GLU) {
+            // h stage-major for this kernel's GEMM2: [N / 32][A][32].
 #pragma unroll
             for (int m = 0; m < 2; ++m) {
               const int f = fb * FEAT + wr * 64 + m * 32 + 8 * q + 4 * lh;
@@ -329,7 +334,8 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
               uint2 pk;
               pk.x = pack_bf16x2(hv[0], hv[1]);
               pk.y = pack_bf16x2(hv[2], hv[3]);
-              *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) + orow + f) = pk;
+              *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) +
+                                        ((size_t)(f / 32) * a.A + (p0 + i)) * 32 + f % 32) = pk;
             }
           } else {
 #pragma unroll

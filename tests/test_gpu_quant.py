@@ -1,7 +1,7 @@
 """GPU check of the fp8-MFMA variant's h quantisation: its GEMM1 (the big-tile kernel) writes h
 rounded to bf16, then as e4m3 codes with one E8M0 scale per 32 features of a row (stage-major,
 in 4-byte words per 64 features).  The same
-kernel with the big-tile variant stores the bf16 h itself, from the same accumulation, so the codes
+kernel with the big-tile variant stores the bf16 h itself (stage-major), from the same accumulation, so the codes
 and scales must equal those of the test-side MX quantiser (tests/mx_ref.py, written from the OCP
 formats) applied to that bf16 h, bit for bit."""
 import numpy as np
@@ -43,8 +43,9 @@ def test_h_quantised_bit_exact(small_fp8, T, alpha, seed):
     log(f"h quantisation T={T}: GEMM1 of {names[big]} then of {names[big8]}")
     path.fused_stage(0, T, big)
     torch.cuda.synchronize()
+    # The big-tile kernel's h is stage-major: [I / 32][A][32] bf16.
     h = path.ws[lo["h"]: lo["h"] + A * sh.I * 2].view(torch.bfloat16).float().cpu().numpy()
-    h = h.astype(np.float64).reshape(A, sh.I)
+    h = h.astype(np.float64).reshape(sh.I // 32, A, 32).transpose(1, 0, 2).reshape(A, sh.I)
     path.fused_stage(0, T, big8)
     torch.cuda.synchronize()
     # Stage-major: codes [I / 64][A][64], scale words [I / 64][A][4] whose bytes 0 and 1 are the
