@@ -20,6 +20,9 @@ instrumented one with an event between every two kernels (per-kernel times).
 roofline = the dominant kernel (grouped GEMM1 + SwiGLU): algorithmic bytes
 (W1 and W3 of every touched expert + the token rows) / its mean duration,
 timed with HIP events on its own stream in the instrumented steps.
+per_point = each point's path latency with its own roofline: the touched
+experts' three matrices + x + y + ids and gates over 8 TB/s (roofline_us) and
+roofline_us / path_us (roofline_frac).
 cpu_baseline = the fp64 CPU oracle on every sweep point in full, geomean of its
 per-point layer times (us, like value).
 dispatch_trace = the other half of the metric, after the timed region: a
@@ -965,6 +968,13 @@ def gemm1_alg_bytes(shape, U: int, T: int, wbytes: float) -> float:
     return U * 2 * shape.I * shape.H * wbytes + T * shape.H * 2
 
 
+def path_alg_bytes(shape, U: int, T: int, wbytes: float) -> float:
+    """Algorithmic HBM bytes of one decode layer call (a2-a8): W1, W3 and W2 of the U touched
+    experts at `wbytes` per weight, x read and y written (T H bf16 each), ids and gates (8 B
+    per assignment).  Over 8 TB/s it is the path's roofline time."""
+    return U * 3 * shape.I * shape.H * wbytes + 2 * T * shape.H * 2 + 8 * T * shape.k
+
+
 def prefill_alg(shape, T: int, counts) -> tuple:
     """Algorithmic FLOPs and HBM bytes of one a6-a8 call: 6 H I per assignment; the weights of
     the touched experts (fp8: codes and block scales), x and y, ids and gates."""
@@ -1353,8 +1363,13 @@ def main():
         arr = np.array(v)
         med = np.median(arr, axis=0) * 1e3
         cl = np.array(clean_rec[T, a]) * 1e3
+        # Path roofline: the mean over the point's routings of its algorithmic bytes / 8 TB/s.
+        t_roof = float(np.mean([path_alg_bytes(shape, U[T, a, r], T, wbytes) for r in range(REPS)])) \
+            / HBM_PEAK_GBS / 1e3
         per_point[f"T{T}_a{a}"] = {
             "path_us": round(float(np.median(cl)), 1),
+            "roofline_us": round(t_roof, 1),
+            "roofline_frac": round(t_roof / float(np.median(cl)), 4),
             "path_us_mean": round(float(cl.mean()), 1),
             "instrumented_path_us": round(float(med[0]), 1),
             "gemm1_us": round(float(med[1]), 1),

@@ -40,6 +40,16 @@ def test_decode_gemm1_algorithmic_bytes():
     assert b.gemm1_alg_bytes(sh, 54, 8, 2.0) == 54 * 58_720_256 + 8 * 7168 * 2
 
 
+def test_decode_path_algorithmic_bytes():
+    # All three matrices of one DeepSeek-V3 expert: 88,080,384 B in bf16; T = 1 touches 8 experts
+    # (704,643,072 B, 88.1 us at 8 TB/s) and moves x and y (2 x 14,336 B) and 64 B of ids and gates.
+    b = _bench()
+    sh = synth.DS
+    assert b.path_alg_bytes(sh, 1, 0, 2.0) == 88_080_384
+    assert b.path_alg_bytes(sh, 8, 1, 2.0) == 8 * 88_080_384 + 2 * 14_336 + 64
+    assert abs(b.path_alg_bytes(sh, 8, 1, 2.0) / 8e12 * 1e6 - 88.1) < 0.05
+
+
 def test_oracle_leg_measures_and_extrapolates():
     # Every row taken: the call's time is the measured one.  A sample of rows: scaled by the
     # call's assignments over the sample's, and marked as extrapolated.
