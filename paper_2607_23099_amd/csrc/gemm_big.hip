@@ -1,9 +1,10 @@
 // Big-tile class of the grouped expert GEMMs (a6, a7) for prefill-sized token counts, where the
 // work is bound by the matrix cores rather than by the weight stream.
 //
-// One workgroup of 4 waves per CU.  A work item is (tile of up to 256 tokens of one expert,
-// 256 weight rows): for GEMM1 the rows are 128 features of W1 (gate) and the same 128 of W3
-// (up), so the SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.  h
+// One workgroup of 8 waves per CU, two per SIMD, so that one wave's MFMAs run while the other
+// waits on its moves.  A work item is (tile of up to 256 tokens of one expert, 256 weight
+// rows): for GEMM1 the rows are 128 features of W1 (gate) and the same 128 of W3 (up), so the
+// SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.  h
 // passes between the two stage-major ([I / 32][A][32] bf16), so that each of GEMM2's token
 // moves reads 1 KB in one piece.
 //
@@ -15,9 +16,9 @@
 // weights) lane l gathers row l % 16, columns 8 (l / 16) .. + 7, which is the same order.
 // Every operand read is then one linear, conflict-free 16-byte LDS read per lane.
 //
-// The 4 waves tile the 256 x 256 output 2 x 2: wave (wt, wr) owns 128 tokens x 128 weight rows,
-// 4 x 4 MFMA blocks of 32 x 32 (32x32x16 bf16, 256 fp32 accumulators per lane).  Per 16-column
-// k-step a wave reads 8 KB of LDS for 16 MFMAs, i.e. 1/64 B of LDS per FLOP.
+// The 8 waves tile the 256 x 256 output 2 x 4: wave (wt, wr) owns 128 tokens x 64 weight rows,
+// 2 x 4 MFMA blocks of 32 x 32 (32x32x16 bf16, 128 fp32 accumulators per lane).  Per 16-column
+// k-step a wave reads 6 KB of LDS for 8 MFMAs, i.e. 1/43 B of LDS per FLOP.
 #include <type_traits>
 
 #include "common.h"
@@ -33,6 +34,8 @@ constexpr int kBigBK = 32;     // K columns per stage: one fragment column
 constexpr uint32_t kFrag = 1024;                              // one bf16 fragment
 constexpr uint32_t kBigTokBytes = kBigBM / 16 * kFrag;        // 16 KB of token fragments
 constexpr int kBigMaxSk = 128;  // fp8 scale columns per row held in LDS (K <= 16384)
+constexpr int kBigThreads = 512;  // 8 waves
+constexpr int kBigWaves = kBigThreads / 64;
 
 // LDS ring: as many stages as fit in the 160 KB of a CU, so the DMAs run kBufs - 1 stages
 // (3 to 4 us of MFMA work) ahead of the reads.  A stage is 16 KB of token fragments plus
@@ -42,7 +45,7 @@ struct BigCfg {
   static constexpr int kBufs = FP8 ? 6 : 5;
   static constexpr uint32_t kStage = kBigTokBytes + kBigRows / 16 * kFrag / (FP8 ? 2 : 1);
   static constexpr size_t kScaleOff = kBufs * (size_t)kStage;
-  static constexpr size_t kLds = kScaleOff + (FP8 ? 4 * 2 * kBigMaxSk * 4 : 0);
+  static constexpr size_t kLds = kScaleOff + (FP8 ? kBigWaves * 2 * kBigMaxSk * 4 : 0);
   static_assert(kLds <= 160 * 1024, "LDS of one CU");
 };
 
@@ -79,15 +82,15 @@ template <bool GLU, bool FP8, bool PK>
 __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx) {
   constexpr int FEAT = GLU ? kBigRows / 2 : kBigRows;  // output features per item
   constexpr int EB = FP8 ? 1 : 2;
-  constexpr int NWDMA = FP8 ? 2 : 4;                   // weight DMAs per wave per stage
-  constexpr int D = 4 + NWDMA;                         // vector-memory ops per pipeline iteration
+  constexpr int NWDMA = FP8 ? 1 : 2;                   // weight DMAs per wave per stage
+  constexpr int D = 2 + NWDMA;                         // vector-memory ops per pipeline iteration
   using Cfg = BigCfg<FP8>;
   constexpr int NB = Cfg::kBufs;
   constexpr uint32_t SB = Cfg::kStage;
   using WRaw = typename std::conditional<FP8, uint2, uint4>::type;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wt = wave >> 1, wr = wave & 1;  // token half, weight-row half of the output
+  const int wt = wave >> 2, wr = wave & 3;  // token half, weight-row quarter of the output
   const int32_t* __restrict__ list = a.tiles.list[4];
   const int n_tiles = tile_count(list, a);
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
@@ -123,30 +126,30 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       ok = false;
     }
     if (ok) {
-    // Token fragments this wave moves: row blocks 4 * wave + j of the tile; lane l moves row
+    // Token fragments this wave moves: row blocks 2 * wave + j of the tile; lane l moves row
     // l % 16, columns 8 (l / 16) .. + 7 of the stage (padding rows read as zero).  GEMM1
     // gathers rows perm[p] / k of x.  GEMM2 reads h stage-major ([K / 32][A][32], as this
     // kernel's GEMM1 writes it): a stage's rows of the tile are contiguous, so a move reads 1 KB
     // in one piece, through a resource per stage over those rows.
     const int p0u = __builtin_amdgcn_readfirstlane(p0), rowsu = __builtin_amdgcn_readfirstlane(rows);
     __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, GLU ? (uint32_t)((size_t)(a.A / a.k) * K * 2) : 0u);
-    uint32_t xo[4];
+    uint32_t xo[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = (4 * wave + j) * 16 + lr;
+    for (int j = 0; j < 2; ++j) {
+      const int r = (2 * wave + j) * 16 + lr;
       if (r < rows) {
         xo[j] = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) * (uint32_t)K * 2u + lg * 16u : (uint32_t)r * 64u + lg * 16u;
       } else {
         xo[j] = kOobOffset;
       }
     }
-    // Weight fragments this wave moves: item row blocks 4 * wave .. + 3.  GEMM1: item blocks
-    // 0..7 are W1 features fb * 128 + 16 b, blocks 8..15 the same features of W3.  An fp8
-    // fragment is 512 B, so one move carries two row blocks (lanes 0..31 and 32..63).
+    // Weight fragments this wave moves: item row blocks 2 * wave, 2 * wave + 1.  GEMM1: item
+    // blocks 0..7 are W1 features fb * 128 + 16 b, blocks 8..15 the same features of W3.  An fp8
+    // fragment is 512 B, so one move carries both row blocks (lanes 0..31 and 32..63).
     const size_t slab = (size_t)N * K * EB;
     const __amdgpu_buffer_rsrc_t rw =
-        make_rsrc(((GLU && wave >= 2) ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
-    const uint32_t rb0 = GLU ? (uint32_t)fb * 8u + (wave & 1) * 4u : (uint32_t)fb * 16u + wave * 4u;
+        make_rsrc(((GLU && wave >= 4) ? wb : wa) + (size_t)e * slab, (uint32_t)slab);
+    const uint32_t rb0 = GLU ? (uint32_t)fb * 8u + (wave & 3) * 2u : (uint32_t)fb * 16u + wave * 2u;
     uint32_t wo[NWDMA];
 #pragma unroll
     for (int j = 0; j < NWDMA; ++j) {
@@ -163,7 +166,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
     auto dma_stage = [&](int st, lds_t* sb) __attribute__((always_inline)) {
       if (!GLU) rx = make_rsrc(a.x + ((size_t)st * a.A + p0u) * 32, (uint32_t)rowsu * 64u);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) dma16(rx, sb + (4 * wave + j) * kFrag, xo[j], GLU ? (uint32_t)st * 64u : 0u);
+      for (int j = 0; j < 2; ++j) dma16(rx, sb + (2 * wave + j) * kFrag, xo[j], GLU ? (uint32_t)st * 64u : 0u);
 #pragma unroll
       for (int j = 0; j < NWDMA; ++j) {
         const uint32_t so = FP8 ? (PK ? (uint32_t)st * 512u : (uint32_t)st * 32u)
@@ -177,7 +180,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
     lds_f32* sc_lds = nullptr;
     if constexpr (FP8) {
       const int sk = K / 128;
-      const int srow = GLU ? fb : fb * 2 + wr;
+      const int srow = GLU ? fb : fb * 2 + (wr >> 1);
       const bool srow_ok = srow < N / 128;
       const size_t sbase = ((size_t)e * (N / 128) + (srow_ok ? srow : 0)) * sk;
       lds_f32* wsc = reinterpret_cast<lds_f32*>(lds + Cfg::kScaleOff) + wave * 2 * kBigMaxSk;
@@ -192,16 +195,16 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       sc_lds = wsc;
     }
 
-    // Wave (wt, wr) accumulates 4 x 4 MFMA blocks of 32 x 32: block (m, n) = weight rows
-    // 32 m .. + 31 of the wave's 128 (GEMM1: m = 0, 1 gate features, m = 2, 3 the same up
+    // Wave (wt, wr) accumulates 2 x 4 MFMA blocks of 32 x 32: block (m, n) = weight rows
+    // 32 m .. + 31 of the wave's 64 (GEMM1: m = 0 the gate features, m = 1 the same up
     // features) x the 32 tokens of token block 2 n + wt.  Interleaving the token blocks of the
     // two token waves splits a short tile evenly between them; a wave multiplies only its
     // first nn blocks, those holding valid rows (rows beyond `rows` are never stored, so the
     // blocks after them need no MFMA).
     const int nn = min(4, max(0, ((rows + 31) / 32 - wt + 1) / 2));
-    floatx16 acc[4][4];
+    floatx16 acc[2][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < 2; ++m)
 #pragma unroll
       for (int n = 0; n < 4; ++n)
 #pragma unroll
@@ -211,7 +214,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
     // takes row l % 32 (fragment row block (l % 32) / 16, row l % 16 in it) and the 8-column
     // chunk 2 ks + l / 32 of the 32-column fragment.
     struct Ops {
-      WRaw w[4];
+      WRaw w[2];
       uint4 t[4];
       float sg, su;  // fp8: block scales of the stage
     };
@@ -223,8 +226,8 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
         if (GLU) o.su = sc_lds[kBigMaxSk + (st >> 2)];
       }
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const int wrb = (GLU ? (m < 2 ? wr * 4 + 2 * m : 8 + wr * 4 + 2 * (m - 2)) : wr * 8 + 2 * m) + (l32 >> 4);
+      for (int m = 0; m < 2; ++m) {
+        const int wrb = (GLU ? (m == 0 ? 2 * wr : 8 + 2 * wr) : 4 * wr + 2 * m) + (l32 >> 4);
         if constexpr (FP8) {
           const lds_t* blk = cur + kBigTokBytes + (wrb >> 1) * kFrag + (wrb & 1) * 512;
           if (PK) o.w[m] = lds_read8(blk + (lr + 16 * c) * 8);
@@ -241,9 +244,9 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       constexpr int NN = decltype(nn_c)::value;
       if constexpr (NN == 0) return;
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
+      for (int m = 0; m < 2; ++m) {
         uint4 wv;
-        if constexpr (FP8) wv = fp8x8_to_bf16x8(o.w[m], (GLU && m >= 2) ? o.su : o.sg);
+        if constexpr (FP8) wv = fp8x8_to_bf16x8(o.w[m], (GLU && m == 1) ? o.su : o.sg);
         else wv = o.w[m];
 #pragma unroll
         for (int n = 0; n < NN; ++n) acc[m][n] = mfma32x32x16(wv, o.t[n], acc[m][n]);
@@ -285,33 +288,30 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
         const size_t orow = (size_t)(p0 + i) * N;
         if constexpr (GLU && FP8) {
           if (mx) {
-            // Block m (32 features fb * FEAT + wr * 64 + 32 m ..) of token i: lane l and lane
-            // l ^ 32 hold its 32 values, so the block maximum takes one exchange.
+            // The wave's 32 features fb * FEAT + wr * 32 .. of token i: lane l and lane l ^ 32
+            // hold them, so the block maximum takes one exchange.
+            float hb[16];
+            float amax = 0.f;
 #pragma unroll
-            for (int m = 0; m < 2; ++m) {
-              float hb[16];
-              float amax = 0.f;
+            for (int j = 0; j < 16; ++j) {
+              const float g = acc[0][n][j], u = acc[1][n][j];
+              hb[j] = (float)(__bf16)(g / (1.0f + __expf(-g)) * u);
+              amax = fmaxf(amax, fabsf(hb[j]));
+            }
+            amax = fmaxf(amax, __shfl_xor(amax, 32));
+            const uint32_t sc = mx_scale_byte(amax);
+            const float inv = mx_inv_scale(sc);
+            if (i < rows) {
+              // Stage-major for GEMM2's 64-column stages: codes [N / 64][A][64], scale words
+              // [N / 64][A][4] (byte (f0 / 32) % 2; bytes 2 and 3 unused).
+              const int f0 = fb * FEAT + wr * 32;
+              const size_t srow = (size_t)(f0 / 64) * a.A + (p0 + i);
+              uint8_t* h8 = reinterpret_cast<uint8_t*>(a.out) + srow * 64 + f0 % 64;
 #pragma unroll
-              for (int j = 0; j < 16; ++j) {
-                const float g = acc[m][n][j], u = acc[m + 2][n][j];
-                hb[j] = (float)(__bf16)(g / (1.0f + __expf(-g)) * u);
-                amax = fmaxf(amax, fabsf(hb[j]));
-              }
-              amax = fmaxf(amax, __shfl_xor(amax, 32));
-              const uint32_t sc = mx_scale_byte(amax);
-              const float inv = mx_inv_scale(sc);
-              if (i < rows) {
-                // Stage-major for GEMM2's 64-column stages: codes [N / 64][A][64], scale words
-                // [N / 64][A][4] (byte (f0 / 32) % 2; bytes 2 and 3 unused).
-                const int f0 = fb * FEAT + wr * 64 + m * 32;
-                const size_t srow = (size_t)(f0 / 64) * a.A + (p0 + i);
-                uint8_t* h8 = reinterpret_cast<uint8_t*>(a.out) + srow * 64 + f0 % 64;
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                  *reinterpret_cast<uint32_t*>(h8 + 8 * q + 4 * lh) =
-                      e4m3x4(hb[4 * q] * inv, hb[4 * q + 1] * inv, hb[4 * q + 2] * inv, hb[4 * q + 3] * inv);
-                if (lh == 0) a.o8s[srow * 4 + (f0 / 32) % 2] = (uint8_t)sc;
-              }
+              for (int q = 0; q < 4; ++q)
+                *reinterpret_cast<uint32_t*>(h8 + 8 * q + 4 * lh) =
+                    e4m3x4(hb[4 * q] * inv, hb[4 * q + 1] * inv, hb[4 * q + 2] * inv, hb[4 * q + 3] * inv);
+              if (lh == 0) a.o8s[srow * 4 + (f0 / 32) % 2] = (uint8_t)sc;
             }
             continue;
           }
@@ -321,26 +321,23 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
         for (int q = 0; q < 4; ++q) {
           if (GLU) {
             // h stage-major for this kernel's GEMM2: [N / 32][A][32].
+            const int f = fb * FEAT + wr * 32 + 8 * q + 4 * lh;
+            if (f >= N) continue;
+            float hv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float g = acc[0][n][4 * q + r], u = acc[1][n][4 * q + r];
+              hv[r] = g / (1.0f + __expf(-g)) * u;
+            }
+            uint2 pk;
+            pk.x = pack_bf16x2(hv[0], hv[1]);
+            pk.y = pack_bf16x2(hv[2], hv[3]);
+            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) +
+                                      ((size_t)(f / 32) * a.A + (p0 + i)) * 32 + f % 32) = pk;
+          } else {
 #pragma unroll
             for (int m = 0; m < 2; ++m) {
               const int f = fb * FEAT + wr * 64 + m * 32 + 8 * q + 4 * lh;
-              if (f >= N) continue;
-              float hv[4];
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                const float g = acc[m][n][4 * q + r], u = acc[m + 2][n][4 * q + r];
-                hv[r] = g / (1.0f + __expf(-g)) * u;
-              }
-              uint2 pk;
-              pk.x = pack_bf16x2(hv[0], hv[1]);
-              pk.y = pack_bf16x2(hv[2], hv[3]);
-              *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) +
-                                        ((size_t)(f / 32) * a.A + (p0 + i)) * 32 + f % 32) = pk;
-            }
-          } else {
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-              const int f = fb * FEAT + wr * 128 + m * 32 + 8 * q + 4 * lh;
               if (f >= N) continue;
               uint2 pk;
               pk.x = pack_bf16x2(acc[m][n][4 * q], acc[m][n][4 * q + 1]);
@@ -385,7 +382,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
 }
 
 template <bool GLU, bool FP8, bool PK>
-__global__ void __launch_bounds__(kGemmThreads, 1) k_gemm_big(GemmArgs a) {
+__global__ void __launch_bounds__(kBigThreads, 1) k_gemm_big(GemmArgs a) {
   extern __shared__ __attribute__((aligned(1024))) uint8_t big_smem[];
   pin_gemm_args(a);
   flag_stale_tiles(a);
@@ -404,11 +401,11 @@ __global__ void __launch_bounds__(kGemmThreads, 1) k_gemm_big(GemmArgs a) {
 template <bool GLU>
 hipError_t launch_big_stage(const GemmArgs& a, int grid, hipStream_t stream) {
   if (a.fp8) {
-    if (a.packed) hipLaunchKernelGGL((k_gemm_big<GLU, true, true>), dim3(grid), dim3(kGemmThreads), BigCfg<true>::kLds, stream, a);
-    else hipLaunchKernelGGL((k_gemm_big<GLU, true, false>), dim3(grid), dim3(kGemmThreads), BigCfg<true>::kLds, stream, a);
+    if (a.packed) hipLaunchKernelGGL((k_gemm_big<GLU, true, true>), dim3(grid), dim3(kBigThreads), BigCfg<true>::kLds, stream, a);
+    else hipLaunchKernelGGL((k_gemm_big<GLU, true, false>), dim3(grid), dim3(kBigThreads), BigCfg<true>::kLds, stream, a);
   } else {
-    if (a.packed) hipLaunchKernelGGL((k_gemm_big<GLU, false, true>), dim3(grid), dim3(kGemmThreads), BigCfg<false>::kLds, stream, a);
-    else hipLaunchKernelGGL((k_gemm_big<GLU, false, false>), dim3(grid), dim3(kGemmThreads), BigCfg<false>::kLds, stream, a);
+    if (a.packed) hipLaunchKernelGGL((k_gemm_big<GLU, false, true>), dim3(grid), dim3(kBigThreads), BigCfg<false>::kLds, stream, a);
+    else hipLaunchKernelGGL((k_gemm_big<GLU, false, false>), dim3(grid), dim3(kBigThreads), BigCfg<false>::kLds, stream, a);
   }
   return hipGetLastError();
 }
