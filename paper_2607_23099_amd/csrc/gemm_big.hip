@@ -4,17 +4,17 @@
 // One workgroup of 8 waves per CU, two per SIMD, so that one wave's MFMAs run while the other
 // waits on its moves.  A work item is (tile of up to 256 tokens of one expert, 256 weight
 // rows): for GEMM1 the rows are 128 features of W1 (gate) and the same 128 of W3 (up), so the
-// SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.  h
-// passes between the two stage-major ([I / 32][A][32] bf16), so that each of GEMM2's token
-// moves reads 1 KB in one piece.
+// SwiGLU epilogue stays inside a wave; for GEMM2 they are 256 rows of W2.  h passes between
+// the two stage-major ([I / BK][A][BK] bf16, BK the stage width below), so that each of
+// GEMM2's token moves reads whole contiguous rows of the tile.
 //
-// Each K stage of 64 columns moves the item's token rows and weight rows into LDS with direct
-// buffer -> LDS loads (no registers on the way), double-buffered so that stage s + 1 is in
-// flight while stage s is multiplied.  Both operands land in LDS in MFMA fragment order: a
-// fragment (16 rows x 32 columns of bf16, 1 KB) holds lane l's 16 bytes at l * 16.  For
-// fragment-packed weights that is a plain contiguous copy; for token rows (and row-major
-// weights) lane l gathers row l % 16, columns 8 (l / 16) .. + 7, which is the same order.
-// Every operand read is then one linear, conflict-free 16-byte LDS read per lane.
+// Each K stage of 64 columns moves the item's token rows and weight rows into an LDS ring with
+// direct buffer -> LDS loads (no registers on the way), the moves running ahead of the MFMAs.
+// Weights land in MFMA fragment order: a fragment (16 rows x 32 columns, 1 KB of bf16) holds
+// lane l's 16 bytes at l * 16, a plain contiguous copy for fragment-packed weights; row-major
+// weights are gathered into the same order.  Tokens land as 128-byte rows with XOR-swizzled
+// 16-byte chunks.  Every operand read is one 16-byte LDS read per lane, free of bank
+// conflicts.
 //
 // The 8 waves tile the 256 x 256 output 2 x 4: wave (wt, wr) owns 128 tokens x 64 weight rows,
 // 2 x 4 MFMA blocks of 32 x 32 (32x32x16 bf16, 128 fp32 accumulators per lane).  Per 16-column
@@ -30,20 +30,24 @@ namespace {
 
 constexpr int kBigBM = 256;    // tokens per tile
 constexpr int kBigRows = 256;  // weight rows per item
-constexpr int kBigBK = 32;     // K columns per stage: one fragment column
 constexpr uint32_t kFrag = 1024;                              // one bf16 fragment
-constexpr uint32_t kBigTokBytes = kBigBM / 16 * kFrag;        // 16 KB of token fragments
 constexpr int kBigMaxSk = 128;  // fp8 scale columns per row held in LDS (K <= 16384)
 constexpr int kBigThreads = 512;  // 8 waves
 constexpr int kBigWaves = kBigThreads / 64;
 
-// LDS ring: as many stages as fit in the 160 KB of a CU, so the DMAs run kBufs - 1 stages
-// (3 to 4 us of MFMA work) ahead of the reads.  A stage is 16 KB of token fragments plus
-// 16 KB of bf16 (8 KB of fp8) weight fragments; fp8 adds the per-wave scale rows.
+// LDS ring of K stages of 64 columns: 32 KB of token rows, then the weights of the stage's two
+// 32-column halves (2 x 16 KB of bf16 fragments, 2 x 8 KB of fp8), as many stages as fit in
+// the 160 KB of a CU (2 bf16, 3 fp8 beside the per-wave scale rows).  A token row of a stage
+// is one 128-byte line, so each gathered row costs one L1 -> L2 request: the operand feed is
+// bound by that request stream rather than by bytes, and 32-column stages, with two
+// half-line requests per row and stage, ran 4-7% slower for all their deeper ring.
 template <bool FP8>
 struct BigCfg {
-  static constexpr int kBufs = FP8 ? 6 : 5;
-  static constexpr uint32_t kStage = kBigTokBytes + kBigRows / 16 * kFrag / (FP8 ? 2 : 1);
+  static constexpr int kBK = 64;  // K columns per stage
+  static constexpr int kBufs = FP8 ? 3 : 2;
+  static constexpr uint32_t kTok = kBigBM * kBK * 2;                               // token bytes
+  static constexpr uint32_t kWHalf = kBigRows / 16 * kFrag / (FP8 ? 2 : 1);        // weights / 32 columns
+  static constexpr uint32_t kStage = kTok + kBK / 32 * kWHalf;
   static constexpr size_t kScaleOff = kBufs * (size_t)kStage;
   static constexpr size_t kLds = kScaleOff + (FP8 ? kBigWaves * 2 * kBigMaxSk * 4 : 0);
   static_assert(kLds <= 160 * 1024, "LDS of one CU");
@@ -82,9 +86,11 @@ template <bool GLU, bool FP8, bool PK>
 __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx) {
   constexpr int FEAT = GLU ? kBigRows / 2 : kBigRows;  // output features per item
   constexpr int EB = FP8 ? 1 : 2;
-  constexpr int NWDMA = FP8 ? 1 : 2;                   // weight DMAs per wave per stage
-  constexpr int D = 2 + NWDMA;                         // vector-memory ops per pipeline iteration
   using Cfg = BigCfg<FP8>;
+  constexpr int BK = Cfg::kBK;
+  constexpr int NTOK = Cfg::kTok / kFrag / kBigWaves;  // token DMAs per wave per stage
+  constexpr int NWDMA = FP8 ? 1 : 2;                   // weight DMAs per wave per 32 columns
+  constexpr int D = NTOK + NWDMA * BK / 32;            // vector-memory ops per pipeline iteration
   constexpr int NB = Cfg::kBufs;
   constexpr uint32_t SB = Cfg::kStage;
   using WRaw = typename std::conditional<FP8, uint2, uint4>::type;
@@ -96,7 +102,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
   const int2* __restrict__ ent = reinterpret_cast<const int2*>(list + 2);
   const int K = a.K, N = a.N;
   const int n_fb = (N + FEAT - 1) / FEAT;
-  const int nst = K / kBigBK;
+  const int nst = K / BK;
   const uint8_t* __restrict__ wa = reinterpret_cast<const uint8_t*>(a.wa);
   const uint8_t* __restrict__ wb = reinterpret_cast<const uint8_t*>(a.wb);
   const int lr = lane & 15, lg = lane >> 4, l32 = lane & 31, lh = lane >> 5;
@@ -126,19 +132,22 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       ok = false;
     }
     if (ok) {
-    // Token fragments this wave moves: row blocks 2 * wave + j of the tile; lane l moves row
-    // l % 16, columns 8 (l / 16) .. + 7 of the stage (padding rows read as zero).  GEMM1
-    // gathers rows perm[p] / k of x.  GEMM2 reads h stage-major ([K / 32][A][32], as this
-    // kernel's GEMM1 writes it): a stage's rows of the tile are contiguous, so a move reads 1 KB
-    // in one piece, through a resource per stage over those rows.
+    // Token moves of this wave (padding rows read as zero).  GEMM1 gathers rows perm[p] / k of
+    // x; GEMM2 reads h stage-major ([K / BK][A][BK], as this kernel's GEMM1 writes it), whose
+    // rows of one stage are contiguous, through a resource per stage over the tile's rows.
+    // Move j carries rows 8 (NTOK wave + j) .. + 7 of the tile, 128 bytes each: lane l moves
+    // row r = 8 (NTOK wave + j) + l / 8, its 16-byte chunk c = (l % 8) ^ ((r / 2) % 8), which
+    // lands at slot l % 8 of the row.  The swizzle puts the 16 rows that one read phase of an
+    // MFMA operand touches on 16 distinct bank groups.
     const int p0u = __builtin_amdgcn_readfirstlane(p0), rowsu = __builtin_amdgcn_readfirstlane(rows);
     __amdgpu_buffer_rsrc_t rx = make_rsrc(a.x, GLU ? (uint32_t)((size_t)(a.A / a.k) * K * 2) : 0u);
-    uint32_t xo[2];
+    uint32_t xo[NTOK];
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int r = (2 * wave + j) * 16 + lr;
+    for (int j = 0; j < NTOK; ++j) {
+      const int r = 8 * (NTOK * wave + j) + (lane >> 3);
+      const uint32_t cb = (uint32_t)(((lane & 7) ^ ((r >> 1) & 7)) * 16);
       if (r < rows) {
-        xo[j] = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) * (uint32_t)K * 2u + lg * 16u : (uint32_t)r * 64u + lg * 16u;
+        xo[j] = GLU ? (uint32_t)(a.perm[p0 + r] / a.k) * (uint32_t)K * 2u + cb : (uint32_t)r * (BK * 2u) + cb;
       } else {
         xo[j] = kOobOffset;
       }
@@ -164,14 +173,17 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
       }
     }
     auto dma_stage = [&](int st, lds_t* sb) __attribute__((always_inline)) {
-      if (!GLU) rx = make_rsrc(a.x + ((size_t)st * a.A + p0u) * 32, (uint32_t)rowsu * 64u);
+      if (!GLU) rx = make_rsrc(a.x + ((size_t)st * a.A + p0u) * BK, (uint32_t)rowsu * (BK * 2u));
 #pragma unroll
-      for (int j = 0; j < 2; ++j) dma16(rx, sb + (2 * wave + j) * kFrag, xo[j], GLU ? (uint32_t)st * 64u : 0u);
+      for (int j = 0; j < NTOK; ++j) dma16(rx, sb + (NTOK * wave + j) * kFrag, xo[j], GLU ? (uint32_t)st * (BK * 2u) : 0u);
 #pragma unroll
-      for (int j = 0; j < NWDMA; ++j) {
-        const uint32_t so = FP8 ? (PK ? (uint32_t)st * 512u : (uint32_t)st * 32u)
-                                : (PK ? (uint32_t)st * 1024u : (uint32_t)st * 64u);
-        dma16(rw, sb + kBigTokBytes + (NWDMA * wave + j) * kFrag, wo[j], so);
+      for (int h = 0; h < BK / 32; ++h) {
+        const uint32_t s32 = (uint32_t)st * (BK / 32) + h;  // 32-column block of K
+#pragma unroll
+        for (int j = 0; j < NWDMA; ++j) {
+          const uint32_t so = FP8 ? (PK ? s32 * 512u : s32 * 32u) : (PK ? s32 * 1024u : s32 * 64u);
+          dma16(rw, sb + Cfg::kTok + h * Cfg::kWHalf + (NWDMA * wave + j) * kFrag, wo[j], so);
+        }
       }
     };
 
@@ -210,9 +222,10 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[m][n][r] = 0.f;
 
-    // Operands of one 16-column k-step (ks = 0, 1 of a stage).  A 32x32x16 operand lane l
-    // takes row l % 32 (fragment row block (l % 32) / 16, row l % 16 in it) and the 8-column
-    // chunk 2 ks + l / 32 of the 32-column fragment.
+    // Operands of one 16-column k-step (ks = 0 .. BK / 16 - 1 of a stage).  A 32x32x16 operand
+    // lane l takes row l % 32 and the 8-column chunk 2 ks + l / 32 of the stage: for weights,
+    // fragment row block (l % 32) / 16, row l % 16 in it, of the stage's 32-column half ks / 2;
+    // for tokens, the swizzled slot of that chunk in the token row.
     struct Ops {
       WRaw w[2];
       uint4 t[4];
@@ -220,25 +233,28 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
     };
     auto read_ops = [&](int ks, int st, const lds_t* cur, Ops& o, auto nn_c) __attribute__((always_inline)) {
       constexpr int NN = decltype(nn_c)::value;
-      const int c = 2 * ks + lh;
+      const int c = 2 * (ks & 1) + lh;  // chunk within the 32-column half
+      const lds_t* wcur = cur + Cfg::kTok + (ks >> 1) * Cfg::kWHalf;
       if constexpr (FP8) {
-        o.sg = sc_lds[st >> 2];
-        if (GLU) o.su = sc_lds[kBigMaxSk + (st >> 2)];
+        o.sg = sc_lds[(st * BK) >> 7];
+        if (GLU) o.su = sc_lds[kBigMaxSk + ((st * BK) >> 7)];
       }
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
         const int wrb = (GLU ? (m == 0 ? 2 * wr : 8 + 2 * wr) : 4 * wr + 2 * m) + (l32 >> 4);
         if constexpr (FP8) {
-          const lds_t* blk = cur + kBigTokBytes + (wrb >> 1) * kFrag + (wrb & 1) * 512;
+          const lds_t* blk = wcur + (wrb >> 1) * kFrag + (wrb & 1) * 512;
           if (PK) o.w[m] = lds_read8(blk + (lr + 16 * c) * 8);
-          else o.w[m] = lds_read8(blk + (ks * 16 + lr) * 16 + 8 * lh);
+          else o.w[m] = lds_read8(blk + ((ks & 1) * 16 + lr) * 16 + 8 * lh);
         } else {
-          o.w[m] = lds_read16(cur + kBigTokBytes + wrb * kFrag + (lr + 16 * c) * 16);
+          o.w[m] = lds_read16(wcur + wrb * kFrag + (lr + 16 * c) * 16);
         }
       }
 #pragma unroll
-      for (int n = 0; n < NN; ++n)
-        o.t[n] = lds_read16(cur + (4 * n + 2 * wt + (l32 >> 4)) * kFrag + (lr + 16 * c) * 16);
+      for (int n = 0; n < NN; ++n) {
+        const int r = 32 * (2 * n + wt) + l32, cc = 2 * ks + lh;
+        o.t[n] = lds_read16(cur + r * 128 + ((cc ^ ((r >> 1) & 7)) << 4));
+      }
     };
     auto mma = [&](const Ops& o, auto nn_c) __attribute__((always_inline)) {
       constexpr int NN = decltype(nn_c)::value;
@@ -266,14 +282,17 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
     auto iter = [&](lds_t* __restrict__ dst, const lds_t* __restrict__ cur, int t, auto first, auto nn_c)
         __attribute__((always_inline)) {
       dma_stage(min(t + NB - 1, nst - 1), dst);
-      read_ops(0, t, cur, A, nn_c);
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (!decltype(first)::value) mma(B, nn_c);
-      __builtin_amdgcn_sched_barrier(0);
-      read_ops(1, t, cur, B, nn_c);
-      __builtin_amdgcn_sched_barrier(0);
-      mma(A, nn_c);
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kp = 0; kp < BK / 32; ++kp) {
+        read_ops(2 * kp, t, cur, A, nn_c);
+        __builtin_amdgcn_sched_barrier(0);
+        if (kp > 0 || !decltype(first)::value) mma(B, nn_c);
+        __builtin_amdgcn_sched_barrier(0);
+        read_ops(2 * kp + 1, t, cur, B, nn_c);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(A, nn_c);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       wait_cnt<(NB - 2) * D, 0>();
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
@@ -320,7 +339,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           if (GLU) {
-            // h stage-major for this kernel's GEMM2: [N / 32][A][32].
+            // h stage-major for this kernel's GEMM2 (its stages of BK columns): [N / BK][A][BK].
             const int f = fb * FEAT + wr * 32 + 8 * q + 4 * lh;
             if (f >= N) continue;
             float hv[4];
@@ -333,7 +352,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& a, lds_t* lds, bool mx)
             pk.x = pack_bf16x2(hv[0], hv[1]);
             pk.y = pack_bf16x2(hv[2], hv[3]);
             *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.out) +
-                                      ((size_t)(f / 32) * a.A + (p0 + i)) * 32 + f % 32) = pk;
+                                      ((size_t)(f / BK) * a.A + (p0 + i)) * BK + f % BK) = pk;
           } else {
 #pragma unroll
             for (int m = 0; m < 2; ++m) {

@@ -43,9 +43,10 @@ def test_h_quantised_bit_exact(small_fp8, T, alpha, seed):
     log(f"h quantisation T={T}: GEMM1 of {names[big]} then of {names[big8]}")
     path.fused_stage(0, T, big)
     torch.cuda.synchronize()
-    # The big-tile kernel's h is stage-major: [I / 32][A][32] bf16.
+    # The big-tile kernel's h is stage-major in its GEMM2's stages, 64 columns with fp8
+    # weights: [I / 64][A][64] bf16.
     h = path.ws[lo["h"]: lo["h"] + A * sh.I * 2].view(torch.bfloat16).float().cpu().numpy()
-    h = h.astype(np.float64).reshape(sh.I // 32, A, 32).transpose(1, 0, 2).reshape(A, sh.I)
+    h = h.astype(np.float64).reshape(sh.I // 64, A, 64).transpose(1, 0, 2).reshape(A, sh.I)
     path.fused_stage(0, T, big8)
     torch.cuda.synchronize()
     # Stage-major: codes [I / 64][A][64], scale words [I / 64][A][4] whose bytes 0 and 1 are the
