@@ -1,6 +1,6 @@
 // fp8-MFMA class of the grouped expert GEMMs for fp8 weights at prefill-sized token counts: the
 // grouped GEMM2 (a7) with both operands in OCP e4m3, multiplied by the gfx950 scaled MFMA
-// v_mfma_scale_f32_16x16x128_f8f6f4 at twice the bf16 rate and with half the LDS and L2 bytes of
+// v_mfma_scale_f32_32x32x64_f8f6f4 at twice the bf16 rate and with half the LDS and L2 bytes of
 // a bf16 token operand per FLOP.
 //
 // Tokens.  The operand is h from GEMM1 of the same variant (the big-tile kernel's SwiGLU
@@ -9,24 +9,26 @@
 // activations: quantising x as well would put the layer's error near the fp8 tolerance, while h
 // alone stays well inside it.
 //
-// Weights.  The layer's fp8 W2 with its fp32 scale per 128 x 128 block.  One MFMA spans K = 128,
-// exactly one block column, so each MFMA result is multiplied by its block's scale and added to an
-// fp32 accumulator: acc += s_w * mfma(w, h, 0).
+// Weights.  The layer's fp8 W2 with its fp32 scale per 128 x 128 block.  A block scale
+// s = 2^x f (f in [1, 2)) splits in two: 2^x is the E8M0 scale of the weight operand in the
+// instruction, and f is carried by the accumulators, which hold the running sum in units of the
+// current block's f (multiplied by f_prev / f when a new 128-column block starts, and by the
+// last f in the epilogue).
 //
 // Work items are (tile of up to 256 tokens of one expert, 256 rows of W2), as in the bf16 big
 // tile.  One workgroup of 8 waves per CU, two per SIMD: wave (wt, wr) owns 128 weight rows x 64
-// tokens (8 x 4 MFMA blocks of 16 x 16, 128 fp32 accumulators per lane), so a wave's
-// accumulators and the partial products it scales stay in VGPRs; the two waves of a SIMD hide
-// each other's LDS and issue latencies.
+// tokens (4 x 2 MFMA blocks of 32 x 32, 128 fp32 accumulators per lane), and the two waves of a
+// SIMD hide each other's LDS and issue latencies.
 //
-// K stages of 128 columns (32 KB of tokens, 32 KB of weights, 1 KB of token scales), double
-// buffered in LDS and filled with direct buffer -> LDS loads while the previous stage is
-// multiplied.
+// K stages of 64 columns (16 KB of token rows, 16 KB of weight rows with padding between row
+// blocks, 1 KB of token scale words) in a 4-deep LDS ring, filled with direct buffer -> LDS loads
+// up to 3 stages ahead of the MFMAs.  h and its scale words are stage-major ([K / 64][A][64] and
+// [K / 64][A][4]), so every token move reads contiguous bytes.
 //
-// Operand layout of v_mfma_scale_f32_16x16x128_f8f6f4 (checked on the device): lane l holds row
-// l % 16, bytes 0..15 = K columns 16 g .. + 15 and bytes 16..31 = columns 64 + 16 g .. + 15
-// (g = l / 16); lane l's scale byte scales row l % 16 over K columns 32 g .. + 31.  The result
-// holds D[4 g + i][l % 16] in register i.
+// Operand layout of v_mfma_scale_f32_32x32x64_f8f6f4 (checked on the device): lane l holds row
+// l % 32, bytes 0..15 = K columns 16 g .. + 15 and bytes 16..31 = columns 32 + 16 g .. + 15
+// (g = l / 32); lane l's scale byte scales row l % 32 over K columns 32 g .. + 31.  The result
+// holds D[8 q + 4 g + i][l % 32] in register 4 q + i.
 #include "common.h"
 #include "device.h"
 #include "queue.h"
