@@ -50,6 +50,7 @@ enum VariantKind : int32_t {
   kTiled = 1,   // LDS-staged token tile, weights streamed per wave, waves tile the output
   kBig = 2,     // own kernel, one workgroup per CU: both operands DMA'd into LDS, 256 x 256 items
   kBig8 = 3,    // fp8 weights: big-tile GEMM1 writing MX-fp8 h, own fp8 x fp8 MFMA GEMM2 kernel
+  kDeep = 4,    // own kernel, one workgroup per CU: tokens in LDS, weights per wave in a deep ring
 };
 
 // Id of the big-tile variant (its kernel is launched separately from the others).
@@ -57,6 +58,9 @@ constexpr int32_t kBigVariant = 7;
 // Id of the fp8-MFMA big-tile variant (fp8 weights only): GEMM1 on the big-tile kernel, GEMM2 on
 // its own kernel.
 constexpr int32_t kBig8Variant = 8;
+
+// Id of the deep-ring variant (its kernel is launched separately from the others).
+constexpr int32_t kDeepVariant = 9;
 
 // Largest token tile of the MXFP4 stream kernel.
 constexpr int32_t kFp4MaxBM = 32;
@@ -143,6 +147,8 @@ hipError_t launch_dispatch(const int32_t* counts, int32_t E, int32_t max_total, 
 // Grouped GEMM stages on a persistent grid sized from the device's CU count.
 hipError_t launch_gemm1(const GemmArgs& a, int cus, hipStream_t stream);
 hipError_t launch_gemm2(const GemmArgs& a, int cus, hipStream_t stream);
+hipError_t launch_deep_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
+hipError_t launch_deep_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_big_gemm1(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t launch_big_gemm2(const GemmArgs& a, int grid, hipStream_t stream);
 hipError_t big_set_lds_limits();

@@ -751,8 +751,10 @@ const VariantDesc kVariants[] = {
 #undef DAMOE_TDESC
     {"big_bm256", kBig, 256, 128, 256, tile_class(256)},  // k_gemm_big, id kBigVariant
     {"big8_bm256", kBig8, 256, 128, 256, tile_class(256)},  // k_gemm_big8, id kBig8Variant (fp8 weights)
+    {"deep_bm64", kDeep, 64, 256, 512, tile_class(64)},     // k_gemm_deep, id kDeepVariant
 };
-static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kBig8Variant + 1, "big-tile variant ids");
+static_assert(kBigVariant == 7 && kBig8Variant == 8, "variant ids are only ever appended");
+static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kDeepVariant + 1, "deep-ring variant id");
 
 constexpr size_t max_lds() {
   size_t m = 0;

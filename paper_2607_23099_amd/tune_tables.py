@@ -30,8 +30,24 @@ REPEAT_BY_DEFAULT = ("dsv3", "dsv3-fp8", "tiny")
 HERE = os.path.dirname(os.path.abspath(__file__))
 
 
+def bucket_grid(max_T: int, grid: str = "octave") -> list:
+    """Tuned token counts up to max_T: the powers of two ("octave"), or also 3 * 2^(i - 1) between
+    them ("half": 1, 2, 3, 4, 6, 8, 12, ...).  A batch of T tokens takes the smallest tuned bucket
+    >= T, so on the half grid every T is within 1.5x of the count its bucket was tuned at (2x on
+    the octave grid)."""
+    if grid not in ("octave", "half"):
+        raise ValueError(f"unknown bucket grid {grid!r}")
+    out, t = [], 1
+    while t <= max_T:
+        out.append(t)
+        if grid == "half" and t >= 2 and 3 * t // 2 <= max_T:
+            out.append(3 * t // 2)
+        t *= 2
+    return out
+
+
 def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, verbose: bool = True,
-               dl=None, repeat_f=None, flush_mib: int = 1024):
+               dl=None, repeat_f=None, flush_mib: int = 1024, grid: str = "octave"):
     import torch
     from . import damoe, synth
     from .moe import DeviceLayer
@@ -41,11 +57,7 @@ def tune_shape(shape_name: str, max_T: int, samples: int, reps: int, seed: int, 
     shape = shapes[shape_name]
     if dl is None:
         dl = DeviceLayer(shape)
-    buckets = []
-    t = 1
-    while t <= max_T:
-        buckets.append(t)
-        t *= 2
+    buckets = bucket_grid(max_T, grid)
     x = torch.empty((max_T, shape.H), dtype=torch.bfloat16, device="cuda")
     synth.fill_bf16_device(x.data_ptr(), x.numel(), seed=synth.x_seed(999), tensor=synth.T_X,
                            slab_elems=x.numel(), sigma=1.0, stream=torch.cuda.current_stream().cuda_stream)
@@ -67,6 +79,8 @@ def main():
     ap.add_argument("--reps", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0x7AB1E)
     ap.add_argument("--out", required=True)
+    ap.add_argument("--grid", choices=["octave", "half"], default="octave",
+                    help="tuned token counts: powers of two, or also 3 * 2^(i - 1) between them")
     ap.add_argument("--flush-mib", type=int, default=1024,
                     help="MiB written before every timed run (evicts the caches, as in the benchmark)")
     rep = ap.add_mutually_exclusive_group()
@@ -75,7 +89,7 @@ def main():
     args = ap.parse_args()
     table, secs, buckets, _ = tune_shape(args.shape, args.max_T, args.samples, args.reps, args.seed,
                                          repeat_f=[] if args.no_repeat else REPEAT_F if args.repeat else None,
-                                         flush_mib=args.flush_mib)
+                                         flush_mib=args.flush_mib, grid=args.grid)
     table.save(args.out)
     print(f"tuned {args.shape}: buckets {buckets}, {len(EXTENDED_SKEWS)} skews, S={args.samples}, "
           f"reps={args.reps} in {secs:.1f} s -> {args.out}", file=sys.stderr, flush=True)
