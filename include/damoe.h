@@ -399,9 +399,14 @@ typedef struct damoe_tune_config {
  * S Dirichlet routings (Gumbel-top-k at T_b tokens) are timed on every
  * variant; kid = the variant with the lowest mean latency; the exemplar is the
  * renormalised centroid of the S sorted unit count vectors.  The repeated-row
- * samples (repeat_f) add exemplars the same way.  The noda row holds
- * each bucket's fastest variant under uniform routing.  Host-synchronous; the
- * only call that allocates device memory on its own. */
+ * samples (repeat_f) add exemplars the same way.  Per bucket, the per-exemplar
+ * kernels are kept only if their mean latency, charged the match and the
+ * launches of the bucket's other kernel classes (measured once: a launched
+ * class that the device did not choose returns at once), beats both the best
+ * single variant and the per-exemplar choice restricted to one kernel class;
+ * otherwise the cheaper of those replaces them.  The noda row holds each
+ * bucket's fastest variant under uniform routing.  Host-synchronous; the only
+ * call that allocates device memory on its own. */
 damoe_status damoe_tune(const damoe_layer* layer /* host */, const damoe_tune_config* cfg,
                         damoe_table** out, hipStream_t stream);
 

@@ -216,6 +216,20 @@ void exemplar(const std::vector<std::vector<int32_t>>& counts, int32_t E, int32_
     if ((st = (x)) != DAMOE_OK) goto done;                 \
   } while (0)
 
+// The kernel class a variant runs on, of the kClasses that a fused call launches separately:
+// the stream and tiled variants share one kernel, the big-tile, fp8-MFMA and deep-ring
+// variants have kernels of their own.  A fused call whose candidates span several classes
+// launches all of them, and those the device did not choose return at once.
+constexpr int32_t kClasses = 4;
+int32_t kernel_class(int32_t v) {
+  switch (damoe::variant(v).kind) {
+    case damoe::kBig: return 1;
+    case damoe::kBig8: return 2;
+    case damoe::kDeep: return 3;
+    default: return 0;
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -278,6 +292,7 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   hipEvent_t e0 = nullptr, e1 = nullptr;
   std::vector<int32_t> t_bucket, t_nex, t_noda, t_kid, t_Q;
   std::vector<double> alphas(cfg->n_skews);
+  std::vector<double> noop(kClasses, 0.0);  // ms
   std::vector<double> lp;
   std::vector<int32_t> ids;
   std::vector<float> w;
@@ -303,6 +318,56 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
   for (int32_t j = 0; j < cfg->n_skews; ++j) {
     alphas[j] = damoe_alpha_search(Eg, (double)Eg / cfg->skew_X[j], a_samples, a_iters, cfg->seed);
     if (cfg->verbose) std::fprintf(stderr, "damoe_tune: ddist:%.2f -> alpha %.5g\n", cfg->skew_X[j], alphas[j]);
+  }
+
+  // Cost of a launched class that runs nothing, per class c: a fused call whose candidates are
+  // a reference variant of another class and c's first variant, with the device-side id on the
+  // reference, against the reference alone; paired runs (each behind the cache flush) on one
+  // uniform routing of a single token, the median difference.  The cost does not depend on
+  // the call's size, and at one token it is not buried in the run-to-run spread of the GEMMs
+  // (at T = 2048 that spread is about 100 us).  Charged below to the per-exemplar choices of
+  // a bucket whose kernels span several classes.
+  {
+    const int32_t T = 1;
+    int32_t first_of[kClasses];
+    for (int32_t c = 0; c < kClasses; ++c) first_of[c] = -1;
+    for (int32_t v = nv - 1; v >= 0; --v)
+      if (damoe_variant_supports(v, L->wdtype)) first_of[kernel_class(v)] = v;
+    lp.assign(Eg, -std::log((double)Eg));
+    sample_routing(g, lp, T, k, E, ep, 0x9000000u, ids, w);
+    TRY_HIP(hipMemcpyAsync(d_ids, ids.data(), sizeof(int32_t) * ids.size(), hipMemcpyHostToDevice, stream));
+    TRY_HIP(hipMemcpyAsync(d_w, w.data(), sizeof(float) * w.size(), hipMemcpyHostToDevice, stream));
+    TRY(damoe_route_histogram(d_ids, T, k, E, d_counts, d_off, d_perm, d_inv, d_nd, d_bucket, ws, ws_bytes,
+                              stream));
+    for (int32_t c = 0; c < kClasses; ++c) {
+      if (first_of[c] < 0) continue;
+      int32_t ref = -1;
+      for (int32_t o = 0; o < kClasses && ref < 0; ++o)
+        if (o != c && first_of[o] >= 0) ref = first_of[o];
+      if (ref < 0) continue;
+      const uint32_t mask = (1u << ref) | (1u << first_of[c]);
+      TRY_HIP(hipMemcpyAsync(d_vid, &ref, sizeof(int32_t), hipMemcpyHostToDevice, stream));
+      const int32_t nrep = 2 * cfg->reps + 1;
+      std::vector<float> diff(nrep);
+      for (int32_t r = 0; r < nrep; ++r) {
+        float t2[2];
+        for (int32_t m = 0; m < 2; ++m) {
+          if (d_flush) TRY_HIP(hipMemsetAsync(d_flush, r & 0xFF, flush_bytes, stream));
+          TRY_HIP(hipEventRecord(e0, stream));
+          TRY(damoe_fused_moe(L, cfg->x, d_w, T, d_perm, d_inv, d_vid, m == 0 ? ref : -1, m == 0 ? 0u : mask, d_y,
+                              ws, ws_bytes, stream));
+          TRY_HIP(hipEventRecord(e1, stream));
+          TRY_HIP(hipEventSynchronize(e1));
+          TRY_HIP(hipEventElapsedTime(&t2[m], e0, e1));
+        }
+        diff[r] = t2[1] - t2[0];
+      }
+      std::nth_element(diff.begin(), diff.begin() + nrep / 2, diff.end());
+      noop[c] = std::max(0.0, (double)diff[nrep / 2]);
+      if (cfg->verbose)
+        std::fprintf(stderr, "damoe_tune: launched class of %s, not chosen: %.1f us\n",
+                     damoe_variant_name(first_of[c]), noop[c] * 1e3);
+    }
   }
 
   for (int32_t b = 0; b < cfg->n_buckets; ++b) {
@@ -467,22 +532,71 @@ damoe_status damoe_tune(const damoe_layer* L, const damoe_tune_config* cfg, damo
       std::nth_element(t_route.begin(), t_route.begin() + nrep / 2, t_route.end());
       std::nth_element(t_match.begin(), t_match.begin() + nrep / 2, t_match.end());
       const double match_cost = std::max(0.0, (double)t_match[nrep / 2] - (double)t_route[nrep / 2]);
-      double adaptive = match_cost;
+      // Mean over the bucket's exemplars of a choice of kernels: their latencies, the match when
+      // they differ, and for each exemplar the launches of the bucket's other kernel classes.
+      auto cost_of = [&](const std::vector<int32_t>& kid) {
+        uint32_t classes = 0;
+        bool differ = false;
+        for (int32_t j = 0; j < n_added; ++j) {
+          classes |= 1u << kernel_class(kid[j]);
+          differ = differ || kid[j] != kid[0];
+        }
+        double c = differ ? match_cost : 0.0;
+        for (int32_t j = 0; j < n_added; ++j) {
+          c += skew_mean[j][kid[j]] / n_added;
+          for (int32_t o = 0; o < kClasses; ++o)
+            if (((classes >> o) & 1u) && o != kernel_class(kid[j])) c += noop[o] / n_added;
+        }
+        return c;
+      };
+      std::vector<int32_t> kid_ad(t_kid.begin() + first_ex, t_kid.end());
+      const double adaptive = cost_of(kid_ad);
       std::vector<double> single(nv, 0.0);
-      for (int32_t j = 0; j < n_added; ++j) {
-        adaptive += skew_mean[j][t_kid[first_ex + j]] / n_added;
+      for (int32_t j = 0; j < n_added; ++j)
         for (int32_t v = 0; v < nv; ++v) single[v] += skew_mean[j][v] / n_added;
-      }
       int32_t best = 0;
       for (int32_t v = 1; v < nv; ++v)
         if (single[v] < single[best]) best = v;
-      const bool collapse = adaptive >= single[best];
-      if (collapse)
-        for (int32_t j = 0; j < n_added; ++j) t_kid[first_ex + j] = best;
+      // The per-exemplar choice restricted to one kernel class (exemplars that quantise alike
+      // pooled as above): one launch per GEMM, the match only if the kernels still differ.
+      std::vector<int32_t> chosen(n_added, best);
+      double chosen_cost = single[best];
+      const char* how = " -> single variant";
+      if (adaptive < chosen_cost) {
+        chosen = kid_ad;
+        chosen_cost = adaptive;
+        how = "";
+      }
+      for (int32_t c = 0; c < kClasses; ++c) {
+        std::vector<int32_t> kid_c(n_added, -1);
+        for (int32_t j = 0; j < n_added; ++j) {
+          double bv = INFINITY;
+          for (int32_t v = 0; v < nv; ++v) {
+            if (kernel_class(v) != c || !damoe_variant_supports(v, L->wdtype)) continue;
+            double pooled = 0.0;
+            for (int32_t u = 0; u < n_added; ++u)
+              if (std::equal(t_Q.begin() + (first_ex + j) * E, t_Q.begin() + (first_ex + j + 1) * E,
+                             t_Q.begin() + (first_ex + u) * E))
+                pooled += skew_mean[u][v];
+            if (pooled < bv) {
+              bv = pooled;
+              kid_c[j] = v;
+            }
+          }
+        }
+        if (kid_c[0] < 0) continue;  // no variant of this class runs these weights
+        const double cc = cost_of(kid_c);
+        if (cc < chosen_cost) {
+          chosen = kid_c;
+          chosen_cost = cc;
+          how = " -> one kernel class";
+        }
+      }
+      std::copy(chosen.begin(), chosen.end(), t_kid.begin() + first_ex);
       if (cfg->verbose)
-        std::fprintf(stderr, "damoe_tune: T=%d match %.1f us; adaptive %.1f us vs %s %.1f us%s\n", T,
-                     match_cost * 1e3, adaptive * 1e3, damoe_variant_name(best), single[best] * 1e3,
-                     collapse ? " -> single variant" : "");
+        std::fprintf(stderr, "damoe_tune: T=%d match %.1f us; adaptive %.1f us vs %s %.1f us; chosen %.1f us%s\n",
+                     T, match_cost * 1e3, adaptive * 1e3, damoe_variant_name(best), single[best] * 1e3,
+                     chosen_cost * 1e3, how);
     }
     // Distribution-unaware baseline: the fastest variant under uniform routing.
     {
