@@ -1036,8 +1036,8 @@ def run_prefill(args):
                     bm = damoe.variant_tile_m(v)
                     pad = float(np.sum(-(-counts // bm) * bm)) / A
                     # The peaks of the MFMAs the variant issues: bf16 for GEMM1 (every variant) and
-                    # for GEMM2, except the fp8-MFMA big tile's fp8 x fp8 GEMM2.
-                    peak2 = 5000.0 if damoe.variant_name(v).startswith("big8") else mfma
+                    # for GEMM2, except the fp8 x fp8 GEMM2 of the fp8-MFMA variants.
+                    peak2 = 5000.0 if damoe.variant_name(v) in ("big8_bm256", "deep8_bm64") else mfma
                     t_mfma_v = (f_alg * 2 / 3 / mfma + f_alg / 3 / peak2) / 1e6  # us
                     t_roof_v = max(b_alg / bw / 1e3, t_mfma_v)
                     peak_v = f_alg / t_mfma_v / 1e6  # the effective MFMA peak of the call, TFLOP/s

@@ -298,10 +298,11 @@ uint32_t damoe_table_effexp_candidates(const damoe_table* table, int32_t T);
  *   y          bf16 [T][H] output, y[t] = sum_j topk_w[t][j] FFN_{ids[t][j]}(x[t])
  * Only experts with at least one token are read.  Stream-ordered.  T * H * 2
  * must stay below 2^31 (32-bit row offsets), else DAMOE_ERR_UNSUPPORTED; so must
- * H and I of fp8 layers stay <= 16384 when a big-tile variant may run, and T k I below
- * 2^31 when the fp8-MFMA variant may.
- * The fp8-MFMA variant (big8_bm256, fp8 weights only) computes GEMM1 as the big-tile
- * variant, then stores h (rounded to bf16) as OCP e4m3 with one E8M0 scale per 32
+ * H and I of fp8 layers stay <= 16384 when a big-tile or deep-ring variant may run, and
+ * T k I below 2^31 when an fp8-MFMA variant may.
+ * The fp8-MFMA variants (fp8 weights only: big8_bm256, and deep8_bm64 whose GEMM1 is the
+ * deep-ring variant's) compute GEMM1 as the big-tile (deep-ring) variant, then store h
+ * (rounded to bf16) as OCP e4m3 with one E8M0 scale per 32
  * features of a row (the smallest power of two that maps the block's largest magnitude
  * to at most 448; round to nearest even), and GEMM2 as fp8 x fp8 MFMA on those codes and
  * the fp8 W2 with its 128x128 block scales (Sec. II-C's low-precision kernels): y carries

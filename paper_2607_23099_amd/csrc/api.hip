@@ -190,7 +190,7 @@ int32_t damoe_variant_tile_m(int32_t v) {
 
 int32_t damoe_variant_supports(int32_t v, int32_t wdtype) {
   if (v < 0 || v >= num_variants()) return 0;
-  if (variant(v).kind == kBig8) return wdtype == DAMOE_W_FP8_B128;
+  if (variant(v).kind == kBig8 || variant(v).kind == kDeep8) return wdtype == DAMOE_W_FP8_B128;
   if (wdtype == DAMOE_W_MXFP4) return variant(v).kind == kStream && variant(v).bm <= kFp4MaxBM;
   return wdtype == DAMOE_W_BF16 || wdtype == DAMOE_W_FP8_B128;
 }
@@ -422,26 +422,27 @@ static damoe_status fused_impl(const damoe_layer* L, int32_t stage_mask, const u
   // The big-tile kernel runs GEMM1 of both big-tile variants.
   const bool big = force_variant >= 0 ? force_variant == kBigVariant : (candidates & big_bit) != 0;
   const bool big8 = force_variant >= 0 ? force_variant == kBig8Variant : (candidates & big8_bit) != 0;
-  const uint32_t deep_bit = 1u << kDeepVariant;
+  const uint32_t deep_bit = 1u << kDeepVariant, deep8_bit = 1u << kDeep8Variant;
   const bool deep = force_variant >= 0 ? force_variant == kDeepVariant : (candidates & deep_bit) != 0;
+  const bool deep8 = force_variant >= 0 ? force_variant == kDeep8Variant : (candidates & deep8_bit) != 0;
   const bool mega = force_variant >= 0 ? force_variant < kBigVariant
-                                       : (candidates & ~(big_bit | big8_bit | deep_bit)) != 0;
+                                       : (candidates & ~(big_bit | big8_bit | deep_bit | deep8_bit)) != 0;
   // The big-tile kernels hold an item's fp8 scale rows in LDS, the deep-ring kernel in two
   // registers per lane: at most 128 scale columns.
-  if ((big || big8 || deep) && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128)
+  if ((big || big8 || deep || deep8) && L->wdtype == DAMOE_W_FP8_B128 && std::max(L->H, L->I) > 128 * 128)
     return DAMOE_ERR_UNSUPPORTED;
   // The fp8-MFMA GEMM2 addresses the stage-major h with 32-bit offsets.
-  if (big8 && (size_t)T * L->k * L->I >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
+  if ((big8 || deep8) && (size_t)T * L->k * L->I >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
   if (stage_mask & 1) {
     if (mega && launch_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
-    if (deep && launch_deep_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if ((deep || deep8) && launch_deep_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if ((big || big8) && launch_big_gemm1(g1, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
   if (stage_mask & 2) {
     if (mega && launch_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if (deep && launch_deep_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
     if (big && launch_big_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
-    if (big8 && launch_big8_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
+    if ((big8 || deep8) && launch_big8_gemm2(g2, dev->cus, stream) != hipSuccess) return DAMOE_ERR_HIP;
   }
   ReduceArgs r{reinterpret_cast<const uint16_t*>(base + lo.out), topk_w, inv_perm, y, T, L->k, L->H};
   if ((stage_mask & 4) && launch_reduce(r, stream) != hipSuccess) return DAMOE_ERR_HIP;
@@ -486,10 +487,11 @@ damoe_status damoe_moe_layer_noalloc(const damoe_table* t, const damoe_layer* L,
   if ((size_t)T * L->H * 2 >= ((size_t)1 << 31)) return DAMOE_ERR_UNSUPPORTED;
   const uint32_t cand = damoe_table_candidates(t, T);
   if (L->wdtype == DAMOE_W_FP8_B128 &&
-      (cand & ((1u << kBigVariant) | (1u << kBig8Variant) | (1u << kDeepVariant))) &&
+      (cand & ((1u << kBigVariant) | (1u << kBig8Variant) | (1u << kDeepVariant) | (1u << kDeep8Variant))) &&
       std::max(L->H, L->I) > 128 * 128)
     return DAMOE_ERR_UNSUPPORTED;
-  if (L->wdtype == DAMOE_W_FP8_B128 && (cand & (1u << kBig8Variant)) && (size_t)T * L->k * L->I >= ((size_t)1 << 31))
+  if (L->wdtype == DAMOE_W_FP8_B128 && (cand & ((1u << kBig8Variant) | (1u << kDeep8Variant))) &&
+      (size_t)T * L->k * L->I >= ((size_t)1 << 31))
     return DAMOE_ERR_UNSUPPORTED;
   damoe_ws_layout lo;
   if (layout(L->E, L->k, L->H, L->I, T, &lo) != DAMOE_OK) return DAMOE_ERR_INVALID_ARG;

@@ -51,6 +51,7 @@ enum VariantKind : int32_t {
   kBig = 2,     // own kernel, one workgroup per CU: both operands DMA'd into LDS, 256 x 256 items
   kBig8 = 3,    // fp8 weights: big-tile GEMM1 writing MX-fp8 h, own fp8 x fp8 MFMA GEMM2 kernel
   kDeep = 4,    // own kernel, one workgroup per CU: tokens in LDS, weights per wave in a deep ring
+  kDeep8 = 5,   // fp8 weights: deep-ring GEMM1 writing MX-fp8 h, the fp8 x fp8 MFMA GEMM2 of kBig8
 };
 
 // Id of the big-tile variant (its kernel is launched separately from the others).
@@ -61,6 +62,9 @@ constexpr int32_t kBig8Variant = 8;
 
 // Id of the deep-ring variant (its kernel is launched separately from the others).
 constexpr int32_t kDeepVariant = 9;
+// Id of the fp8-MFMA deep-ring variant (fp8 weights only): GEMM1 on the deep-ring kernel, GEMM2
+// on the fp8-MFMA kernel of kBig8Variant.
+constexpr int32_t kDeep8Variant = 10;
 
 // Largest token tile of the MXFP4 stream kernel.
 constexpr int32_t kFp4MaxBM = 32;

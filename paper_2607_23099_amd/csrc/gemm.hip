@@ -752,9 +752,11 @@ const VariantDesc kVariants[] = {
     {"big_bm256", kBig, 256, 128, 256, tile_class(256)},  // k_gemm_big, id kBigVariant
     {"big8_bm256", kBig8, 256, 128, 256, tile_class(256)},  // k_gemm_big8, id kBig8Variant (fp8 weights)
     {"deep_bm64", kDeep, 64, 256, 512, tile_class(64)},     // k_gemm_deep, id kDeepVariant
+    // GEMM1 on k_gemm_deep (64-token tiles), GEMM2 on k_gemm_big8 (256-token tiles)
+    {"deep8_bm64", kDeep8, 64, 256, 256, tile_class(64)},   // id kDeep8Variant (fp8 weights)
 };
 static_assert(kBigVariant == 7 && kBig8Variant == 8, "variant ids are only ever appended");
-static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kDeepVariant + 1, "deep-ring variant id");
+static_assert(sizeof(kVariants) / sizeof(kVariants[0]) == kDeep8Variant + 1, "deep-ring variant ids");
 
 constexpr size_t max_lds() {
   size_t m = 0;

@@ -348,7 +348,8 @@ __global__ void __launch_bounds__(kQThreads, 1) k_gemm_big8(GemmArgs a) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
     return;
   }
-  if (v != kBig8Variant) return;  // the device chose a variant of another kernel class
+  // GEMM2 of both fp8-MFMA variants (their GEMM1s write the same MX-fp8 h).
+  if (v != kBig8Variant && v != kDeep8Variant) return;  // the device chose another kernel class
   big8_body<PK>(a, (lds_t*)big8_smem);
 }
 

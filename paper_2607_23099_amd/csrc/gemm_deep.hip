@@ -37,8 +37,12 @@ constexpr uint32_t kDeepStage = (uint32_t)kDeepBM * kDeepBK * 2;   // 16 KB of t
 constexpr size_t kDeepLds = 2 * (size_t)kDeepStage + 16;           // two stages + ticket word
 static_assert(kDeepBM == 16 << kDeepTileClass, "tile list of the class");
 
+// mx: GEMM1 of the fp8-MFMA deep-ring variant (fp8 weights only): h is rounded to bf16 as for
+// the other variants, then quantised to e4m3 with one E8M0 scale per 32 features of a row into
+// out (codes [N / 64][A][64]) and o8s (scale words [N / 64][A][4]), the stage-major operand of
+// the fp8-MFMA GEMM2 (the layout the big-tile kernel writes for it).
 template <bool GLU, bool FP8, bool PK>
-__device__ __forceinline__ void deep_body(const GemmArgs& a, uint8_t* __restrict__ lds) {
+__device__ __forceinline__ void deep_body(const GemmArgs& a, uint8_t* __restrict__ lds, bool mx) {
   constexpr int BM = kDeepBM, NRW = kDeepNRW, NX = BM / 16, D = deep_ring<FP8>();
   // Stages per loop iteration: the ring slot of k-step ks is ks % D, a constant in the body.
   constexpr int G = D / (D % 4 == 0 ? 4 : D % 2 == 0 ? 2 : 1);  // 4 G = lcm(4, D) k-steps
@@ -246,6 +250,37 @@ __device__ __forceinline__ void deep_body(const GemmArgs& a, uint8_t* __restrict
 #pragma unroll
     for (int s = 0; s < NX; ++s) {
       const int i = s * 16 + rl;
+      if constexpr (GLU && FP8) {
+        if (mx) {
+          // The wave's 32 features w0 .. w0 + 31 of token i (a 32-aligned MX block): lane l holds
+          // 4 of each 16-feature half, so the block maximum is a max over the 4 lanes l % 16 +
+          // 16 j, taken before the row check (those lanes share the token).
+          float hb[2][4];
+          float amax = 0.f;
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float g = acc[b][s][r], u = acc[b + 2][s][r];
+              hb[b][r] = (float)(__bf16)(g / (1.0f + __expf(-g)) * u);
+              amax = fmaxf(amax, fabsf(hb[b][r]));
+            }
+          amax = fmaxf(amax, __shfl_xor(amax, 16));
+          amax = fmaxf(amax, __shfl_xor(amax, 32));
+          const uint32_t sc = mx_scale_byte(amax);
+          const float inv = mx_inv_scale(sc);
+          if (i < rows && w0 < N) {
+            const size_t srow = (size_t)(w0 / 64) * a.A + (p0 + i);
+            uint8_t* h8 = reinterpret_cast<uint8_t*>(a.out) + srow * 64 + w0 % 64;
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+              *reinterpret_cast<uint32_t*>(h8 + 16 * b + 4 * gl) =
+                  e4m3x4(hb[b][0] * inv, hb[b][1] * inv, hb[b][2] * inv, hb[b][3] * inv);
+            if (gl == 0) a.o8s[srow * 4 + (w0 / 32) % 2] = (uint8_t)sc;
+          }
+          continue;
+        }
+      }
       if (i >= rows) continue;
       uint16_t* orow = reinterpret_cast<uint16_t*>(a.out) + (size_t)(p0 + i) * N;
       if (GLU) {
@@ -295,8 +330,10 @@ __global__ void __launch_bounds__(kDeepThreads, 1) k_gemm_deep(GemmArgs a) {
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(&a.ctrl[0], DAMOE_DEVERR_VARIANT);
     return;
   }
-  if (v != kDeepVariant) return;  // the device chose a variant of another kernel class
-  deep_body<GLU, FP8, PK>(a, deep_smem);
+  // This kernel runs the deep-ring variant, and GEMM1 of the fp8-MFMA deep-ring variant.
+  const bool mx = GLU && FP8 && v == kDeep8Variant;
+  if (v != kDeepVariant && !mx) return;  // the device chose a variant of another kernel class
+  deep_body<GLU, FP8, PK>(a, deep_smem, mx);
 }
 
 template <bool GLU>

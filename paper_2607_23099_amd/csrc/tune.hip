@@ -218,14 +218,16 @@ void exemplar(const std::vector<std::vector<int32_t>>& counts, int32_t E, int32_
 
 // The kernel class a variant runs on, of the kClasses that a fused call launches separately:
 // the stream and tiled variants share one kernel, the big-tile, fp8-MFMA and deep-ring
-// variants have kernels of their own.  A fused call whose candidates span several classes
+// variants have kernels of their own, and the fp8-MFMA deep-ring variant, which runs the
+// deep-ring GEMM1 and the fp8-MFMA GEMM2, counts as a class of its own.  A fused call whose candidates span several classes
 // launches all of them, and those the device did not choose return at once.
-constexpr int32_t kClasses = 4;
+constexpr int32_t kClasses = 5;
 int32_t kernel_class(int32_t v) {
   switch (damoe::variant(v).kind) {
     case damoe::kBig: return 1;
     case damoe::kBig8: return 2;
     case damoe::kDeep: return 3;
+    case damoe::kDeep8: return 4;
     default: return 0;
   }
 }

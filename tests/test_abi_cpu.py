@@ -45,11 +45,12 @@ def test_status_strings_and_registry():
     assert len(set(names)) == nv and all(names)
     assert damoe.variant_name(nv) == "" and damoe.variant_tile_m(-1) == 0
     assert all(damoe.variant_tile_m(v) in (16, 32, 64, 128, 256) for v in range(nv))
-    # Every variant runs fp8 weights; the fp8-MFMA big tile runs nothing else.
+    # Every variant runs fp8 weights.
     assert all(damoe.variant_supports(v, damoe.W_FP8_B128) for v in range(nv))
-    big8 = names.index("big8_bm256")
-    assert [v for v in range(nv) if not damoe.variant_supports(v, damoe.W_BF16)] == [big8]
-    assert not damoe.variant_supports(big8, damoe.W_MXFP4)
+    # The fp8-MFMA variants (GEMM2 on fp8 codes of h) run fp8 weights only.
+    fp8_only = [names.index("big8_bm256"), names.index("deep8_bm64")]
+    assert [v for v in range(nv) if not damoe.variant_supports(v, damoe.W_BF16)] == fp8_only
+    assert not any(damoe.variant_supports(v, damoe.W_MXFP4) for v in fp8_only)
     assert not damoe.variant_supports(0, 7)
 
 

@@ -1,9 +1,9 @@
-"""GPU check of the fp8-MFMA variant's h quantisation: its GEMM1 (the big-tile kernel) writes h
-rounded to bf16, then as e4m3 codes with one E8M0 scale per 32 features of a row (stage-major,
-in 4-byte words per 64 features).  The same
-kernel with the big-tile variant stores the bf16 h itself (stage-major), from the same accumulation, so the codes
-and scales must equal those of the test-side MX quantiser (tests/mx_ref.py, written from the OCP
-formats) applied to that bf16 h, bit for bit."""
+"""GPU check of the fp8-MFMA variants' h quantisation: their GEMM1 (the big-tile kernel for
+big8_bm256, the deep-ring kernel for deep8_bm64) writes h rounded to bf16, then as e4m3 codes with
+one E8M0 scale per 32 features of a row (stage-major, in 4-byte words per 64 features).  The same
+kernel with the bf16-h variant (big_bm256: h stage-major; deep_bm64: h row-major) stores the bf16 h
+itself, from the same accumulation, so the codes and scales must equal those of the test-side MX
+quantiser (tests/mx_ref.py, written from the OCP formats) applied to that bf16 h, bit for bit."""
 import numpy as np
 import pytest
 
@@ -25,13 +25,14 @@ def small_fp8(request):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("pair", [("big_bm256", "big8_bm256"), ("deep_bm64", "deep8_bm64")], ids=["big", "deep"])
 @pytest.mark.parametrize("T,alpha,seed", [(3, 1.0, 41), (100, 1.0, 42), (600, 0.05, 43)])
-def test_h_quantised_bit_exact(small_fp8, T, alpha, seed):
+def test_h_quantised_bit_exact(small_fp8, pair, T, alpha, seed):
     torch = torch_cuda()
     dl, path = small_fp8
     sh = dl.shape
     names = [damoe.variant_name(v) for v in range(damoe.num_variants())]
-    big, big8 = names.index("big_bm256"), names.index("big8_bm256")
+    big, big8 = names.index(pair[0]), names.index(pair[1])
     r = synth.routing(sh.E, sh.k, T, alpha, [seed])
     path.set_routing(r)
     path.fill_x(T, seed)
@@ -44,9 +45,12 @@ def test_h_quantised_bit_exact(small_fp8, T, alpha, seed):
     path.fused_stage(0, T, big)
     torch.cuda.synchronize()
     # The big-tile kernel's h is stage-major in its GEMM2's stages, 64 columns with fp8
-    # weights: [I / 64][A][64] bf16.
+    # weights: [I / 64][A][64] bf16; the deep-ring kernel's is row-major [A][I].
     h = path.ws[lo["h"]: lo["h"] + A * sh.I * 2].view(torch.bfloat16).float().cpu().numpy()
-    h = h.astype(np.float64).reshape(sh.I // 64, A, 64).transpose(1, 0, 2).reshape(A, sh.I)
+    if pair[0] == "big_bm256":
+        h = h.astype(np.float64).reshape(sh.I // 64, A, 64).transpose(1, 0, 2).reshape(A, sh.I)
+    else:
+        h = h.astype(np.float64).reshape(A, sh.I)
     path.fused_stage(0, T, big8)
     torch.cuda.synchronize()
     # Stage-major: codes [I / 64][A][64], scale words [I / 64][A][4] whose bytes 0 and 1 are the
