@@ -57,11 +57,14 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-# HBM traffic summaries of the decode roofline kernel, per weight format: file, rocprof kernel
-# name prefix, and the bench flag that selects the format.
+# HBM traffic summaries of the decode roofline stage (GEMM1 + SwiGLU), per weight format: file,
+# rocprof kernel name prefixes of the stage's kernels (the first is launched by every call; a
+# call whose device-side choice is another class's variant runs that class's kernel, and the
+# others return at once), and the bench flag that selects the format.
 TRAFFIC = {
-    "bf16": (os.path.join(ROOT, "profiles", "k_gemm_glu_decode_sweep_traffic.txt"), "k_gemm<true", ""),
-    "mxfp4": (os.path.join(ROOT, "profiles", "k_gemm_fp4_glu_decode_sweep_traffic.txt"), "k_gemm_fp4<true",
+    "bf16": (os.path.join(ROOT, "profiles", "k_gemm_glu_decode_sweep_traffic.txt"),
+             ("k_gemm<true", "k_gemm_deep<true", "k_gemm_big<true"), ""),
+    "mxfp4": (os.path.join(ROOT, "profiles", "k_gemm_fp4_glu_decode_sweep_traffic.txt"), ("k_gemm_fp4<true",),
               " --wdtype mxfp4"),
 }
 GEMM_SOURCES = ("csrc/gemm.hip", "csrc/device.h", "csrc/common.h", "csrc/queue.h")
@@ -102,27 +105,31 @@ def summarize_traffic(pmc_dir: str, wdtype: str = "bf16"):
         return [float(r["Counter_Value"]) * 1024 for r in csv.DictReader(open(f))
                 if r["Counter_Name"] == counter and match(r["Kernel_Name"])]
 
-    path, prefix, flag = TRAFFIC[wdtype]
-    is_glu = lambda n: prefix in n
+    path, prefixes, flag = TRAFFIC[wdtype]
+    is_glu = lambda n: any(p_ in n for p_ in prefixes)
     is_copy = lambda n: "copy" in n.lower() or "elementwise" in n.lower()
     n_copy = 4 << 30
     fcal = max(values("copy_fetch", "FETCH_SIZE", is_copy)) / n_copy
     wcal = max(values("copy_write", "WRITE_SIZE", is_copy)) / n_copy
-    fetch = values("fetch", "FETCH_SIZE", is_glu)
-    write = values("write", "WRITE_SIZE", is_glu)
-    per_launch = float(np.mean(fetch)) / fcal + float(np.mean(write)) / wcal
+    # Per GEMM1 call: the bytes of all of the stage's kernels over the calls (launches of the
+    # kernel that every call launches).
+    calls = len(values("fetch", "FETCH_SIZE", lambda n: prefixes[0] in n))
+    fetch = sum(values("fetch", "FETCH_SIZE", is_glu)) / calls
+    write = sum(values("write", "WRITE_SIZE", is_glu)) / calls
+    per_launch = fetch / fcal + write / wcal
     with open(path, "w") as f:
-        f.write(f"# HBM traffic of {prefix}...> (GEMM1 + SwiGLU) over the DeepSeek-V3 decode sweep{flag}\n")
+        f.write(f"# HBM traffic of the GEMM1 + SwiGLU stage ({', '.join(p_ + '...>' for p_ in prefixes)}) over "
+                f"the DeepSeek-V3 decode sweep{flag}, per call\n")
         f.write("# rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv -d <dir>/fetch -- "
                 f"python3 -u bench.py --steps 2 --warmup 1 --no-cpu-baseline --bench-trace-steps 0{flag}\n")
         f.write("# calibration: the same counters on python3 -u bench.py --workload copy --steps 3 "
                 "(4 GiB read + 4 GiB written per call)\n")
         f.write(f"source_digest: {gemm_source_digest()}\n")
-        f.write(f"launches: {len(fetch)}\n")
+        f.write(f"launches: {calls}\n")
         f.write(f"fetch_calibration: {fcal:.4f}\n")
         f.write(f"write_calibration: {wcal:.4f}\n")
-        f.write(f"fetch_bytes_per_launch: {np.mean(fetch) / fcal:.0f}\n")
-        f.write(f"write_bytes_per_launch: {np.mean(write) / wcal:.0f}\n")
+        f.write(f"fetch_bytes_per_launch: {fetch / fcal:.0f}\n")
+        f.write(f"write_bytes_per_launch: {write / wcal:.0f}\n")
         f.write(f"hbm_bytes_per_launch: {per_launch:.0f}\n")
     print(open(path).read())
 
@@ -1400,7 +1407,7 @@ def main():
                                + ("" if force < 0 else f" (forced variant {damoe.variant_name(force)})"),
                    "points": len(points), "table": table_note},
         "roofline": {"bound": "hbm", "kernel": "k_gemm_fp4<GEMM1+SwiGLU>" if args.wdtype == "mxfp4"
-                     else "k_gemm<GEMM1+SwiGLU>", "achieved": round(achieved, 1),
+                     else "GEMM1+SwiGLU stage: k_gemm, k_gemm_deep where dispatched", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(args.wdtype),
                      "algorithmic_bytes_per_launch": round(g1_bytes / max(len(all_events), 1)),
