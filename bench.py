@@ -793,6 +793,9 @@ def run_imbalance(args):
                 path.candidates = 0
                 lat = []
                 for v in range(nv):
+                    if not damoe.variant_supports(v, dl.wdtype):  # fp8-only variants
+                        lat.append(float("inf"))
+                        continue
                     for _ in range(args.warmup):
                         path.fused(T, v)
                     pairs = []
@@ -907,6 +910,9 @@ def run_ep(args):
                     path.candidates = 0
                     lat = []
                     for v in range(nv):
+                        if not damoe.variant_supports(v, path.dl.wdtype):  # fp8-only variants
+                            lat.append(float("inf"))
+                            continue
                         for _ in range(args.warmup):
                             path.fused(tl, v)
                         pairs = []
