@@ -257,20 +257,23 @@ __device__ __forceinline__ void big8_body(const GemmArgs& a, lds_t* lds) {
             }
             xs[n] = (int)sb[kQTok + kQW + (32 * nb + r32) * 4 + g];
           }
-          // Every operand of the stage is read before the first MFMA, into registers of its own,
-          // so the LDS latency is paid once per stage (and hidden by the other wave of the SIMD).
+          // The weight operand of each 32-row block m + 1 is read, into registers of its own,
+          // ahead of the MFMAs of block m, so only the token operands and the first weight block
+          // wait on LDS before the matrix cores start.
           v8i wv[4];
+          wv[0] = read_w(sb, 0);
 #pragma unroll
-          for (int m = 0; m < 4; ++m) wv[m] = read_w(sb, m);
-          __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the MFMAs
-#pragma unroll
-          for (int m = 0; m < 4; ++m)
+          for (int m = 0; m < 4; ++m) {
+            if (m + 1 < 4) wv[m + 1] = read_w(sb, m + 1);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int n = 0; n < NN; ++n) {
               if constexpr (FIRST) acc[m][n] *= rsc;
               acc[m][n] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(wv[m], xt[n], acc[m][n], 0, 0, 0, wexp, 0,
                                                                          xs[n]);
             }
+            __builtin_amdgcn_sched_barrier(0);
+          }
         }
       };
 
