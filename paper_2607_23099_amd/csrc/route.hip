@@ -14,6 +14,7 @@ constexpr int kNW = kRouteThreads / kWave;  // 16 waves
 constexpr int kMaxExemplarRegs = 8;  // exemplar entries prefetched per lane (E <= 512)
 constexpr int kValueBins = 4096;     // counting sort of the histogram when every count is smaller
 constexpr int kIdBatch = 16;         // 64-id chunks loaded together per wave
+constexpr int kRouteSmallA = kNW * 64;  // up to here every wave holds at most one chunk
 
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const int lane = threadIdx.x & 63;
@@ -72,12 +73,14 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
 // wave totals go through LDS, and every wave scans them itself (one LDS read per lane of row
 // 0, a 16-lane DPP scan, two lane reads).  `tmp` holds N * kNW ints.  Returns the block
 // totals in tot[].  Ends with a barrier, so `tmp` may be reused at once.
+// `active` (uniform over a wave): false for a wave whose values are all zero, which skips its
+// scans.
 template <int N>
-__device__ void block_scan(const int (&v)[N], int (&ex)[N], int (&tot)[N], int* tmp) {
+__device__ void block_scan(const int (&v)[N], int (&ex)[N], int (&tot)[N], int* tmp, bool active = true) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int inc[N];
 #pragma unroll
-  for (int c = 0; c < N; ++c) inc[c] = wave_incl_scan(v[c]);
+  for (int c = 0; c < N; ++c) inc[c] = active ? wave_incl_scan(v[c]) : 0;
   if (lane == 63)
 #pragma unroll
     for (int c = 0; c < N; ++c) tmp[c * kNW + w] = inc[c];
@@ -241,7 +244,10 @@ __device__ void dispatch_core(Smem& sm, int E, int total, int ci, const Dispatch
 // the wave's counter of that expert.  Per expert, an exclusive scan of the 16 wave counts
 // gives each wave's starting offset in the expert's segment, so the order inside a segment
 // is the flat order a = t k + j.
-template <bool DISPATCH, bool MULTI>
+// B: 64-id chunks a wave loads together (kIdBatch; 1 for calls of at most kRouteSmallA
+// assignments, where every wave holds one chunk: a smaller kernel, whose code a cold
+// instruction cache fetches sooner).
+template <bool DISPATCH, bool MULTI, int B = kIdBatch>
 __global__ void __launch_bounds__(kRouteThreads)
 k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, DispatchIn d) {
   __shared__ Smem sm;
@@ -278,8 +284,22 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
       const int r = lane + 64 * m, x = w + h * kNW;
       qpre[h][m] = (DISPATCH && x < d.n_ex && r < E) ? d.Q[(size_t)x * E + r] : 0;
     }
-  if (!MULTI)
-    for (int x = tid; x < kNW * E; x += kRouteThreads) sm.wcnt[x / E][x % E] = 0;
+  // The wave's first chunks of ids are requested before the clearing below, so that their
+  // latency overlaps it.
+  int nbits = 1;
+  while ((1 << nbits) < E) ++nbits;
+  const int R = (A + kNW * 64 - 1) / (kNW * 64) * 64;
+  const int a_lo = w * R, a_hi = min(A, a_lo + R);
+  const bool one_batch = R <= 64 * B;
+  int eb[B];
+  const bool pre = !MULTI && a_lo < a_hi;
+  if (pre)
+#pragma unroll
+    for (int q = 0; q < B; ++q) eb[q] = ids[min(a_lo + 64 * q + lane, a_hi - 1)];
+  static_assert(DAMOE_MAX_E <= kRouteThreads, "one thread per expert");
+  if (!MULTI && tid < E)
+#pragma unroll
+    for (int u = 0; u < kNW; ++u) sm.wcnt[u][tid] = 0;
   if (DISPATCH)
     for (int v = tid; v < kValueBins; v += kRouteThreads) sm.vh[v] = 0;
   if (tid == 0) {
@@ -288,28 +308,24 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   }
   __syncthreads();
 
-  // a2: per-wave histogram.  Ids move in batches of kIdBatch chunks (one memory latency per
-  // batch); a range of at most one batch keeps its ids in registers for the scatter.
-  int nbits = 1;
-  while ((1 << nbits) < E) ++nbits;
-  const int R = (A + kNW * 64 - 1) / (kNW * 64) * 64;
-  const int a_lo = w * R, a_hi = min(A, a_lo + R);
-  const bool one_batch = R <= 64 * kIdBatch;
+  // a2: per-wave histogram.  Ids move in batches of B chunks (one memory latency per batch);
+  // a range of at most one batch keeps its ids in registers for the scatter.
   int bad = 0;
-  int eb[kIdBatch];
   if (!MULTI)
-  for (int a0 = a_lo; a0 < a_hi; a0 += 64 * kIdBatch) {
-    // Unconditional loads (index clamped into the range) so the batch issues back to back.
+  for (int a0 = a_lo; a0 < a_hi; a0 += 64 * B) {
+    // Unconditional loads (index clamped into the range) so the batch issues back to back;
+    // the first batch was requested at kernel entry.
+    if (a0 != a_lo)
 #pragma unroll
-    for (int q = 0; q < kIdBatch; ++q) eb[q] = ids[min(a0 + 64 * q + lane, a_hi - 1)];
+      for (int q = 0; q < B; ++q) eb[q] = ids[min(a0 + 64 * q + lane, a_hi - 1)];
 #pragma unroll
-    for (int q = 0; q < kIdBatch; ++q) {
+    for (int q = 0; q < B; ++q) {
       const int a = a0 + 64 * q + lane;
       if (a >= a_hi) eb[q] = -1;
       bad += (a < a_hi && eb[q] >= E) ? 1 : 0;  // negative ids are masked slots, not errors
     }
 #pragma unroll
-    for (int q = 0; q < kIdBatch; ++q) {
+    for (int q = 0; q < B; ++q) {
       if (a0 + 64 * q >= a_hi) break;
       const bool valid = eb[q] >= 0 && eb[q] < E;
       const uint64_t peers = same_expert(eb[q], valid, nbits);
@@ -373,9 +389,11 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   v[0] = c;
 #pragma unroll
   for (int cls = 0; cls < DAMOE_N_TILE_SIZES; ++cls) v[1 + cls] = (c + (16 << cls) - 1) / (16 << cls);
-  const uint64_t sq = wave_sum_u64((uint64_t)c * (uint64_t)c);
+  // Waves past the last expert hold zeros: their scans and sums are skipped.
+  const bool has_experts = w * 64 < E;
+  const uint64_t sq = has_experts ? wave_sum_u64((uint64_t)c * (uint64_t)c) : 0ull;
   if (lane == 0) sm.tmp64[w] = sq;
-  block_scan<1 + DAMOE_N_TILE_SIZES>(v, ex, tot, sm.tmp);
+  block_scan<1 + DAMOE_N_TILE_SIZES>(v, ex, tot, sm.tmp, has_experts);
   const int off = ex[0], total = tot[0];
   if (tid < E) {
     o.counts[tid] = c;
@@ -441,16 +459,16 @@ k_route(const int32_t* __restrict__ ids, int32_t A, int32_t E, RouteOut o, Dispa
   __syncthreads();  // segment bases
 
   // a4: stable scatter, per wave over its own range.
-  for (int a0 = a_lo; a0 < a_hi; a0 += 64 * kIdBatch) {
+  for (int a0 = a_lo; a0 < a_hi; a0 += 64 * B) {
     if (!one_batch) {
 #pragma unroll
-      for (int q = 0; q < kIdBatch; ++q) eb[q] = ids[min(a0 + 64 * q + lane, a_hi - 1)];
+      for (int q = 0; q < B; ++q) eb[q] = ids[min(a0 + 64 * q + lane, a_hi - 1)];
 #pragma unroll
-      for (int q = 0; q < kIdBatch; ++q)
+      for (int q = 0; q < B; ++q)
         if (a0 + 64 * q + lane >= a_hi) eb[q] = -1;
     }
 #pragma unroll
-    for (int q = 0; q < kIdBatch; ++q) {
+    for (int q = 0; q < B; ++q) {
       if (a0 + 64 * q >= a_hi) break;
       const int a = a0 + 64 * q + lane, e = eb[q];
       const bool valid = e >= 0 && e < E;
@@ -658,6 +676,10 @@ template <bool DISPATCH>
 hipError_t run_route(const int32_t* ids, int32_t T, int32_t k, int32_t E, RouteOut o, const DispatchIn& d,
                      int32_t* scratch, hipStream_t stream) {
   const int64_t A = (int64_t)T * k;
+  if (A <= kRouteSmallA) {
+    hipLaunchKernelGGL((k_route<DISPATCH, false, 1>), dim3(1), dim3(kRouteThreads), 0, stream, ids, (int32_t)A, E, o, d);
+    return hipGetLastError();
+  }
   if (A < kRouteMultiMinA) {
     hipLaunchKernelGGL((k_route<DISPATCH, false>), dim3(1), dim3(kRouteThreads), 0, stream, ids, (int32_t)A, E, o, d);
     return hipGetLastError();
