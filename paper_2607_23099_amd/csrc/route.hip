@@ -217,14 +217,25 @@ __device__ void dispatch_core(Smem& sm, int E, int total, int ci, const Dispatch
   }
   __syncthreads();
   if (w == 0) {
-    // First maximum over the exemplars, in index order.
+    // First maximum over the exemplars, in index order: each lane keeps the first maximum of
+    // exemplars lane, lane + 64, ..., then the lanes combine pairwise (the larger score, on a
+    // tie the lower index).
     long long best = 0;
     int bi = -1;
-    for (int x = 0; x < d.n_ex; ++x) {
+    for (int x = lane; x < d.n_ex; x += 64) {
       const long long sc = sm.score[x];
       if (bi < 0 || sc > best) {
         best = sc;
         bi = x;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const long long ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (oi >= 0 && (bi < 0 || ob > best || (ob == best && oi < bi))) {
+        best = ob;
+        bi = oi;
       }
     }
     if (lane == 0) {
